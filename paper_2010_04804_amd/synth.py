@@ -1,0 +1,301 @@
+"""Seeded synthetic ensembles and inputs.
+
+This module only draws random numbers and lays them out as plain node arrays;
+it holds none of the scoring arithmetic, so both the product library and the
+test oracle can be fed from it.
+
+A model is a dict of numpy arrays in "caller" form, one entry per tree node:
+
+    n_trees, n_features, n_outputs, leaf_dim       ints
+    tree_node_offset  int64 [n_trees + 1]  tree t owns nodes [off[t], off[t+1])
+    feature           int32 [nodes]  feature tested by an internal node, -1 at a leaf
+    threshold         float32 [nodes]  rule: x[feature] < threshold goes left
+    left, right       int32 [nodes]  tree-local child ids, -1 at a leaf
+    leaf_value        float32 [nodes * leaf_dim]  read only at leaves
+    tree_class        int32 [n_trees] or None  output column of a scalar-leaf tree
+    aggregation       "sum" | "mean"
+    transform         "none" | "sigmoid" | "softmax"
+    base_score        float32 [n_outputs] or None
+
+Every draw is made in float64 and rounded once to float32. Each config uses
+``SeedSequence(seed).spawn(2)`` as [model stream, data stream], so the rows of
+a smaller batch are a prefix of a larger batch of the same config.
+
+The five workloads stand in for the paper's evaluation models (Sec. 6.1.1:
+500 trees of maximum depth 8 trained on Fraud, Epsilon, Year, Covtype, Higgs
+and Airline), whose datasets and trained models are not available here; they
+copy the shapes only (feature counts, tree counts and depths, class counts).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "CONFIGS",
+    "perfect_forest",
+    "leafwise_forest",
+    "make_model",
+    "make_rows",
+    "make_config",
+    "permute_nodes",
+    "model_stats",
+]
+
+
+def _streams(seed: int):
+    ss = np.random.SeedSequence(seed)
+    m, d = ss.spawn(2)
+    return np.random.Generator(np.random.PCG64(m)), np.random.Generator(np.random.PCG64(d))
+
+
+def _f32(a) -> np.ndarray:
+    return np.asarray(a, dtype=np.float64).astype(np.float32)
+
+
+def perfect_forest(rng, n_trees, depth, n_features, draw_threshold, draw_leaves, leaf_dim=1):
+    """Perfect binary trees of ``depth`` levels of decisions, numbered in
+    breadth-first order (node i has children 2i+1, 2i+2).
+
+    ``draw_threshold(rng, features)`` returns one threshold per internal node
+    given the feature it tests; ``draw_leaves(rng, n)`` returns ``n`` leaf
+    values (``[n, leaf_dim]`` when ``leaf_dim > 1``).
+    """
+    n_int = (1 << depth) - 1
+    n_nodes = 2 * n_int + 1
+    feature = np.full((n_trees, n_nodes), -1, np.int32)
+    threshold = np.zeros((n_trees, n_nodes), np.float32)
+    left = np.full((n_trees, n_nodes), -1, np.int32)
+    right = np.full((n_trees, n_nodes), -1, np.int32)
+    value = np.zeros((n_trees, n_nodes, leaf_dim), np.float32)
+    ids = np.arange(n_int, dtype=np.int32)
+    for t in range(n_trees):
+        f = rng.integers(0, n_features, size=n_int).astype(np.int32)
+        feature[t, :n_int] = f
+        threshold[t, :n_int] = _f32(draw_threshold(rng, f))
+        left[t, :n_int] = 2 * ids + 1
+        right[t, :n_int] = 2 * ids + 2
+        v = np.asarray(draw_leaves(rng, n_int + 1), np.float64).reshape(n_int + 1, leaf_dim)
+        value[t, n_int:, :] = _f32(v)
+    return {
+        "n_trees": n_trees,
+        "n_features": n_features,
+        "leaf_dim": leaf_dim,
+        "tree_node_offset": np.arange(n_trees + 1, dtype=np.int64) * n_nodes,
+        "feature": feature.reshape(-1),
+        "threshold": threshold.reshape(-1),
+        "left": left.reshape(-1),
+        "right": right.reshape(-1),
+        "leaf_value": value.reshape(-1),
+    }
+
+
+def leafwise_forest(rng, n_trees, n_leaves, max_depth, p_deepen, n_features,
+                    draw_threshold, draw_leaves):
+    """Unbalanced trees grown one split at a time until ``n_leaves`` leaves.
+
+    Reading of "random split side chosen with p=0.7 to deepen": after a split,
+    with probability ``p_deepen`` the next split is on one of the two new
+    children (chosen uniformly) if its depth is below ``max_depth``; otherwise
+    the next split is on a leaf drawn uniformly from all leaves of depth below
+    ``max_depth``. Children are appended as (left, right), so node ids follow
+    creation order and the root is node 0.
+    """
+    offs = [0]
+    feats, thrs, lefts, rights, vals = [], [], [], [], []
+    for _ in range(n_trees):
+        depth = [0]
+        feat = [-1]
+        left = [-1]
+        right = [-1]
+        leaves = [0]
+        target = 0
+        while len(leaves) < n_leaves:
+            c1, c2 = len(depth), len(depth) + 1
+            d = depth[target] + 1
+            depth += [d, d]
+            feat += [-1, -1]
+            left += [-1, -1]
+            right += [-1, -1]
+            feat[target] = int(rng.integers(0, n_features))
+            left[target], right[target] = c1, c2
+            leaves.remove(target)
+            leaves += [c1, c2]
+            if len(leaves) >= n_leaves:
+                break
+            if rng.random() < p_deepen:
+                cand = c1 if rng.random() < 0.5 else c2
+                if depth[cand] < max_depth:
+                    target = cand
+                    continue
+            eligible = [l for l in leaves if depth[l] < max_depth]
+            target = eligible[int(rng.integers(0, len(eligible)))]
+        n = len(depth)
+        feat_a = np.asarray(feat, np.int32)
+        internal = feat_a >= 0
+        thr = np.zeros(n, np.float32)
+        thr[internal] = _f32(draw_threshold(rng, feat_a[internal]))
+        val = np.zeros(n, np.float32)
+        val[~internal] = _f32(draw_leaves(rng, int((~internal).sum())))
+        feats.append(feat_a)
+        thrs.append(thr)
+        lefts.append(np.asarray(left, np.int32))
+        rights.append(np.asarray(right, np.int32))
+        vals.append(val)
+        offs.append(offs[-1] + n)
+    return {
+        "n_trees": n_trees,
+        "n_features": n_features,
+        "leaf_dim": 1,
+        "tree_node_offset": np.asarray(offs, np.int64),
+        "feature": np.concatenate(feats),
+        "threshold": np.concatenate(thrs),
+        "left": np.concatenate(lefts),
+        "right": np.concatenate(rights),
+        "leaf_value": np.concatenate(vals),
+    }
+
+
+# ---------------------------------------------------------------------------
+# The five workloads. Each entry gives the recipe; make_config builds it.
+
+CONFIGS = {
+    1: dict(name="tiny GBDT regressor: 10 perfect trees depth 3, 8 features",
+            seed=0, n_rows=1_000),
+    2: dict(name="GBDT binary classifier: 500 perfect trees depth 8, 28 features",
+            seed=2, n_rows=1_000_000, n_rows_small=10_000),
+    3: dict(name="random forest, wide input: 500 perfect trees depth 8, 2000 features, 2 classes",
+            seed=3, n_rows=100_000),
+    4: dict(name="multiclass GBDT: 7 classes x 500 trees depth 8, 54 features",
+            seed=4, n_rows=1_000_000),
+    5: dict(name="unbalanced GBDT: 500 leaf-wise trees, 256 leaves, depth <= 12, 100 features",
+            seed=5, n_rows=1_000_000),
+}
+
+_CFG4_CONT = 10  # config 4: columns 0..9 continuous, 10..53 binary
+
+
+def make_model(cfg: int) -> dict:
+    """The seeded ensemble of workload ``cfg`` (1..5)."""
+    rng, _ = _streams(CONFIGS[cfg]["seed"])
+    if cfg == 1:
+        m = perfect_forest(rng, 10, 3, 8,
+                           lambda r, f: r.random(f.size),
+                           lambda r, n: r.normal(0.0, 0.1, n))
+        m.update(n_outputs=1, tree_class=None, aggregation="sum", transform="none", base_score=None)
+    elif cfg == 2:
+        m = perfect_forest(rng, 500, 8, 28,
+                           lambda r, f: r.standard_normal(f.size),
+                           lambda r, n: r.normal(0.0, 0.05, n))
+        m.update(n_outputs=1, tree_class=None, aggregation="sum", transform="sigmoid", base_score=None)
+    elif cfg == 3:
+        def leaves(r, n):
+            p = r.random(n)
+            return np.stack([1.0 - p, p], axis=1)
+        m = perfect_forest(rng, 500, 8, 2000,
+                           lambda r, f: r.uniform(-1.0, 1.0, f.size),
+                           leaves, leaf_dim=2)
+        m.update(n_outputs=2, tree_class=None, aggregation="mean", transform="none", base_score=None)
+    elif cfg == 4:
+        def thr(r, f):
+            cont = r.standard_normal(f.size)
+            return np.where(f < _CFG4_CONT, cont, 0.5)
+        m = perfect_forest(rng, 3500, 8, 54, thr, lambda r, n: r.normal(0.0, 0.05, n))
+        m.update(n_outputs=7, tree_class=(np.arange(3500) % 7).astype(np.int32),
+                 aggregation="sum", transform="softmax", base_score=None)
+    elif cfg == 5:
+        m = leafwise_forest(rng, 500, 256, 12, 0.7, 100,
+                            lambda r, f: r.random(f.size),
+                            lambda r, n: r.normal(0.0, 0.02, n))
+        m.update(n_outputs=1, tree_class=None, aggregation="sum", transform="none", base_score=None)
+    else:
+        raise ValueError(f"unknown config {cfg}")
+    return m
+
+
+def make_rows(cfg: int, n_rows: int) -> np.ndarray:
+    """``n_rows`` seeded input rows of workload ``cfg``, float32 [n_rows, F]."""
+    _, rng = _streams(CONFIGS[cfg]["seed"])
+    if cfg == 1:
+        x = rng.random((n_rows, 8))
+    elif cfg == 2:
+        x = rng.standard_normal((n_rows, 28))
+    elif cfg == 3:
+        x = rng.uniform(-1.0, 1.0, (n_rows, 2000))
+    elif cfg == 4:
+        x = np.empty((n_rows, 54))
+        x[:, :_CFG4_CONT] = rng.standard_normal((n_rows, _CFG4_CONT))
+        x[:, _CFG4_CONT:] = rng.integers(0, 2, (n_rows, 54 - _CFG4_CONT))
+    elif cfg == 5:
+        x = rng.random((n_rows, 100))
+    else:
+        raise ValueError(f"unknown config {cfg}")
+    return np.ascontiguousarray(_f32(x))
+
+
+def make_config(cfg: int, n_rows: int | None = None):
+    """(model, X) for workload ``cfg``; ``n_rows`` defaults to its batch size."""
+    n = CONFIGS[cfg]["n_rows"] if n_rows is None else n_rows
+    return make_model(cfg), make_rows(cfg, n)
+
+
+def permute_nodes(model: dict, seed: int) -> dict:
+    """The same ensemble with each tree's non-root nodes renumbered at random.
+
+    Node 0 stays the root. Returns a new dict; leaf ids reported against it
+    are in the new numbering (``perm[old] = new`` per tree is stored under
+    ``"_perm"``).
+    """
+    rng = np.random.Generator(np.random.PCG64(seed))
+    off = model["tree_node_offset"]
+    ld = model["leaf_dim"]
+    out = {k: v for k, v in model.items()}
+    feature = model["feature"].copy()
+    threshold = model["threshold"].copy()
+    left = model["left"].copy()
+    right = model["right"].copy()
+    value = model["leaf_value"].reshape(-1, ld).copy()
+    perms = []
+    for t in range(model["n_trees"]):
+        a, b = int(off[t]), int(off[t + 1])
+        n = b - a
+        perm = np.concatenate([[0], 1 + rng.permutation(n - 1)]).astype(np.int32)  # old -> new
+        inv = np.empty(n, np.int32)
+        inv[perm] = np.arange(n, dtype=np.int32)  # new -> old
+        f_old = model["feature"][a:b]
+        feature[a:b] = f_old[inv]
+        threshold[a:b] = model["threshold"][a:b][inv]
+        lo = model["left"][a:b][inv]
+        ro = model["right"][a:b][inv]
+        left[a:b] = np.where(lo >= 0, perm[np.maximum(lo, 0)], -1)
+        right[a:b] = np.where(ro >= 0, perm[np.maximum(ro, 0)], -1)
+        value[a:b] = model["leaf_value"].reshape(-1, ld)[a:b][inv]
+        perms.append(perm)
+    out.update(feature=feature, threshold=threshold, left=left, right=right,
+               leaf_value=value.reshape(-1), _perm=perms)
+    return out
+
+
+def model_stats(model: dict) -> dict:
+    """Shape statistics of an ensemble: max depth, mean leaf depth, node counts."""
+    off = model["tree_node_offset"]
+    depths, leaf_depth_sum, n_leaves = [], 0, 0
+    for t in range(model["n_trees"]):
+        a, b = int(off[t]), int(off[t + 1])
+        d = np.zeros(b - a, np.int64)
+        stack = [0]
+        while stack:
+            v = stack.pop()
+            if model["feature"][a + v] >= 0:
+                for c in (model["left"][a + v], model["right"][a + v]):
+                    d[c] = d[v] + 1
+                    stack.append(int(c))
+        leaf = model["feature"][a:b] < 0
+        depths.append(int(d[leaf].max()))
+        leaf_depth_sum += int(d[leaf].sum())
+        n_leaves += int(leaf.sum())
+    return {
+        "max_depth": max(depths),
+        "mean_leaf_depth": leaf_depth_sum / max(n_leaves, 1),
+        "n_nodes": int(off[-1]),
+        "n_leaves": n_leaves,
+    }

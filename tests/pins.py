@@ -1,0 +1,455 @@
+"""Pins for the oracle: checks that hold independently of the oracle's own code.
+
+Each ``pin_*`` function takes an oracle library handle (the built oracle, or a
+mutant of it compiled by the mutation test) and raises AssertionError when the
+oracle disagrees with what the paper and the mathematics fix:
+
+* ``pin_golden``: hand-traced trees (tests/golden), including ties, -0.0, NaN
+  and infinities;
+* ``pin_brute_force``: enumeration of every root-to-leaf path and its
+  predicates; exactly one leaf's predicates all hold, and it is the walk's;
+* ``pin_gemm_closed_form``: Table 3's A/B/C/D/E tensors built here from their
+  definitions; for every outcome vector of the internal predicates the unique
+  column with (T.C)_k == D_k is the walk's leaf, and so is the leaf reached by
+  Algorithm 3's heap arithmetic on the perfect-padded tree (Sec. 4.1);
+* ``pin_closed_forms``: results with a closed form (depth-0 trees, +-inf
+  thresholds, copies of one tree, one-hot votes, sigmoid(0), softmax of equal
+  or shifted logits);
+* ``pin_sklearn``: scikit-learn's own tree walk (``apply``/``predict``/
+  ``predict_proba``) on fitted trees, a library routine the oracle reduces to.
+"""
+from __future__ import annotations
+
+import itertools
+import math
+import os
+
+import numpy as np
+
+import oracle
+from paper_2010_04804_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+# ---------------------------------------------------------------------------
+# helpers
+
+def model_from_trees(trees, n_features, n_outputs=1, leaf_dim=1, tree_class=None,
+                     aggregation="sum", transform="none", base_score=None):
+    """trees: list of lists of (feature, threshold, left, right, value or [values])."""
+    off = [0]
+    f, t, l, r, v = [], [], [], [], []
+    for tr in trees:
+        for (ff, tt, ll, rr, vv) in tr:
+            f.append(ff)
+            t.append(tt)
+            l.append(ll)
+            r.append(rr)
+            v.extend(np.atleast_1d(np.asarray(vv, np.float64)).tolist() if leaf_dim > 1 else [vv])
+        off.append(off[-1] + len(tr))
+    return {
+        "n_trees": len(trees), "n_features": n_features, "n_outputs": n_outputs,
+        "leaf_dim": leaf_dim,
+        "tree_node_offset": np.asarray(off, np.int64),
+        "feature": np.asarray(f, np.int32), "threshold": np.asarray(t, np.float32),
+        "left": np.asarray(l, np.int32), "right": np.asarray(r, np.int32),
+        "leaf_value": np.asarray(v, np.float32),
+        "tree_class": None if tree_class is None else np.asarray(tree_class, np.int32),
+        "aggregation": aggregation, "transform": transform,
+        "base_score": None if base_score is None else np.asarray(base_score, np.float32),
+    }
+
+
+def load_golden(name="hand_traced_two_trees.txt"):
+    trees, rows = {}, []
+    with open(os.path.join(GOLDEN, name)) as fh:
+        for line in fh:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            parts = line.split()
+            if parts[0] == "node":
+                name_, nid = parts[1], int(parts[2])
+                ff, tt, ll, rr, vv = int(parts[3]), float(parts[4]), int(parts[5]), int(parts[6]), float(parts[7])
+                trees.setdefault(name_, {})[nid] = (ff, tt, ll, rr, vv)
+            elif parts[0] == "row":
+                arrow = parts.index("->")
+                x = [float(s) for s in parts[1:arrow]]
+                rest = parts[arrow + 1:]
+                rows.append((x, [int(s) for s in rest[:-1]], float(rest[-1])))
+    names = sorted(trees)
+    tree_list = [[trees[n][i] for i in range(len(trees[n]))] for n in names]
+    return tree_list, rows
+
+
+def tree_view(model, t):
+    a, b = int(model["tree_node_offset"][t]), int(model["tree_node_offset"][t + 1])
+    return (model["feature"][a:b], model["threshold"][a:b], model["left"][a:b], model["right"][a:b])
+
+
+def root_to_leaf_paths(feat, left, right):
+    """{leaf: [(node, went_left), ...]} for every leaf, by explicit recursion."""
+    paths = {}
+
+    def rec(v, path):
+        if feat[v] < 0:
+            paths[int(v)] = path
+            return
+        rec(int(left[v]), path + [(int(v), True)])
+        rec(int(right[v]), path + [(int(v), False)])
+
+    rec(0, [])
+    return paths
+
+
+def brute_force_leaf(model, t, x):
+    """The unique leaf whose every path predicate holds (asserts uniqueness)."""
+    feat, thr, left, right = tree_view(model, t)
+    hits = []
+    for leaf, path in root_to_leaf_paths(feat, left, right).items():
+        ok = True
+        for node, went_left in path:
+            pred = bool(np.float32(x[feat[node]]) < np.float32(thr[node]))
+            if pred != went_left:
+                ok = False
+                break
+        if ok:
+            hits.append(leaf)
+    assert len(hits) == 1, f"tree {t}: {len(hits)} leaves fire"
+    return hits[0]
+
+
+def table3_tensors(feat, thr, left, right):
+    """Table 3's tensors for one tree, from their definitions.
+
+    Internal nodes I and leaves L are taken in ascending caller id order. A is
+    [F x |I|] (A[i, j] = 1 iff I_j tests feature i), B[j] is I_j's threshold,
+    C[j, k] = +1 if L_k is in I_j's left subtree, -1 if in its right subtree,
+    else 0, and D[k] counts the nodes on L_k's root path that are the left
+    child of their parent.
+    """
+    internal = [v for v in range(len(feat)) if feat[v] >= 0]
+    leaves = [v for v in range(len(feat)) if feat[v] < 0]
+    F = int(max(feat.max() + 1, 1))
+    A = np.zeros((F, len(internal)))
+    for j, v in enumerate(internal):
+        A[feat[v], j] = 1
+    B = np.asarray([thr[v] for v in internal], np.float32)
+
+    def subtree(v):
+        out, stack = set(), [v]
+        while stack:
+            u = stack.pop()
+            out.add(u)
+            if feat[u] >= 0:
+                stack += [int(left[u]), int(right[u])]
+        return out
+
+    C = np.zeros((len(internal), len(leaves)))
+    for j, v in enumerate(internal):
+        ls, rs = subtree(int(left[v])), subtree(int(right[v]))
+        for k, u in enumerate(leaves):
+            C[j, k] = 1 if u in ls else (-1 if u in rs else 0)
+    parent = {}
+    for v in internal:
+        parent[int(left[v])] = (v, True)
+        parent[int(right[v])] = (v, False)
+    D = np.zeros(len(leaves))
+    for k, u in enumerate(leaves):
+        w = u
+        while w in parent:
+            p, is_left = parent[w]
+            D[k] += 1 if is_left else 0
+            w = p
+    return internal, leaves, A, B, C, D
+
+
+def ptt_leaf(feat, thr, left, right, x):
+    """Algorithm 3 on the perfect-padded tree (Sec. 4.1), 1-based heap.
+
+    The tree is padded to the perfect tree of its own depth D: every position
+    of the heap keeps the original node it descends from; below an original
+    leaf the padded decision nodes compare anything (here: feature 0 against
+    0.0) and all their leaves map back to that original leaf.
+    """
+    depth = {0: 0}
+    order = [0]
+    for v in order:
+        if feat[v] >= 0:
+            for c in (int(left[v]), int(right[v])):
+                depth[c] = depth[v] + 1
+                order.append(c)
+    D = max(depth[v] for v in order if feat[v] < 0)
+    pos = {1: 0}  # heap position -> original node reached there
+    for i in range(1, 1 << D):
+        v = pos[i]
+        if feat[v] >= 0:
+            pos[2 * i], pos[2 * i + 1] = int(left[v]), int(right[v])
+        else:
+            pos[2 * i], pos[2 * i + 1] = v, v
+    i = 1
+    for _ in range(D):
+        v = pos[i]
+        f, t = (int(feat[v]), thr[v]) if feat[v] >= 0 else (0, np.float32(0))
+        i = 2 * i + (0 if np.float32(x[f]) < np.float32(t) else 1)
+    return pos[i]
+
+
+# ---------------------------------------------------------------------------
+# pins
+
+def pin_golden(lib):
+    trees, rows = load_golden()
+    m = model_from_trees(trees, 3)
+    X = np.asarray([r[0] for r in rows], np.float32)
+    raw, out, ids = oracle.predict(m, X, lib=lib, n_threads=2)
+    want_ids = np.asarray([r[1] for r in rows], np.int32)
+    want_sum = np.asarray([r[2] for r in rows])
+    assert np.array_equal(ids, want_ids), (ids, want_ids)
+    assert np.array_equal(raw[:, 0], want_sum), (raw[:, 0], want_sum)
+    assert np.array_equal(out[:, 0], want_sum)
+    # MEAN of the same ensemble divides by the tree count
+    m2 = dict(m, aggregation="mean")
+    raw2, _, _ = oracle.predict(m2, X, lib=lib)
+    assert np.allclose(raw2[:, 0], want_sum / 2, rtol=0, atol=1e-12)
+
+
+def random_small_ensemble(seed, n_trees=6, n_features=5):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    parts = []
+    for t in range(n_trees):
+        kind = t % 3
+        if kind == 0:
+            d = int(rng.integers(0, 4))
+            m = synth.perfect_forest(rng, 1, d, n_features, lambda r, f: r.normal(0, 1, f.size),
+                                     lambda r, n: r.normal(0, 1, n))
+        else:
+            nl = int(rng.integers(2, 12))
+            m = synth.leafwise_forest(rng, 1, nl, 6, 0.7, n_features,
+                                      lambda r, f: r.normal(0, 1, f.size),
+                                      lambda r, n: r.normal(0, 1, n))
+        parts.append(m)
+    off = [0]
+    for p in parts:
+        off.append(off[-1] + int(p["tree_node_offset"][-1]))
+    model = {
+        "n_trees": n_trees, "n_features": n_features, "n_outputs": 1, "leaf_dim": 1,
+        "tree_node_offset": np.asarray(off, np.int64),
+        "feature": np.concatenate([p["feature"] for p in parts]),
+        "threshold": np.concatenate([p["threshold"] for p in parts]),
+        "left": np.concatenate([p["left"] for p in parts]),
+        "right": np.concatenate([p["right"] for p in parts]),
+        "leaf_value": np.concatenate([p["leaf_value"] for p in parts]),
+        "tree_class": None, "aggregation": "sum", "transform": "none", "base_score": None,
+    }
+    return synth.permute_nodes(model, seed + 1000)
+
+
+def tricky_rows(rng, model, n):
+    """Rows mixing normal draws, exact threshold values (ties), NaN and +-inf."""
+    F = model["n_features"]
+    X = rng.normal(0, 1, (n, F)).astype(np.float32)
+    thr = model["threshold"][model["feature"] >= 0]
+    mask = rng.random((n, F))
+    X[mask < 0.3] = rng.choice(thr, size=int((mask < 0.3).sum()))
+    X[(mask >= 0.3) & (mask < 0.35)] = np.nan
+    X[(mask >= 0.35) & (mask < 0.38)] = np.inf
+    X[(mask >= 0.38) & (mask < 0.41)] = -np.inf
+    return X
+
+
+def pin_brute_force(lib, seeds=range(6), n_rows=60):
+    for seed in seeds:
+        m = random_small_ensemble(seed)
+        rng = np.random.Generator(np.random.PCG64(seed + 77))
+        X = tricky_rows(rng, m, n_rows)
+        raw, _, ids = oracle.predict(m, X, lib=lib, n_threads=3)
+        for r in range(n_rows):
+            acc = 0.0
+            for t in range(m["n_trees"]):
+                leaf = brute_force_leaf(m, t, X[r])
+                assert ids[r, t] == leaf, (seed, r, t, ids[r, t], leaf)
+                acc += float(m["leaf_value"][int(m["tree_node_offset"][t]) + leaf])
+            assert math.isclose(raw[r, 0], acc, rel_tol=1e-12, abs_tol=1e-12), (raw[r, 0], acc)
+
+
+def pin_gemm_closed_form(lib, seeds=range(8)):
+    """Every predicate-outcome vector of small trees (Table 3, Algorithms 1 and 3)."""
+    for seed in seeds:
+        rng = np.random.Generator(np.random.PCG64(seed))
+        if seed % 2 == 0:
+            d = 1 + seed // 2 % 3
+            base = synth.perfect_forest(rng, 1, d, 1, lambda r, f: np.zeros(f.size),
+                                        lambda r, n: r.normal(0, 1, n))
+        else:
+            base = synth.leafwise_forest(rng, 1, int(rng.integers(2, 8)), 5, 0.7, 1,
+                                         lambda r, f: np.zeros(f.size),
+                                         lambda r, n: r.normal(0, 1, n))
+        base.update(n_outputs=1, tree_class=None, aggregation="sum", transform="none",
+                    base_score=None)
+        m = synth.permute_nodes(base, seed + 5)
+        feat = m["feature"].copy()
+        internal = np.flatnonzero(feat >= 0)
+        # each internal node tests its own feature against 0.5: x = 0 -> true, x = 1 -> false
+        feat[internal] = np.arange(internal.size, dtype=np.int32)
+        thr = m["threshold"].copy()
+        thr[internal] = 0.5
+        m.update(feature=feat, threshold=thr, n_features=max(int(internal.size), 1))
+        ii, ll, A, B, C, D = table3_tensors(feat, thr, m["left"], m["right"])
+        n_int = len(ii)
+        combos = np.asarray(list(itertools.product([0.0, 1.0], repeat=max(n_int, 1))), np.float32)
+        X = combos[:, : m["n_features"]]
+        _, _, ids = oracle.predict(m, X, lib=lib)
+        T1 = (X @ A[: m["n_features"]] < B).astype(np.float64)  # Algorithm 1, first two steps
+        S = T1 @ C
+        for r in range(X.shape[0]):
+            cols = np.flatnonzero(S[r] == D)
+            assert len(cols) == 1, (seed, r, S[r], D)
+            assert ll[cols[0]] == ids[r, 0], (seed, r, ll[cols[0]], ids[r, 0])
+            assert ptt_leaf(feat, thr, m["left"], m["right"], X[r]) == ids[r, 0]
+
+
+def pin_closed_forms(lib):
+    rng = np.random.Generator(np.random.PCG64(11))
+    X = rng.normal(0, 1, (40, 4)).astype(np.float32)
+    # depth-0 trees: the score is the sum of their values
+    vals = [0.5, -1.25, 2.0]
+    m = model_from_trees([[(-1, 0, -1, -1, v)] for v in vals], 4)
+    raw, _, ids = oracle.predict(m, X, lib=lib)
+    assert np.all(ids == 0) and np.allclose(raw, sum(vals), rtol=0, atol=0)
+    # a perfect tree with every threshold +inf sends finite rows to its leftmost
+    # leaf, -inf to its rightmost
+    for thr_v, want in ((np.inf, 7), (-np.inf, 14)):
+        p = synth.perfect_forest(rng, 1, 3, 4, lambda r, f: np.full(f.size, thr_v),
+                                 lambda r, n: np.arange(n, dtype=np.float64))
+        p.update(n_outputs=1, tree_class=None, aggregation="sum", transform="none", base_score=None)
+        raw, _, ids = oracle.predict(p, X, lib=lib)
+        assert np.all(ids == want), (thr_v, ids[:5])
+        assert np.all(raw[:, 0] == want - 7)
+    # T copies of one tree: T x its score (SUM), its score (MEAN)
+    one = synth.make_model(1)
+    single = {k: v for k, v in one.items()}
+    a, b = int(one["tree_node_offset"][0]), int(one["tree_node_offset"][1])
+    for key in ("feature", "threshold", "left", "right", "leaf_value"):
+        single[key] = one[key][a:b]
+    single.update(n_trees=1, tree_node_offset=np.asarray([0, b - a], np.int64))
+    copies = dict(single, n_trees=5, tree_node_offset=np.arange(6, dtype=np.int64) * (b - a))
+    for key in ("feature", "threshold", "left", "right", "leaf_value"):
+        copies[key] = np.tile(single[key], 5)
+    Xc = synth.make_rows(1, 50)
+    r1, _, i1 = oracle.predict(single, Xc, lib=lib)
+    r5, _, i5 = oracle.predict(copies, Xc, lib=lib)
+    assert np.array_equal(i5, np.repeat(i1, 5, axis=1))
+    assert np.allclose(r5, 5 * r1, rtol=1e-15, atol=0)
+    r5m, _, _ = oracle.predict(dict(copies, aggregation="mean"), Xc, lib=lib)
+    assert np.allclose(r5m, r1, rtol=1e-15, atol=0)
+    # one-hot class votes averaged over trees are vote fractions
+    votes = rng.integers(0, 3, 7)
+    trees = [[(-1, 0, -1, -1, np.eye(3)[c])] for c in votes]
+    mv = model_from_trees(trees, 4, n_outputs=3, leaf_dim=3, aggregation="mean")
+    raw, out, _ = oracle.predict(mv, X, lib=lib)
+    frac = np.bincount(votes, minlength=3) / 7.0
+    assert np.allclose(raw, frac, rtol=0, atol=1e-15) and np.allclose(out, frac, atol=1e-15)
+    # sigmoid(0) = 1/2 and sigmoid(ln 3) = 3/4
+    for v, want in ((0.0, 0.5), (math.log(3.0), 0.75)):
+        ms = model_from_trees([[(-1, 0, -1, -1, np.float32(v))]], 4, transform="sigmoid")
+        raw, out, _ = oracle.predict(ms, X, lib=lib)
+        assert np.allclose(out, want, rtol=0, atol=1e-7), (v, out[0])
+    # softmax of equal logits is 1/K; adding one constant to every logit changes nothing
+    K = 4
+    m_eq = model_from_trees([[(-1, 0, -1, -1, 0.75)] for _ in range(K)], 4, n_outputs=K,
+                            tree_class=list(range(K)), transform="softmax")
+    _, out, _ = oracle.predict(m_eq, X, lib=lib)
+    assert np.allclose(out, 1.0 / K, rtol=0, atol=1e-15)
+    gb = synth.make_model(1)
+    trees_k = []
+    cls = []
+    for t in range(gb["n_trees"]):
+        a, b = int(gb["tree_node_offset"][t]), int(gb["tree_node_offset"][t + 1])
+        tr = list(zip(gb["feature"][a:b], gb["threshold"][a:b], gb["left"][a:b],
+                      gb["right"][a:b], gb["leaf_value"][a:b]))
+        trees_k.append(tr)
+        cls.append(t % K)
+    base = model_from_trees(trees_k, 8, n_outputs=K, tree_class=cls, transform="softmax")
+    shifted = model_from_trees(trees_k + [[(-1, 0, -1, -1, 0.5)] for _ in range(K)], 8,
+                               n_outputs=K, tree_class=cls + list(range(K)), transform="softmax")
+    Xk = synth.make_rows(1, 30)
+    rb, ob, _ = oracle.predict(base, Xk, lib=lib)
+    rs, os_, _ = oracle.predict(shifted, Xk, lib=lib)
+    assert np.allclose(rs - rb, 0.5, rtol=0, atol=1e-12)
+    assert np.allclose(ob, os_, rtol=0, atol=1e-12)
+    assert np.allclose(ob.sum(axis=1), 1.0, atol=1e-12)
+    # the softmax is the normalised exponential: ratios of outputs are exp(logit differences)
+    assert np.allclose(ob[:, 1] / ob[:, 0], np.exp(rb[:, 1] - rb[:, 0]), rtol=1e-12)
+    # base score is added after aggregation
+    mb = model_from_trees([[(-1, 0, -1, -1, 1.0)], [(-1, 0, -1, -1, 3.0)]], 4,
+                          aggregation="mean", base_score=[0.25])
+    raw, _, _ = oracle.predict(mb, X, lib=lib)
+    assert np.all(raw == 2.25)
+
+
+def sklearn_to_model(est_trees, n_features, n_outputs, leaf_dim, aggregation, leaf_fn):
+    """Caller-form model from fitted scikit-learn trees.
+
+    scikit-learn sends x <= t left with float32 x and float64 t. For float32 x
+    that is x < t' with t' the next float32 above the largest float32 <= t.
+    """
+    off = [0]
+    f, th, l, r, v = [], [], [], [], []
+    for tr in est_trees:
+        tt = tr.tree_
+        n = tt.node_count
+        feat = np.where(tt.children_left >= 0, tt.feature, -1).astype(np.int32)
+        t64 = tt.threshold
+        t32 = t64.astype(np.float32)
+        t32 = np.where(t32.astype(np.float64) > t64, np.nextafter(t32, np.float32(-np.inf)), t32)
+        tprime = np.nextafter(t32, np.float32(np.inf)).astype(np.float32)
+        f.append(feat)
+        th.append(np.where(feat >= 0, tprime, 0).astype(np.float32))
+        l.append(tt.children_left.astype(np.int32))
+        r.append(tt.children_right.astype(np.int32))
+        v.append(leaf_fn(tt).reshape(-1).astype(np.float32))
+        off.append(off[-1] + n)
+    return {
+        "n_trees": len(est_trees), "n_features": n_features, "n_outputs": n_outputs,
+        "leaf_dim": leaf_dim, "tree_node_offset": np.asarray(off, np.int64),
+        "feature": np.concatenate(f), "threshold": np.concatenate(th),
+        "left": np.concatenate(l), "right": np.concatenate(r),
+        "leaf_value": np.concatenate(v), "tree_class": None, "aggregation": aggregation,
+        "transform": "none", "base_score": None,
+    }
+
+
+def pin_sklearn(lib):
+    try:
+        from sklearn.ensemble import RandomForestClassifier, RandomForestRegressor
+    except ImportError:  # pragma: no cover - scikit-learn is optional
+        return False
+    rng = np.random.Generator(np.random.PCG64(5))
+    Xtr = rng.normal(0, 1, (400, 6)).astype(np.float32)
+    ytr = (Xtr[:, 0] + 0.5 * Xtr[:, 1] ** 2 - Xtr[:, 2] + rng.normal(0, 0.3, 400)).astype(np.float64)
+    Xte = rng.normal(0, 1, (300, 6)).astype(np.float32)
+    Xte[:50] = Xtr[:50]  # rows sitting exactly on training values, where thresholds lie between
+    reg = RandomForestRegressor(n_estimators=7, max_depth=6, random_state=0).fit(Xtr, ytr)
+    m = sklearn_to_model(reg.estimators_, 6, 1, 1, "mean", lambda tt: tt.value[:, 0, 0])
+    raw, _, ids = oracle.predict(m, Xte, lib=lib)
+    want_ids = np.stack([e.apply(Xte) for e in reg.estimators_], axis=1)
+    assert np.array_equal(ids, want_ids)
+    # leaf values were rounded to float32 once; compare to the same rounding
+    per_tree = np.stack([e.tree_.value[:, 0, 0].astype(np.float32)[e.apply(Xte)]
+                         for e in reg.estimators_], axis=1).astype(np.float64)
+    assert np.allclose(raw[:, 0], per_tree.mean(axis=1), rtol=1e-14, atol=1e-14)
+    assert np.allclose(raw[:, 0], reg.predict(Xte), rtol=1e-6, atol=1e-6)
+    ycl = (ytr > 0.3).astype(int) + (ytr > 1.2).astype(int)
+    clf = RandomForestClassifier(n_estimators=9, max_depth=7, random_state=1).fit(Xtr, ycl)
+
+    def probs(tt):
+        val = tt.value[:, 0, :]
+        return val / val.sum(axis=1, keepdims=True)
+
+    mc = sklearn_to_model(clf.estimators_, 6, 3, 3, "mean", probs)
+    raw, out, ids = oracle.predict(mc, Xte, lib=lib)
+    assert np.array_equal(ids, np.stack([e.apply(Xte) for e in clf.estimators_], axis=1))
+    assert np.allclose(out, clf.predict_proba(Xte), rtol=0, atol=2e-7)
+    return True
