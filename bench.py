@@ -1,0 +1,183 @@
+"""Throughput of batched tree-ensemble scoring on one MI355X.
+
+Default workload: the GBDT binary classifier of 500 perfect trees of depth 8
+over 28 features, scoring a batch of 1,000,000 rows (scores and per-tree leaf
+ids), strategy chosen by the selector. One step = one hb_predict over the
+whole batch with inputs already resident in HBM.
+
+Prints one JSON line (rank 0, N = 1) with rows/s, the roofline of the
+dominant kernel measured with HIP events on the launch stream, and the CPU
+oracle's rate on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "rows/sec scored, 500-tree depth-8 ensemble, 1M rows; % HBM / MFMA peak"
+HBM_PEAK = 8.0e12            # B/s, MI355X HBM3E
+INT8_PEAK = 5.0e15           # dense int8 MFMA ops/s
+KERNEL = {"ptt": "traverse_kernel<true,...>", "tt": "traverse_kernel<false,...>",
+          "gemm": "gemm_kernel"}
+
+
+def algorithmic_bytes(info, n, F, leaves, strategy):
+    """HBM bytes one launch must move: X read once, scores (and leaf ids)
+    written once, the strategy's compiled tables read once."""
+    K, T = info["n_outputs"], info["n_trees"]
+    b = n * F * 4 + n * K * 4 + info["table_bytes"][strategy]
+    if leaves:
+        b += n * T * 4
+    return b
+
+
+def gemm_ops(model, n):
+    """2 * n * sum_t |I_t| * |L_t| (the path-matrix contraction only)."""
+    off = model["tree_node_offset"]
+    tot = 0
+    for t in range(model["n_trees"]):
+        f = model["feature"][off[t]:off[t + 1]]
+        i = int((f >= 0).sum())
+        tot += i * (f.size - i)
+    return 2 * n * tot
+
+
+def cpu_baseline(model, cfg, seconds_target=15.0):
+    import oracle
+    from paper_2010_04804_amd import synth
+
+    cores = min(len(os.sched_getaffinity(0)), 16)
+    probe = synth.make_rows(cfg, 2000)
+    t0 = time.perf_counter()
+    oracle.predict(model, probe, leaves=True, n_threads=cores)
+    dt = max(time.perf_counter() - t0, 1e-6)
+    n = int(min(max(2000 * seconds_target / dt, 2000), 1_000_000))
+    X = synth.make_rows(cfg, n)
+    t0 = time.perf_counter()
+    oracle.predict(model, X, leaves=True, n_threads=cores)
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "rows/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {n} rows of the same workload, scores and leaf ids, "
+                      f"{dt:.1f} s on {cores} threads"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--rows", type=int, default=None)
+    ap.add_argument("--strategy", default="auto", choices=["auto", "ptt", "tt", "gemm"])
+    ap.add_argument("--no-leaves", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--extra", action="store_true",
+                    help="also time scores-only and the forced GEMM strategy")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
+                                   "(rows shard across GPUs with no exchange step; see the design notes)"}))
+        sys.exit(2)
+
+    import torch
+
+    import paper_2010_04804_amd as hb
+    from paper_2010_04804_amd import synth
+
+    cfg = args.config
+    n = args.rows or synth.CONFIGS[cfg]["n_rows"]
+    model = synth.make_model(cfg)
+    X = synth.make_rows(cfg, n)
+    dev = torch.device("cuda:0")
+    h = hb.compile(model, device=0)
+    info = h.info()
+    strategy = h.select(n) if args.strategy == "auto" else args.strategy
+    leaves = not args.no_leaves
+    Xd = torch.from_numpy(X).to(dev)
+    scores = torch.empty((n, info["n_outputs"]), dtype=torch.float32, device=dev)
+    ids = torch.empty((n, info["n_trees"]), dtype=torch.int32, device=dev) if leaves else None
+    stream = torch.cuda.current_stream(dev)
+
+    def step(strat=strategy, with_ids=ids):
+        hb.predict_ptr(h, Xd.data_ptr(), n, scores.data_ptr(),
+                       with_ids.data_ptr() if with_ids is not None else None, strat, stream.cuda_stream)
+
+    def timed(fn, steps, warmup):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for _ in range(steps):
+            fn()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / steps  # ms per launch
+
+    print(f"[bench] config {cfg}, {n} rows, strategy {strategy}, leaf ids {leaves}", flush=True)
+    t_wall0 = time.perf_counter()
+    ms = timed(step, args.steps, args.warmup)
+    wall = time.perf_counter() - t_wall0
+    rows_per_s = n / (ms * 1e-3)
+    F = info["n_features"]
+    if strategy == "gemm":
+        ops = gemm_ops(model, n)
+        achieved = ops / (ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": INT8_PEAK / 1e12, "unit": "TOP/s",
+                "frac": achieved * 1e12 / INT8_PEAK, "traffic": None,
+                "kernel": KERNEL["gemm"], "avg_launch_ms": ms, "ops_per_launch": ops}
+    else:
+        b = algorithmic_bytes(info, n, F, leaves, strategy)
+        achieved = b / (ms * 1e-3)
+        roof = {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK, "traffic": None, "kernel": KERNEL[strategy],
+                "avg_launch_ms": ms, "bytes_per_launch": b}
+    out = {
+        "metric": METRIC, "value": rows_per_s, "unit": "rows/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": synth.CONFIGS[cfg]["name"], "rows": n, "trees": info["n_trees"],
+                   "max_depth": info["max_depth"], "features": F, "strategy": strategy,
+                   "leaf_ids": leaves},
+        "roofline": roof,
+        "timed_wall_s": wall,
+    }
+    # parity spot check of the timed outputs against the oracle (not timed)
+    import oracle
+    rows = np.random.Generator(np.random.PCG64(0)).choice(n, min(n, 2000), replace=False)
+    o_raw, o_out, o_ids = oracle.predict(model, X[rows])
+    rt = torch.from_numpy(rows).to(dev)
+    sc = scores[rt].cpu().numpy().astype(np.float64)
+    ok = bool(np.all(np.abs(sc - o_out) <= 1e-5 * (1 + np.abs(o_out))))
+    if leaves:
+        ok = ok and bool(np.array_equal(ids[rt].cpu().numpy(), o_ids))
+    out["parity_sample_ok"] = ok
+    if args.extra:
+        ms_s = timed(lambda: step(strategy, None), args.steps, args.warmup)
+        out["scores_only"] = {"ms": ms_s, "rows_per_s": n / (ms_s * 1e-3)}
+        if strategy != "gemm" and info["feasible"]["gemm"]:
+            ng = min(n, 100_000)
+            ms_g = timed(lambda: hb.predict_ptr(h, Xd.data_ptr(), ng, scores.data_ptr(),
+                                                ids.data_ptr() if ids is not None else None, "gemm",
+                                                stream.cuda_stream), max(2, args.steps // 4), 1)
+            ops = gemm_ops(model, ng)
+            out["gemm"] = {"rows": ng, "ms": ms_g, "rows_per_s": ng / (ms_g * 1e-3),
+                           "tops": ops / (ms_g * 1e-3) / 1e12,
+                           "mfma_frac": ops / (ms_g * 1e-3) / INT8_PEAK}
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(model, cfg)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,176 @@
+/*
+ * hb.h -- batched tree-ensemble inference on AMD Instinct MI355X (gfx950).
+ *
+ * A trained ensemble of binary decision trees (gradient-boosted trees or a
+ * random forest) is compiled once into device-resident tensors and then
+ * scores batches of rows, every row against every tree. This follows the
+ * problem statement of Sec. 4.1 ("Compiling Tree-based Models") of
+ * Nakandala et al., "A Tensor Compiler for Unified Machine Learning
+ * Prediction Serving" (OSDI 2020): input records X in R^{n x |F|}, one
+ * prediction per record; trees over numerical features whose decision nodes
+ * all perform x[f] < threshold (true goes to the left child). Three
+ * compilation strategies are provided, each an exact reformulation of the
+ * plain root-to-leaf walk:
+ *
+ *   HB_STRATEGY_GEMM  Algorithm 1 with the tensors of Table 3: all decision
+ *                     nodes evaluated, the path encoded by a 0/+-1 matrix
+ *                     product (int8 matrix cores) and matched against D.
+ *   HB_STRATEGY_TT    Algorithm 2 (TreeTraversal) with the tensors of Table 5:
+ *                     level-synchronous descent through child arrays.
+ *   HB_STRATEGY_PTT   Algorithm 3 (PerfectTreeTraversal) with the tensors of
+ *                     Table 6: trees padded to perfect trees, children found
+ *                     by heap arithmetic.
+ *   HB_STRATEGY_AUTO  the selector of Sec. 5.1 re-derived for this device,
+ *                     keyed on depth, balance and batch size.
+ *
+ * All functions are thread-safe except that a handle must not be destroyed
+ * while another call uses it. No C++ exception crosses this interface. Every
+ * non-zero return leaves a message for hb_last_error() on the calling thread.
+ */
+#ifndef HB_H_
+#define HB_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- return codes ------------------------------------------------------- */
+#define HB_OK 0
+#define HB_ERR_INVALID_ARG (-1)   /* NULL pointer, bad size, bad enum value */
+#define HB_ERR_INVALID_MODEL (-2) /* not a tree: cycle, shared or unreachable
+                                     node, child/feature out of range, NaN
+                                     threshold, bad class id */
+#define HB_ERR_UNSUPPORTED (-3)   /* strategy infeasible for this ensemble
+                                     (depth or size limits below) */
+#define HB_ERR_OOM (-4)           /* host or device allocation failed */
+#define HB_ERR_HIP (-5)           /* a HIP runtime call or launch failed */
+
+/* ---- enums -------------------------------------------------------------- */
+enum hb_strategy {
+  HB_STRATEGY_AUTO = 0,
+  HB_STRATEGY_GEMM = 1,
+  HB_STRATEGY_TT = 2,
+  HB_STRATEGY_PTT = 3
+};
+/* Ensemble aggregation over trees, per output column: SUM, or MEAN (the
+ * paper's ReduceMean over the batched tree dimension, Sec. 4.1). */
+enum hb_aggregation { HB_AGG_SUM = 0, HB_AGG_MEAN = 1 };
+/* Post-transform of the aggregated margin (Table 2 lists Sigmoid and
+ * Softmax among the tensor operators used). Softmax subtracts the row max. */
+enum hb_transform { HB_POST_NONE = 0, HB_POST_SIGMOID = 1, HB_POST_SOFTMAX = 2 };
+
+/* ---- limits ------------------------------------------------------------- */
+#define HB_MAX_OUTPUTS 16          /* n_outputs (columns of the score)      */
+#define HB_PTT_MAX_DEPTH 12        /* PTT tables grow as 2^depth per tree   */
+#define HB_TT_MAX_NODES 65535      /* nodes per tree for TT (16-bit ids)    */
+#define HB_MAX_FEATURES 65535      /* features (16-bit ids in TT records)   */
+#define HB_GEMM_MAX_LEAVES 256     /* leaves per tree for GEMM              */
+
+/*
+ * The ensemble, in host memory, owned by the caller and only read (copied)
+ * by hb_compile. Tree t owns nodes [tree_node_offset[t], tree_node_offset[t+1])
+ * of every per-node array; node ids inside a tree are local (0 .. count-1)
+ * and local node 0 is the root. A node is a leaf iff feature < 0.
+ */
+typedef struct hb_ensemble_desc {
+  int32_t n_trees;                 /* >= 1                                   */
+  int32_t n_features;              /* >= 1, columns of X                     */
+  int32_t n_outputs;               /* K: 1 .. HB_MAX_OUTPUTS                 */
+  int32_t leaf_dim;                /* 1 (scalar leaves) or n_outputs         */
+  const int64_t *tree_node_offset; /* [n_trees + 1], strictly increasing, [0] == 0 */
+  const int32_t *feature;          /* [nodes] in [0, n_features), -1 at leaves */
+  const float *threshold;          /* [nodes]; read at internal nodes only   */
+  const int32_t *left;             /* [nodes] local child id, -1 at leaves   */
+  const int32_t *right;            /* [nodes] local child id, -1 at leaves   */
+  const float *leaf_value;         /* [nodes * leaf_dim]; read at leaves only */
+  const int32_t *tree_class;       /* [n_trees] output column of each tree when
+                                      leaf_dim == 1; NULL means column 0     */
+  int32_t aggregation;             /* enum hb_aggregation                    */
+  int32_t transform;               /* enum hb_transform                      */
+  const float *base_score;         /* [n_outputs] added after aggregation, or NULL */
+} hb_ensemble_desc;
+
+typedef struct hb_handle hb_handle;
+
+typedef struct hb_info {
+  int32_t n_trees, n_features, n_outputs, leaf_dim;
+  int32_t max_depth;               /* max internal nodes on a root-leaf path */
+  int32_t device;                  /* HIP device id, or -1 for a host-only handle */
+  int64_t n_nodes, n_internal, n_leaves;
+  double balance;                  /* sum_t (2^D - 1) / sum_t internal_t, D = max_depth */
+  int32_t default_strategy;        /* hint given to hb_compile               */
+  int32_t feasible[4];             /* indexed by enum hb_strategy (AUTO = 1) */
+  int64_t table_bytes[4];          /* bytes of compiled tensors per strategy */
+  int32_t gemm_shapes;             /* distinct tree shapes (C/D matrices)    */
+  int32_t ptt_depth;               /* D used by PTT (= max_depth)            */
+} hb_info;
+
+/*
+ * Compile an ensemble. Validates the trees, renumbers each breadth-first
+ * (children adjacent), builds the tensors of every feasible strategy
+ * (Tables 3, 5 and 6) and, for device >= 0, uploads them to that HIP device
+ * with synchronous copies. device == -1 builds a host-only handle whose
+ * tensors can be inspected with hb_table() but which hb_predict rejects.
+ * strategy_hint becomes the handle's default strategy (AUTO allowed); a
+ * forced hint that is infeasible returns HB_ERR_UNSUPPORTED.
+ * On success *out owns all device memory; release it with hb_destroy.
+ */
+int hb_compile(const hb_ensemble_desc *desc, int strategy_hint, int device, hb_handle **out);
+
+/*
+ * Score n_rows rows. X, scores and leaf_ids are device pointers on the
+ * handle's device:
+ *   X        float32 [n_rows, n_features], row-major, contiguous, read only;
+ *   scores   float32 [n_rows, n_outputs], row-major: the aggregated margin
+ *            after the transform;
+ *   leaf_ids int32 [n_rows, n_trees], row-major, or NULL to skip: the
+ *            caller's local node id of the leaf each row reaches in each tree
+ *            (the same for every strategy).
+ * strategy: HB_STRATEGY_AUTO uses the handle's default, or the selector when
+ * that is AUTO too. The work is enqueued on `stream` (a hipStream_t; NULL is
+ * the default stream) without any host synchronisation; launch errors are
+ * reported, execution errors surface on the stream. n_rows == 0 returns
+ * HB_OK and enqueues nothing. Concurrent calls on one handle are allowed:
+ * the compiled tensors are read only and no scratch memory is shared.
+ */
+int hb_predict(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
+               int strategy, void *stream);
+
+/* The strategy hb_predict would run for this batch size under AUTO. */
+int hb_select_strategy(const hb_handle *h, int64_t n_rows);
+
+/* Shape statistics, feasibility and table sizes of a compiled handle. */
+int hb_query(const hb_handle *h, hb_info *info);
+
+/*
+ * Host copy of one compiled tensor, for inspection and testing: *data points
+ * into memory owned by the handle (valid until hb_destroy), *bytes is its
+ * size. Names per strategy:
+ *   PTT : "node" (uint32 pairs {threshold bits, feature} per tree, max(2^D, 2)
+ *         heap slots, slot 0 unused), "leaf_value" (float [T][2^D][leaf_dim]),
+ *         "leaf_id" (int32 [T][2^D])
+ *   TT  : "node" (uint32 pairs {threshold bits, feature | right << 16} per
+ *         tree, n_pad slots, n_pad even; a leaf holds {-inf, own id << 16}),
+ *         "depth" (int32 [T]), "leaf_value"
+ *         (float [T][n_pad][leaf_dim]), "leaf_id" (int32 [T][n_pad]),
+ *         "dims" (int32 {n_pad})
+ *   GEMM: "node" (uint32 pairs {threshold bits, feature} [T][k_pad]),
+ *         "shape" (int32 [T]), "ct" (int8 [S][l_pad][k_pad], 4*C^T),
+ *         "bias" (int32 [S][l_pad]), "leaf_value" (float [T][l_pad][leaf_dim]),
+ *         "leaf_id" (int32 [T][l_pad]), "dims" (int32 {k_pad, l_pad, S})
+ * Returns HB_ERR_INVALID_ARG for an unknown name or an infeasible strategy.
+ */
+int hb_table(const hb_handle *h, int strategy, const char *name, const void **data, int64_t *bytes);
+
+/* Synchronise the handle's device and free everything it owns. NULL is a no-op. */
+void hb_destroy(hb_handle *h);
+
+/* Message for the last non-zero return on this thread ("" if none). */
+const char *hb_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HB_H_ */

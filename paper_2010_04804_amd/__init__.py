@@ -1,0 +1,215 @@
+"""Batched tree-ensemble inference on MI355X: Python binding of libhb.
+
+This module only marshals arguments into the C-ABI declared in
+``include/hb.h`` (``hb_compile``, ``hb_predict``, ``hb_query``, ``hb_table``,
+``hb_select_strategy``, ``hb_destroy``, ``hb_last_error``). Every step of
+scoring runs in the library's HIP kernels; PyTorch only supplies device
+memory and the current stream. If ``libhb.so`` has not been built, importing
+works but every call raises.
+
+Models are dicts in the caller form described in :mod:`.synth`.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+__all__ = ["compile", "predict", "predict_ptr", "Handle", "HBError", "STRATEGY", "load_library",
+           "LIB_PATH"]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhb.so")
+
+STRATEGY = {"auto": 0, "gemm": 1, "tt": 2, "ptt": 3}
+STRATEGY_NAME = {v: k for k, v in STRATEGY.items()}
+AGG = {"sum": 0, "mean": 1}
+POST = {"none": 0, "sigmoid": 1, "softmax": 2}
+ERR = {-1: "INVALID_ARG", -2: "INVALID_MODEL", -3: "UNSUPPORTED", -4: "OOM", -5: "HIP"}
+
+_P = ctypes.c_void_p
+
+
+class hb_ensemble_desc(ctypes.Structure):
+    _fields_ = [
+        ("n_trees", ctypes.c_int32), ("n_features", ctypes.c_int32),
+        ("n_outputs", ctypes.c_int32), ("leaf_dim", ctypes.c_int32),
+        ("tree_node_offset", _P), ("feature", _P), ("threshold", _P), ("left", _P),
+        ("right", _P), ("leaf_value", _P), ("tree_class", _P),
+        ("aggregation", ctypes.c_int32), ("transform", ctypes.c_int32), ("base_score", _P),
+    ]
+
+
+class hb_info(ctypes.Structure):
+    _fields_ = [
+        ("n_trees", ctypes.c_int32), ("n_features", ctypes.c_int32),
+        ("n_outputs", ctypes.c_int32), ("leaf_dim", ctypes.c_int32),
+        ("max_depth", ctypes.c_int32), ("device", ctypes.c_int32),
+        ("n_nodes", ctypes.c_int64), ("n_internal", ctypes.c_int64), ("n_leaves", ctypes.c_int64),
+        ("balance", ctypes.c_double), ("default_strategy", ctypes.c_int32),
+        ("feasible", ctypes.c_int32 * 4), ("table_bytes", ctypes.c_int64 * 4),
+        ("gemm_shapes", ctypes.c_int32), ("ptt_depth", ctypes.c_int32),
+    ]
+
+
+class HBError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"hb error {code} ({ERR.get(code, '?')}): {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libhb.so; raises if it is missing (there is no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built: run __graft_entry__.build() "
+                           "(or python -m paper_2010_04804_amd.build)")
+    lib = ctypes.CDLL(path)
+    lib.hb_compile.restype = ctypes.c_int
+    lib.hb_compile.argtypes = [ctypes.POINTER(hb_ensemble_desc), ctypes.c_int, ctypes.c_int,
+                               ctypes.POINTER(_P)]
+    lib.hb_predict.restype = ctypes.c_int
+    lib.hb_predict.argtypes = [_P, _P, ctypes.c_int64, _P, _P, ctypes.c_int, _P]
+    lib.hb_select_strategy.restype = ctypes.c_int
+    lib.hb_select_strategy.argtypes = [_P, ctypes.c_int64]
+    lib.hb_query.restype = ctypes.c_int
+    lib.hb_query.argtypes = [_P, ctypes.POINTER(hb_info)]
+    lib.hb_table.restype = ctypes.c_int
+    lib.hb_table.argtypes = [_P, ctypes.c_int, ctypes.c_char_p, ctypes.POINTER(_P),
+                             ctypes.POINTER(ctypes.c_int64)]
+    lib.hb_destroy.restype = None
+    lib.hb_destroy.argtypes = [_P]
+    lib.hb_last_error.restype = ctypes.c_char_p
+    lib.hb_last_error.argtypes = []
+    _lib = lib
+    return lib
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise HBError(rc, load_library().hb_last_error().decode())
+    return rc
+
+
+def _strategy(s) -> int:
+    return STRATEGY[s] if isinstance(s, str) else int(s)
+
+
+class Handle:
+    """A compiled ensemble (owns the library handle)."""
+
+    def __init__(self, ptr: int, device: int):
+        self._ptr = ptr
+        self.device = device
+
+    @property
+    def ptr(self):
+        if not self._ptr:
+            raise RuntimeError("handle already destroyed")
+        return self._ptr
+
+    def info(self) -> dict:
+        inf = hb_info()
+        _check(load_library().hb_query(self.ptr, ctypes.byref(inf)))
+        out = {name: getattr(inf, name) for name, _ in hb_info._fields_}
+        out["feasible"] = {STRATEGY_NAME[i]: bool(inf.feasible[i]) for i in range(4)}
+        out["table_bytes"] = {STRATEGY_NAME[i]: int(inf.table_bytes[i]) for i in range(4)}
+        return out
+
+    def select(self, n_rows: int) -> str:
+        rc = load_library().hb_select_strategy(self.ptr, int(n_rows))
+        if rc < 0:
+            _check(rc)
+        return STRATEGY_NAME[rc]
+
+    def table(self, strategy, name: str, dtype) -> np.ndarray:
+        """A copy of one compiled tensor (see hb_table in include/hb.h)."""
+        data, nbytes = _P(), ctypes.c_int64()
+        _check(load_library().hb_table(self.ptr, _strategy(strategy), name.encode(),
+                                       ctypes.byref(data), ctypes.byref(nbytes)))
+        buf = (ctypes.c_char * nbytes.value).from_address(data.value) if nbytes.value else b""
+        return np.frombuffer(bytes(buf), dtype=dtype).copy()
+
+    def close(self):
+        if self._ptr:
+            load_library().hb_destroy(self._ptr)
+            self._ptr = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _arr(a, dtype):
+    return None if a is None else np.ascontiguousarray(a, dtype=dtype)
+
+
+def compile(model: dict, strategy="auto", device: int = 0) -> Handle:
+    """Compile a caller-form model dict. ``device=-1`` builds a host-only handle."""
+    lib = load_library()
+    keep = {
+        "off": _arr(model["tree_node_offset"], np.int64),
+        "feature": _arr(model["feature"], np.int32),
+        "threshold": _arr(model["threshold"], np.float32),
+        "left": _arr(model["left"], np.int32),
+        "right": _arr(model["right"], np.int32),
+        "value": _arr(model["leaf_value"], np.float32),
+        "tree_class": _arr(model.get("tree_class"), np.int32),
+        "base": _arr(model.get("base_score"), np.float32),
+    }
+
+    def p(a):
+        return None if a is None else a.ctypes.data
+
+    d = hb_ensemble_desc(
+        int(model["n_trees"]), int(model["n_features"]), int(model["n_outputs"]),
+        int(model["leaf_dim"]), p(keep["off"]), p(keep["feature"]), p(keep["threshold"]),
+        p(keep["left"]), p(keep["right"]), p(keep["value"]), p(keep["tree_class"]),
+        AGG[model["aggregation"]], POST[model["transform"]], p(keep["base"]))
+    h = _P()
+    _check(lib.hb_compile(ctypes.byref(d), _strategy(strategy), int(device), ctypes.byref(h)))
+    return Handle(h.value, device)
+
+
+def predict_ptr(h: Handle, x_ptr: int, n_rows: int, scores_ptr: int, ids_ptr: int | None,
+                strategy="auto", stream: int | None = None):
+    """hb_predict on raw device pointers (no allocation, no synchronisation)."""
+    _check(load_library().hb_predict(h.ptr, x_ptr, int(n_rows), scores_ptr, ids_ptr or None,
+                                     _strategy(strategy), stream or None))
+
+
+def predict(h: Handle, X, strategy="auto", leaves: bool = True, out=None, stream=None):
+    """Score a float32 CUDA tensor ``X`` [n, F].
+
+    Returns ``(scores [n, K] float32, leaf_ids [n, T] int32 or None)`` as torch
+    tensors on X's device, enqueued on ``stream`` (default: torch's current
+    stream) without synchronising.
+    """
+    import torch
+
+    if not (isinstance(X, torch.Tensor) and X.is_cuda and X.dtype == torch.float32):
+        raise TypeError("X must be a float32 CUDA tensor")
+    if X.dim() != 2:
+        raise ValueError("X must be 2-D")
+    X = X.contiguous()
+    info = h.info()
+    n = X.shape[0]
+    if X.shape[1] != info["n_features"]:
+        raise ValueError(f"X has {X.shape[1]} columns, model expects {info['n_features']}")
+    if out is None:
+        scores = torch.empty((n, info["n_outputs"]), dtype=torch.float32, device=X.device)
+        ids = torch.empty((n, info["n_trees"]), dtype=torch.int32, device=X.device) if leaves else None
+    else:
+        scores, ids = out
+    if stream is None:
+        stream = torch.cuda.current_stream(X.device).cuda_stream
+    predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), ids.data_ptr() if ids is not None else None,
+                strategy, stream)
+    return scores, ids

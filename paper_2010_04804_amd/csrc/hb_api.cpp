@@ -1,0 +1,627 @@
+// hb_api.cpp -- the C-ABI of libhb: validation, canonical renumbering, the
+// per-strategy tensor builders (Tables 3, 5 and 6 of Sec. 4.1), the strategy
+// selector (Sec. 5.1) and device upload. The scoring itself runs only in the
+// HIP kernels of hb_kernels.hip; there is no host fallback.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <limits>
+#include <map>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "hb.h"
+#include "hb_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const std::string &msg) {
+  g_last_error = msg;
+  return code;
+}
+
+uint32_t fbits(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  return u;
+}
+
+// One tree renumbered breadth-first: canonical node 0 is the root and the two
+// children of an internal node get consecutive ids (left, then right).
+struct CanonTree {
+  std::vector<int32_t> caller;  // canonical -> caller-local id
+  std::vector<int32_t> feat;    // -1 at leaves
+  std::vector<float> thr;
+  std::vector<int32_t> left;    // canonical left child (right = left + 1), -1 at leaves
+  std::vector<int32_t> parent;  // -1 at the root
+  std::vector<int32_t> depth;
+  int32_t max_depth = 0;
+  int32_t n_internal = 0, n_leaves = 0;
+  int32_t size() const { return (int32_t)caller.size(); }
+};
+
+int canonicalise(const hb_ensemble_desc *d, int32_t t, CanonTree *ct) {
+  const int64_t base = d->tree_node_offset[t];
+  const int64_t n64 = d->tree_node_offset[t + 1] - base;
+  if (n64 < 1 || n64 > (int64_t)std::numeric_limits<int32_t>::max() / 2)
+    return fail(HB_ERR_INVALID_MODEL, "tree " + std::to_string(t) + ": bad node count");
+  const int32_t n = (int32_t)n64;
+  std::vector<int32_t> canon_of(n, -1);
+  ct->caller.clear();
+  ct->caller.reserve(n);
+  ct->caller.push_back(0);
+  canon_of[0] = 0;
+  for (size_t i = 0; i < ct->caller.size(); ++i) {
+    const int32_t v = ct->caller[i];
+    const int32_t f = d->feature[base + v];
+    if (f < 0) continue;
+    if (f >= d->n_features)
+      return fail(HB_ERR_INVALID_MODEL, "tree " + std::to_string(t) + " node " +
+                                            std::to_string(v) + ": feature out of range");
+    if (std::isnan(d->threshold[base + v]))
+      return fail(HB_ERR_INVALID_MODEL, "tree " + std::to_string(t) + " node " +
+                                            std::to_string(v) + ": NaN threshold");
+    const int32_t kids[2] = {d->left[base + v], d->right[base + v]};
+    for (int32_t c : kids) {
+      if (c < 0 || c >= n)
+        return fail(HB_ERR_INVALID_MODEL, "tree " + std::to_string(t) + " node " +
+                                              std::to_string(v) + ": child out of range");
+      if (canon_of[c] >= 0)
+        return fail(HB_ERR_INVALID_MODEL, "tree " + std::to_string(t) + " node " +
+                                              std::to_string(c) + ": reached twice (cycle or shared node)");
+      canon_of[c] = (int32_t)ct->caller.size();
+      ct->caller.push_back(c);
+    }
+  }
+  if ((int32_t)ct->caller.size() != n)
+    return fail(HB_ERR_INVALID_MODEL, "tree " + std::to_string(t) + ": " +
+                                          std::to_string(n - (int32_t)ct->caller.size()) +
+                                          " node(s) unreachable from the root");
+  ct->feat.assign(n, -1);
+  ct->thr.assign(n, 0.0f);
+  ct->left.assign(n, -1);
+  ct->parent.assign(n, -1);
+  ct->depth.assign(n, 0);
+  ct->max_depth = 0;
+  ct->n_internal = ct->n_leaves = 0;
+  for (int32_t c = 0; c < n; ++c) {
+    const int32_t v = ct->caller[c];
+    const int32_t f = d->feature[base + v];
+    if (f < 0) {
+      ++ct->n_leaves;
+      ct->max_depth = std::max(ct->max_depth, ct->depth[c]);
+      continue;
+    }
+    ++ct->n_internal;
+    ct->feat[c] = f;
+    ct->thr[c] = d->threshold[base + v];
+    const int32_t l = canon_of[d->left[base + v]];
+    const int32_t r = canon_of[d->right[base + v]];
+    if (r != l + 1) return fail(HB_ERR_INVALID_MODEL, "internal: breadth-first order broken");
+    ct->left[c] = l;
+    ct->parent[l] = ct->parent[r] = c;
+    ct->depth[l] = ct->depth[r] = ct->depth[c] + 1;
+  }
+  return HB_OK;
+}
+
+template <class T>
+struct DevBuf {
+  T *ptr = nullptr;
+  size_t count = 0;
+};
+
+}  // namespace
+
+struct hb_handle {
+  hb_info info{};
+  int32_t device = -1;
+  // host copies of the compiled tensors
+  std::vector<int32_t> tree_class;
+  std::vector<float> base_score;
+  bool has_base = false;
+  // PTT
+  std::vector<uint32_t> ptt_node;
+  std::vector<float> ptt_leaf_value;
+  std::vector<int32_t> ptt_leaf_id;
+  // TT
+  std::vector<uint32_t> tt_node;
+  std::vector<int32_t> tt_depth, tt_dims;
+  std::vector<float> tt_leaf_value;
+  std::vector<int32_t> tt_leaf_id;
+  int32_t tt_n_pad = 0;
+  // GEMM
+  std::vector<uint32_t> gemm_node;
+  std::vector<int32_t> gemm_shape, gemm_bias, gemm_dims;
+  std::vector<int8_t> gemm_ct;
+  std::vector<float> gemm_leaf_value;
+  std::vector<int32_t> gemm_leaf_id;
+  int32_t gemm_k_pad = 0, gemm_l_pad = 0, gemm_n_shapes = 0;
+  // device
+  std::vector<void *> allocations;
+  hb::EnsembleDev ens{};
+  hb::PttDev ptt{};
+  hb::TtDev tt{};
+  hb::GemmDev gemm{};
+};
+
+namespace {
+
+// Sec. 5.1 picks GEMM for shallow trees or small batches, PTT up to depth 10
+// and TT beyond. These constants are the MI355X re-derivation: PTT while the
+// padded perfect tree stays within a small multiple of the real node count.
+constexpr int32_t kAutoPttMaxDepth = 10;
+constexpr double kAutoPttMaxBalance = 4.0;
+constexpr int32_t kAutoGemmMaxDepth = 2;
+
+int select_strategy(const hb_handle *h, int64_t n_rows) {
+  (void)n_rows;
+  const hb_info &I = h->info;
+  if (I.feasible[HB_STRATEGY_GEMM] && I.max_depth <= kAutoGemmMaxDepth) return HB_STRATEGY_GEMM;
+  if (I.feasible[HB_STRATEGY_PTT] && I.max_depth <= kAutoPttMaxDepth &&
+      I.balance <= kAutoPttMaxBalance)
+    return HB_STRATEGY_PTT;
+  if (I.feasible[HB_STRATEGY_TT]) return HB_STRATEGY_TT;
+  if (I.feasible[HB_STRATEGY_PTT]) return HB_STRATEGY_PTT;
+  return HB_STRATEGY_GEMM;
+}
+
+void build_ptt(hb_handle *h, const hb_ensemble_desc *d, const std::vector<CanonTree> &trees) {
+  const int32_t D = h->info.max_depth;
+  const int64_t S = int64_t(1) << D;
+  const int64_t NS = std::max<int64_t>(S, 2);  // node slots per tree (slot 0 unused)
+  const int32_t ld = d->leaf_dim;
+  const int32_t T = d->n_trees;
+  h->ptt_node.assign((size_t)(T * NS * 2), 0u);
+  h->ptt_leaf_value.assign((size_t)(T * S * ld), 0.0f);
+  h->ptt_leaf_id.assign((size_t)(T * S), 0);
+  std::vector<int32_t> at(2 * S);  // heap position -> canonical node it descends from
+  for (int32_t t = 0; t < T; ++t) {
+    const CanonTree &ct = trees[t];
+    const int64_t base = d->tree_node_offset[t];
+    at[1] = 0;
+    for (int64_t p = 1; p < S; ++p) {
+      const int32_t c = at[p];
+      uint32_t *rec = &h->ptt_node[(size_t)((t * NS + p) * 2)];
+      if (ct.feat[c] >= 0) {
+        rec[0] = fbits(ct.thr[c]);
+        rec[1] = (uint32_t)ct.feat[c];
+        at[2 * p] = ct.left[c];
+        at[2 * p + 1] = ct.left[c] + 1;
+      } else {
+        // Sec. 4.1: a leaf above depth D becomes a perfect subtree whose
+        // decisions are free; every leaf under it maps to the original leaf.
+        rec[0] = fbits(0.0f);
+        rec[1] = 0u;
+        at[2 * p] = at[2 * p + 1] = c;
+      }
+    }
+    for (int64_t s = 0; s < S; ++s) {
+      const int32_t c = D == 0 ? 0 : at[S + s];
+      const int32_t v = ct.caller[c];
+      h->ptt_leaf_id[(size_t)(t * S + s)] = v;
+      for (int32_t k = 0; k < ld; ++k)
+        h->ptt_leaf_value[(size_t)((t * S + s) * ld + k)] = d->leaf_value[(base + v) * ld + k];
+    }
+  }
+}
+
+void build_tt(hb_handle *h, const hb_ensemble_desc *d, const std::vector<CanonTree> &trees) {
+  int32_t n_pad = 2;
+  for (const CanonTree &ct : trees) n_pad = std::max(n_pad, ct.size());
+  n_pad += n_pad & 1;  // even, so a tree's records are a whole number of 16-byte words
+  h->tt_n_pad = n_pad;
+  const int32_t ld = d->leaf_dim;
+  const int32_t T = d->n_trees;
+  const uint32_t ninf = fbits(-std::numeric_limits<float>::infinity());
+  h->tt_node.assign((size_t)T * n_pad * 2, 0u);
+  h->tt_depth.assign(T, 0);
+  h->tt_leaf_value.assign((size_t)T * n_pad * ld, 0.0f);
+  h->tt_leaf_id.assign((size_t)T * n_pad, 0);
+  for (int32_t t = 0; t < T; ++t) {
+    const CanonTree &ct = trees[t];
+    const int64_t base = d->tree_node_offset[t];
+    h->tt_depth[t] = ct.max_depth;
+    for (int32_t c = 0; c < n_pad; ++c) {
+      uint32_t *rec = &h->tt_node[((size_t)t * n_pad + c) * 2];
+      if (c < ct.size() && ct.feat[c] >= 0) {
+        rec[0] = fbits(ct.thr[c]);
+        rec[1] = (uint32_t)ct.feat[c] | ((uint32_t)(ct.left[c] + 1) << 16);
+      } else {
+        // Table 5 makes leaves point to themselves; here a leaf's threshold
+        // is -inf so the rule always takes the stored "right" id, itself.
+        rec[0] = ninf;
+        rec[1] = (uint32_t)c << 16;
+      }
+      if (c < ct.size()) {
+        const int32_t v = ct.caller[c];
+        h->tt_leaf_id[(size_t)t * n_pad + c] = v;
+        if (ct.feat[c] < 0)
+          for (int32_t k = 0; k < ld; ++k)
+            h->tt_leaf_value[((size_t)t * n_pad + c) * ld + k] = d->leaf_value[(base + v) * ld + k];
+      }
+    }
+  }
+  h->tt_dims = {n_pad};
+}
+
+void build_gemm(hb_handle *h, const hb_ensemble_desc *d, const std::vector<CanonTree> &trees) {
+  const int32_t T = d->n_trees;
+  const int32_t ld = d->leaf_dim;
+  int32_t max_i = 1, max_l = 1;
+  for (const CanonTree &ct : trees) {
+    max_i = std::max(max_i, ct.n_internal);
+    max_l = std::max(max_l, ct.n_leaves);
+  }
+  const int32_t k_pad = (max_i + 63) / 64 * 64;
+  const int32_t l_pad = (max_l + 15) / 16 * 16;
+  h->gemm_k_pad = k_pad;
+  h->gemm_l_pad = l_pad;
+  const uint32_t ninf = fbits(-std::numeric_limits<float>::infinity());
+  h->gemm_node.assign((size_t)T * k_pad * 2, 0u);
+  for (size_t i = 0; i < h->gemm_node.size(); i += 2) h->gemm_node[i] = ninf;
+  h->gemm_shape.assign(T, 0);
+  h->gemm_leaf_value.assign((size_t)T * l_pad * ld, 0.0f);
+  h->gemm_leaf_id.assign((size_t)T * l_pad, 0);
+  h->gemm_ct.clear();
+  h->gemm_bias.clear();
+  std::map<std::vector<uint8_t>, int32_t> shapes;
+  std::vector<int32_t> kidx, leaves;
+  for (int32_t t = 0; t < T; ++t) {
+    const CanonTree &ct = trees[t];
+    const int64_t base = d->tree_node_offset[t];
+    const int32_t n = ct.size();
+    // k: internal nodes in breadth-first order
+    kidx.assign(n, -1);
+    int32_t k = 0;
+    for (int32_t c = 0; c < n; ++c)
+      if (ct.feat[c] >= 0) {
+        kidx[c] = k;
+        uint32_t *rec = &h->gemm_node[((size_t)t * k_pad + k) * 2];
+        rec[0] = fbits(ct.thr[c]);
+        rec[1] = (uint32_t)ct.feat[c];
+        ++k;
+      }
+    // l: leaves left to right (depth-first, left child first)
+    leaves.clear();
+    std::vector<int32_t> stack{0};
+    while (!stack.empty()) {
+      const int32_t c = stack.back();
+      stack.pop_back();
+      if (ct.feat[c] < 0) {
+        leaves.push_back(c);
+      } else {
+        stack.push_back(ct.left[c] + 1);
+        stack.push_back(ct.left[c]);
+      }
+    }
+    for (int32_t l = 0; l < (int32_t)leaves.size(); ++l) {
+      const int32_t v = ct.caller[leaves[l]];
+      h->gemm_leaf_id[(size_t)t * l_pad + l] = v;
+      for (int32_t q = 0; q < ld; ++q)
+        h->gemm_leaf_value[((size_t)t * l_pad + l) * ld + q] = d->leaf_value[(base + v) * ld + q];
+    }
+    // the shape: breadth-first leaf flags determine the tree's structure
+    std::vector<uint8_t> key(n);
+    for (int32_t c = 0; c < n; ++c) key[c] = ct.feat[c] < 0;
+    auto it = shapes.find(key);
+    if (it != shapes.end()) {
+      h->gemm_shape[t] = it->second;
+      continue;
+    }
+    const int32_t s = (int32_t)shapes.size();
+    shapes.emplace(std::move(key), s);
+    h->gemm_shape[t] = s;
+    h->gemm_ct.resize((size_t)(s + 1) * l_pad * k_pad, 0);
+    h->gemm_bias.resize((size_t)(s + 1) * l_pad, -(1 << 30));
+    int8_t *C = &h->gemm_ct[(size_t)s * l_pad * k_pad];
+    for (int32_t l = 0; l < (int32_t)leaves.size(); ++l) {
+      // Table 3: C is +1 where the leaf lies in a node's left subtree and -1
+      // in its right subtree; D counts the left edges on the leaf's root path.
+      int32_t dl = 0;
+      for (int32_t c = leaves[l]; ct.parent[c] >= 0; c = ct.parent[c]) {
+        const int32_t p = ct.parent[c];
+        const bool is_left = ct.left[p] == c;
+        C[(size_t)l * k_pad + kidx[p]] = is_left ? 4 : -4;
+        dl += is_left;
+      }
+      h->gemm_bias[(size_t)s * l_pad + l] = l - 256 * dl;
+    }
+  }
+  h->gemm_n_shapes = (int32_t)shapes.size();
+  h->gemm_dims = {k_pad, l_pad, h->gemm_n_shapes};
+}
+
+template <class T>
+int upload(hb_handle *h, const std::vector<T> &src, const T **dst) {
+  if (src.empty()) {
+    *dst = nullptr;
+    return HB_OK;
+  }
+  void *p = nullptr;
+  const size_t bytes = src.size() * sizeof(T);
+  hipError_t e = hipMalloc(&p, bytes);
+  if (e != hipSuccess) return fail(HB_ERR_OOM, std::string("hipMalloc: ") + hipGetErrorString(e));
+  h->allocations.push_back(p);
+  e = hipMemcpy(p, src.data(), bytes, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return fail(HB_ERR_HIP, std::string("hipMemcpy: ") + hipGetErrorString(e));
+  *dst = static_cast<const T *>(p);
+  return HB_OK;
+}
+
+void release(hb_handle *h) {
+  if (!h) return;
+  if (h->device >= 0 && !h->allocations.empty()) {
+    int prev = -1;
+    (void)hipGetDevice(&prev);
+    (void)hipSetDevice(h->device);
+    (void)hipDeviceSynchronize();
+    for (void *p : h->allocations) (void)hipFree(p);
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+  delete h;
+}
+
+int validate_desc(const hb_ensemble_desc *d) {
+  if (!d) return fail(HB_ERR_INVALID_ARG, "desc is NULL");
+  if (d->n_trees < 1) return fail(HB_ERR_INVALID_ARG, "n_trees must be >= 1");
+  if (d->n_features < 1) return fail(HB_ERR_INVALID_ARG, "n_features must be >= 1");
+  if (d->n_outputs < 1 || d->n_outputs > HB_MAX_OUTPUTS)
+    return fail(HB_ERR_INVALID_ARG, "n_outputs must be in [1, " + std::to_string(HB_MAX_OUTPUTS) + "]");
+  if (d->leaf_dim != 1 && d->leaf_dim != d->n_outputs)
+    return fail(HB_ERR_INVALID_ARG, "leaf_dim must be 1 or n_outputs");
+  if (!d->tree_node_offset || !d->feature || !d->threshold || !d->left || !d->right || !d->leaf_value)
+    return fail(HB_ERR_INVALID_ARG, "a per-node array is NULL");
+  if (d->aggregation != HB_AGG_SUM && d->aggregation != HB_AGG_MEAN)
+    return fail(HB_ERR_INVALID_ARG, "bad aggregation");
+  if (d->transform < HB_POST_NONE || d->transform > HB_POST_SOFTMAX)
+    return fail(HB_ERR_INVALID_ARG, "bad transform");
+  if (d->tree_node_offset[0] != 0) return fail(HB_ERR_INVALID_ARG, "tree_node_offset[0] must be 0");
+  for (int32_t t = 0; t < d->n_trees; ++t)
+    if (d->tree_node_offset[t + 1] <= d->tree_node_offset[t])
+      return fail(HB_ERR_INVALID_ARG, "tree_node_offset must be strictly increasing");
+  if (d->leaf_dim == 1 && d->tree_class)
+    for (int32_t t = 0; t < d->n_trees; ++t)
+      if (d->tree_class[t] < 0 || d->tree_class[t] >= d->n_outputs)
+        return fail(HB_ERR_INVALID_MODEL, "tree_class out of range at tree " + std::to_string(t));
+  return HB_OK;
+}
+
+int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **out) {
+  int rc = validate_desc(d);
+  if (rc) return rc;
+  if (hint < HB_STRATEGY_AUTO || hint > HB_STRATEGY_PTT) return fail(HB_ERR_INVALID_ARG, "bad strategy hint");
+  if (device < -1) return fail(HB_ERR_INVALID_ARG, "bad device");
+  const int32_t T = d->n_trees;
+  std::vector<CanonTree> trees(T);
+  int64_t n_nodes = 0, n_int = 0, n_leaf = 0;
+  int32_t D = 0, max_nodes = 0, max_leaves = 0;
+  for (int32_t t = 0; t < T; ++t) {
+    rc = canonicalise(d, t, &trees[t]);
+    if (rc) return rc;
+    n_nodes += trees[t].size();
+    n_int += trees[t].n_internal;
+    n_leaf += trees[t].n_leaves;
+    D = std::max(D, trees[t].max_depth);
+    max_nodes = std::max(max_nodes, trees[t].size());
+    max_leaves = std::max(max_leaves, trees[t].n_leaves);
+  }
+  hb_handle *h = new (std::nothrow) hb_handle();
+  if (!h) return fail(HB_ERR_OOM, "out of host memory");
+  hb_info &I = h->info;
+  I.n_trees = T;
+  I.n_features = d->n_features;
+  I.n_outputs = d->n_outputs;
+  I.leaf_dim = d->leaf_dim;
+  I.max_depth = D;
+  I.device = device;
+  I.n_nodes = n_nodes;
+  I.n_internal = n_int;
+  I.n_leaves = n_leaf;
+  I.balance = n_int > 0 ? (double)T * (double)((int64_t(1) << D) - 1) / (double)n_int : 1.0;
+  I.default_strategy = hint;
+  I.ptt_depth = D;
+  // The traversal kernels stage at least one tree's tables in LDS.
+  const int64_t per_slot = 12 + 4 * (int64_t)d->leaf_dim;
+  const int64_t ptt_tree_bytes = per_slot * std::max<int64_t>(int64_t(1) << std::min(D, 30), 2);
+  const int64_t tt_tree_bytes = per_slot * (max_nodes + 1);
+  I.feasible[HB_STRATEGY_PTT] = D <= HB_PTT_MAX_DEPTH && ptt_tree_bytes <= hb::kTreeLdsLimit;
+  I.feasible[HB_STRATEGY_TT] = max_nodes <= HB_TT_MAX_NODES && d->n_features <= HB_MAX_FEATURES &&
+                               tt_tree_bytes <= hb::kTreeLdsLimit;
+  I.feasible[HB_STRATEGY_GEMM] = max_leaves <= HB_GEMM_MAX_LEAVES;
+  I.feasible[HB_STRATEGY_AUTO] =
+      I.feasible[HB_STRATEGY_PTT] || I.feasible[HB_STRATEGY_TT] || I.feasible[HB_STRATEGY_GEMM];
+  if (!I.feasible[hint]) {
+    delete h;
+    return fail(HB_ERR_UNSUPPORTED, "requested strategy is infeasible for this ensemble");
+  }
+  h->device = device;
+  try {
+    if (I.feasible[HB_STRATEGY_PTT]) build_ptt(h, d, trees);
+    if (I.feasible[HB_STRATEGY_TT]) build_tt(h, d, trees);
+    if (I.feasible[HB_STRATEGY_GEMM]) build_gemm(h, d, trees);
+  } catch (const std::bad_alloc &) {
+    delete h;
+    return fail(HB_ERR_OOM, "out of host memory building tables");
+  }
+  I.gemm_shapes = h->gemm_n_shapes;
+  I.table_bytes[HB_STRATEGY_PTT] = (int64_t)(h->ptt_node.size() * 4 + h->ptt_leaf_value.size() * 4 +
+                                             h->ptt_leaf_id.size() * 4);
+  I.table_bytes[HB_STRATEGY_TT] = (int64_t)(h->tt_node.size() * 4 + h->tt_depth.size() * 4 +
+                                            h->tt_leaf_value.size() * 4 + h->tt_leaf_id.size() * 4);
+  I.table_bytes[HB_STRATEGY_GEMM] =
+      (int64_t)(h->gemm_node.size() * 4 + h->gemm_shape.size() * 4 + h->gemm_ct.size() +
+                h->gemm_bias.size() * 4 + h->gemm_leaf_value.size() * 4 + h->gemm_leaf_id.size() * 4);
+  h->tree_class.assign(T, 0);
+  if (d->leaf_dim == 1 && d->tree_class)
+    for (int32_t t = 0; t < T; ++t) h->tree_class[t] = d->tree_class[t];
+  if (d->base_score) {
+    h->has_base = true;
+    h->base_score.assign(d->base_score, d->base_score + d->n_outputs);
+  }
+  hb::EnsembleDev &E = h->ens;
+  E.n_trees = T;
+  E.n_features = d->n_features;
+  E.n_outputs = d->n_outputs;
+  E.leaf_dim = d->leaf_dim;
+  E.aggregation = d->aggregation;
+  E.transform = d->transform;
+  if (device >= 0) {
+    int count = 0;
+    if (hipGetDeviceCount(&count) != hipSuccess || device >= count) {
+      delete h;
+      return fail(HB_ERR_HIP, "no such HIP device");
+    }
+    int prev = -1;
+    (void)hipGetDevice(&prev);
+    if (hipSetDevice(device) != hipSuccess) {
+      delete h;
+      return fail(HB_ERR_HIP, "hipSetDevice failed");
+    }
+    const uint32_t *pn = nullptr;
+    rc = upload(h, h->tree_class, &E.tree_class);
+    if (!rc && h->has_base) rc = upload(h, h->base_score, &E.base_score);
+    if (!rc && I.feasible[HB_STRATEGY_PTT]) {
+      rc = upload(h, h->ptt_node, &pn);
+      h->ptt.node = reinterpret_cast<const uint2 *>(pn);
+      if (!rc) rc = upload(h, h->ptt_leaf_value, &h->ptt.leaf_value);
+      if (!rc) rc = upload(h, h->ptt_leaf_id, &h->ptt.leaf_id);
+      h->ptt.depth = D;
+    }
+    if (!rc && I.feasible[HB_STRATEGY_TT]) {
+      rc = upload(h, h->tt_node, &pn);
+      h->tt.node = reinterpret_cast<const uint2 *>(pn);
+      if (!rc) rc = upload(h, h->tt_depth, &h->tt.depth);
+      if (!rc) rc = upload(h, h->tt_leaf_value, &h->tt.leaf_value);
+      if (!rc) rc = upload(h, h->tt_leaf_id, &h->tt.leaf_id);
+      h->tt.n_pad = h->tt_n_pad;
+      h->tt.max_depth = D;
+    }
+    if (!rc && I.feasible[HB_STRATEGY_GEMM]) {
+      rc = upload(h, h->gemm_node, &pn);
+      h->gemm.node = reinterpret_cast<const uint2 *>(pn);
+      if (!rc) rc = upload(h, h->gemm_shape, &h->gemm.shape);
+      if (!rc) rc = upload(h, h->gemm_ct, &h->gemm.ct);
+      if (!rc) rc = upload(h, h->gemm_bias, &h->gemm.bias);
+      if (!rc) rc = upload(h, h->gemm_leaf_value, &h->gemm.leaf_value);
+      if (!rc) rc = upload(h, h->gemm_leaf_id, &h->gemm.leaf_id);
+      h->gemm.k_pad = h->gemm_k_pad;
+      h->gemm.l_pad = h->gemm_l_pad;
+      h->gemm.n_shapes = h->gemm_n_shapes;
+    }
+    if (prev >= 0) (void)hipSetDevice(prev);
+    if (rc) {
+      std::string msg = g_last_error;
+      release(h);
+      return fail(rc, msg);
+    }
+  }
+  *out = h;
+  return HB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int hb_compile(const hb_ensemble_desc *desc, int strategy_hint, int device, hb_handle **out) {
+  g_last_error.clear();
+  if (!out) return fail(HB_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  try {
+    return compile_impl(desc, strategy_hint, device, out);
+  } catch (const std::bad_alloc &) {
+    return fail(HB_ERR_OOM, "out of host memory");
+  } catch (...) {
+    return fail(HB_ERR_INVALID_ARG, "unexpected exception in hb_compile");
+  }
+}
+
+int hb_select_strategy(const hb_handle *h, int64_t n_rows) {
+  if (!h) return fail(HB_ERR_INVALID_ARG, "handle is NULL");
+  if (h->info.default_strategy != HB_STRATEGY_AUTO) return h->info.default_strategy;
+  return select_strategy(h, n_rows);
+}
+
+int hb_predict(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
+               int strategy, void *stream) {
+  if (!h) return fail(HB_ERR_INVALID_ARG, "handle is NULL");
+  if (h->device < 0) return fail(HB_ERR_INVALID_ARG, "host-only handle: compile with a device to predict");
+  if (n_rows < 0) return fail(HB_ERR_INVALID_ARG, "n_rows < 0");
+  if (strategy < HB_STRATEGY_AUTO || strategy > HB_STRATEGY_PTT) return fail(HB_ERR_INVALID_ARG, "bad strategy");
+  if (strategy == HB_STRATEGY_AUTO) strategy = hb_select_strategy(h, n_rows);
+  if (!h->info.feasible[strategy]) return fail(HB_ERR_UNSUPPORTED, "strategy infeasible for this ensemble");
+  if (n_rows == 0) return HB_OK;
+  if (!X || !scores) return fail(HB_ERR_INVALID_ARG, "X or scores is NULL");
+  if (n_rows > (int64_t)std::numeric_limits<int32_t>::max())
+    return fail(HB_ERR_INVALID_ARG, "n_rows above 2^31 - 1");
+  int prev = -1;
+  (void)hipGetDevice(&prev);
+  if (prev != h->device && hipSetDevice(h->device) != hipSuccess) return fail(HB_ERR_HIP, "hipSetDevice failed");
+  std::string err;
+  int rc = HB_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  try {
+    if (strategy == HB_STRATEGY_PTT)
+      rc = hb::launch_ptt(h->ens, h->ptt, X, n_rows, scores, leaf_ids, s, &err);
+    else if (strategy == HB_STRATEGY_TT)
+      rc = hb::launch_tt(h->ens, h->tt, X, n_rows, scores, leaf_ids, s, &err);
+    else
+      rc = hb::launch_gemm(h->ens, h->gemm, X, n_rows, scores, leaf_ids, s, &err);
+  } catch (...) {
+    rc = HB_ERR_HIP;
+    err = "unexpected exception in hb_predict";
+  }
+  if (prev >= 0 && prev != h->device) (void)hipSetDevice(prev);
+  if (rc) return fail(rc, err);
+  return HB_OK;
+}
+
+int hb_query(const hb_handle *h, hb_info *info) {
+  if (!h || !info) return fail(HB_ERR_INVALID_ARG, "NULL argument");
+  *info = h->info;
+  return HB_OK;
+}
+
+int hb_table(const hb_handle *h, int strategy, const char *name, const void **data, int64_t *bytes) {
+  if (!h || !name || !data || !bytes) return fail(HB_ERR_INVALID_ARG, "NULL argument");
+  if (strategy < HB_STRATEGY_GEMM || strategy > HB_STRATEGY_PTT || !h->info.feasible[strategy])
+    return fail(HB_ERR_INVALID_ARG, "strategy has no tables");
+  const std::string n(name);
+  auto give = [&](const auto &v) {
+    *data = v.data();
+    *bytes = (int64_t)(v.size() * sizeof(v[0]));
+    return HB_OK;
+  };
+  if (strategy == HB_STRATEGY_PTT) {
+    if (n == "node") return give(h->ptt_node);
+    if (n == "leaf_value") return give(h->ptt_leaf_value);
+    if (n == "leaf_id") return give(h->ptt_leaf_id);
+  } else if (strategy == HB_STRATEGY_TT) {
+    if (n == "node") return give(h->tt_node);
+    if (n == "depth") return give(h->tt_depth);
+    if (n == "leaf_value") return give(h->tt_leaf_value);
+    if (n == "leaf_id") return give(h->tt_leaf_id);
+    if (n == "dims") return give(h->tt_dims);
+  } else {
+    if (n == "node") return give(h->gemm_node);
+    if (n == "shape") return give(h->gemm_shape);
+    if (n == "ct") return give(h->gemm_ct);
+    if (n == "bias") return give(h->gemm_bias);
+    if (n == "leaf_value") return give(h->gemm_leaf_value);
+    if (n == "leaf_id") return give(h->gemm_leaf_id);
+    if (n == "dims") return give(h->gemm_dims);
+  }
+  return fail(HB_ERR_INVALID_ARG, "unknown table name");
+}
+
+void hb_destroy(hb_handle *h) { release(h); }
+
+const char *hb_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,74 @@
+// hb_internal.h -- shared between the host compiler (hb_api.cpp) and the
+// device kernels (hb_kernels.hip): device views of the compiled tensors and
+// the launcher entry points. Not part of the public C-ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+
+#include "hb.h"
+
+namespace hb {
+
+// Largest per-tree table the traversal kernels can stage: the 160 KiB of LDS
+// of a gfx950 CU less the leaf-id staging buffer.
+constexpr int64_t kTreeLdsLimit = 160 * 1024 - 4 * 1024;
+
+// Ensemble-wide parameters every kernel needs.
+struct EnsembleDev {
+  int32_t n_trees, n_features, n_outputs, leaf_dim;
+  int32_t aggregation, transform;
+  const int32_t *tree_class;  // [T] device; output column of a scalar-leaf tree
+  const float *base_score;    // [K] device, or nullptr
+};
+
+// PerfectTreeTraversal tensors (Table 6, Algorithm 3), 1-based heap per tree:
+// slot p in [1, 2^D) is a decision node, the children of p are 2p and 2p+1,
+// and after D steps the index lies in [2^D, 2^(D+1)); leaf slot = index - 2^D.
+struct PttDev {
+  const uint2 *node;        // [T][2^D] {threshold bits, feature}; slot 0 unused
+  const float *leaf_value;  // [T][2^D][leaf_dim]
+  const int32_t *leaf_id;   // [T][2^D] caller-local node id
+  int32_t depth;            // D
+};
+
+// TreeTraversal tensors (Table 5, Algorithm 2), breadth-first per tree with
+// siblings adjacent (left = right - 1). Leaves loop to themselves: threshold
+// -inf (no x is below it, NaN included) and right = the leaf's own id.
+struct TtDev {
+  const uint2 *node;        // [T][n_pad] {threshold bits, feature | right << 16}
+  const int32_t *depth;     // [T] levels to descend per tree
+  const float *leaf_value;  // [T][n_pad][leaf_dim], indexed by node id
+  const int32_t *leaf_id;   // [T][n_pad] caller-local node id
+  int32_t n_pad;
+  int32_t max_depth;
+};
+
+// GEMM tensors (Table 3, Algorithm 1). Internal nodes in breadth-first order
+// give the reduction index k; leaves in left-to-right order give column l.
+// ct holds 4*C^T so that, with predicates encoded as 0/64, one product term
+// is +-256 and the accumulator started at bias[l] = l - 256*D[l] ends at
+// 256*((T.C)_l - D_l) + l: non-negative exactly at the selected leaf.
+struct GemmDev {
+  const uint2 *node;        // [T][k_pad] {threshold bits, feature}; padding: -inf
+  const int32_t *shape;     // [T] index into ct / bias
+  const int8_t *ct;         // [S][l_pad][k_pad]
+  const int32_t *bias;      // [S][l_pad]; padded columns hold a large negative
+  const float *leaf_value;  // [T][l_pad][leaf_dim]
+  const int32_t *leaf_id;   // [T][l_pad]
+  int32_t k_pad, l_pad, n_shapes;
+};
+
+// Each launcher checks its arguments against what the kernel and its grid
+// assume, enqueues on `stream`, and returns HB_OK or an error code with a
+// message in *err.
+int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_rows,
+               float *scores, int32_t *leaf_ids, hipStream_t stream, std::string *err);
+int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_rows,
+              float *scores, int32_t *leaf_ids, hipStream_t stream, std::string *err);
+int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t n_rows,
+                float *scores, int32_t *leaf_ids, hipStream_t stream, std::string *err);
+
+}  // namespace hb

@@ -1,0 +1,358 @@
+// hb_kernels.hip -- gfx950 kernels for batched tree-ensemble scoring.
+//
+// Traversal kernels (PerfectTreeTraversal, Algorithm 3; TreeTraversal,
+// Algorithm 2 of Sec. 4.1). One lane owns one row; a workgroup owns
+// kRows = 256 consecutive rows and walks them through every tree:
+//   * the rows' features are copied once into LDS, feature-major with an odd
+//     row stride, so the per-visit gather x[f] of 64 lanes (64 rows, any f)
+//     hits 64 different banks;
+//   * the trees are staged through LDS in chunks of a power-of-two number of
+//     trees; all lanes of a wave visit the same tree, so node records at one
+//     level come from a small contiguous range (broadcast-friendly);
+//   * each wave advances G trees at once (independent index chains) so LDS
+//     latency overlaps;
+//   * leaf ids are staged in LDS and written out row-contiguously;
+//   * aggregation is per lane in double precision, in tree order, with no
+//     atomics, so results are bitwise reproducible.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <string>
+
+#include "hb_internal.h"
+
+namespace hb {
+namespace {
+
+constexpr int kRows = 256;             // rows (= threads) per workgroup
+constexpr int kXStride = kRows + 1;    // LDS row stride of the feature tile
+constexpr int kGroup = 4;              // trees advanced together per wave
+
+struct TravArgs {
+  const float *X;
+  int64_t n_rows;
+  int32_t F;
+  float *scores;
+  int32_t *leaf_ids;
+  int32_t T, K, LD, aggregation, transform;
+  const int32_t *tree_class;
+  const float *base_score;
+  const uint2 *node;          // [T][slots]
+  const float *leaf_value;    // [T][leaf_slots][LD]
+  const int32_t *leaf_id;     // [T][leaf_slots]
+  const int32_t *tree_depth;  // TT: [T]
+  int32_t slots;              // node records per tree
+  int32_t leaf_slots;         // leaf entries per tree
+  int32_t depth;              // PTT: D
+  int32_t lg_tc;              // log2 of trees per LDS chunk
+  int32_t x_in_lds;           // informational; the template decides
+};
+
+__device__ __forceinline__ float as_float(uint32_t u) { return __uint_as_float(u); }
+
+// LDS bytes of the feature tile, rounded up so the tables after it stay
+// 16-byte aligned for the vector copies.
+__host__ __device__ constexpr size_t xtile_bytes(int F) { return ((size_t)F * kXStride * 4 + 15) / 16 * 16; }
+
+// Aggregated margin -> transformed score, in double precision.
+template <int KMAX>
+__device__ __forceinline__ void finish_row(const TravArgs &a, const double (&acc)[KMAX], int64_t row) {
+  double s[KMAX];
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    double v = acc[k];
+    if (a.aggregation == HB_AGG_MEAN) v /= (double)a.T;
+    if (a.base_score && k < a.K) v += (double)a.base_score[k];
+    s[k] = v;
+  }
+  if (a.transform == HB_POST_SIGMOID) {
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) s[k] = 1.0 / (1.0 + exp(-s[k]));
+  } else if (a.transform == HB_POST_SOFTMAX) {
+    double m = s[0];
+#pragma unroll
+    for (int k = 1; k < KMAX; ++k)
+      if (k < a.K) m = fmax(m, s[k]);
+    double z = 0.0;
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k)
+      if (k < a.K) {
+        s[k] = exp(s[k] - m);
+        z += s[k];
+      }
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) s[k] /= z;
+  }
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k)
+    if (k < a.K) a.scores[row * a.K + k] = (float)s[k];
+}
+
+template <bool PERFECT, bool X_LDS, int KMAX, bool LEAF_VEC>
+__global__ __launch_bounds__(kRows) void traverse_kernel(TravArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x;
+  const int64_t r0 = (int64_t)blockIdx.x * kRows;
+  const int64_t row = r0 + tid;
+  const bool valid = row < a.n_rows;
+  const int nblk = (int)min((int64_t)kRows, a.n_rows - r0);
+  const int tc_full = 1 << a.lg_tc;
+  const int LD = LEAF_VEC ? a.LD : 1;
+
+  size_t off = 0;
+  float *xs = reinterpret_cast<float *>(smem);
+  if (X_LDS) off += xtile_bytes(a.F);
+  uint2 *nodes = reinterpret_cast<uint2 *>(smem + off);
+  off += (size_t)tc_full * a.slots * 8;
+  float *lvals = reinterpret_cast<float *>(smem + off);
+  off += (size_t)tc_full * a.leaf_slots * LD * 4;
+  int32_t *lids = reinterpret_cast<int32_t *>(smem + off);
+  off += (size_t)tc_full * a.leaf_slots * 4;
+  int32_t *stage = reinterpret_cast<int32_t *>(smem + off);
+  const int stage_stride = tc_full + ((tc_full & 1) ? 0 : 1);
+
+  if (X_LDS) {
+    const float *src = a.X + r0 * a.F;
+    const int total = kRows * a.F;
+    for (int i = tid; i < total; i += kRows) {
+      const int r = i / a.F;
+      const int f = i - r * a.F;
+      xs[f * kXStride + r] = r < nblk ? src[i] : 0.0f;
+    }
+  }
+  // rows past the end read row n-1 (in bounds) and are never written
+  const float *xrow = a.X + (valid ? row : a.n_rows - 1) * a.F;
+
+  double acc[KMAX];
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) acc[k] = 0.0;
+
+  for (int t0 = 0; t0 < a.T; t0 += tc_full) {
+    const int tc = min(tc_full, a.T - t0);
+    __syncthreads();
+    {  // stage this chunk's tables (contiguous in global memory)
+      const uint4 *src = reinterpret_cast<const uint4 *>(a.node + (size_t)t0 * a.slots);
+      uint4 *dst = reinterpret_cast<uint4 *>(nodes);
+      const int n16 = tc * a.slots / 2;  // slots is even
+      for (int i = tid; i < n16; i += kRows) dst[i] = src[i];
+      const float *sv = a.leaf_value + (size_t)t0 * a.leaf_slots * LD;
+      const int nv = tc * a.leaf_slots * LD;
+      for (int i = tid; i < nv; i += kRows) lvals[i] = sv[i];
+      const int32_t *si = a.leaf_id + (size_t)t0 * a.leaf_slots;
+      const int ni = tc * a.leaf_slots;
+      for (int i = tid; i < ni; i += kRows) lids[i] = si[i];
+    }
+    __syncthreads();
+
+    for (int j = 0; j < tc; j += kGroup) {
+      uint32_t idx[kGroup];
+      int jj[kGroup];
+#pragma unroll
+      for (int g = 0; g < kGroup; ++g) {
+        jj[g] = min(j + g, tc - 1);  // a short tail repeats the last tree, unused
+        idx[g] = PERFECT ? 1u : 0u;
+      }
+      int levels;
+      if (PERFECT) {
+        levels = a.depth;
+      } else {
+        levels = 0;
+#pragma unroll
+        for (int g = 0; g < kGroup; ++g) levels = max(levels, a.tree_depth[t0 + jj[g]]);
+      }
+      for (int lvl = 0; lvl < levels; ++lvl) {
+#pragma unroll
+        for (int g = 0; g < kGroup; ++g) {
+          const uint2 rec = nodes[jj[g] * a.slots + idx[g]];
+          const uint32_t f = PERFECT ? rec.y : (rec.y & 0xffffu);
+          const float x = X_LDS ? xs[f * kXStride + tid] : xrow[f];
+          const bool go_left = x < as_float(rec.x);
+          if (PERFECT)
+            idx[g] = 2u * idx[g] + (go_left ? 0u : 1u);  // Algorithm 3's heap step
+          else
+            idx[g] = (rec.y >> 16) - (go_left ? 1u : 0u);  // left = right - 1
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < kGroup; ++g) {
+        if (j + g >= tc) break;  // uniform
+        const uint32_t slot = PERFECT ? idx[g] - (uint32_t)a.leaf_slots : idx[g];
+        const int lrec = jj[g] * a.leaf_slots + (int)slot;
+        if (LEAF_VEC) {
+#pragma unroll
+          for (int k = 0; k < KMAX; ++k)
+            if (k < LD) acc[k] += (double)lvals[lrec * LD + k];
+        } else if (KMAX == 1) {
+          acc[0] += (double)lvals[lrec];
+        } else {
+          const int c = __builtin_amdgcn_readfirstlane(a.tree_class[t0 + j + g]);
+          const double v = (double)lvals[lrec];
+#pragma unroll
+          for (int k = 0; k < KMAX; ++k)
+            if (k == c) acc[k] += v;
+        }
+        if (a.leaf_ids) stage[tid * stage_stride + j + g] = lids[lrec];
+      }
+    }
+    if (a.leaf_ids) {
+      __syncthreads();
+      const int total = nblk << a.lg_tc;
+      for (int i = tid; i < total; i += kRows) {
+        const int r = i >> a.lg_tc;
+        const int jt = i & (tc_full - 1);
+        if (jt < tc) a.leaf_ids[(r0 + r) * a.T + t0 + jt] = stage[r * stage_stride + jt];
+      }
+    }
+  }
+  if (valid) finish_row<KMAX>(a, acc, row);
+  (void)xrow;
+}
+
+using KernelFn = void (*)(TravArgs);
+
+template <bool PERFECT, bool X_LDS>
+KernelFn pick_k(int kmax, bool vec) {
+  if (vec) {
+    switch (kmax) {
+      case 2: return traverse_kernel<PERFECT, X_LDS, 2, true>;
+      case 8: return traverse_kernel<PERFECT, X_LDS, 8, true>;
+      default: return traverse_kernel<PERFECT, X_LDS, 16, true>;
+    }
+  }
+  switch (kmax) {
+    case 1: return traverse_kernel<PERFECT, X_LDS, 1, false>;
+    case 2: return traverse_kernel<PERFECT, X_LDS, 2, false>;
+    case 8: return traverse_kernel<PERFECT, X_LDS, 8, false>;
+    default: return traverse_kernel<PERFECT, X_LDS, 16, false>;
+  }
+}
+
+int kmax_for(int K) { return K <= 1 ? 1 : K <= 2 ? 2 : K <= 8 ? 8 : 16; }
+
+int max_dynamic_lds(std::string *err) {
+  int dev = 0, v = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return -1;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) {
+    *err = "hipDeviceGetAttribute(MaxSharedMemoryPerBlock) failed";
+    return -1;
+  }
+  return v;
+}
+
+// Chooses the feature-tile placement and the chunk size, then launches.
+int launch_traverse(bool perfect, TravArgs a, hipStream_t stream, std::string *err) {
+  if (a.n_rows <= 0) return HB_OK;
+  const int lds_max = max_dynamic_lds(err);
+  if (lds_max <= 0) return HB_ERR_HIP;
+  const int LD = a.LD;
+  const size_t per_tree = (size_t)a.slots * 8 + (size_t)a.leaf_slots * LD * 4 + (size_t)a.leaf_slots * 4;
+  auto need = [&](bool xl, int tc) {
+    const int stride = tc + ((tc & 1) ? 0 : 1);
+    return (xl ? xtile_bytes(a.F) : 0) + (size_t)tc * per_tree + (size_t)kRows * stride * 4;
+  };
+  // Prefer two workgroups per CU (half the LDS) with at least kGroup trees per
+  // chunk; otherwise use the whole LDS; keep the feature tile when it fits.
+  const size_t half = (size_t)lds_max / 2;
+  bool x_lds = false;
+  int tc = 0;
+  for (int pass = 0; pass < 4 && tc == 0; ++pass) {
+    const bool xl = pass < 2 && xtile_bytes(a.F) <= (size_t)lds_max / 4 * 3;
+    const size_t budget = (pass % 2 == 0) ? half : (size_t)lds_max;
+    for (int c = 16; c >= (pass % 2 == 0 ? kGroup : 1); c >>= 1)
+      if (need(xl, c) <= budget) {
+        tc = c;
+        x_lds = xl;
+        break;
+      }
+  }
+  if (tc == 0) {
+    *err = "tree tables too large for LDS staging";
+    return HB_ERR_UNSUPPORTED;
+  }
+  a.lg_tc = __builtin_ctz((unsigned)tc);
+  a.x_in_lds = x_lds;
+  const size_t lds = need(x_lds, tc);
+  const bool vec = LD > 1;
+  const int kmax = kmax_for(vec ? LD : a.K);
+  KernelFn fn = perfect ? (x_lds ? pick_k<true, true>(kmax, vec) : pick_k<true, false>(kmax, vec))
+                        : (x_lds ? pick_k<false, true>(kmax, vec) : pick_k<false, false>(kmax, vec));
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) {
+    *err = std::string("hipFuncSetAttribute: ") + hipGetErrorString(e);
+    return HB_ERR_HIP;
+  }
+  const int64_t blocks = (a.n_rows + kRows - 1) / kRows;
+  hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kRows), lds, stream, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) {
+    *err = std::string("kernel launch: ") + hipGetErrorString(e);
+    return HB_ERR_HIP;
+  }
+  return HB_OK;
+}
+
+TravArgs common_args(const EnsembleDev &e, const float *X, int64_t n, float *scores, int32_t *ids) {
+  TravArgs a{};
+  a.X = X;
+  a.n_rows = n;
+  a.F = e.n_features;
+  a.scores = scores;
+  a.leaf_ids = ids;
+  a.T = e.n_trees;
+  a.K = e.n_outputs;
+  a.LD = e.leaf_dim;
+  a.aggregation = e.aggregation;
+  a.transform = e.transform;
+  a.tree_class = e.tree_class;
+  a.base_score = e.base_score;
+  return a;
+}
+
+}  // namespace
+
+int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_rows, float *scores,
+               int32_t *leaf_ids, hipStream_t stream, std::string *err) {
+  if (!t.node || !t.leaf_value || !t.leaf_id || t.depth < 0 || t.depth > HB_PTT_MAX_DEPTH) {
+    *err = "PTT tables missing";
+    return HB_ERR_INVALID_ARG;
+  }
+  TravArgs a = common_args(e, X, n_rows, scores, leaf_ids);
+  a.node = t.node;
+  a.leaf_value = t.leaf_value;
+  a.leaf_id = t.leaf_id;
+  a.depth = t.depth;
+  a.slots = 1 << t.depth;
+  a.leaf_slots = 1 << t.depth;
+  if (a.slots < 2) a.slots = 2;  // depth 0 still stores two (unused) records per tree
+  return launch_traverse(true, a, stream, err);
+}
+
+int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_rows, float *scores,
+              int32_t *leaf_ids, hipStream_t stream, std::string *err) {
+  if (!t.node || !t.leaf_value || !t.leaf_id || !t.depth || t.n_pad < 1) {
+    *err = "TT tables missing";
+    return HB_ERR_INVALID_ARG;
+  }
+  if (t.n_pad % 2) {
+    *err = "TT node slots must be even";
+    return HB_ERR_INVALID_ARG;
+  }
+  TravArgs a = common_args(e, X, n_rows, scores, leaf_ids);
+  a.node = t.node;
+  a.leaf_value = t.leaf_value;
+  a.leaf_id = t.leaf_id;
+  a.tree_depth = t.depth;
+  a.slots = t.n_pad;
+  a.leaf_slots = t.n_pad;
+  return launch_traverse(false, a, stream, err);
+}
+
+int launch_gemm(const EnsembleDev &, const GemmDev &, const float *, int64_t, float *, int32_t *,
+                hipStream_t, std::string *err) {
+  *err = "GEMM strategy not built yet";
+  return HB_ERR_UNSUPPORTED;
+}
+
+}  // namespace hb

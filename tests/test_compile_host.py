@@ -1,0 +1,141 @@
+"""hb_compile's tensors (host-only handles, no GPU): hand-derived tables,
+size formulas, and Algorithms 1-3 run over them in numpy against the oracle."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2010_04804_amd as hb
+from paper_2010_04804_amd import synth
+import emulate
+import pins
+
+
+def host(model, strategy="auto"):
+    return hb.compile(model, strategy=strategy, device=-1)
+
+
+def golden_model():
+    trees, _ = pins.load_golden()
+    return pins.model_from_trees(trees, 3)
+
+
+def test_tree_a_gemm_tensors_match_table3_by_hand():
+    # Tree A of the golden fixture: node 0 tests f0<0.5, node 1 f1<0.25,
+    # node 2 f2<0.75; leaves 3,4,5,6 left to right. From Table 3's definitions:
+    #   C (internal x leaf) = [[+1,+1,-1,-1], [+1,-1,0,0], [0,0,+1,-1]]
+    #   D (left edges on each leaf's root path) = [2, 1, 1, 0]
+    h = host(golden_model())
+    k_pad, l_pad, S = h.table("gemm", "dims", np.int32)
+    assert (k_pad, l_pad, S) == (64, 16, 2)
+    shape = h.table("gemm", "shape", np.int32)
+    ct = h.table("gemm", "ct", np.int8).reshape(S, l_pad, k_pad)[shape[0]]
+    want_c = np.array([[1, 1, -1, -1], [1, -1, 0, 0], [0, 0, 1, -1]])
+    assert np.array_equal(ct[:4, :3], 4 * want_c.T)
+    assert not ct[4:].any() and not ct[:, 3:].any()
+    bias = h.table("gemm", "bias", np.int32).reshape(S, l_pad)[shape[0]]
+    D = np.array([2, 1, 1, 0])
+    assert np.array_equal(bias[:4], np.arange(4) - 256 * D)
+    assert np.all(bias[4:] < -(1 << 20))
+    lid = h.table("gemm", "leaf_id", np.int32).reshape(2, l_pad)
+    assert list(lid[0, :4]) == [3, 4, 5, 6]
+    # tree B (depth-first caller numbering) leaves left to right: 2, 3, 6, 7, 8
+    assert list(lid[1, :5]) == [2, 3, 6, 7, 8]
+    node = h.table("gemm", "node", np.uint32).reshape(2, k_pad, 2)
+    assert list(node[0, :3, 1]) == [0, 1, 2]
+    assert list(node[0, :3, 0].view(np.float32)) == [0.5, 0.25, 0.75]
+    assert np.all(np.isneginf(node[0, 3:, 0].view(np.float32)))
+
+
+def test_tree_b_ptt_padding_by_hand():
+    # Tree B has depth 3 (node 5 sits under node 4); leaves 2 and 3 are at
+    # depth 2 and leaf 8 at depth 2, so each is padded into 2 perfect leaves.
+    h = host(golden_model())
+    assert h.info()["ptt_depth"] == 3
+    lid = h.table("ptt", "leaf_id", np.int32).reshape(2, 8)
+    assert list(lid[1]) == [2, 2, 3, 3, 6, 7, 8, 8]
+    assert list(lid[0]) == [3, 3, 4, 4, 5, 5, 6, 6]
+    node = h.table("ptt", "node", np.uint32).reshape(2, 8, 2)
+    # heap slot 1 = root (f1 < 0), 2 = node 1 (f0 < -1), 3 = node 4 (f2 < 2),
+    # 6 = node 5 (f0 < 1); slots 4, 5, 7 are padding below leaves
+    assert list(node[1, [1, 2, 3, 6], 1]) == [1, 0, 2, 0]
+    assert list(node[1, [1, 2, 3, 6], 0].view(np.float32)) == [0.0, -1.0, 2.0, 1.0]
+
+
+def test_tree_b_tt_records_by_hand():
+    h = host(golden_model())
+    n_pad = int(h.table("tt", "dims", np.int32)[0])
+    assert n_pad == 10  # 9 nodes rounded up to even
+    node = h.table("tt", "node", np.uint32).reshape(2, n_pad, 2)
+    lid = h.table("tt", "leaf_id", np.int32).reshape(2, n_pad)
+    # breadth-first order of tree B: 0, 1, 4, 2, 3, 5, 8, 6, 7
+    assert list(lid[1, :9]) == [0, 1, 4, 2, 3, 5, 8, 6, 7]
+    # canonical internal nodes 0, 1, 2, 5 (caller 0, 1, 4, 5) store their right
+    # child (left = right - 1); leaves 3, 4, 6, 7, 8 and padding 9 point to themselves
+    right = node[1, :, 1] >> 16
+    assert list(right) == [2, 4, 6, 3, 4, 8, 6, 7, 8, 9]
+    thr = node[1, :, 0].view(np.float32)
+    assert list(thr[[0, 1, 2, 5]]) == [0.0, -1.0, 2.0, 1.0]
+    assert np.all(np.isneginf(thr[[3, 4, 6, 7, 8, 9]]))
+    assert list(h.table("tt", "depth", np.int32)) == [2, 3]
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_table_sizes_follow_table4(cfg):
+    m = synth.make_model(cfg)
+    h = host(m)
+    info = h.info()
+    T, D, ld = info["n_trees"], info["max_depth"], info["leaf_dim"]
+    tb = info["table_bytes"]
+    S = 1 << D
+    # PTT: O(2^D) per tree: node records, leaf values and ids
+    assert tb["ptt"] == T * max(S, 2) * 8 + T * S * ld * 4 + T * S * 4
+    # TT: O(|N|) per tree (padded to the largest tree)
+    n_pad = int(h.table("tt", "dims", np.int32)[0])
+    assert n_pad >= max(np.diff(m["tree_node_offset"]))
+    assert tb["tt"] == T * n_pad * 8 + T * 4 + T * n_pad * ld * 4 + T * n_pad * 4
+    # GEMM: C is |I| x |L| per distinct shape
+    k_pad, l_pad, nshape = (int(v) for v in h.table("gemm", "dims", np.int32))
+    assert h.table("gemm", "ct", np.int8).size == nshape * l_pad * k_pad
+    if cfg in (1, 2, 3, 4):
+        assert nshape == 1 and info["balance"] == 1.0
+    else:
+        assert info["balance"] > 2.0
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("strategy", ["ptt", "tt", "gemm"])
+def test_emulated_algorithms_match_oracle(cfg, strategy):
+    m = synth.make_model(cfg)
+    n = 48 if cfg in (3, 4, 5) else 200
+    X = synth.make_rows(cfg, n)
+    if cfg == 4:
+        X = X[:24]
+    h = host(m)
+    ids, raw = getattr(emulate, strategy)(h, m, X)
+    o_raw, _, o_ids = oracle.predict(m, X)
+    assert np.array_equal(ids, o_ids)
+    assert np.allclose(raw, o_raw, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("strategy", ["ptt", "tt", "gemm"])
+def test_emulated_algorithms_on_tricky_ensembles(seed, strategy):
+    """Random unbalanced ensembles with permuted numbering, ties, NaN, +-inf."""
+    m = pins.random_small_ensemble(seed)
+    X = pins.tricky_rows(np.random.Generator(np.random.PCG64(seed)), m, 300)
+    h = host(m)
+    ids, raw = getattr(emulate, strategy)(h, m, X)
+    o_raw, _, o_ids = oracle.predict(m, X)
+    assert np.array_equal(ids, o_ids)
+    assert np.allclose(raw, o_raw, rtol=1e-12, atol=1e-12)
+
+
+def test_selector_choices():
+    assert host(synth.make_model(2)).select(1_000_000) == "ptt"
+    assert host(synth.make_model(4)).select(1_000_000) == "ptt"
+    assert host(synth.make_model(5)).select(1_000_000) == "tt"
+    shallow = synth.perfect_forest(np.random.Generator(np.random.PCG64(0)), 4, 2, 3,
+                                   lambda r, f: r.random(f.size), lambda r, n: r.random(n))
+    shallow.update(n_outputs=1, tree_class=None, aggregation="sum", transform="none", base_score=None)
+    assert host(shallow).select(1000) == "gemm"
+    assert hb.compile(synth.make_model(2), strategy="tt", device=-1).select(10) == "tt"

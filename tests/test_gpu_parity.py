@@ -1,0 +1,187 @@
+"""GPU parity: the HIP path through the C-ABI against the CPU oracle.
+
+Leaf ids must be identical; scores must satisfy |gpu - oracle| <= 1e-5 (1 + |oracle|)
+elementwise, with the oracle aggregating in double precision. Every case
+prints its config, strategy and size before touching the GPU.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2010_04804_amd as hb
+from paper_2010_04804_amd import synth
+import pins
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+STRATEGIES = ["ptt", "tt", "gemm"]
+TOL = 1e-5
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+_handles = {}
+
+
+def handle(cfg):
+    if cfg not in _handles:
+        _handles[cfg] = (synth.make_model(cfg), None)
+        _handles[cfg] = (_handles[cfg][0], hb.compile(_handles[cfg][0], device=0))
+    return _handles[cfg]
+
+
+def run(h, X, strategy, leaves=True, stream=None):
+    Xd = torch.from_numpy(X).cuda()
+    s, ids = hb.predict(h, Xd, strategy=strategy, leaves=leaves, stream=stream)
+    torch.cuda.synchronize()
+    return s.cpu().numpy(), (ids.cpu().numpy() if ids is not None else None)
+
+
+def check(model, X, scores, ids, label):
+    o_raw, o_out, o_ids = oracle.predict(model, X)
+    if ids is not None:
+        bad = np.argwhere(ids != o_ids)
+        assert bad.size == 0, f"{label}: {len(bad)} leaf ids differ, first {bad[:5].tolist()}"
+    err = np.abs(scores.astype(np.float64) - o_out)
+    lim = TOL * (1.0 + np.abs(o_out))
+    worst = float((err / lim).max()) if err.size else 0.0
+    assert np.all(err <= lim), f"{label}: score error {worst:.3g} x tolerance"
+    return worst
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES)
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_config_parity(cfg, strategy):
+    model, h = handle(cfg)
+    n = {1: 1000, 2: 10_000, 3: 2000, 4: 3000, 5: 10_000}[cfg]
+    say("config", cfg, strategy, "rows", n)
+    X = synth.make_rows(cfg, n)
+    scores, ids = run(h, X, strategy)
+    check(model, X, scores, ids, f"cfg{cfg}/{strategy}")
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES)
+@pytest.mark.parametrize("n", [1, 2, 63, 65, 255, 257, 513])
+def test_ragged_batches(strategy, n):
+    model, h = handle(2)
+    say("ragged", strategy, n)
+    X = synth.make_rows(2, n)
+    scores, ids = run(h, X, strategy)
+    check(model, X, scores, ids, f"ragged{n}/{strategy}")
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES)
+def test_empty_batch_enqueues_nothing(strategy):
+    model, h = handle(1)
+    say("empty", strategy)
+    X = torch.empty((0, 8), dtype=torch.float32, device="cuda")
+    s, ids = hb.predict(h, X, strategy=strategy)
+    torch.cuda.synchronize()
+    assert s.shape == (0, 1) and ids.shape == (0, 10)
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES)
+@pytest.mark.parametrize("seed", range(4))
+def test_tricky_ensembles(strategy, seed):
+    """Unbalanced trees, permuted numbering, ties, NaN and +-inf inputs."""
+    m = pins.random_small_ensemble(seed)
+    X = pins.tricky_rows(np.random.Generator(np.random.PCG64(seed)), m, 700)
+    say("tricky", strategy, seed)
+    h = hb.compile(m, device=0)
+    scores, ids = run(h, X, strategy)
+    check(m, X, scores, ids, f"tricky{seed}/{strategy}")
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES)
+def test_permuted_numbering_and_mixed_aggregations(strategy):
+    base = synth.make_model(3)
+    m = synth.permute_nodes(base, 9)
+    m["base_score"] = np.asarray([0.25, -0.5], np.float32)
+    X = synth.make_rows(3, 700)
+    say("permuted cfg3", strategy)
+    h = hb.compile(m, device=0)
+    scores, ids = run(h, X, strategy)
+    check(m, X, scores, ids, f"perm/{strategy}")
+    gb = synth.make_model(4)
+    gb["transform"] = "sigmoid"
+    gb["base_score"] = np.linspace(-1, 1, 7).astype(np.float32)
+    X4 = synth.make_rows(4, 600)
+    h4 = hb.compile(gb, device=0)
+    scores, ids = run(h4, X4, strategy)
+    check(gb, X4, scores, ids, f"sigmoid7/{strategy}")
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES)
+def test_scores_only_and_determinism(strategy):
+    model, h = handle(5)
+    X = synth.make_rows(5, 4096)
+    say("determinism", strategy)
+    s1, i1 = run(h, X, strategy)
+    s2, i2 = run(h, X, strategy)
+    s3, i3 = run(h, X, strategy, leaves=False)
+    assert i3 is None
+    assert np.array_equal(i1, i2)
+    assert np.array_equal(s1.view(np.uint32), s2.view(np.uint32))
+    assert np.array_equal(s1.view(np.uint32), s3.view(np.uint32))
+
+
+def test_strategies_agree_bitwise_on_leaf_ids():
+    model, h = handle(4)
+    X = synth.make_rows(4, 1500)
+    say("cross-strategy cfg4")
+    out = {s: run(h, X, s) for s in STRATEGIES}
+    for s in STRATEGIES[1:]:
+        assert np.array_equal(out[s][1], out["ptt"][1])
+
+
+def test_non_default_stream():
+    model, h = handle(2)
+    X = synth.make_rows(2, 5000)
+    say("side stream")
+    st = torch.cuda.Stream()
+    with torch.cuda.stream(st):
+        Xd = torch.from_numpy(X).to("cuda", non_blocking=False)
+        s, ids = hb.predict(h, Xd, strategy="auto")
+    st.synchronize()
+    check(model, X, s.cpu().numpy(), ids.cpu().numpy(), "stream")
+
+
+def test_full_size_headline_sampled():
+    """Config 2 at 1,000,000 rows in the benchmark's launch configuration:
+    every row's score and leaf ids on a seeded sample of 20,000 rows."""
+    model, h = handle(2)
+    X = synth.make_rows(2, 1_000_000)
+    say("full size cfg2 1M auto")
+    Xd = torch.from_numpy(X).cuda()
+    s, ids = hb.predict(h, Xd, strategy="auto")
+    torch.cuda.synchronize()
+    rows = np.sort(np.random.Generator(np.random.PCG64(1)).choice(1_000_000, 20_000, replace=False))
+    rows[-1] = 999_999
+    rows_t = torch.from_numpy(rows).cuda()
+    check(model, X[rows], s[rows_t].cpu().numpy(), ids[rows_t].cpu().numpy(), "cfg2-1M")
+    # every score is a probability and every leaf id is a leaf of its tree
+    sc = s.cpu().numpy()
+    assert np.all((sc >= 0) & (sc <= 1))
+    leaf_nodes = (model["feature"] < 0).reshape(500, 511)
+    ids_all = ids.cpu().numpy()
+    assert leaf_nodes[np.arange(500)[None, :], ids_all].all()
+
+
+def test_invalid_arguments_raise():
+    model, h = handle(1)
+    say("invalid args")
+    with pytest.raises(hb.HBError):
+        hb.predict_ptr(h, 0, 10, 0, None)
+    with pytest.raises(hb.HBError):
+        hb.predict_ptr(h, 1, -1, 1, None)
+    with pytest.raises(hb.HBError):
+        hb.predict_ptr(h, 1, 1, 1, None, strategy=7)
