@@ -50,6 +50,15 @@ def gemm_ops(model, n):
     return 2 * n * tot
 
 
+def gemm_available(h):
+    import paper_2010_04804_amd as hb
+    try:
+        hb.predict_ptr(h, 0, 0, 0, None, "gemm")
+        return True
+    except hb.HBError:
+        return False
+
+
 def cpu_baseline(model, cfg, seconds_target=15.0):
     import oracle
     from paper_2010_04804_amd import synth
@@ -165,7 +174,7 @@ def main():
     if args.extra:
         ms_s = timed(lambda: step(strategy, None), args.steps, args.warmup)
         out["scores_only"] = {"ms": ms_s, "rows_per_s": n / (ms_s * 1e-3)}
-        if strategy != "gemm" and info["feasible"]["gemm"]:
+        if strategy != "gemm" and info["feasible"]["gemm"] and gemm_available(h):
             ng = min(n, 100_000)
             ms_g = timed(lambda: hb.predict_ptr(h, Xd.data_ptr(), ng, scores.data_ptr(),
                                                 ids.data_ptr() if ids is not None else None, "gemm",

@@ -10,6 +10,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libhb.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+SOURCES = ["hb_api.cpp", "hb_kernels.hip", "hb_fast_ptt_256.hip", "hb_fast_ptt_512.hip",
+           "hb_fast_tt_256.hip", "hb_fast_tt_512.hip"]
 
 # -packed-fp32-ops: no packed fp32 instructions in device code (the host pass
 # warns that it does not know the feature; that is harmless).
@@ -19,15 +21,31 @@ DEVICE_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
 
 def build(verbose: bool = False) -> str:
     inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
-    srcs = [os.path.join(CSRC, "hb_api.cpp"), os.path.join(CSRC, "hb_kernels.hip")]
+    srcs = [os.path.join(CSRC, f) for f in SOURCES]
+    objdir = os.path.join(PKG, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    objs, procs = [], []
+    for src in srcs:  # compile translation units in parallel
+        obj = os.path.join(objdir, os.path.basename(src) + ".o")
+        cmd = [HIPCC, *DEVICE_FLAGS, *inc, "-c", "-o", obj, src]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))
+        objs.append(obj)
+    failed = False
+    for src, p in procs:
+        out, _ = p.communicate()
+        if p.returncode != 0:
+            sys.stderr.write(out)
+            failed = True
+    if failed:
+        raise RuntimeError("hipcc failed building libhb.so")
     tmp = LIB + ".tmp"
-    cmd = [HIPCC, *DEVICE_FLAGS, *inc, "-shared", "-o", tmp, *srcs]
-    if verbose:
-        print(" ".join(cmd), flush=True)
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError("hipcc failed building libhb.so")
+        raise RuntimeError("hipcc failed linking libhb.so")
     os.replace(tmp, LIB)
     return LIB
 

@@ -110,12 +110,6 @@ int canonicalise(const hb_ensemble_desc *d, int32_t t, CanonTree *ct) {
   return HB_OK;
 }
 
-template <class T>
-struct DevBuf {
-  T *ptr = nullptr;
-  size_t count = 0;
-};
-
 }  // namespace
 
 struct hb_handle {
@@ -142,6 +136,9 @@ struct hb_handle {
   std::vector<float> gemm_leaf_value;
   std::vector<int32_t> gemm_leaf_id;
   int32_t gemm_k_pad = 0, gemm_l_pad = 0, gemm_n_shapes = 0;
+  // packed blocks of the fast traversal kernels (device layout only)
+  std::vector<uint32_t> ptt_fast, tt_fast;
+  int32_t ptt_fast_chunks = 0, tt_fast_lg = 0, tt_fast_chunks = 0;
   // device
   std::vector<void *> allocations;
   hb::EnsembleDev ens{};
@@ -248,6 +245,69 @@ void build_tt(hb_handle *h, const hb_ensemble_desc *d, const std::vector<CanonTr
     }
   }
   h->tt_dims = {n_pad};
+}
+
+// Packed blocks for the fast kernels (scalar leaves only); see hb_internal.h.
+void build_fast(hb_handle *h, const hb_ensemble_desc *d, const std::vector<CanonTree> &trees) {
+  if (d->leaf_dim != 1) return;
+  const int32_t T = d->n_trees;
+  const int32_t D = h->info.max_depth;
+  if (h->info.feasible[HB_STRATEGY_PTT] && D >= 1 && D <= hb::kFastMaxLg) {
+    const int tb = hb::fast_tree_bytes(0, D);
+    const int tc = hb::fast_tc(tb);
+    const int chunks = ((T + tc - 1) / tc + 3) / 4 * 4;  // whole groups of 4 chunks
+    const size_t words = (size_t)tb / 4;
+    const size_t S = (size_t)1 << D;
+    h->ptt_fast.assign((size_t)chunks * tc * words, 0u);
+    for (int32_t t = 0; t < T; ++t) {
+      uint32_t *blk = &h->ptt_fast[(size_t)t * words];
+      for (size_t p = 1; p < S; ++p) {
+        blk[2 * p] = h->ptt_node[((size_t)t * S + p) * 2];
+        blk[2 * p + 1] = h->ptt_node[((size_t)t * S + p) * 2 + 1];
+      }
+      for (size_t q = 0; q < S; ++q) {
+        blk[2 * (S + q)] = fbits(h->ptt_leaf_value[(size_t)t * S + q]);
+        blk[2 * (S + q) + 1] = (uint32_t)h->ptt_leaf_id[(size_t)t * S + q];
+      }
+    }
+    h->ptt_fast_chunks = chunks;
+  }
+  int32_t max_nodes = 1;
+  for (const CanonTree &ct : trees) max_nodes = std::max(max_nodes, ct.size());
+  int lg = 1;
+  while ((1 << lg) < max_nodes) ++lg;
+  if (h->info.feasible[HB_STRATEGY_TT] && lg <= hb::kFastMaxLg) {
+    const int tb = hb::fast_tree_bytes(1, lg);
+    const int tc = hb::fast_tc(tb);
+    const int chunks = ((T + tc - 1) / tc + 3) / 4 * 4;
+    const size_t words = (size_t)tb / 4;
+    const size_t NP = (size_t)1 << lg;
+    h->tt_fast.assign((size_t)chunks * tc * words, 0u);
+    for (int32_t t = 0; t < T; ++t) {
+      const CanonTree &ct = trees[t];
+      const int64_t base = d->tree_node_offset[t];
+      uint32_t *blk = &h->tt_fast[(size_t)t * words];
+      for (size_t c = 0; c < NP; ++c) {
+        uint32_t *rec = blk + 4 * c;
+        if (c < (size_t)ct.size() && ct.feat[c] >= 0) {
+          rec[0] = fbits(ct.thr[c]);
+          rec[1] = (uint32_t)ct.feat[c];
+          rec[2] = 16u * (uint32_t)ct.left[c];
+          rec[3] = 16u * (uint32_t)(ct.left[c] + 1);
+        } else {
+          rec[2] = rec[3] = 16u * (uint32_t)c;  // leaves (and padding) stay put
+        }
+        uint32_t *lr = blk + 4 * NP + 2 * c;
+        if (c < (size_t)ct.size()) {
+          const int32_t v = ct.caller[c];
+          lr[0] = ct.feat[c] < 0 ? fbits(d->leaf_value[base + v]) : 0u;
+          lr[1] = (uint32_t)v;
+        }
+      }
+    }
+    h->tt_fast_lg = lg;
+    h->tt_fast_chunks = chunks;
+  }
 }
 
 void build_gemm(hb_handle *h, const hb_ensemble_desc *d, const std::vector<CanonTree> &trees) {
@@ -445,6 +505,7 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
     if (I.feasible[HB_STRATEGY_PTT]) build_ptt(h, d, trees);
     if (I.feasible[HB_STRATEGY_TT]) build_tt(h, d, trees);
     if (I.feasible[HB_STRATEGY_GEMM]) build_gemm(h, d, trees);
+    build_fast(h, d, trees);
   } catch (const std::bad_alloc &) {
     delete h;
     return fail(HB_ERR_OOM, "out of host memory building tables");
@@ -492,6 +553,11 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
       if (!rc) rc = upload(h, h->ptt_leaf_value, &h->ptt.leaf_value);
       if (!rc) rc = upload(h, h->ptt_leaf_id, &h->ptt.leaf_id);
       h->ptt.depth = D;
+      if (!rc && !h->ptt_fast.empty()) {
+        rc = upload(h, h->ptt_fast, &pn);
+        h->ptt.fast = reinterpret_cast<const uint4 *>(pn);
+        h->ptt.fast_chunks = h->ptt_fast_chunks;
+      }
     }
     if (!rc && I.feasible[HB_STRATEGY_TT]) {
       rc = upload(h, h->tt_node, &pn);
@@ -501,6 +567,12 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
       if (!rc) rc = upload(h, h->tt_leaf_id, &h->tt.leaf_id);
       h->tt.n_pad = h->tt_n_pad;
       h->tt.max_depth = D;
+      if (!rc && !h->tt_fast.empty()) {
+        rc = upload(h, h->tt_fast, &pn);
+        h->tt.fast = reinterpret_cast<const uint4 *>(pn);
+        h->tt.fast_lg = h->tt_fast_lg;
+        h->tt.fast_chunks = h->tt_fast_chunks;
+      }
     }
     if (!rc && I.feasible[HB_STRATEGY_GEMM]) {
       rc = upload(h, h->gemm_node, &pn);

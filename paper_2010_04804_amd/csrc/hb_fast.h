@@ -1,0 +1,244 @@
+// hb_fast.h -- the fast traversal kernel template (see the comment below);
+// included by hb_fast_ptt.hip and hb_fast_tt.hip, which instantiate it.
+#pragma once
+
+#include "hb_device.h"
+
+namespace hb {
+namespace {
+
+// ---------------------------------------------------------------------------
+// Fast traversal kernels for scalar leaves and inputs whose feature tile fits
+// in LDS. Differences from traverse_kernel:
+//   * each tree owns one packed block (node records, then leaf records
+//     {value, caller id}); chunks of TC consecutive blocks are double-buffered
+//     in LDS: chunk c+1 is loaded into registers before chunk c is walked and
+//     stored to LDS after it, so one barrier per chunk suffices and the load
+//     latency hides behind the walk;
+//   * trees of a chunk and levels are fully unrolled with compile-time LDS
+//     offsets, and the walk state is the byte offset of the current record;
+//   * PTT: heap index a lives as s = 8a; the child is 2s + 8*(x >= t) and,
+//     after D steps, s is exactly the offset of the leaf record (leaves follow
+//     the 2^D node slots);
+//   * TT: a node record {threshold, feature, left offset, right offset}
+//     makes a step one select; leaves point to themselves.
+
+// Barrier for LDS traffic only: orders this workgroup's LDS accesses across
+// the barrier without waiting for outstanding global stores (the leaf-id
+// writes keep draining while the next chunk is walked).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// One chunk of tree blocks held in registers between its global load (issued
+// before the current chunk is walked) and its LDS store (after the walk).
+// Native vector words (not the HIP uint4 struct) so they stay in VGPRs.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+template <int ROWS, int N16>
+struct ChunkPrefetch {
+  static constexpr int PER = (N16 + ROWS - 1) / ROWS;
+  u32x4 v[PER];
+  // every lane loads (a clamped, in-bounds index)
+  __device__ __forceinline__ void load(const uint4 *__restrict__ src) {
+    const u32x4 *s = reinterpret_cast<const u32x4 *>(src);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) v[i] = s[min(i * ROWS + (int)threadIdx.x, N16 - 1)];
+  }
+  __device__ __forceinline__ void store(uint4 *dst) const {
+    u32x4 *d = reinterpret_cast<u32x4 *>(dst);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int u = i * ROWS + (int)threadIdx.x;
+      if (u < N16) d[u] = v[i];
+    }
+  }
+};
+
+template <int MODE>
+constexpr int kFastMaxLgFor = MODE == 0 ? 10 : 11;
+
+template <int MODE, int LG, bool MULTI>
+struct FastCfg {
+  static constexpr int TB = fast_tree_bytes(MODE, LG);
+  static constexpr int TC = fast_tc(TB);
+  static constexpr int CHUNK16 = TC * TB / 16;
+  static constexpr int KMAX = MULTI ? HB_MAX_OUTPUTS : 1;
+};
+
+template <int MODE, int LG, bool MULTI, int ROWS, int B, int Q>
+__device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI>::CHUNK16],
+                                           const float *xs, uint32_t lane4,
+                                           double (&acc)[FastCfg<MODE, LG, MULTI>::KMAX],
+                                           int32_t (&ids)[4 * FastCfg<MODE, LG, MULTI>::TC]) {
+  using C = FastCfg<MODE, LG, MULTI>;
+  constexpr int TC = C::TC;
+  constexpr int TB = C::TB;
+  // chunk c is in tbuf[B] (the barrier that ended the previous chunk made it
+  // visible); fetch chunk c+1 into registers while walking chunk c
+  ChunkPrefetch<ROWS, C::CHUNK16> next;
+  const bool more = c + 1 < a.n_chunks;
+  next.load(a.blocks + (size_t)(more ? c + 1 : c) * C::CHUNK16);
+  __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the walk
+  const unsigned char *base = reinterpret_cast<const unsigned char *>(tbuf[B]);
+  const unsigned char *xb = reinterpret_cast<const unsigned char *>(xs);
+  const int t0 = c * TC;
+  uint32_t s[TC];
+  if (MODE == 0) {
+#pragma unroll
+    for (int g = 0; g < TC; ++g) s[g] = 8u;  // heap index 1
+#pragma unroll
+    for (int lvl = 0; lvl < LG; ++lvl) {
+#pragma unroll
+      for (int g = 0; g < TC; ++g) {
+        const uint2 rec = *reinterpret_cast<const uint2 *>(base + g * TB + s[g]);
+        const float x = *reinterpret_cast<const float *>(xb + __umul24(rec.y, ROWS * 4u) + lane4);
+        s[g] = 2u * s[g] + (x < as_float(rec.x) ? 0u : 8u);  // Algorithm 3's heap step, in bytes
+      }
+    }
+  } else {
+    int levels = 0;
+#pragma unroll
+    for (int g = 0; g < TC; ++g) levels = max(levels, a.tree_depth[min(t0 + g, a.out.T - 1)]);
+#pragma unroll
+    for (int g = 0; g < TC; ++g) s[g] = 0u;  // root record
+    for (int lvl = 0; lvl < levels; ++lvl) {
+#pragma unroll
+      for (int g = 0; g < TC; ++g) {
+        const uint4 rec = *reinterpret_cast<const uint4 *>(base + g * TB + s[g]);
+        const float x = *reinterpret_cast<const float *>(xb + __umul24(rec.y, ROWS * 4u) + lane4);
+        s[g] = x < as_float(rec.x) ? rec.z : rec.w;  // Algorithm 2's step: left or right child
+      }
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < TC; ++g) {
+    const int t = t0 + g;
+    const uint32_t loff = MODE == 0 ? s[g] : (1u << LG) * 16u + (s[g] >> 1);
+    const uint2 lr = *reinterpret_cast<const uint2 *>(base + g * TB + loff);
+    ids[Q * TC + g] = (int32_t)lr.y;
+    if (t < a.out.T) {
+      const double v = (double)as_float(lr.x);
+      if (MULTI) {
+        const int cls = __builtin_amdgcn_readfirstlane(a.tree_class[t]);
+#pragma unroll
+        for (int k = 0; k < C::KMAX; ++k)
+          if (k == cls) acc[k] += v;
+      } else {
+        acc[0] += v;
+      }
+    }
+  }
+  if (more) next.store(tbuf[B ^ 1]);  // nobody reads tbuf[B^1] during chunk c
+  lds_barrier();
+}
+
+// Writes the leaf ids of G = 4 TC consecutive trees (held in registers, one
+// row per lane) as whole row segments: each wave passes its rows through a
+// 16-row LDS staging area (16-byte blocks XOR-swizzled by row to spread
+// banks) so that every store instruction writes G*4-byte segments of 64*16/G
+// rows instead of one 16-byte piece of 64 rows.
+template <int G>
+__device__ __forceinline__ void flush_ids(const FastArgs &a, int4 *stage, const int32_t (&ids)[G], int64_t r0w,
+                                          int t0) {
+  constexpr int NB = G / 4;  // 16-byte blocks per row segment
+  const int lane = threadIdx.x & 63;
+  const int ntrees = min(G, a.out.T - t0);
+  if (a.ids_vec) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      if ((lane >> 4) == p) {
+        const int r = lane & 15;
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          stage[r * NB + (b ^ (r & (NB - 1)))] = make_int4(ids[4 * b], ids[4 * b + 1], ids[4 * b + 2], ids[4 * b + 3]);
+      }
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int i = 0; i < (16 * NB + 63) / 64; ++i) {
+        const int q = i * 64 + lane;
+        const int r = q / NB;
+        const int b = q % NB;
+        const int64_t grow = r0w + 16 * p + r;
+        if (q < 16 * NB && grow < a.n_rows && 4 * b < ntrees) {
+          const int4 v = stage[r * NB + (b ^ (r & (NB - 1)))];
+          *reinterpret_cast<int4 *>(a.leaf_ids + grow * a.out.T + t0 + 4 * b) = v;
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  } else {
+    const int64_t row = r0w + lane;
+    if (row < a.n_rows) {
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+        if (g < ntrees) a.leaf_ids[row * a.out.T + t0 + g] = ids[g];
+    }
+  }
+}
+
+template <int MODE, int LG, bool MULTI, int ROWS>
+__global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
+  using C = FastCfg<MODE, LG, MULTI>;
+  constexpr int G = 4 * C::TC;
+  __shared__ __align__(16) uint4 tbuf[2][C::CHUNK16];
+  __shared__ __align__(16) int4 idstage[ROWS / 64][16 * (G / 4)];
+  extern __shared__ __align__(16) float fxs[];  // [F][ROWS]
+  const int tid = threadIdx.x;
+  const int64_t r0 = (int64_t)blockIdx.x * ROWS;
+  const int64_t row = r0 + tid;
+  const bool valid = row < a.n_rows;
+  {
+    ChunkPrefetch<ROWS, C::CHUNK16> first;
+    first.load(a.blocks);
+    first.store(tbuf[0]);
+  }
+  {  // each lane copies its own row into column tid of the tile (and only
+     // ever reads that column back, so the tile needs no barrier)
+    const float *src = a.X + (valid ? row : r0) * a.F;
+    if ((a.F & 3) == 0 && (reinterpret_cast<uintptr_t>(a.X) & 15) == 0) {
+      for (int f = 0; f < a.F; f += 4) {
+        const float4 v = valid ? *reinterpret_cast<const float4 *>(src + f) : make_float4(0, 0, 0, 0);
+        fxs[(f + 0) * ROWS + tid] = v.x;
+        fxs[(f + 1) * ROWS + tid] = v.y;
+        fxs[(f + 2) * ROWS + tid] = v.z;
+        fxs[(f + 3) * ROWS + tid] = v.w;
+      }
+    } else {
+      for (int f = 0; f < a.F; ++f) fxs[f * ROWS + tid] = valid ? src[f] : 0.0f;
+    }
+  }
+  lds_barrier();
+  const uint32_t lane4 = (uint32_t)tid * 4u;
+  double acc[C::KMAX];
+#pragma unroll
+  for (int k = 0; k < C::KMAX; ++k) acc[k] = 0.0;
+  int32_t ids[G];
+  const int64_t r0w = r0 + (tid & ~63);
+  for (int c = 0; c < a.n_chunks; c += 4) {  // chunk count is a multiple of 4
+    fast_chunk<MODE, LG, MULTI, ROWS, 0, 0>(a, c, tbuf, fxs, lane4, acc, ids);
+    fast_chunk<MODE, LG, MULTI, ROWS, 1, 1>(a, c + 1, tbuf, fxs, lane4, acc, ids);
+    fast_chunk<MODE, LG, MULTI, ROWS, 0, 2>(a, c + 2, tbuf, fxs, lane4, acc, ids);
+    fast_chunk<MODE, LG, MULTI, ROWS, 1, 3>(a, c + 3, tbuf, fxs, lane4, acc, ids);
+    if (a.leaf_ids) flush_ids<G>(a, idstage[tid >> 6], ids, r0w, c * C::TC);
+  }
+  if (valid) {
+    finish_row<C::KMAX>(a.out, acc, row);
+  }
+}
+
+
+template <int MODE, bool MULTI, int ROWS, int LG = 1>
+FastFn pick_fast(int lg) {
+  if constexpr (LG > kFastMaxLgFor<MODE>) {
+    return nullptr;
+  } else {
+    if (lg == LG) return fast_kernel<MODE, LG, MULTI, ROWS>;
+    return pick_fast<MODE, MULTI, ROWS, LG + 1>(lg);
+  }
+}
+
+}  // namespace
+}  // namespace hb

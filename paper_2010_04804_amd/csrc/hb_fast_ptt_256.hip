@@ -1,0 +1,11 @@
+// hb_fast_ptt_256.hip -- instantiations of the fast PerfectTreeTraversal kernel
+// for 256-row workgroups (one translation unit each, so they build in parallel).
+#include "hb_fast.h"
+
+namespace hb {
+
+FastFn fast_ptt_kernel_256(int lg, bool multi) {
+  return multi ? pick_fast<0, true, 256>(lg) : pick_fast<0, false, 256>(lg);
+}
+
+}  // namespace hb

@@ -1,0 +1,11 @@
+// hb_fast_ptt_512.hip -- instantiations of the fast PerfectTreeTraversal kernel
+// for 512-row workgroups (one translation unit each, so they build in parallel).
+#include "hb_fast.h"
+
+namespace hb {
+
+FastFn fast_ptt_kernel_512(int lg, bool multi) {
+  return multi ? pick_fast<0, true, 512>(lg) : pick_fast<0, false, 512>(lg);
+}
+
+}  // namespace hb

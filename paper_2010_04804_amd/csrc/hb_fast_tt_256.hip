@@ -1,0 +1,11 @@
+// hb_fast_tt_256.hip -- instantiations of the fast TreeTraversal kernel
+// for 256-row workgroups (one translation unit each, so they build in parallel).
+#include "hb_fast.h"
+
+namespace hb {
+
+FastFn fast_tt_kernel_256(int lg, bool multi) {
+  return multi ? pick_fast<1, true, 256>(lg) : pick_fast<1, false, 256>(lg);
+}
+
+}  // namespace hb

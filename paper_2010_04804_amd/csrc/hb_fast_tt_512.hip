@@ -1,0 +1,11 @@
+// hb_fast_tt_512.hip -- instantiations of the fast TreeTraversal kernel
+// for 512-row workgroups (one translation unit each, so they build in parallel).
+#include "hb_fast.h"
+
+namespace hb {
+
+FastFn fast_tt_kernel_512(int lg, bool multi) {
+  return multi ? pick_fast<1, true, 512>(lg) : pick_fast<1, false, 512>(lg);
+}
+
+}  // namespace hb

@@ -16,6 +16,28 @@ namespace hb {
 // of a gfx950 CU less the leaf-id staging buffer.
 constexpr int64_t kTreeLdsLimit = 160 * 1024 - 4 * 1024;
 
+// Packed per-tree blocks for the fast traversal kernels (scalar leaves).
+// A tree's block holds 2^lg node records followed by 2^lg leaf records
+// {value bits, caller id} (8 bytes each):
+//   PTT (mode 0, lg = D): node record p = {threshold bits, feature} for heap
+//     index p in [1, 2^D) (slot 0 unused); the leaf record of heap index
+//     a in [2^D, 2^(D+1)) sits at byte 8a of the block.
+//   TT (mode 1, 2^lg >= nodes): node record c = {threshold bits, feature,
+//     16 * left child, 16 * right child} (16 bytes; a leaf points to itself
+//     on both sides); the leaf record of node c sits at 16 * 2^lg + 8c.
+// Blocks are grouped in chunks of fast_tc() trees staged through LDS; the
+// tree count is padded with zero blocks to a multiple of four chunks.
+constexpr int kFastTableLds = 64 * 1024;
+constexpr int fast_node_bytes(int mode) { return mode == 0 ? 8 : 16; }
+constexpr int fast_tree_bytes(int mode, int lg) { return (1 << lg) * (fast_node_bytes(mode) + 8); }
+constexpr int fast_tc(int tree_bytes) {
+  return 2 * 8 * tree_bytes <= kFastTableLds   ? 8
+         : 2 * 4 * tree_bytes <= kFastTableLds ? 4
+         : 2 * 2 * tree_bytes <= kFastTableLds ? 2
+                                                : 1;
+}
+constexpr int kFastMaxLg = 12;
+
 // Ensemble-wide parameters every kernel needs.
 struct EnsembleDev {
   int32_t n_trees, n_features, n_outputs, leaf_dim;
@@ -32,6 +54,8 @@ struct PttDev {
   const float *leaf_value;  // [T][2^D][leaf_dim]
   const int32_t *leaf_id;   // [T][2^D] caller-local node id
   int32_t depth;            // D
+  const uint4 *fast;        // packed blocks (mode 0, lg = D), or nullptr
+  int32_t fast_chunks;
 };
 
 // TreeTraversal tensors (Table 5, Algorithm 2), breadth-first per tree with
@@ -44,6 +68,9 @@ struct TtDev {
   const int32_t *leaf_id;   // [T][n_pad] caller-local node id
   int32_t n_pad;
   int32_t max_depth;
+  const uint4 *fast;        // packed blocks (mode 1), or nullptr
+  int32_t fast_lg;
+  int32_t fast_chunks;
 };
 
 // GEMM tensors (Table 3, Algorithm 1). Internal nodes in breadth-first order

@@ -20,7 +20,7 @@
 #include <cstdint>
 #include <string>
 
-#include "hb_internal.h"
+#include "hb_device.h"
 
 namespace hb {
 namespace {
@@ -28,6 +28,10 @@ namespace {
 constexpr int kRows = 256;             // rows (= threads) per workgroup
 constexpr int kXStride = kRows + 1;    // LDS row stride of the feature tile
 constexpr int kGroup = 4;              // trees advanced together per wave
+
+// LDS bytes of the feature tile, rounded up so the tables after it stay
+// 16-byte aligned for the vector copies.
+constexpr size_t xtile_bytes(int F) { return ((size_t)F * kXStride * 4 + 15) / 16 * 16; }
 
 struct TravArgs {
   const float *X;
@@ -48,46 +52,6 @@ struct TravArgs {
   int32_t lg_tc;              // log2 of trees per LDS chunk
   int32_t x_in_lds;           // informational; the template decides
 };
-
-__device__ __forceinline__ float as_float(uint32_t u) { return __uint_as_float(u); }
-
-// LDS bytes of the feature tile, rounded up so the tables after it stay
-// 16-byte aligned for the vector copies.
-__host__ __device__ constexpr size_t xtile_bytes(int F) { return ((size_t)F * kXStride * 4 + 15) / 16 * 16; }
-
-// Aggregated margin -> transformed score, in double precision.
-template <int KMAX>
-__device__ __forceinline__ void finish_row(const TravArgs &a, const double (&acc)[KMAX], int64_t row) {
-  double s[KMAX];
-#pragma unroll
-  for (int k = 0; k < KMAX; ++k) {
-    double v = acc[k];
-    if (a.aggregation == HB_AGG_MEAN) v /= (double)a.T;
-    if (a.base_score && k < a.K) v += (double)a.base_score[k];
-    s[k] = v;
-  }
-  if (a.transform == HB_POST_SIGMOID) {
-#pragma unroll
-    for (int k = 0; k < KMAX; ++k) s[k] = 1.0 / (1.0 + exp(-s[k]));
-  } else if (a.transform == HB_POST_SOFTMAX) {
-    double m = s[0];
-#pragma unroll
-    for (int k = 1; k < KMAX; ++k)
-      if (k < a.K) m = fmax(m, s[k]);
-    double z = 0.0;
-#pragma unroll
-    for (int k = 0; k < KMAX; ++k)
-      if (k < a.K) {
-        s[k] = exp(s[k] - m);
-        z += s[k];
-      }
-#pragma unroll
-    for (int k = 0; k < KMAX; ++k) s[k] /= z;
-  }
-#pragma unroll
-  for (int k = 0; k < KMAX; ++k)
-    if (k < a.K) a.scores[row * a.K + k] = (float)s[k];
-}
 
 template <bool PERFECT, bool X_LDS, int KMAX, bool LEAF_VEC>
 __global__ __launch_bounds__(kRows) void traverse_kernel(TravArgs a) {
@@ -205,9 +169,10 @@ __global__ __launch_bounds__(kRows) void traverse_kernel(TravArgs a) {
       }
     }
   }
-  if (valid) finish_row<KMAX>(a, acc, row);
+  if (valid) finish_row<KMAX>(OutArgs{a.scores, a.T, a.K, a.aggregation, a.transform, a.base_score}, acc, row);
   (void)xrow;
 }
+
 
 using KernelFn = void (*)(TravArgs);
 
@@ -293,6 +258,59 @@ int launch_traverse(bool perfect, TravArgs a, hipStream_t stream, std::string *e
   return HB_OK;
 }
 
+constexpr int kNotApplicable = 1;
+
+// Launches the fast kernel when its layout exists and its LDS fits; returns
+// kNotApplicable to fall back to traverse_kernel.
+int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t *depth,
+                const EnsembleDev &e, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
+                hipStream_t stream, std::string *err) {
+  if (!blocks || lg < 1 || lg > kFastMaxLg || e.leaf_dim != 1) return kNotApplicable;
+  const int lds_max = max_dynamic_lds(err);
+  if (lds_max <= 0) return HB_ERR_HIP;
+  const int tb = fast_tree_bytes(mode, lg);
+  const size_t table = (size_t)2 * fast_tc(tb) * tb;
+  // static LDS: the two chunk buffers and the leaf-id staging (rows x 4 TC ids);
+  // dynamic LDS: the feature tile (F x rows floats)
+  const int tc = fast_tc(tb);
+  auto fits = [&](int rows) {
+    return table + (size_t)rows * 4 * tc + (size_t)e.n_features * rows * 4 <= (size_t)lds_max;
+  };
+  int rows = 512;
+  if (!fits(rows) || n_rows < 64 * 512) rows = 256;
+  if (!fits(rows)) return kNotApplicable;
+  const size_t xbytes = (size_t)e.n_features * rows * 4;
+  const bool multi = e.n_outputs > 1;
+  FastFn fn = mode == 0 ? (rows == 512 ? fast_ptt_kernel_512(lg, multi) : fast_ptt_kernel_256(lg, multi))
+                        : (rows == 512 ? fast_tt_kernel_512(lg, multi) : fast_tt_kernel_256(lg, multi));
+  if (!fn) return kNotApplicable;
+  FastArgs a{};
+  a.X = X;
+  a.n_rows = n_rows;
+  a.F = e.n_features;
+  a.leaf_ids = leaf_ids;
+  a.out = OutArgs{scores, e.n_trees, e.n_outputs, e.aggregation, e.transform, e.base_score};
+  a.tree_class = e.tree_class;
+  a.blocks = blocks;
+  a.tree_depth = depth;
+  a.n_chunks = chunks;
+  a.ids_vec = (e.n_trees % 4 == 0) && ((reinterpret_cast<uintptr_t>(leaf_ids) & 15) == 0);
+  hipError_t rc = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)xbytes);
+  if (rc != hipSuccess) {
+    *err = std::string("hipFuncSetAttribute: ") + hipGetErrorString(rc);
+    return HB_ERR_HIP;
+  }
+  const int64_t blocks_n = (n_rows + rows - 1) / rows;
+  hipLaunchKernelGGL(fn, dim3((unsigned)blocks_n), dim3(rows), xbytes, stream, a);
+  rc = hipGetLastError();
+  if (rc != hipSuccess) {
+    *err = std::string("kernel launch: ") + hipGetErrorString(rc);
+    return HB_ERR_HIP;
+  }
+  return HB_OK;
+}
+
 TravArgs common_args(const EnsembleDev &e, const float *X, int64_t n, float *scores, int32_t *ids) {
   TravArgs a{};
   a.X = X;
@@ -318,6 +336,10 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
     *err = "PTT tables missing";
     return HB_ERR_INVALID_ARG;
   }
+  if (n_rows <= 0) return HB_OK;
+  const int rc = launch_fast(0, t.depth, t.fast, t.fast_chunks, nullptr, e, X, n_rows, scores, leaf_ids,
+                             stream, err);
+  if (rc != kNotApplicable) return rc;
   TravArgs a = common_args(e, X, n_rows, scores, leaf_ids);
   a.node = t.node;
   a.leaf_value = t.leaf_value;
@@ -339,6 +361,10 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
     *err = "TT node slots must be even";
     return HB_ERR_INVALID_ARG;
   }
+  if (n_rows <= 0) return HB_OK;
+  const int rc = launch_fast(1, t.fast_lg, t.fast, t.fast_chunks, t.depth, e, X, n_rows, scores, leaf_ids,
+                             stream, err);
+  if (rc != kNotApplicable) return rc;
   TravArgs a = common_args(e, X, n_rows, scores, leaf_ids);
   a.node = t.node;
   a.leaf_value = t.leaf_value;
