@@ -54,6 +54,50 @@ __device__ __forceinline__ void finish_row(const OutArgs &a, const double (&acc)
     if (k < a.K) a.scores[row * a.K + k] = (float)s[k];
 }
 
+// Writes the leaf ids of G consecutive trees (held in registers, one row per
+// lane) as whole row segments: each wave passes its rows through a
+// 16-row LDS staging area (16-byte blocks XOR-swizzled by row to spread
+// banks) so that every store instruction writes G*4-byte segments of 64*16/G
+// rows instead of one 16-byte piece of 64 rows.
+template <int G>
+__device__ __forceinline__ void flush_ids(int32_t *leaf_ids, int64_t n_rows, int T, bool ids_vec, int4 *stage,
+                                          const int32_t (&ids)[G], int64_t r0w, int t0) {
+  constexpr int NB = G / 4;  // 16-byte blocks per row segment
+  const int lane = threadIdx.x & 63;
+  const int ntrees = min(G, T - t0);
+  if (ids_vec) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      if ((lane >> 4) == p) {
+        const int r = lane & 15;
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          stage[r * NB + (b ^ (r & (NB - 1)))] = make_int4(ids[4 * b], ids[4 * b + 1], ids[4 * b + 2], ids[4 * b + 3]);
+      }
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int i = 0; i < (16 * NB + 63) / 64; ++i) {
+        const int q = i * 64 + lane;
+        const int r = q / NB;
+        const int b = q % NB;
+        const int64_t grow = r0w + 16 * p + r;
+        if (q < 16 * NB && grow < n_rows && 4 * b < ntrees) {
+          const int4 v = stage[r * NB + (b ^ (r & (NB - 1)))];
+          *reinterpret_cast<int4 *>(leaf_ids + grow * T + t0 + 4 * b) = v;
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  } else {
+    const int64_t row = r0w + lane;
+    if (row < n_rows) {
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+        if (g < ntrees) leaf_ids[row * T + t0 + g] = ids[g];
+    }
+  }
+}
+
 // ---- fast traversal kernels (instantiated in hb_fast_ptt.hip / hb_fast_tt.hip)
 
 // Rows (= threads) per workgroup: 512 when the row tile fits next to the

@@ -135,50 +135,6 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   lds_barrier();
 }
 
-// Writes the leaf ids of G = 4 TC consecutive trees (held in registers, one
-// row per lane) as whole row segments: each wave passes its rows through a
-// 16-row LDS staging area (16-byte blocks XOR-swizzled by row to spread
-// banks) so that every store instruction writes G*4-byte segments of 64*16/G
-// rows instead of one 16-byte piece of 64 rows.
-template <int G>
-__device__ __forceinline__ void flush_ids(const FastArgs &a, int4 *stage, const int32_t (&ids)[G], int64_t r0w,
-                                          int t0) {
-  constexpr int NB = G / 4;  // 16-byte blocks per row segment
-  const int lane = threadIdx.x & 63;
-  const int ntrees = min(G, a.out.T - t0);
-  if (a.ids_vec) {
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      if ((lane >> 4) == p) {
-        const int r = lane & 15;
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-          stage[r * NB + (b ^ (r & (NB - 1)))] = make_int4(ids[4 * b], ids[4 * b + 1], ids[4 * b + 2], ids[4 * b + 3]);
-      }
-      __builtin_amdgcn_wave_barrier();
-#pragma unroll
-      for (int i = 0; i < (16 * NB + 63) / 64; ++i) {
-        const int q = i * 64 + lane;
-        const int r = q / NB;
-        const int b = q % NB;
-        const int64_t grow = r0w + 16 * p + r;
-        if (q < 16 * NB && grow < a.n_rows && 4 * b < ntrees) {
-          const int4 v = stage[r * NB + (b ^ (r & (NB - 1)))];
-          *reinterpret_cast<int4 *>(a.leaf_ids + grow * a.out.T + t0 + 4 * b) = v;
-        }
-      }
-      __builtin_amdgcn_wave_barrier();
-    }
-  } else {
-    const int64_t row = r0w + lane;
-    if (row < a.n_rows) {
-#pragma unroll
-      for (int g = 0; g < G; ++g)
-        if (g < ntrees) a.leaf_ids[row * a.out.T + t0 + g] = ids[g];
-    }
-  }
-}
-
 template <int MODE, int LG, bool MULTI, int ROWS>
 __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   using C = FastCfg<MODE, LG, MULTI>;
@@ -222,7 +178,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
     fast_chunk<MODE, LG, MULTI, ROWS, 1, 1>(a, c + 1, tbuf, fxs, lane4, acc, ids);
     fast_chunk<MODE, LG, MULTI, ROWS, 0, 2>(a, c + 2, tbuf, fxs, lane4, acc, ids);
     fast_chunk<MODE, LG, MULTI, ROWS, 1, 3>(a, c + 3, tbuf, fxs, lane4, acc, ids);
-    if (a.leaf_ids) flush_ids<G>(a, idstage[tid >> 6], ids, r0w, c * C::TC);
+    if (a.leaf_ids) flush_ids<G>(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, idstage[tid >> 6], ids, r0w, c * C::TC);
   }
   if (valid) {
     finish_row<C::KMAX>(a.out, acc, row);

@@ -1,0 +1,336 @@
+// hb_gemm.hip -- the GEMM strategy (Algorithm 1 with the tensors of Table 3,
+// Sec. 4.1) on the int8 matrix cores of gfx950.
+//
+// Algorithm 1 multiplies X by A (a selection of one feature per decision
+// node), compares with B, multiplies the 0/1 outcome by C (+1 for leaves in
+// a node's left subtree, -1 in its right subtree), tests equality with D and
+// maps the one-hot leaf through E. Here:
+//   * X.A < B is evaluated as a gather and a compare (never a float product,
+//     which would turn a NaN or infinite feature into NaN for every node);
+//     the outcome is encoded as the int8 value 64 (true) or 0;
+//   * the path product runs as v_mfma_i32_16x16x64_i8 with the A operand
+//     4*C^T (leaves x decision nodes) and the B operand the encoded outcomes
+//     (decision nodes x rows), so every product term is 0 or +-256;
+//   * the accumulator starts at bias[l] = l - 256*D[l], so it ends at
+//     256*((T.C)_l - D_l) + l. (T.C)_l <= D_l with equality only for the
+//     selected leaf, hence the selected leaf's column is the unique
+//     non-negative value, and the maximum over columns is that column index:
+//     the "== D" test and the leaf lookup of the one-hot product collapse
+//     into one v_max per accumulator element;
+//   * the leaf's value and caller id are then gathered (E of Table 3).
+// Lane layout of v_mfma_i32_16x16x64_i8 (checked on the device): lane l
+// supplies A[m = l%16][k = 16(l/16) .. +15] and B[k = 16(l/16) .. +15][n = l%16]
+// and receives D[4(l/16) + i][n = l%16], i = 0..3.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <string>
+
+#include "hb_device.h"
+
+namespace hb {
+namespace {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kGRows = 256;                // rows per workgroup: 4 waves x 64 rows
+constexpr int kGXStride = kGRows + 8;      // feature-tile stride (spreads lane groups over banks)
+constexpr int kCtPad = 16;                 // bytes appended to each C^T row in LDS
+constexpr int kTG = 2;                     // trees per staged chunk of node records
+constexpr int kIdGroup = 32;               // trees per leaf-id flush
+
+struct GemmArgs {
+  const float *X;
+  int64_t n_rows;
+  int32_t F;
+  int32_t *leaf_ids;
+  OutArgs out;
+  const int32_t *tree_class;
+  int32_t LD;
+  const uint2 *node;        // [T][k_pad] {threshold bits, feature}
+  const int32_t *shape;     // [T]
+  const int8_t *ct;         // [S][l_pad][k_pad]
+  const int32_t *bias;      // [S][l_pad]
+  const float *leaf_value;  // [T][l_pad][LD]
+  const int32_t *leaf_id;   // [T][l_pad]
+  int32_t k_pad, l_pad;
+  int32_t ids_vec;
+};
+
+// LDS bytes of one tree's node records: groups of 16 records (128 B) are
+// followed by 16 B of padding, so the four lane groups of a wave, which read
+// 16 consecutive records each, start 36 banks apart.
+__host__ __device__ constexpr int node_lds_bytes(int k_pad) { return k_pad * 9; }
+__host__ __device__ constexpr int node_lds_off(int k) { return k * 8 + (k / 16) * 16; }
+
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+__device__ __forceinline__ int hmax4(v4i v) { return max(max(v[0], v[1]), max(v[2], v[3])); }
+
+// Stages the node records of trees [t0, t0 + kTG) (clamped to T) into `dst`
+// with the padded layout; 16 B (two records) per lane per step.
+__device__ __forceinline__ void stage_nodes(const GemmArgs &a, int t0, unsigned char *dst) {
+  const int per_tree16 = a.k_pad / 2;
+  const int total = kTG * per_tree16;
+  for (int u = threadIdx.x; u < total; u += kGRows) {
+    const int g = u / per_tree16;
+    const int q = u - g * per_tree16;
+    const int t = min(t0 + g, a.out.T - 1);
+    const u32x4 v = reinterpret_cast<const u32x4 *>(a.node + (size_t)t * a.k_pad)[q];
+    *reinterpret_cast<u32x4 *>(dst + g * node_lds_bytes(a.k_pad) + node_lds_off(2 * q)) = v;
+  }
+}
+
+// KB: 64-node slices of the decision-node dimension; KMODE: 0 scalar leaves
+// and one output, 1 scalar leaves with a class per tree, 2 vector leaves.
+template <int KB, bool CT_LDS, bool X_LDS, int KMODE>
+__global__ __launch_bounds__(kGRows) void gemm_kernel(GemmArgs a) {
+  constexpr int KMAX = KMODE == 0 ? 1 : HB_MAX_OUTPUTS;
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ __align__(16) int4 idstage[kGRows / 64][16 * (kIdGroup / 4)];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int g4 = lane >> 4;  // lane group: k slice of the operands, leaf quad of the result
+  const int r16 = lane & 15;
+  const int wave = tid >> 6;
+  const int64_t r0 = (int64_t)blockIdx.x * kGRows;
+  const int64_t r0w = r0 + wave * 64;
+  const int64_t row = r0w + lane;  // the row this lane owns after the reduction
+  const bool valid = row < a.n_rows;
+  const int LT = a.l_pad / 16;
+  const int ct_stride = a.k_pad + kCtPad;
+
+  // ---- LDS carve-up: [feature tile][C^T][bias][node chunks x2]
+  size_t off = 0;
+  float *xs = reinterpret_cast<float *>(smem);
+  if (X_LDS) off += ((size_t)a.F * kGXStride * 4 + 15) / 16 * 16;
+  int8_t *cts = reinterpret_cast<int8_t *>(smem + off);
+  int32_t *bias_s = nullptr;
+  if (CT_LDS) {
+    off += (size_t)a.l_pad * ct_stride;
+    bias_s = reinterpret_cast<int32_t *>(smem + off);
+    off += (size_t)a.l_pad * 4;
+  }
+  unsigned char *nodes = smem + off;
+  const int chunk_bytes = kTG * node_lds_bytes(a.k_pad);
+
+  if (X_LDS) {
+    for (int f = 0; f < a.F; ++f)
+      xs[f * kGXStride + tid] = (r0 + tid < a.n_rows) ? a.X[(r0 + tid) * a.F + f] : 0.0f;
+  }
+  if (CT_LDS) {
+    const int row16 = a.k_pad / 16;
+    for (int u = tid; u < a.l_pad * row16; u += kGRows) {
+      const int l = u / row16;
+      const int q = u - l * row16;
+      *reinterpret_cast<u32x4 *>(cts + (size_t)l * ct_stride + q * 16) =
+          reinterpret_cast<const u32x4 *>(a.ct + (size_t)l * a.k_pad)[q];
+    }
+    for (int u = tid; u < a.l_pad; u += kGRows) bias_s[u] = a.bias[u];
+  }
+  stage_nodes(a, 0, nodes);
+  lds_sync();
+
+  double acc[KMAX];
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) acc[k] = 0.0;
+  int32_t ids[kIdGroup];
+#pragma unroll
+  for (int q = 0; q < kIdGroup; ++q) ids[q] = 0;
+
+  const float *xrow[4];
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) {
+    const int64_t rr = r0w + rt * 16 + r16;
+    xrow[rt] = a.X + (rr < a.n_rows ? rr : a.n_rows - 1) * a.F;
+  }
+
+  const int n_chunks = (a.out.T + kTG - 1) / kTG;
+  for (int c = 0; c < n_chunks; ++c) {
+    const unsigned char *cur = nodes + (c & 1) * chunk_bytes;
+    for (int tg = 0; tg < kTG; ++tg) {
+      const int t = c * kTG + tg;
+      if (t >= a.out.T) break;  // uniform
+      const unsigned char *nb = cur + tg * node_lds_bytes(a.k_pad);
+      // ---- B operand: encoded outcomes of this lane's 16 nodes per slice, 4 row tiles
+      v4i bop[4][KB];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        uint2 rec[16];
+        const unsigned char *rb = nb + node_lds_off(kb * 64 + 16 * g4);
+#pragma unroll
+        for (int j = 0; j < 16; j += 2) {
+          const u32x4 v = *reinterpret_cast<const u32x4 *>(rb + j * 8);
+          rec[j] = make_uint2(v[0], v[1]);
+          rec[j + 1] = make_uint2(v[2], v[3]);
+        }
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            uint32_t w = 0;
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              const uint2 rr = rec[4 * q + b];
+              const float x = X_LDS ? xs[rr.y * kGXStride + wave * 64 + rt * 16 + r16] : xrow[rt][rr.y];
+              w |= (x < as_float(rr.x) ? 0x40u : 0u) << (8 * b);
+            }
+            bop[rt][kb][q] = (int)w;
+          }
+        }
+      }
+      // ---- path product and "== D": running maximum of 256 (T.C - D) + l
+      const int s = CT_LDS ? 0 : a.shape[t];
+      const int8_t *ctg = a.ct + (size_t)s * a.l_pad * a.k_pad;
+      const int32_t *bg = a.bias + (size_t)s * a.l_pad;
+      int best[4] = {INT_MIN, INT_MIN, INT_MIN, INT_MIN};
+      for (int lt = 0; lt < LT; ++lt) {
+        v4i b4;
+        if (CT_LDS)
+          b4 = *reinterpret_cast<const v4i *>(bias_s + lt * 16 + 4 * g4);
+        else
+          b4 = *reinterpret_cast<const v4i *>(bg + lt * 16 + 4 * g4);
+        v4i d[4] = {b4, b4, b4, b4};
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+          v4i av;
+          if (CT_LDS)
+            av = *reinterpret_cast<const v4i *>(cts + (size_t)(lt * 16 + r16) * ct_stride + kb * 64 + 16 * g4);
+          else
+            av = *reinterpret_cast<const v4i *>(ctg + (size_t)(lt * 16 + r16) * a.k_pad + kb * 64 + 16 * g4);
+#pragma unroll
+          for (int rt = 0; rt < 4; ++rt) d[rt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bop[rt][kb], d[rt], 0, 0, 0);
+        }
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) best[rt] = max(best[rt], hmax4(d[rt]));
+      }
+      // rows are spread over the four lane groups: combine them
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        best[rt] = max(best[rt], __shfl_xor(best[rt], 16));
+        best[rt] = max(best[rt], __shfl_xor(best[rt], 32));
+      }
+      // lane l owns row l of the wave (row tile l/16, row l%16)
+      int col = g4 == 0 ? best[0] : g4 == 1 ? best[1] : g4 == 2 ? best[2] : best[3];
+      col = min(max(col, 0), a.l_pad - 1);  // a valid tree always yields a column in range
+      const size_t lrec = (size_t)t * a.l_pad + (size_t)col;
+      if (KMODE == 2) {
+#pragma unroll
+        for (int k = 0; k < KMAX; ++k)
+          if (k < a.LD) acc[k] += (double)a.leaf_value[lrec * a.LD + k];
+      } else if (KMODE == 0) {
+        acc[0] += (double)a.leaf_value[lrec];
+      } else {
+        const int cls = __builtin_amdgcn_readfirstlane(a.tree_class[t]);
+        const double v = (double)a.leaf_value[lrec];
+#pragma unroll
+        for (int k = 0; k < KMAX; ++k)
+          if (k == cls) acc[k] += v;
+      }
+      const int slot = t % kIdGroup;
+#pragma unroll
+      for (int q = 0; q < kIdGroup; ++q)
+        if (q == slot) ids[q] = a.leaf_id[lrec];
+      if (a.leaf_ids && (slot == kIdGroup - 1 || t == a.out.T - 1))
+        flush_ids<kIdGroup>(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, idstage[wave], ids, r0w, t - slot);
+    }
+    if (c + 1 < n_chunks) {
+      lds_sync();  // everyone is done with the other buffer (chunk c - 1)
+      stage_nodes(a, (c + 1) * kTG, nodes + ((c + 1) & 1) * chunk_bytes);
+      lds_sync();
+    }
+  }
+  if (valid) finish_row<KMAX>(a.out, acc, row);
+}
+
+using GemmFn = void (*)(GemmArgs);
+
+template <int KB, bool CT, bool XL>
+GemmFn pick_mode(int kmode) {
+  if (kmode == 0) return gemm_kernel<KB, CT, XL, 0>;
+  if (kmode == 1) return gemm_kernel<KB, CT, XL, 1>;
+  return gemm_kernel<KB, CT, XL, 2>;
+}
+
+template <int KB>
+GemmFn pick_gemm(bool ct, bool xl, int kmode) {
+  if (ct) return xl ? pick_mode<KB, true, true>(kmode) : pick_mode<KB, true, false>(kmode);
+  return xl ? pick_mode<KB, false, true>(kmode) : pick_mode<KB, false, false>(kmode);
+}
+
+}  // namespace
+
+int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t n_rows, float *scores,
+                int32_t *leaf_ids, hipStream_t stream, std::string *err) {
+  if (!t.node || !t.shape || !t.ct || !t.bias || !t.leaf_value || !t.leaf_id) {
+    *err = "GEMM tables missing";
+    return HB_ERR_INVALID_ARG;
+  }
+  if (t.k_pad % 64 || t.k_pad < 64 || t.k_pad > 256 || t.l_pad % 16 || t.l_pad < 16 || t.l_pad > 256) {
+    *err = "GEMM tables have an unexpected shape";
+    return HB_ERR_INVALID_ARG;
+  }
+  if (n_rows <= 0) return HB_OK;
+  int dev = 0, lds_max = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) {
+    *err = "hipDeviceGetAttribute failed";
+    return HB_ERR_HIP;
+  }
+  const size_t static_lds = (size_t)(kGRows / 64) * 16 * (kIdGroup / 4) * 16;
+  const size_t nodes = 2 * (size_t)kTG * node_lds_bytes(t.k_pad);
+  const size_t ct_bytes = (size_t)t.l_pad * (t.k_pad + kCtPad) + (size_t)t.l_pad * 4;
+  const size_t x_bytes = ((size_t)e.n_features * kGXStride * 4 + 15) / 16 * 16;
+  const size_t budget = (size_t)lds_max - static_lds;
+  const bool ct = t.n_shapes == 1 && ct_bytes + nodes <= budget;
+  const bool xl = (ct ? ct_bytes : 0) + nodes + x_bytes <= budget;
+  const size_t dyn = (xl ? x_bytes : 0) + (ct ? ct_bytes : 0) + nodes;
+  if (dyn > budget) {
+    *err = "GEMM node tables do not fit in LDS";
+    return HB_ERR_UNSUPPORTED;
+  }
+  const int kmode = e.leaf_dim > 1 ? 2 : (e.n_outputs > 1 ? 1 : 0);
+  const int kb = t.k_pad / 64;
+  GemmFn fn = kb == 1 ? pick_gemm<1>(ct, xl, kmode)
+              : kb == 2 ? pick_gemm<2>(ct, xl, kmode)
+              : kb == 3 ? pick_gemm<3>(ct, xl, kmode)
+                        : pick_gemm<4>(ct, xl, kmode);
+  GemmArgs a{};
+  a.X = X;
+  a.n_rows = n_rows;
+  a.F = e.n_features;
+  a.leaf_ids = leaf_ids;
+  a.out = OutArgs{scores, e.n_trees, e.n_outputs, e.aggregation, e.transform, e.base_score};
+  a.tree_class = e.tree_class;
+  a.LD = e.leaf_dim;
+  a.node = t.node;
+  a.shape = t.shape;
+  a.ct = t.ct;
+  a.bias = t.bias;
+  a.leaf_value = t.leaf_value;
+  a.leaf_id = t.leaf_id;
+  a.k_pad = t.k_pad;
+  a.l_pad = t.l_pad;
+  a.ids_vec = (e.n_trees % 4 == 0) && ((reinterpret_cast<uintptr_t>(leaf_ids) & 15) == 0);
+  hipError_t rc = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+  if (rc != hipSuccess) {
+    *err = std::string("hipFuncSetAttribute: ") + hipGetErrorString(rc);
+    return HB_ERR_HIP;
+  }
+  const int64_t blocks = (n_rows + kGRows - 1) / kGRows;
+  hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kGRows), dyn, stream, a);
+  rc = hipGetLastError();
+  if (rc != hipSuccess) {
+    *err = std::string("kernel launch: ") + hipGetErrorString(rc);
+    return HB_ERR_HIP;
+  }
+  return HB_OK;
+}
+
+}  // namespace hb

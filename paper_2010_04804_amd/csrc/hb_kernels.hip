@@ -375,10 +375,5 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
   return launch_traverse(false, a, stream, err);
 }
 
-int launch_gemm(const EnsembleDev &, const GemmDev &, const float *, int64_t, float *, int32_t *,
-                hipStream_t, std::string *err) {
-  *err = "GEMM strategy not built yet";
-  return HB_ERR_UNSUPPORTED;
-}
 
 }  // namespace hb
