@@ -1,38 +1,66 @@
 """Throughput of batched tree-ensemble scoring on one MI355X.
 
 Default workload: the GBDT binary classifier of 500 perfect trees of depth 8
-over 28 features, scoring a batch of 1,000,000 rows (scores and per-tree leaf
-ids), strategy chosen by the selector. One step = one hb_predict over the
-whole batch with inputs already resident in HBM.
+over 28 features (sigmoid of the summed leaves), scoring a resident batch of
+1,000,000 rows into scores and per-tree leaf ids, with the strategy the
+selector picks. One step is one hb_predict over the whole batch.
 
-Prints one JSON line (rank 0, N = 1) with rows/s, the roofline of the
-dominant kernel measured with HIP events on the launch stream, and the CPU
-oracle's rate on a bounded sample of the same workload.
+Prints one JSON line with rows/s, the roofline of the dominant kernel (its
+average launch time measured with HIP events on the launch stream), the other
+two strategies timed on the same workload, and the CPU oracle's rate on a
+bounded sample of the same workload.
 """
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
-
-import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "rows/sec scored, 500-tree depth-8 ensemble, 1M rows; % HBM / MFMA peak"
-HBM_PEAK = 8.0e12            # B/s, MI355X HBM3E
-INT8_PEAK = 5.0e15           # dense int8 MFMA ops/s
-KERNEL = {"ptt": "traverse_kernel<true,...>", "tt": "traverse_kernel<false,...>",
-          "gemm": "gemm_kernel"}
+HBM_PEAK = 8.0e12   # B/s, MI355X HBM3E
+INT8_PEAK = 5.0e15  # dense int8 MFMA ops/s, MI355X
+KERNEL = {"ptt": "fast_kernel<0, D, ...> (PerfectTreeTraversal)",
+          "tt": "fast_kernel<1, lg, ...> (TreeTraversal)",
+          "gemm": "gemm_kernel<KB, ...> (GEMM, int8 MFMA)"}
+PROFILES = os.path.join(ROOT, "profiles")
+CSRC = os.path.join(ROOT, "paper_2010_04804_amd", "csrc")
 
 
-def algorithmic_bytes(info, n, F, leaves, strategy):
+def kernel_source_sha() -> str:
+    """Hash of the library sources: counter summaries recorded against another
+    hash describe a different kernel and are not reported."""
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(CSRC, "*"))):
+        with open(p, "rb") as fh:
+            h.update(os.path.basename(p).encode())
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(config: int, strategy: str, rows: int, leaves: bool):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, or None."""
+    sha = kernel_source_sha()
+    pat = re.compile(r"traffic_record: config=(\d+) strategy=(\w+) rows=(\d+) leaves=(\d) "
+                     r"source_sha=(\w+) fetch_bytes=(\d+) write_bytes=(\d+)")
+    for p in glob.glob(os.path.join(PROFILES, "*.md")):
+        for m in pat.finditer(open(p).read()):
+            if (int(m[1]), m[2], int(m[3]), int(m[4]), m[5]) == (config, strategy, rows, int(leaves), sha):
+                return int(m[6]) + int(m[7])
+    return None
+
+
+def algorithmic_bytes(info, n, leaves, strategy):
     """HBM bytes one launch must move: X read once, scores (and leaf ids)
     written once, the strategy's compiled tables read once."""
-    K, T = info["n_outputs"], info["n_trees"]
+    K, T, F = info["n_outputs"], info["n_trees"], info["n_features"]
     b = n * F * 4 + n * K * 4 + info["table_bytes"][strategy]
     if leaves:
         b += n * T * 4
@@ -40,7 +68,8 @@ def algorithmic_bytes(info, n, F, leaves, strategy):
 
 
 def gemm_ops(model, n):
-    """2 * n * sum_t |I_t| * |L_t| (the path-matrix contraction only)."""
+    """2 n sum_t |I_t| |L_t|: the path-matrix contraction of Algorithm 1 only
+    (the feature selection and the leaf gather count as zero operations)."""
     off = model["tree_node_offset"]
     tot = 0
     for t in range(model["n_trees"]):
@@ -50,16 +79,9 @@ def gemm_ops(model, n):
     return 2 * n * tot
 
 
-def gemm_available(h):
-    import paper_2010_04804_amd as hb
-    try:
-        hb.predict_ptr(h, 0, 0, 0, None, "gemm")
-        return True
-    except hb.HBError:
-        return False
-
-
 def cpu_baseline(model, cfg, seconds_target=15.0):
+    """The oracle as it stands, timed on this host on the first rows of the
+    same workload (bounded to about seconds_target of CPU time)."""
     import oracle
     from paper_2010_04804_amd import synth
 
@@ -74,7 +96,7 @@ def cpu_baseline(model, cfg, seconds_target=15.0):
     oracle.predict(model, X, leaves=True, n_threads=cores)
     dt = time.perf_counter() - t0
     return {"value": n / dt, "unit": "rows/s", "cores": cores, "kind": "oracle",
-            "sample": f"first {n} rows of the same workload, scores and leaf ids, "
+            "sample": f"first {n} rows of the same workload (scores and leaf ids), "
                       f"{dt:.1f} s on {cores} threads"}
 
 
@@ -83,17 +105,19 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2, the headline)")
     ap.add_argument("--rows", type=int, default=None)
     ap.add_argument("--strategy", default="auto", choices=["auto", "ptt", "tt", "gemm"])
-    ap.add_argument("--no-leaves", action="store_true")
+    ap.add_argument("--no-leaves", action="store_true", help="scores only")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--extra", action="store_true",
-                    help="also time scores-only and the forced GEMM strategy")
+    ap.add_argument("--only-main", action="store_true", help="skip the other strategies")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a 1 GiB device copy (to scale HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
-                                   "(rows shard across GPUs with no exchange step; see the design notes)"}))
+        print(json.dumps({"error": f"--gpus {args.gpus}: this build runs on one GPU only. Rows are "
+                                   "independent, so N GPUs would each score n/N rows with a "
+                                   "replica of the compiled tables and no exchange step."}))
         sys.exit(2)
 
     import torch
@@ -115,75 +139,76 @@ def main():
     ids = torch.empty((n, info["n_trees"]), dtype=torch.int32, device=dev) if leaves else None
     stream = torch.cuda.current_stream(dev)
 
-    def step(strat=strategy, with_ids=ids):
+    def step(strat):
         hb.predict_ptr(h, Xd.data_ptr(), n, scores.data_ptr(),
-                       with_ids.data_ptr() if with_ids is not None else None, strat, stream.cuda_stream)
+                       ids.data_ptr() if ids is not None else None, strat, stream.cuda_stream)
 
-    def timed(fn, steps, warmup):
+    def timed(strat, steps, warmup):
+        """Average launch time in ms, HIP events recorded on the launch stream."""
         for _ in range(warmup):
-            fn()
+            step(strat)
         torch.cuda.synchronize()
         ev0 = torch.cuda.Event(enable_timing=True)
         ev1 = torch.cuda.Event(enable_timing=True)
         ev0.record(stream)
         for _ in range(steps):
-            fn()
+            step(strat)
         ev1.record(stream)
         torch.cuda.synchronize()
-        return ev0.elapsed_time(ev1) / steps  # ms per launch
+        return ev0.elapsed_time(ev1) / steps
 
-    print(f"[bench] config {cfg}, {n} rows, strategy {strategy}, leaf ids {leaves}", flush=True)
-    t_wall0 = time.perf_counter()
-    ms = timed(step, args.steps, args.warmup)
-    wall = time.perf_counter() - t_wall0
-    rows_per_s = n / (ms * 1e-3)
-    F = info["n_features"]
-    if strategy == "gemm":
-        ops = gemm_ops(model, n)
-        achieved = ops / (ms * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": INT8_PEAK / 1e12, "unit": "TOP/s",
-                "frac": achieved * 1e12 / INT8_PEAK, "traffic": None,
-                "kernel": KERNEL["gemm"], "avg_launch_ms": ms, "ops_per_launch": ops}
-    else:
-        b = algorithmic_bytes(info, n, F, leaves, strategy)
+    def roofline(strat, ms):
+        if strat == "gemm":
+            ops = gemm_ops(model, n)
+            achieved = ops / (ms * 1e-3)
+            return {"bound": "mfma", "achieved": achieved / 1e12, "peak": INT8_PEAK / 1e12,
+                    "unit": "TOP/s", "frac": achieved / INT8_PEAK, "traffic": None,
+                    "kernel": KERNEL[strat], "avg_launch_ms": ms, "ops_per_launch": ops}
+        b = algorithmic_bytes(info, n, leaves, strat)
         achieved = b / (ms * 1e-3)
-        roof = {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK, "traffic": None, "kernel": KERNEL[strategy],
-                "avg_launch_ms": ms, "bytes_per_launch": b}
+        return {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK, "traffic": recorded_traffic(cfg, strat, n, leaves),
+                "kernel": KERNEL[strat], "avg_launch_ms": ms, "bytes_per_launch": b}
+
+    print(f"[bench] config {cfg}: {n} rows, strategy {strategy}, leaf ids {leaves}", flush=True)
+    t_wall = time.perf_counter()
+    ms = timed(strategy, args.steps, args.warmup)
+    t_wall = time.perf_counter() - t_wall
+    print(f"[bench] {strategy}: {ms:.4f} ms per step", flush=True)
+    stats = synth.model_stats(model)
     out = {
-        "metric": METRIC, "value": rows_per_s, "unit": "rows/s", "n_gpus": 1,
+        "metric": METRIC, "value": n / (ms * 1e-3), "unit": "rows/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-        "data": "synthetic",
+        "data": "synthetic: seeded random trees and rows of the workload's shape",
         "config": {"workload": synth.CONFIGS[cfg]["name"], "rows": n, "trees": info["n_trees"],
-                   "max_depth": info["max_depth"], "features": F, "strategy": strategy,
-                   "leaf_ids": leaves},
-        "roofline": roof,
-        "timed_wall_s": wall,
+                   "max_depth": stats["max_depth"], "features": info["n_features"],
+                   "outputs": info["n_outputs"], "strategy": strategy, "leaf_ids": leaves},
+        "roofline": roofline(strategy, ms),
+        "timed_wall_s": t_wall,
     }
-    # parity spot check of the timed outputs against the oracle (not timed)
-    import oracle
-    rows = np.random.Generator(np.random.PCG64(0)).choice(n, min(n, 2000), replace=False)
-    o_raw, o_out, o_ids = oracle.predict(model, X[rows])
-    rt = torch.from_numpy(rows).to(dev)
-    sc = scores[rt].cpu().numpy().astype(np.float64)
-    ok = bool(np.all(np.abs(sc - o_out) <= 1e-5 * (1 + np.abs(o_out))))
-    if leaves:
-        ok = ok and bool(np.array_equal(ids[rt].cpu().numpy(), o_ids))
-    out["parity_sample_ok"] = ok
-    if args.extra:
-        ms_s = timed(lambda: step(strategy, None), args.steps, args.warmup)
-        out["scores_only"] = {"ms": ms_s, "rows_per_s": n / (ms_s * 1e-3)}
-        if strategy != "gemm" and info["feasible"]["gemm"] and gemm_available(h):
-            ng = min(n, 100_000)
-            ms_g = timed(lambda: hb.predict_ptr(h, Xd.data_ptr(), ng, scores.data_ptr(),
-                                                ids.data_ptr() if ids is not None else None, "gemm",
-                                                stream.cuda_stream), max(2, args.steps // 4), 1)
-            ops = gemm_ops(model, ng)
-            out["gemm"] = {"rows": ng, "ms": ms_g, "rows_per_s": ng / (ms_g * 1e-3),
-                           "tops": ops / (ms_g * 1e-3) / 1e12,
-                           "mfma_frac": ops / (ms_g * 1e-3) / INT8_PEAK}
+    if not args.only_main:
+        others = {}
+        for s in ("ptt", "tt", "gemm"):
+            if s == strategy or not info["feasible"][s]:
+                continue
+            k = args.steps if s != "gemm" else max(2, args.steps // 5)
+            mss = timed(s, k, 1)
+            print(f"[bench] {s}: {mss:.4f} ms per step", flush=True)
+            r = roofline(s, mss)
+            others[s] = {"rows_per_s": n / (mss * 1e-3), "ms": mss, "bound": r["bound"],
+                         "achieved": r["achieved"], "unit": r["unit"], "frac": r["frac"]}
+        out["other_strategies"] = others
+    if args.copy_calibration:
+        # a plain device copy of exactly 1 GiB, to scale FETCH_SIZE / WRITE_SIZE
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = 1 << 30
     if not args.no_cpu:
+        print("[bench] timing the CPU oracle", flush=True)
         out["cpu_baseline"] = cpu_baseline(model, cfg)
     print(json.dumps(out), flush=True)
 
