@@ -255,7 +255,7 @@ void build_fast(hb_handle *h, const hb_ensemble_desc *d, const std::vector<Canon
   if (h->info.feasible[HB_STRATEGY_PTT] && D >= 1 && D <= hb::kFastMaxLg) {
     const int tb = hb::fast_tree_bytes(0, D);
     const int tc = hb::fast_tc(tb);
-    const int chunks = ((T + tc - 1) / tc + 3) / 4 * 4;  // whole groups of 4 chunks
+    const int chunks = (T + hb::kFastIdGroup - 1) / hb::kFastIdGroup * (hb::kFastIdGroup / tc);
     const size_t words = (size_t)tb / 4;
     const size_t S = (size_t)1 << D;
     h->ptt_fast.assign((size_t)chunks * tc * words, 0u);
@@ -279,7 +279,7 @@ void build_fast(hb_handle *h, const hb_ensemble_desc *d, const std::vector<Canon
   if (h->info.feasible[HB_STRATEGY_TT] && lg <= hb::kFastMaxLg) {
     const int tb = hb::fast_tree_bytes(1, lg);
     const int tc = hb::fast_tc(tb);
-    const int chunks = ((T + tc - 1) / tc + 3) / 4 * 4;
+    const int chunks = (T + hb::kFastIdGroup - 1) / hb::kFastIdGroup * (hb::kFastIdGroup / tc);
     const size_t words = (size_t)tb / 4;
     const size_t NP = (size_t)1 << lg;
     h->tt_fast.assign((size_t)chunks * tc * words, 0u);

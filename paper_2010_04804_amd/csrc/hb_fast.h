@@ -11,10 +11,10 @@ namespace {
 // Fast traversal kernels for scalar leaves and inputs whose feature tile fits
 // in LDS. Differences from traverse_kernel:
 //   * each tree owns one packed block (node records, then leaf records
-//     {value, caller id}); chunks of TC consecutive blocks are double-buffered
-//     in LDS: chunk c+1 is loaded into registers before chunk c is walked and
-//     stored to LDS after it, so one barrier per chunk suffices and the load
-//     latency hides behind the walk;
+//     {value, caller id}); chunks of TC consecutive blocks pass through LDS:
+//     chunk c+1 is loaded into registers before chunk c is walked and stored
+//     to LDS after it (into the other buffer when double-buffered), so the
+//     load latency hides behind the walk;
 //   * trees of a chunk and levels are fully unrolled with compile-time LDS
 //     offsets, and the walk state is the byte offset of the current record;
 //   * PTT: heap index a lives as s = 8a; the child is 2s + 8*(x >= t) and,
@@ -64,6 +64,8 @@ template <int MODE, int LG, bool MULTI>
 struct FastCfg {
   static constexpr int TB = fast_tree_bytes(MODE, LG);
   static constexpr int TC = fast_tc(TB);
+  static constexpr int BUFS = fast_bufs(TB);
+  static constexpr int CPF = kFastIdGroup / TC;  // chunks per leaf-id flush
   static constexpr int CHUNK16 = TC * TB / 16;
   static constexpr int KMAX = MULTI ? HB_MAX_OUTPUTS : 1;
 };
@@ -72,7 +74,7 @@ template <int MODE, int LG, bool MULTI, int ROWS, int B, int Q>
 __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI>::CHUNK16],
                                            const float *xs, uint32_t lane4,
                                            double (&acc)[FastCfg<MODE, LG, MULTI>::KMAX],
-                                           int32_t (&ids)[4 * FastCfg<MODE, LG, MULTI>::TC]) {
+                                           int32_t (&ids)[kFastIdGroup]) {
   using C = FastCfg<MODE, LG, MULTI>;
   constexpr int TC = C::TC;
   constexpr int TB = C::TB;
@@ -131,15 +133,35 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
       }
     }
   }
-  if (more) next.store(tbuf[B ^ 1]);  // nobody reads tbuf[B^1] during chunk c
-  lds_barrier();
+  if (C::BUFS == 2) {
+    if (more) next.store(tbuf[B ^ 1]);  // nobody reads tbuf[B^1] during chunk c
+    lds_barrier();
+  } else {
+    lds_barrier();  // every wave is done with the single buffer
+    if (more) next.store(tbuf[0]);
+    lds_barrier();
+  }
+}
+
+// The CPF chunks between two leaf-id flushes, unrolled so that buffer
+// indices and id slots are compile-time constants.
+template <int MODE, int LG, bool MULTI, int ROWS, int Q>
+__device__ __forceinline__ void fast_group(const FastArgs &a, int c0, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI>::CHUNK16],
+                                           const float *xs, uint32_t lane4,
+                                           double (&acc)[FastCfg<MODE, LG, MULTI>::KMAX],
+                                           int32_t (&ids)[kFastIdGroup]) {
+  using C = FastCfg<MODE, LG, MULTI>;
+  if constexpr (Q < C::CPF) {
+    fast_chunk<MODE, LG, MULTI, ROWS, C::BUFS == 2 ? (Q & 1) : 0, Q>(a, c0 + Q, tbuf, xs, lane4, acc, ids);
+    fast_group<MODE, LG, MULTI, ROWS, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids);
+  }
 }
 
 template <int MODE, int LG, bool MULTI, int ROWS>
 __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   using C = FastCfg<MODE, LG, MULTI>;
-  constexpr int G = 4 * C::TC;
-  __shared__ __align__(16) uint4 tbuf[2][C::CHUNK16];
+  constexpr int G = kFastIdGroup;
+  __shared__ __align__(16) uint4 tbuf[C::BUFS][C::CHUNK16];
   __shared__ __align__(16) int4 idstage[ROWS / 64][16 * (G / 4)];
   extern __shared__ __align__(16) float fxs[];  // [F][ROWS]
   const int tid = threadIdx.x;
@@ -173,12 +195,10 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   for (int k = 0; k < C::KMAX; ++k) acc[k] = 0.0;
   int32_t ids[G];
   const int64_t r0w = r0 + (tid & ~63);
-  for (int c = 0; c < a.n_chunks; c += 4) {  // chunk count is a multiple of 4
-    fast_chunk<MODE, LG, MULTI, ROWS, 0, 0>(a, c, tbuf, fxs, lane4, acc, ids);
-    fast_chunk<MODE, LG, MULTI, ROWS, 1, 1>(a, c + 1, tbuf, fxs, lane4, acc, ids);
-    fast_chunk<MODE, LG, MULTI, ROWS, 0, 2>(a, c + 2, tbuf, fxs, lane4, acc, ids);
-    fast_chunk<MODE, LG, MULTI, ROWS, 1, 3>(a, c + 3, tbuf, fxs, lane4, acc, ids);
-    if (a.leaf_ids) flush_ids<G>(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, idstage[tid >> 6], ids, r0w, c * C::TC);
+  for (int c = 0; c < a.n_chunks; c += C::CPF) {  // chunk count is a multiple of CPF
+    fast_group<MODE, LG, MULTI, ROWS, 0>(a, c, tbuf, fxs, lane4, acc, ids);
+    if (a.leaf_ids)
+      flush_ids<G>(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, idstage[tid >> 6], ids, r0w, c * C::TC);
   }
   if (valid) {
     finish_row<C::KMAX>(a.out, acc, row);

@@ -25,17 +25,26 @@ constexpr int64_t kTreeLdsLimit = 160 * 1024 - 4 * 1024;
 //   TT (mode 1, 2^lg >= nodes): node record c = {threshold bits, feature,
 //     16 * left child, 16 * right child} (16 bytes; a leaf points to itself
 //     on both sides); the leaf record of node c sits at 16 * 2^lg + 8c.
-// Blocks are grouped in chunks of fast_tc() trees staged through LDS; the
-// tree count is padded with zero blocks to a multiple of four chunks.
+// Blocks are grouped in chunks of fast_tc() trees staged through LDS, either
+// double-buffered (the next chunk is stored while nobody reads its buffer) or
+// single-buffered with twice as many trees per chunk (more independent walks
+// per wave, one extra barrier per chunk), whichever fits more trees in the
+// 64 KiB table budget. Leaf ids are flushed every kFastIdGroup trees, and the
+// tree count is padded with zero blocks to a multiple of kFastIdGroup.
 constexpr int kFastTableLds = 64 * 1024;
+constexpr int kFastIdGroup = 32;
 constexpr int fast_node_bytes(int mode) { return mode == 0 ? 8 : 16; }
 constexpr int fast_tree_bytes(int mode, int lg) { return (1 << lg) * (fast_node_bytes(mode) + 8); }
-constexpr int fast_tc(int tree_bytes) {
-  return 2 * 8 * tree_bytes <= kFastTableLds   ? 8
-         : 2 * 4 * tree_bytes <= kFastTableLds ? 4
-         : 2 * 2 * tree_bytes <= kFastTableLds ? 2
-                                                : 1;
+constexpr int fast_pow2_fit(int budget, int tree_bytes) {
+  int t = 16;
+  while (t > 1 && t * tree_bytes > budget) t >>= 1;
+  return t;
 }
+constexpr bool fast_single(int tree_bytes) {
+  return fast_pow2_fit(kFastTableLds, tree_bytes) > fast_pow2_fit(kFastTableLds / 2, tree_bytes);
+}
+constexpr int fast_bufs(int tree_bytes) { return fast_single(tree_bytes) ? 1 : 2; }
+constexpr int fast_tc(int tree_bytes) { return fast_pow2_fit(kFastTableLds / fast_bufs(tree_bytes), tree_bytes); }
 constexpr int kFastMaxLg = 12;
 
 // Ensemble-wide parameters every kernel needs.

@@ -269,12 +269,11 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
   const int lds_max = max_dynamic_lds(err);
   if (lds_max <= 0) return HB_ERR_HIP;
   const int tb = fast_tree_bytes(mode, lg);
-  const size_t table = (size_t)2 * fast_tc(tb) * tb;
-  // static LDS: the two chunk buffers and the leaf-id staging (rows x 4 TC ids);
+  const size_t table = (size_t)fast_bufs(tb) * fast_tc(tb) * tb;
+  // static LDS: the chunk buffer(s) and the leaf-id staging;
   // dynamic LDS: the feature tile (F x rows floats)
-  const int tc = fast_tc(tb);
-  auto fits = [&](int rows) {
-    return table + (size_t)rows * 4 * tc + (size_t)e.n_features * rows * 4 <= (size_t)lds_max;
+  auto fits = [&](int rows) {  // + leaf-id staging: rows x kFastIdGroup int32
+    return table + (size_t)rows * kFastIdGroup + (size_t)e.n_features * rows * 4 <= (size_t)lds_max;
   };
   int rows = 512;
   if (!fits(rows) || n_rows < 64 * 512) rows = 256;
