@@ -34,10 +34,11 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kGRows = 256;                // rows per workgroup: 4 waves x 64 rows
-constexpr int kGXStride = kGRows + 8;      // feature-tile stride (spreads lane groups over banks)
+// Rows per workgroup: 64 per wave, 8 waves (two per SIMD, so one wave's
+// predicate phase overlaps another's matrix phase) when LDS allows, else 4.
+// The feature tile's stride is the row count + 8 (spreads lane groups over banks).
 constexpr int kCtPad = 16;                 // bytes appended to each C^T row in LDS
-constexpr int kTG = 2;                     // trees per staged chunk of node records
+constexpr int kTG = 4;                     // trees per staged chunk of node records
 constexpr int kIdGroup = 32;               // trees per leaf-id flush
 
 struct GemmArgs {
@@ -72,33 +73,53 @@ __device__ __forceinline__ void lds_sync() {
 
 __device__ __forceinline__ int hmax4(v4i v) { return max(max(v[0], v[1]), max(v[2], v[3])); }
 
-// Stages the node records of trees [t0, t0 + kTG) (clamped to T) into `dst`
-// with the padded layout; 16 B (two records) per lane per step.
-__device__ __forceinline__ void stage_nodes(const GemmArgs &a, int t0, unsigned char *dst) {
-  const int per_tree16 = a.k_pad / 2;
-  const int total = kTG * per_tree16;
-  for (int u = threadIdx.x; u < total; u += kGRows) {
-    const int g = u / per_tree16;
-    const int q = u - g * per_tree16;
-    const int t = min(t0 + g, a.out.T - 1);
-    const u32x4 v = reinterpret_cast<const u32x4 *>(a.node + (size_t)t * a.k_pad)[q];
-    *reinterpret_cast<u32x4 *>(dst + g * node_lds_bytes(a.k_pad) + node_lds_off(2 * q)) = v;
+// Node records of one chunk of kTG trees, held in registers between their
+// global load (issued before the current chunk is walked) and their store to
+// LDS (after it), in the padded layout; 16 B (two records) per lane per step.
+// Native vectors so they stay in VGPRs.
+template <int ROWS>
+struct NodePrefetch {
+  static constexpr int PER = kTG * 256 / 2 / ROWS;  // k_pad <= 256
+  u32x4 v[PER];
+  __device__ __forceinline__ void load(const GemmArgs &a, int t0) {
+    const int per_tree16 = a.k_pad / 2;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int u = min(i * ROWS + (int)threadIdx.x, kTG * per_tree16 - 1);
+      const int g = u / per_tree16;
+      const int q = u - g * per_tree16;
+      const int t = min(t0 + g, a.out.T - 1);
+      v[i] = reinterpret_cast<const u32x4 *>(a.node + (size_t)t * a.k_pad)[q];
+    }
   }
-}
+  __device__ __forceinline__ void store(const GemmArgs &a, unsigned char *dst) const {
+    const int per_tree16 = a.k_pad / 2;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int u = i * ROWS + (int)threadIdx.x;
+      if (u < kTG * per_tree16) {
+        const int g = u / per_tree16;
+        const int q = u - g * per_tree16;
+        *reinterpret_cast<u32x4 *>(dst + g * node_lds_bytes(a.k_pad) + node_lds_off(2 * q)) = v[i];
+      }
+    }
+  }
+};
 
 // KB: 64-node slices of the decision-node dimension; KMODE: 0 scalar leaves
 // and one output, 1 scalar leaves with a class per tree, 2 vector leaves.
-template <int KB, bool CT_LDS, bool X_LDS, int KMODE>
-__global__ __launch_bounds__(kGRows) void gemm_kernel(GemmArgs a) {
+template <int KB, bool CT_LDS, bool X_LDS, int KMODE, int ROWS>
+__global__ __launch_bounds__(ROWS) void gemm_kernel(GemmArgs a) {
   constexpr int KMAX = KMODE == 0 ? 1 : HB_MAX_OUTPUTS;
+  constexpr int XS = ROWS + 8;
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ __align__(16) int4 idstage[kGRows / 64][16 * (kIdGroup / 4)];
+  __shared__ __align__(16) int4 idstage[ROWS / 64][16 * (kIdGroup / 4)];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int g4 = lane >> 4;  // lane group: k slice of the operands, leaf quad of the result
   const int r16 = lane & 15;
   const int wave = tid >> 6;
-  const int64_t r0 = (int64_t)blockIdx.x * kGRows;
+  const int64_t r0 = (int64_t)blockIdx.x * ROWS;
   const int64_t r0w = r0 + wave * 64;
   const int64_t row = r0w + lane;  // the row this lane owns after the reduction
   const bool valid = row < a.n_rows;
@@ -108,7 +129,7 @@ __global__ __launch_bounds__(kGRows) void gemm_kernel(GemmArgs a) {
   // ---- LDS carve-up: [feature tile][C^T][bias][node chunks x2]
   size_t off = 0;
   float *xs = reinterpret_cast<float *>(smem);
-  if (X_LDS) off += ((size_t)a.F * kGXStride * 4 + 15) / 16 * 16;
+  if (X_LDS) off += ((size_t)a.F * XS * 4 + 15) / 16 * 16;
   int8_t *cts = reinterpret_cast<int8_t *>(smem + off);
   int32_t *bias_s = nullptr;
   if (CT_LDS) {
@@ -121,19 +142,23 @@ __global__ __launch_bounds__(kGRows) void gemm_kernel(GemmArgs a) {
 
   if (X_LDS) {
     for (int f = 0; f < a.F; ++f)
-      xs[f * kGXStride + tid] = (r0 + tid < a.n_rows) ? a.X[(r0 + tid) * a.F + f] : 0.0f;
+      xs[f * XS + tid] = (r0 + tid < a.n_rows) ? a.X[(r0 + tid) * a.F + f] : 0.0f;
   }
   if (CT_LDS) {
     const int row16 = a.k_pad / 16;
-    for (int u = tid; u < a.l_pad * row16; u += kGRows) {
+    for (int u = tid; u < a.l_pad * row16; u += ROWS) {
       const int l = u / row16;
       const int q = u - l * row16;
       *reinterpret_cast<u32x4 *>(cts + (size_t)l * ct_stride + q * 16) =
           reinterpret_cast<const u32x4 *>(a.ct + (size_t)l * a.k_pad)[q];
     }
-    for (int u = tid; u < a.l_pad; u += kGRows) bias_s[u] = a.bias[u];
+    for (int u = tid; u < a.l_pad; u += ROWS) bias_s[u] = a.bias[u];
   }
-  stage_nodes(a, 0, nodes);
+  {
+    NodePrefetch<ROWS> first;
+    first.load(a, 0);
+    first.store(a, nodes);
+  }
   lds_sync();
 
   double acc[KMAX];
@@ -153,6 +178,10 @@ __global__ __launch_bounds__(kGRows) void gemm_kernel(GemmArgs a) {
   const int n_chunks = (a.out.T + kTG - 1) / kTG;
   for (int c = 0; c < n_chunks; ++c) {
     const unsigned char *cur = nodes + (c & 1) * chunk_bytes;
+    const bool more = c + 1 < n_chunks;
+    NodePrefetch<ROWS> next;
+    next.load(a, more ? (c + 1) * kTG : c * kTG);
+    __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the walk
     for (int tg = 0; tg < kTG; ++tg) {
       const int t = c * kTG + tg;
       if (t >= a.out.T) break;  // uniform
@@ -161,24 +190,20 @@ __global__ __launch_bounds__(kGRows) void gemm_kernel(GemmArgs a) {
       v4i bop[4][KB];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
-        uint2 rec[16];
         const unsigned char *rb = nb + node_lds_off(kb * 64 + 16 * g4);
 #pragma unroll
-        for (int j = 0; j < 16; j += 2) {
-          const u32x4 v = *reinterpret_cast<const u32x4 *>(rb + j * 8);
-          rec[j] = make_uint2(v[0], v[1]);
-          rec[j + 1] = make_uint2(v[2], v[3]);
-        }
+        for (int q = 0; q < 4; ++q) {  // four records -> one byte-packed dword per row tile
+          const u32x4 v0 = *reinterpret_cast<const u32x4 *>(rb + q * 32);
+          const u32x4 v1 = *reinterpret_cast<const u32x4 *>(rb + q * 32 + 16);
+          const uint2 rec[4] = {make_uint2(v0[0], v0[1]), make_uint2(v0[2], v0[3]), make_uint2(v1[0], v1[1]),
+                                make_uint2(v1[2], v1[3])};
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) {
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
+          for (int rt = 0; rt < 4; ++rt) {
             uint32_t w = 0;
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
-              const uint2 rr = rec[4 * q + b];
-              const float x = X_LDS ? xs[rr.y * kGXStride + wave * 64 + rt * 16 + r16] : xrow[rt][rr.y];
-              w |= (x < as_float(rr.x) ? 0x40u : 0u) << (8 * b);
+              const float x = X_LDS ? xs[rec[b].y * XS + wave * 64 + rt * 16 + r16] : xrow[rt][rec[b].y];
+              w |= (x < as_float(rec[b].x) ? 0x40u : 0u) << (8 * b);
             }
             bop[rt][kb][q] = (int)w;
           }
@@ -239,28 +264,28 @@ __global__ __launch_bounds__(kGRows) void gemm_kernel(GemmArgs a) {
       if (a.leaf_ids && (slot == kIdGroup - 1 || t == a.out.T - 1))
         flush_ids<kIdGroup>(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, idstage[wave], ids, r0w, t - slot);
     }
-    if (c + 1 < n_chunks) {
-      lds_sync();  // everyone is done with the other buffer (chunk c - 1)
-      stage_nodes(a, (c + 1) * kTG, nodes + ((c + 1) & 1) * chunk_bytes);
-      lds_sync();
-    }
+    // the other buffer held chunk c - 1, which every wave finished before the
+    // barrier that ended it
+    if (more) next.store(a, nodes + ((c + 1) & 1) * chunk_bytes);
+    lds_sync();
   }
   if (valid) finish_row<KMAX>(a.out, acc, row);
 }
 
 using GemmFn = void (*)(GemmArgs);
 
-template <int KB, bool CT, bool XL>
+template <int KB, bool CT, bool XL, int ROWS>
 GemmFn pick_mode(int kmode) {
-  if (kmode == 0) return gemm_kernel<KB, CT, XL, 0>;
-  if (kmode == 1) return gemm_kernel<KB, CT, XL, 1>;
-  return gemm_kernel<KB, CT, XL, 2>;
+  if (kmode == 0) return gemm_kernel<KB, CT, XL, 0, ROWS>;
+  if (kmode == 1) return gemm_kernel<KB, CT, XL, 1, ROWS>;
+  return gemm_kernel<KB, CT, XL, 2, ROWS>;
 }
 
 template <int KB>
-GemmFn pick_gemm(bool ct, bool xl, int kmode) {
-  if (ct) return xl ? pick_mode<KB, true, true>(kmode) : pick_mode<KB, true, false>(kmode);
-  return xl ? pick_mode<KB, false, true>(kmode) : pick_mode<KB, false, false>(kmode);
+GemmFn pick_gemm(bool ct, bool xl, int kmode, int rows) {
+  if (rows == 512) return ct && xl ? pick_mode<KB, true, true, 512>(kmode) : nullptr;
+  if (ct) return xl ? pick_mode<KB, true, true, 256>(kmode) : pick_mode<KB, true, false, 256>(kmode);
+  return xl ? pick_mode<KB, false, true, 256>(kmode) : pick_mode<KB, false, false, 256>(kmode);
 }
 
 }  // namespace
@@ -282,24 +307,29 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
     *err = "hipDeviceGetAttribute failed";
     return HB_ERR_HIP;
   }
-  const size_t static_lds = (size_t)(kGRows / 64) * 16 * (kIdGroup / 4) * 16;
   const size_t nodes = 2 * (size_t)kTG * node_lds_bytes(t.k_pad);
   const size_t ct_bytes = (size_t)t.l_pad * (t.k_pad + kCtPad) + (size_t)t.l_pad * 4;
-  const size_t x_bytes = ((size_t)e.n_features * kGXStride * 4 + 15) / 16 * 16;
-  const size_t budget = (size_t)lds_max - static_lds;
-  const bool ct = t.n_shapes == 1 && ct_bytes + nodes <= budget;
-  const bool xl = (ct ? ct_bytes : 0) + nodes + x_bytes <= budget;
-  const size_t dyn = (xl ? x_bytes : 0) + (ct ? ct_bytes : 0) + nodes;
-  if (dyn > budget) {
+  auto x_bytes = [&](int rows) { return ((size_t)e.n_features * (rows + 8) * 4 + 15) / 16 * 16; };
+  auto stage_bytes = [&](int rows) { return (size_t)(rows / 64) * 16 * (kIdGroup / 4) * 16; };
+  const bool ct = t.n_shapes == 1 && ct_bytes + nodes + stage_bytes(256) <= (size_t)lds_max;
+  int rows = 256;
+  if (ct && n_rows >= 64 * 512 && ct_bytes + nodes + x_bytes(512) + stage_bytes(512) <= (size_t)lds_max) rows = 512;
+  const bool xl = (ct ? ct_bytes : 0) + nodes + x_bytes(rows) + stage_bytes(rows) <= (size_t)lds_max;
+  const size_t dyn = (xl ? x_bytes(rows) : 0) + (ct ? ct_bytes : 0) + nodes;
+  if (dyn + stage_bytes(rows) > (size_t)lds_max) {
     *err = "GEMM node tables do not fit in LDS";
     return HB_ERR_UNSUPPORTED;
   }
   const int kmode = e.leaf_dim > 1 ? 2 : (e.n_outputs > 1 ? 1 : 0);
   const int kb = t.k_pad / 64;
-  GemmFn fn = kb == 1 ? pick_gemm<1>(ct, xl, kmode)
-              : kb == 2 ? pick_gemm<2>(ct, xl, kmode)
-              : kb == 3 ? pick_gemm<3>(ct, xl, kmode)
-                        : pick_gemm<4>(ct, xl, kmode);
+  GemmFn fn = kb == 1 ? pick_gemm<1>(ct, xl, kmode, rows)
+              : kb == 2 ? pick_gemm<2>(ct, xl, kmode, rows)
+              : kb == 3 ? pick_gemm<3>(ct, xl, kmode, rows)
+                        : pick_gemm<4>(ct, xl, kmode, rows);
+  if (!fn) {
+    *err = "no GEMM kernel for this configuration";
+    return HB_ERR_UNSUPPORTED;
+  }
   GemmArgs a{};
   a.X = X;
   a.n_rows = n_rows;
@@ -323,8 +353,8 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
     *err = std::string("hipFuncSetAttribute: ") + hipGetErrorString(rc);
     return HB_ERR_HIP;
   }
-  const int64_t blocks = (n_rows + kGRows - 1) / kGRows;
-  hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kGRows), dyn, stream, a);
+  const int64_t blocks = (n_rows + rows - 1) / rows;
+  hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(rows), dyn, stream, a);
   rc = hipGetLastError();
   if (rc != hipSuccess) {
     *err = std::string("kernel launch: ") + hipGetErrorString(rc);
