@@ -272,6 +272,177 @@ __global__ __launch_bounds__(ROWS) void gemm_kernel(GemmArgs a) {
   if (valid) finish_row<KMAX>(a.out, acc, row);
 }
 
+// ---------------------------------------------------------------------------
+// Software-pipelined variant for trees with 193..255 decision nodes and
+// 241..256 leaves (perfect depth-8 trees): KB = 4 slices, 16 leaf tiles.
+// While the 16 matrix instructions of leaf tile lt of tree t run, the wave
+// builds slice lt of tree t+1's predicate operand (one 64-node slice and four
+// records per lane group per tile), so the matrix cores and the vector ALUs
+// work at the same time within one wave. Node records are read from the L1/L2
+// copy of the tables two slices ahead (four records per lane group, one
+// 128-byte line per group), so no staging and no barrier is needed in the loop.
+
+struct PipeRecs {
+  u32x4 lo, hi;  // four node records {threshold bits, feature}
+};
+
+__device__ __forceinline__ PipeRecs pipe_load(const GemmArgs &a, int t, int unit, int g4) {
+  const int k = (unit >> 2) * 64 + 16 * g4 + 4 * (unit & 3);
+  const u32x4 *p = reinterpret_cast<const u32x4 *>(a.node + (size_t)t * a.k_pad + k);
+  return PipeRecs{p[0], p[1]};
+}
+
+// Encoded outcomes (bytes 0/64) of four decision nodes for the four row tiles.
+template <int XS>
+__device__ __forceinline__ void pipe_pred(const PipeRecs &r, const float *xs, int xrow0, v4i (&dst)[4], int q) {
+  const uint32_t thr[4] = {r.lo[0], r.lo[2], r.hi[0], r.hi[2]};
+  const uint32_t fea[4] = {r.lo[1], r.lo[3], r.hi[1], r.hi[3]};
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) {
+    uint32_t w = 0;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const float x = xs[fea[b] * XS + xrow0 + rt * 16];
+      w |= (x < as_float(thr[b]) ? 0x40u : 0u) << (8 * b);
+    }
+    dst[rt][q] = (int)w;
+  }
+}
+
+template <int KMODE, int ROWS>
+struct PipeState {
+  static constexpr int KMAX = KMODE == 0 ? 1 : HB_MAX_OUTPUTS;
+  double acc[KMAX];
+};
+
+// One tree: the path product of tree t from `cur`, and tree t+1's operand into `nxt`.
+template <int KMODE, int ROWS>
+__device__ __forceinline__ void pipe_tree(const GemmArgs &a, int t, const v4i (&cur)[4][4], v4i (&nxt)[4][4],
+                                          const float *xs, const int8_t *cts, const int32_t *bias_s, int ct_stride,
+                                          int wave, int g4, int r16, int64_t r0w, int4 *stage,
+                                          PipeState<KMODE, ROWS> &st) {
+  constexpr int XS = ROWS + 8;
+  const int tn = min(t + 1, a.out.T - 1);
+  const int xrow0 = wave * 64 + r16;
+  PipeRecs r0 = pipe_load(a, tn, 0, g4);
+  PipeRecs r1 = pipe_load(a, tn, 1, g4);
+  int best[4] = {INT_MIN, INT_MIN, INT_MIN, INT_MIN};
+#pragma unroll
+  for (int lt = 0; lt < 16; ++lt) {
+    const v4i b4 = *reinterpret_cast<const v4i *>(bias_s + lt * 16 + 4 * g4);
+    v4i d[4] = {b4, b4, b4, b4};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const v4i av = *reinterpret_cast<const v4i *>(cts + (lt * 16 + r16) * ct_stride + kb * 64 + 16 * g4);
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) d[rt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, cur[rt][kb], d[rt], 0, 0, 0);
+    }
+    // slice lt of the next tree: kb = lt / 4, records 4 (lt % 4) .. +3 of each lane group
+    PipeRecs r2 = r1;
+    if (lt + 2 < 16) r2 = pipe_load(a, tn, lt + 2, g4);
+    {
+      v4i slice[4];
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) slice[rt] = nxt[rt][lt >> 2];
+      pipe_pred<XS>(r0, xs, xrow0, slice, lt & 3);
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) nxt[rt][lt >> 2] = slice[rt];
+    }
+    r0 = r1;
+    r1 = r2;
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) best[rt] = max(best[rt], hmax4(d[rt]));
+    // one leaf tile per scheduling region: keeps live ranges (and registers) bounded
+    __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) {
+    best[rt] = max(best[rt], __shfl_xor(best[rt], 16));
+    best[rt] = max(best[rt], __shfl_xor(best[rt], 32));
+  }
+  int col = g4 == 0 ? best[0] : g4 == 1 ? best[1] : g4 == 2 ? best[2] : best[3];
+  col = min(max(col, 0), a.l_pad - 1);  // a valid tree always yields a column in range
+  const size_t lrec = (size_t)t * a.l_pad + (size_t)col;
+  if (KMODE == 2) {
+#pragma unroll
+    for (int k = 0; k < PipeState<KMODE, ROWS>::KMAX; ++k)
+      if (k < a.LD) st.acc[k] += (double)a.leaf_value[lrec * a.LD + k];
+  } else if (KMODE == 0) {
+    st.acc[0] += (double)a.leaf_value[lrec];
+  } else {
+    const int cls = __builtin_amdgcn_readfirstlane(a.tree_class[t]);
+    const double v = (double)a.leaf_value[lrec];
+#pragma unroll
+    for (int k = 0; k < PipeState<KMODE, ROWS>::KMAX; ++k)
+      if (k == cls) st.acc[k] += v;
+  }
+  // leaf ids go straight out (this kernel is bound by the matrix cores, and
+  // holding 32 ids per lane would cost the registers the pipeline needs)
+  const int64_t row = r0w + (threadIdx.x & 63);
+  if (a.leaf_ids && row < a.n_rows) a.leaf_ids[row * a.out.T + t] = a.leaf_id[lrec];
+  (void)stage;
+}
+
+template <int KMODE, int ROWS>
+__global__ __launch_bounds__(ROWS) void gemm_pipe_kernel(GemmArgs a) {
+  constexpr int XS = ROWS + 8;
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ __align__(16) int4 idstage[ROWS / 64][16 * (kIdGroup / 4)];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int g4 = lane >> 4;
+  const int r16 = lane & 15;
+  const int wave = tid >> 6;
+  const int64_t r0 = (int64_t)blockIdx.x * ROWS;
+  const int64_t r0w = r0 + wave * 64;
+  const int64_t row = r0w + lane;
+  const int ct_stride = a.k_pad + kCtPad;
+  float *xs = reinterpret_cast<float *>(smem);
+  const size_t xbytes = ((size_t)a.F * XS * 4 + 15) / 16 * 16;
+  int8_t *cts = reinterpret_cast<int8_t *>(smem + xbytes);
+  int32_t *bias_s = reinterpret_cast<int32_t *>(smem + xbytes + (size_t)a.l_pad * ct_stride);
+  for (int f = 0; f < a.F; ++f) xs[f * XS + tid] = (r0 + tid < a.n_rows) ? a.X[(r0 + tid) * a.F + f] : 0.0f;
+  {
+    const int row16 = a.k_pad / 16;
+    for (int u = tid; u < a.l_pad * row16; u += ROWS) {
+      const int l = u / row16;
+      const int q = u - l * row16;
+      *reinterpret_cast<u32x4 *>(cts + (size_t)l * ct_stride + q * 16) =
+          reinterpret_cast<const u32x4 *>(a.ct + (size_t)l * a.k_pad)[q];
+    }
+    for (int u = tid; u < a.l_pad; u += ROWS) bias_s[u] = a.bias[u];
+  }
+  lds_sync();
+
+  PipeState<KMODE, ROWS> st;
+#pragma unroll
+  for (int k = 0; k < PipeState<KMODE, ROWS>::KMAX; ++k) st.acc[k] = 0.0;
+  // operand of tree 0
+  v4i opa[4][4], opb[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) opa[i][j] = opb[i][j] = v4i{0, 0, 0, 0};
+  const int xrow0 = wave * 64 + r16;
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    v4i slice[4];
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) slice[rt] = opa[rt][u >> 2];
+    pipe_pred<XS>(pipe_load(a, 0, u, g4), xs, xrow0, slice, u & 3);
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) opa[rt][u >> 2] = slice[rt];
+  }
+  for (int t = 0; t < a.out.T; ++t) {
+    pipe_tree<KMODE, ROWS>(a, t, opa, opb, xs, cts, bias_s, ct_stride, wave, g4, r16, r0w, idstage[wave], st);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) opa[i][j] = opb[i][j];
+  }
+  if (row < a.n_rows) finish_row<PipeState<KMODE, ROWS>::KMAX>(a.out, st.acc, row);
+}
+
 using GemmFn = void (*)(GemmArgs);
 
 template <int KB, bool CT, bool XL, int ROWS>
@@ -315,7 +486,7 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
   int rows = 256;
   if (ct && n_rows >= 64 * 512 && ct_bytes + nodes + x_bytes(512) + stage_bytes(512) <= (size_t)lds_max) rows = 512;
   const bool xl = (ct ? ct_bytes : 0) + nodes + x_bytes(rows) + stage_bytes(rows) <= (size_t)lds_max;
-  const size_t dyn = (xl ? x_bytes(rows) : 0) + (ct ? ct_bytes : 0) + nodes;
+  size_t dyn = (xl ? x_bytes(rows) : 0) + (ct ? ct_bytes : 0) + nodes;
   if (dyn + stage_bytes(rows) > (size_t)lds_max) {
     *err = "GEMM node tables do not fit in LDS";
     return HB_ERR_UNSUPPORTED;
@@ -326,6 +497,14 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
               : kb == 2 ? pick_gemm<2>(ct, xl, kmode, rows)
               : kb == 3 ? pick_gemm<3>(ct, xl, kmode, rows)
                         : pick_gemm<4>(ct, xl, kmode, rows);
+  if (ct && xl && kb == 4 && t.l_pad == 256) {  // the software-pipelined kernel needs no node chunks
+    const size_t need = x_bytes(rows) + ct_bytes;
+    if (need + stage_bytes(rows) <= (size_t)lds_max) {
+      fn = rows == 512 ? (kmode == 0 ? gemm_pipe_kernel<0, 512> : kmode == 1 ? gemm_pipe_kernel<1, 512> : gemm_pipe_kernel<2, 512>)
+                       : (kmode == 0 ? gemm_pipe_kernel<0, 256> : kmode == 1 ? gemm_pipe_kernel<1, 256> : gemm_pipe_kernel<2, 256>);
+      dyn = need;
+    }
+  }
   if (!fn) {
     *err = "no GEMM kernel for this configuration";
     return HB_ERR_UNSUPPORTED;
