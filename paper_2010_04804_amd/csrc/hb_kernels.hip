@@ -258,6 +258,114 @@ int launch_traverse(bool perfect, TravArgs a, hipStream_t stream, std::string *e
   return HB_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Trees across lanes (small batches and wide rows). A workgroup owns R rows,
+// copies them to LDS once, and lane t walks trees t, t + 256, ... for each of
+// its rows (node records from the L1/L2 copy of the tables, reused across the
+// R rows). Leaf ids come out contiguous per row; the per-lane partial sums are
+// combined in a fixed order: a butterfly within each wave, then the four wave
+// totals in wave order, so results are reproducible run to run.
+constexpr int kLaneThreads = 256;
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+  return v;
+}
+
+template <bool PERFECT, int KMAX, bool LEAF_VEC, int R>
+__global__ __launch_bounds__(kLaneThreads) void lanes_kernel(TravArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  float *xs = reinterpret_cast<float *>(smem);  // [R][F]
+  double *red = reinterpret_cast<double *>(smem + (((size_t)R * a.F * 4 + 15) / 16 * 16));  // [4][R][KMAX]
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int64_t r0 = (int64_t)blockIdx.x * R;
+  const int nr = (int)min((int64_t)R, a.n_rows - r0);
+  for (int i = tid; i < R * a.F; i += kLaneThreads) {
+    const int r = i / a.F;
+    xs[i] = r < nr ? a.X[r0 * a.F + i] : 0.0f;
+  }
+  __syncthreads();
+  const int LD = LEAF_VEC ? a.LD : 1;
+  double acc[R][KMAX];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) acc[r][k] = 0.0;
+  for (int t = tid; t < a.T; t += kLaneThreads) {
+    const uint2 *node = a.node + (size_t)t * a.slots;
+    const int levels = PERFECT ? a.depth : a.tree_depth[t];
+    const int cls = (!LEAF_VEC && KMAX > 1) ? a.tree_class[t] : 0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const float *x = xs + r * a.F;
+      uint32_t idx = PERFECT ? 1u : 0u;
+      for (int lvl = 0; lvl < levels; ++lvl) {
+        const uint2 rec = node[idx];
+        const uint32_t f = PERFECT ? rec.y : (rec.y & 0xffffu);
+        const bool go_left = x[f] < as_float(rec.x);
+        idx = PERFECT ? 2u * idx + (go_left ? 0u : 1u) : (rec.y >> 16) - (go_left ? 1u : 0u);
+      }
+      const uint32_t slot = PERFECT ? idx - (uint32_t)a.leaf_slots : idx;
+      const size_t lrec = (size_t)t * a.leaf_slots + slot;
+      if (LEAF_VEC) {
+#pragma unroll
+        for (int k = 0; k < KMAX; ++k)
+          if (k < LD) acc[r][k] += (double)a.leaf_value[lrec * LD + k];
+      } else {
+        const double v = (double)a.leaf_value[lrec];
+#pragma unroll
+        for (int k = 0; k < KMAX; ++k) acc[r][k] += (k == cls) ? v : 0.0;
+      }
+      if (a.leaf_ids && r < nr) a.leaf_ids[(r0 + r) * a.T + t] = a.leaf_id[lrec];
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+      const double w = wave_sum(acc[r][k]);
+      if (lane == 0) red[(wave * R + r) * KMAX + k] = w;
+    }
+  __syncthreads();
+  if (tid < nr) {
+    double tot[KMAX];
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+      double v = 0.0;
+#pragma unroll
+      for (int w = 0; w < kLaneThreads / 64; ++w) v += red[(w * R + tid) * KMAX + k];
+      tot[k] = v;
+    }
+    finish_row<KMAX>(OutArgs{a.scores, a.T, a.K, a.aggregation, a.transform, a.base_score}, tot, r0 + tid);
+  }
+}
+
+using LanesFn = void (*)(TravArgs);
+
+template <bool PERFECT, int R>
+LanesFn pick_lanes_r(int kmax, bool vec) {
+  if (vec) {
+    switch (kmax) {
+      case 2: return lanes_kernel<PERFECT, 2, true, R>;
+      case 8: return lanes_kernel<PERFECT, 8, true, R>;
+      default: return lanes_kernel<PERFECT, 16, true, R>;
+    }
+  }
+  switch (kmax) {
+    case 1: return lanes_kernel<PERFECT, 1, false, R>;
+    case 2: return lanes_kernel<PERFECT, 2, false, R>;
+    case 8: return lanes_kernel<PERFECT, 8, false, R>;
+    default: return lanes_kernel<PERFECT, 16, false, R>;
+  }
+}
+
+// Rows below which the trees-across-lanes kernel beats the row-parallel ones
+// (one workgroup per row keeps every CU busy down to a few hundred rows).
+constexpr int64_t kLanesMaxRows = 4096;
+
 constexpr int kNotApplicable = 1;
 
 // Launches the fast kernel when its layout exists and its LDS fits; returns
@@ -310,6 +418,37 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
   return HB_OK;
 }
 
+// Launches lanes_kernel; returns kNotApplicable if R rows of the input do not
+// fit in LDS.
+int launch_lanes(bool perfect, const TravArgs &a, hipStream_t stream, std::string *err) {
+  const int lds_max = max_dynamic_lds(err);
+  if (lds_max <= 0) return HB_ERR_HIP;
+  const bool vec = a.LD > 1;
+  const int kmax = kmax_for(vec ? a.LD : a.K);
+  // four rows per workgroup when the batch is large enough and the sums are few
+  int R = (a.n_rows > 4 * 256 && kmax <= 2) ? 4 : 1;
+  auto need = [&](int r) { return ((size_t)r * a.F * 4 + 15) / 16 * 16 + (size_t)4 * r * kmax * 8; };
+  if (need(R) > (size_t)lds_max) R = 1;
+  if (need(R) > (size_t)lds_max) return kNotApplicable;
+  LanesFn fn = perfect ? (R == 4 ? pick_lanes_r<true, 4>(kmax, vec) : pick_lanes_r<true, 1>(kmax, vec))
+                       : (R == 4 ? pick_lanes_r<false, 4>(kmax, vec) : pick_lanes_r<false, 1>(kmax, vec));
+  const size_t lds = need(R);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)lds);
+  if (e != hipSuccess) {
+    *err = std::string("hipFuncSetAttribute: ") + hipGetErrorString(e);
+    return HB_ERR_HIP;
+  }
+  const int64_t blocks = (a.n_rows + R - 1) / R;
+  hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kLaneThreads), lds, stream, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) {
+    *err = std::string("kernel launch: ") + hipGetErrorString(e);
+    return HB_ERR_HIP;
+  }
+  return HB_OK;
+}
+
 TravArgs common_args(const EnsembleDev &e, const float *X, int64_t n, float *scores, int32_t *ids) {
   TravArgs a{};
   a.X = X;
@@ -336,9 +475,6 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
     return HB_ERR_INVALID_ARG;
   }
   if (n_rows <= 0) return HB_OK;
-  const int rc = launch_fast(0, t.depth, t.fast, t.fast_chunks, nullptr, e, X, n_rows, scores, leaf_ids,
-                             stream, err);
-  if (rc != kNotApplicable) return rc;
   TravArgs a = common_args(e, X, n_rows, scores, leaf_ids);
   a.node = t.node;
   a.leaf_value = t.leaf_value;
@@ -347,6 +483,12 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
   a.slots = 1 << t.depth;
   a.leaf_slots = 1 << t.depth;
   if (a.slots < 2) a.slots = 2;  // depth 0 still stores two (unused) records per tree
+  int rc = kNotApplicable;
+  if (n_rows <= kLanesMaxRows) rc = launch_lanes(true, a, stream, err);
+  if (rc == kNotApplicable)
+    rc = launch_fast(0, t.depth, t.fast, t.fast_chunks, nullptr, e, X, n_rows, scores, leaf_ids, stream, err);
+  if (rc == kNotApplicable) rc = launch_lanes(true, a, stream, err);  // wide rows
+  if (rc != kNotApplicable) return rc;
   return launch_traverse(true, a, stream, err);
 }
 
@@ -361,9 +503,6 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
     return HB_ERR_INVALID_ARG;
   }
   if (n_rows <= 0) return HB_OK;
-  const int rc = launch_fast(1, t.fast_lg, t.fast, t.fast_chunks, t.depth, e, X, n_rows, scores, leaf_ids,
-                             stream, err);
-  if (rc != kNotApplicable) return rc;
   TravArgs a = common_args(e, X, n_rows, scores, leaf_ids);
   a.node = t.node;
   a.leaf_value = t.leaf_value;
@@ -371,6 +510,12 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
   a.tree_depth = t.depth;
   a.slots = t.n_pad;
   a.leaf_slots = t.n_pad;
+  int rc = kNotApplicable;
+  if (n_rows <= kLanesMaxRows) rc = launch_lanes(false, a, stream, err);
+  if (rc == kNotApplicable)
+    rc = launch_fast(1, t.fast_lg, t.fast, t.fast_chunks, t.depth, e, X, n_rows, scores, leaf_ids, stream, err);
+  if (rc == kNotApplicable) rc = launch_lanes(false, a, stream, err);  // wide rows
+  if (rc != kNotApplicable) return rc;
   return launch_traverse(false, a, stream, err);
 }
 

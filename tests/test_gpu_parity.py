@@ -79,6 +79,20 @@ def test_ragged_batches(strategy, n):
     check(model, X, scores, ids, f"ragged{n}/{strategy}")
 
 
+@pytest.mark.parametrize("strategy", ["ptt", "tt"])
+@pytest.mark.parametrize("cfg,n", [(2, 1025), (2, 1027), (2, 4096), (2, 4097), (4, 4095),
+                                   (3, 4093), (3, 20_001)])
+def test_tree_parallel_boundaries(cfg, n, strategy):
+    """Batch sizes around the switch between the trees-across-lanes kernel and
+    the row-parallel one, and its four-rows-per-workgroup form with a ragged
+    last workgroup; config 3's 2000-feature rows take it at every size."""
+    model, h = handle(cfg)
+    say("tree-parallel", cfg, strategy, n)
+    X = synth.make_rows(cfg, n)
+    scores, ids = run(h, X, strategy)
+    check(model, X, scores, ids, f"lanes cfg{cfg}/{n}/{strategy}")
+
+
 @pytest.mark.parametrize("strategy", STRATEGIES)
 def test_empty_batch_enqueues_nothing(strategy):
     model, h = handle(1)
