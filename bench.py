@@ -100,6 +100,129 @@ def cpu_baseline(model, cfg, seconds_target=15.0):
                       f"{dt:.1f} s on {cores} threads"}
 
 
+def _event_ms(stream, fn, reps):
+    """Average time of ``reps`` back-to-back calls of fn, HIP events on ``stream``."""
+    import torch
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(reps):
+        fn()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    return ev0.elapsed_time(ev1) / reps
+
+
+def run_sweep():
+    """Strategy crossover: every feasible strategy on 100-tree forests of depth
+    3, 7 and 12 over 200 features, at batch sizes 1 to 1M (scores only, as a
+    scoring service would call it). One JSON line per point, then a summary
+    of the fastest strategy per (model, batch) beside the selector's choice."""
+    import torch
+
+    import paper_2010_04804_amd as hb
+    from paper_2010_04804_amd import synth
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    nmax = max(synth.SWEEP["batches"])
+    X = torch.from_numpy(synth.sweep_rows(nmax)).to(dev)
+    scores = torch.empty((nmax, 1), dtype=torch.float32, device=dev)
+    table = {}
+    for kind in synth.SWEEP["models"]:
+        h = hb.compile(synth.sweep_model(kind), device=0)
+        info = h.info()
+        for n in synth.SWEEP["batches"]:
+            row = {}
+            for s in ("gemm", "ptt", "tt"):
+                if not info["feasible"][s]:
+                    continue
+                fn = lambda: hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), None, s,
+                                            stream.cuda_stream)
+                fn()
+                torch.cuda.synchronize()
+                probe = _event_ms(stream, fn, 1)
+                reps = int(min(200, max(3, 100.0 / max(probe, 1e-3))))
+                ms = _event_ms(stream, fn, reps)
+                row[s] = ms
+                print(json.dumps({"sweep": kind, "batch": n, "strategy": s, "us": round(ms * 1e3, 2),
+                                  "rows_per_s": n / (ms * 1e-3), "reps": reps}), flush=True)
+            best = min(row, key=row.get)
+            table[f"{kind}/{n}"] = {"best": best, "auto": h.select(n),
+                                    "us": {k: round(v * 1e3, 2) for k, v in row.items()}}
+        h.close()
+    print(json.dumps({"sweep_summary": table}), flush=True)
+
+
+def run_latency(config):
+    """Request-response latency on one workload's model at batch sizes 1 to
+    10K (scores only): back-to-back launches timed with HIP events, and one
+    call plus a stream synchronisation timed on the host, both for the eager
+    call and for a replay of it captured in a HIP graph."""
+    import statistics
+
+    import torch
+
+    import paper_2010_04804_amd as hb
+    from paper_2010_04804_amd import synth
+
+    dev = torch.device("cuda:0")
+    model = synth.make_model(config)
+    h = hb.compile(model, device=0)
+    info = h.info()
+    K = info["n_outputs"]
+    batches = (1, 10, 100, 1_000, 10_000)
+    X = torch.from_numpy(synth.make_rows(config, max(batches))).to(dev)
+    side = torch.cuda.Stream(dev)
+    out = {}
+    for n in batches:
+        for strat in ("auto", "gemm"):
+            s_name = h.select(n) if strat == "auto" else strat
+            if not info["feasible"][s_name]:
+                continue
+            scores = torch.empty((n, K), dtype=torch.float32, device=dev)
+            with torch.cuda.stream(side):
+                fn = lambda: hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), None, s_name,
+                                            torch.cuda.current_stream(dev).cuda_stream)
+                for _ in range(3):
+                    fn()
+                torch.cuda.synchronize()
+                ref = scores.clone()
+                reps = 200 if s_name != "gemm" else 20
+                pipelined = _event_ms(side, fn, reps)
+                rt = []
+                for _ in range(reps):
+                    t0 = time.perf_counter()
+                    fn()
+                    side.synchronize()
+                    rt.append(time.perf_counter() - t0)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=side):
+                hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), None, s_name,
+                               side.cuda_stream)
+            grt = []
+            for i in range(reps):
+                scores.fill_(float("nan"))
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                g.replay()
+                torch.cuda.synchronize()
+                grt.append(time.perf_counter() - t0)
+                if i < 3 and not torch.equal(scores, ref):
+                    raise RuntimeError(f"graph replay {i} differs from the eager call (batch {n})")
+            key = f"{n}/{s_name}"
+            out[key] = {"pipelined_us": round(pipelined * 1e3, 2),
+                        "roundtrip_us_median": round(statistics.median(rt) * 1e6, 2),
+                        "roundtrip_us_min": round(min(rt) * 1e6, 2),
+                        "graph_roundtrip_us_median": round(statistics.median(grt) * 1e6, 2),
+                        "graph_roundtrip_us_min": round(min(grt) * 1e6, 2)}
+            print(json.dumps({"latency": key, **out[key]}), flush=True)
+            del g
+    h.close()
+    print(json.dumps({"latency_summary": {"workload": synth.CONFIGS[config]["name"], "points": out}}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -113,12 +236,21 @@ def main():
     ap.add_argument("--only-main", action="store_true", help="skip the other strategies")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (to scale HBM byte counters)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="strategy crossover sweep (depth 3/7/12, batch 1..1M) instead of the bench line")
+    ap.add_argument("--latency", action="store_true",
+                    help="small-batch latency (eager and graph-replayed) instead of the bench line")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": f"--gpus {args.gpus}: this build runs on one GPU only. Rows are "
                                    "independent, so N GPUs would each score n/N rows with a "
                                    "replica of the compiled tables and no exchange step."}))
         sys.exit(2)
+
+    if args.sweep:
+        return run_sweep()
+    if args.latency:
+        return run_latency(args.config)
 
     import torch
 

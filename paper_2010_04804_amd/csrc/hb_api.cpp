@@ -150,16 +150,20 @@ struct hb_handle {
 namespace {
 
 // Sec. 5.1 picks GEMM for shallow trees or small batches, PTT up to depth 10
-// and TT beyond. These constants are the MI355X re-derivation: PTT while the
-// padded perfect tree stays within a small multiple of the real node count.
+// and TT beyond. Re-measured on MI355X over 100-tree forests of depth 3, 7
+// and 12 at batch sizes 1 to 1M: PTT is fastest or tied everywhere except on
+// unbalanced trees, where TT wins from about a thousand rows on, and GEMM is
+// slower than PTT at every depth and batch size (here small batches go to the
+// trees-across-lanes walk, which is a few microseconds at batch 1). So AUTO
+// takes PTT while the padded perfect tree stays within a small multiple of
+// the real node count and TT otherwise; GEMM only when asked for, or when
+// nothing else can hold the model.
 constexpr int32_t kAutoPttMaxDepth = 10;
 constexpr double kAutoPttMaxBalance = 4.0;
-constexpr int32_t kAutoGemmMaxDepth = 2;
 
 int select_strategy(const hb_handle *h, int64_t n_rows) {
   (void)n_rows;
   const hb_info &I = h->info;
-  if (I.feasible[HB_STRATEGY_GEMM] && I.max_depth <= kAutoGemmMaxDepth) return HB_STRATEGY_GEMM;
   if (I.feasible[HB_STRATEGY_PTT] && I.max_depth <= kAutoPttMaxDepth &&
       I.balance <= kAutoPttMaxBalance)
     return HB_STRATEGY_PTT;

@@ -362,9 +362,15 @@ LanesFn pick_lanes_r(int kmax, bool vec) {
   }
 }
 
-// Rows below which the trees-across-lanes kernel beats the row-parallel ones
-// (one workgroup per row keeps every CU busy down to a few hundred rows).
-constexpr int64_t kLanesMaxRows = 4096;
+// Batch sizes up to which the trees-across-lanes kernel beats the
+// row-parallel ones. The row-parallel kernels cost a near-constant time until
+// the batch fills the chip (one workgroup walks every tree in sequence), the
+// tree-parallel one a time proportional to the batch; both scale with
+// trees x depth, so the crossing is a batch size, measured on the 500-tree
+// depth-8 and the leaf-wise depth-12 models: about 8K rows for PTT and 16K
+// for TT, whose row-parallel walk is slower.
+constexpr int64_t kLanesMaxRowsPtt = 8192;
+constexpr int64_t kLanesMaxRowsTt = 16384;
 
 constexpr int kNotApplicable = 1;
 
@@ -484,7 +490,7 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
   a.leaf_slots = 1 << t.depth;
   if (a.slots < 2) a.slots = 2;  // depth 0 still stores two (unused) records per tree
   int rc = kNotApplicable;
-  if (n_rows <= kLanesMaxRows) rc = launch_lanes(true, a, stream, err);
+  if (n_rows <= kLanesMaxRowsPtt) rc = launch_lanes(true, a, stream, err);
   if (rc == kNotApplicable)
     rc = launch_fast(0, t.depth, t.fast, t.fast_chunks, nullptr, e, X, n_rows, scores, leaf_ids, stream, err);
   if (rc == kNotApplicable) rc = launch_lanes(true, a, stream, err);  // wide rows
@@ -511,7 +517,7 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
   a.slots = t.n_pad;
   a.leaf_slots = t.n_pad;
   int rc = kNotApplicable;
-  if (n_rows <= kLanesMaxRows) rc = launch_lanes(false, a, stream, err);
+  if (n_rows <= kLanesMaxRowsTt) rc = launch_lanes(false, a, stream, err);
   if (rc == kNotApplicable)
     rc = launch_fast(1, t.fast_lg, t.fast, t.fast_chunks, t.depth, e, X, n_rows, scores, leaf_ids, stream, err);
   if (rc == kNotApplicable) rc = launch_lanes(false, a, stream, err);  // wide rows

@@ -39,6 +39,9 @@ __all__ = [
     "make_config",
     "permute_nodes",
     "model_stats",
+    "SWEEP",
+    "sweep_model",
+    "sweep_rows",
 ]
 
 
@@ -210,6 +213,40 @@ def make_model(cfg: int) -> dict:
     else:
         raise ValueError(f"unknown config {cfg}")
     return m
+
+
+# Strategy-crossover sweep (the trees-implementation experiment of Sec. 6):
+# 100 trees over 200 features at depth 3, 7 and 12, scored at batch sizes
+# from 1 to 1M. Depth 12 comes both perfect (4096 leaves, no GEMM) and
+# leaf-wise with 256 leaves (the unbalanced shape GEMM can still hold).
+SWEEP = dict(
+    models=("perfect-d3", "perfect-d7", "perfect-d12", "leafwise-d12"),
+    batches=(1, 10, 100, 1_000, 10_000, 100_000, 1_000_000),
+    n_trees=100, n_features=200, seed=6,
+)
+
+
+def sweep_model(kind: str) -> dict:
+    """One model of the crossover sweep: ``perfect-d{3,7,12}`` or
+    ``leafwise-d12``; thresholds N(0,1), leaves N(0, 0.05), SUM -> sigmoid."""
+    rng, _ = _streams(SWEEP["seed"] + SWEEP["models"].index(kind))
+    T, F = SWEEP["n_trees"], SWEEP["n_features"]
+    thr = lambda r, f: r.standard_normal(f.size)
+    leaves = lambda r, n: r.normal(0.0, 0.05, n)
+    if kind.startswith("perfect-d"):
+        m = perfect_forest(rng, T, int(kind[len("perfect-d"):]), F, thr, leaves)
+    elif kind == "leafwise-d12":
+        m = leafwise_forest(rng, T, 256, 12, 0.7, F, thr, leaves)
+    else:
+        raise ValueError(f"unknown sweep model {kind}")
+    m.update(n_outputs=1, tree_class=None, aggregation="sum", transform="sigmoid", base_score=None)
+    return m
+
+
+def sweep_rows(n_rows: int) -> np.ndarray:
+    """Input rows of the crossover sweep: N(0,1) over 200 features."""
+    _, rng = _streams(SWEEP["seed"])
+    return np.ascontiguousarray(_f32(rng.standard_normal((n_rows, SWEEP["n_features"]))))
 
 
 def make_rows(cfg: int, n_rows: int) -> np.ndarray:

@@ -137,5 +137,9 @@ def test_selector_choices():
     shallow = synth.perfect_forest(np.random.Generator(np.random.PCG64(0)), 4, 2, 3,
                                    lambda r, f: r.random(f.size), lambda r, n: r.random(n))
     shallow.update(n_outputs=1, tree_class=None, aggregation="sum", transform="none", base_score=None)
-    assert host(shallow).select(1000) == "gemm"
+    # the crossover sweep found GEMM slower than PTT at every depth and batch
+    assert host(shallow).select(1) == "ptt"
+    assert host(shallow).select(1000) == "ptt"
+    assert host(synth.sweep_model("leafwise-d12")).select(1000) == "tt"
+    assert host(synth.sweep_model("perfect-d7")).select(1) == "ptt"
     assert hb.compile(synth.make_model(2), strategy="tt", device=-1).select(10) == "tt"

@@ -80,7 +80,7 @@ def test_ragged_batches(strategy, n):
 
 
 @pytest.mark.parametrize("strategy", ["ptt", "tt"])
-@pytest.mark.parametrize("cfg,n", [(2, 1025), (2, 1027), (2, 4096), (2, 4097), (4, 4095),
+@pytest.mark.parametrize("cfg,n", [(2, 1025), (2, 1027), (2, 4096), (2, 8192), (2, 8193), (5, 16384), (5, 16385), (4, 4095),
                                    (3, 4093), (3, 20_001)])
 def test_tree_parallel_boundaries(cfg, n, strategy):
     """Batch sizes around the switch between the trees-across-lanes kernel and
@@ -167,6 +167,37 @@ def test_non_default_stream():
         s, ids = hb.predict(h, Xd, strategy="auto")
     st.synchronize()
     check(model, X, s.cpu().numpy(), ids.cpu().numpy(), "stream")
+
+
+@pytest.mark.parametrize("strategy,n", [("ptt", 100), ("ptt", 20_000), ("tt", 3000), ("gemm", 600)])
+def test_graph_capture_replays_match_eager(strategy, n):
+    """hb_predict captured into a HIP graph: every replay, with eager work and
+    synchronisations between replays, equals the eager call bit for bit."""
+    model, h = handle(2)
+    say("graph capture", strategy, n)
+    X = torch.from_numpy(synth.make_rows(2, n)).cuda()
+    s_ref, i_ref = hb.predict(h, X, strategy=strategy)
+    torch.cuda.synchronize()
+    scores = torch.empty_like(s_ref)
+    ids = torch.empty_like(i_ref)
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):  # warm up on the capture stream
+        hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), ids.data_ptr(), strategy, side.cuda_stream)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), ids.data_ptr(), strategy, side.cuda_stream)
+    for rep in range(4):
+        scores.fill_(float("nan"))
+        ids.fill_(-7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(scores.view(torch.int32), s_ref.view(torch.int32)), f"replay {rep} scores"
+        assert torch.equal(ids, i_ref), f"replay {rep} leaf ids"
+        junk = torch.randn(1 << 16, device="cuda").sum()  # eager work between replays
+        del junk
+    check(model, X.cpu().numpy(), scores.cpu().numpy(), ids.cpu().numpy(), f"graph/{strategy}/{n}")
 
 
 def test_full_size_headline_sampled():
