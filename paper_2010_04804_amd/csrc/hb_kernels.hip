@@ -206,38 +206,46 @@ int max_dynamic_lds(std::string *err) {
 }
 
 // Chooses the feature-tile placement and the chunk size, then launches.
+// LDS bytes of traverse_kernel with or without the feature tile and tc trees
+// per chunk.
+size_t traverse_lds(const TravArgs &a, bool xl, int tc) {
+  const size_t per_tree = (size_t)a.slots * 8 + (size_t)a.leaf_slots * a.LD * 4 + (size_t)a.leaf_slots * 4;
+  const int stride = tc + ((tc & 1) ? 0 : 1);
+  return (xl ? xtile_bytes(a.F) : 0) + (size_t)tc * per_tree + (size_t)kRows * stride * 4;
+}
+
+// Picks traverse_kernel's chunk size and feature-tile placement: two
+// workgroups per CU (half the LDS) with at least kGroup trees per chunk if
+// possible, else the whole LDS; the feature tile stays in LDS when it fits.
+// Returns the trees per chunk, 0 if even one tree does not fit.
+int traverse_plan(const TravArgs &a, int lds_max, bool *x_lds) {
+  const size_t half = (size_t)lds_max / 2;
+  for (int pass = 0; pass < 4; ++pass) {
+    const bool xl = pass < 2 && xtile_bytes(a.F) <= (size_t)lds_max / 4 * 3;
+    const size_t budget = (pass % 2 == 0) ? half : (size_t)lds_max;
+    for (int c = 16; c >= (pass % 2 == 0 ? kGroup : 1); c >>= 1)
+      if (traverse_lds(a, xl, c) <= budget) {
+        *x_lds = xl;
+        return c;
+      }
+  }
+  return 0;
+}
+
 int launch_traverse(bool perfect, TravArgs a, hipStream_t stream, std::string *err) {
   if (a.n_rows <= 0) return HB_OK;
   const int lds_max = max_dynamic_lds(err);
   if (lds_max <= 0) return HB_ERR_HIP;
   const int LD = a.LD;
-  const size_t per_tree = (size_t)a.slots * 8 + (size_t)a.leaf_slots * LD * 4 + (size_t)a.leaf_slots * 4;
-  auto need = [&](bool xl, int tc) {
-    const int stride = tc + ((tc & 1) ? 0 : 1);
-    return (xl ? xtile_bytes(a.F) : 0) + (size_t)tc * per_tree + (size_t)kRows * stride * 4;
-  };
-  // Prefer two workgroups per CU (half the LDS) with at least kGroup trees per
-  // chunk; otherwise use the whole LDS; keep the feature tile when it fits.
-  const size_t half = (size_t)lds_max / 2;
   bool x_lds = false;
-  int tc = 0;
-  for (int pass = 0; pass < 4 && tc == 0; ++pass) {
-    const bool xl = pass < 2 && xtile_bytes(a.F) <= (size_t)lds_max / 4 * 3;
-    const size_t budget = (pass % 2 == 0) ? half : (size_t)lds_max;
-    for (int c = 16; c >= (pass % 2 == 0 ? kGroup : 1); c >>= 1)
-      if (need(xl, c) <= budget) {
-        tc = c;
-        x_lds = xl;
-        break;
-      }
-  }
+  const int tc = traverse_plan(a, lds_max, &x_lds);
   if (tc == 0) {
     *err = "tree tables too large for LDS staging";
     return HB_ERR_UNSUPPORTED;
   }
   a.lg_tc = __builtin_ctz((unsigned)tc);
   a.x_in_lds = x_lds;
-  const size_t lds = need(x_lds, tc);
+  const size_t lds = traverse_lds(a, x_lds, tc);
   const bool vec = LD > 1;
   const int kmax = kmax_for(vec ? LD : a.K);
   KernelFn fn = perfect ? (x_lds ? pick_k<true, true>(kmax, vec) : pick_k<true, false>(kmax, vec))
@@ -424,6 +432,16 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
   return HB_OK;
 }
 
+// True when traverse_kernel would have to read the features from global
+// memory (rows too wide for its LDS tile) or cannot stage a single tree:
+// lanes_kernel is then the better choice at any batch size, since it stages a
+// few whole rows per workgroup and reads node records through the caches.
+bool rows_too_wide(const TravArgs &a, std::string *err) {
+  const int lds_max = max_dynamic_lds(err);
+  bool x_lds = false;
+  return lds_max > 0 && (traverse_plan(a, lds_max, &x_lds) == 0 || !x_lds);
+}
+
 // Launches lanes_kernel; returns kNotApplicable if R rows of the input do not
 // fit in LDS.
 int launch_lanes(bool perfect, const TravArgs &a, hipStream_t stream, std::string *err) {
@@ -493,7 +511,7 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
   if (n_rows <= kLanesMaxRowsPtt) rc = launch_lanes(true, a, stream, err);
   if (rc == kNotApplicable)
     rc = launch_fast(0, t.depth, t.fast, t.fast_chunks, nullptr, e, X, n_rows, scores, leaf_ids, stream, err);
-  if (rc == kNotApplicable) rc = launch_lanes(true, a, stream, err);  // wide rows
+  if (rc == kNotApplicable && rows_too_wide(a, err)) rc = launch_lanes(true, a, stream, err);
   if (rc != kNotApplicable) return rc;
   return launch_traverse(true, a, stream, err);
 }
@@ -520,7 +538,7 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
   if (n_rows <= kLanesMaxRowsTt) rc = launch_lanes(false, a, stream, err);
   if (rc == kNotApplicable)
     rc = launch_fast(1, t.fast_lg, t.fast, t.fast_chunks, t.depth, e, X, n_rows, scores, leaf_ids, stream, err);
-  if (rc == kNotApplicable) rc = launch_lanes(false, a, stream, err);  // wide rows
+  if (rc == kNotApplicable && rows_too_wide(a, err)) rc = launch_lanes(false, a, stream, err);
   if (rc != kNotApplicable) return rc;
   return launch_traverse(false, a, stream, err);
 }

@@ -93,6 +93,34 @@ def test_tree_parallel_boundaries(cfg, n, strategy):
     check(model, X, scores, ids, f"lanes cfg{cfg}/{n}/{strategy}")
 
 
+def _vector_forest(n_features, n_trees, depth, seed):
+    rng = np.random.Generator(np.random.PCG64(seed))
+
+    def leaves(r, n):
+        p = r.random(n)
+        return np.stack([1.0 - p, p], axis=1)
+
+    m = synth.perfect_forest(rng, n_trees, depth, n_features,
+                             lambda r, f: r.standard_normal(f.size), leaves, leaf_dim=2)
+    m.update(n_outputs=2, tree_class=None, aggregation="mean", transform="none", base_score=None)
+    return m, rng
+
+
+@pytest.mark.parametrize("strategy", ["ptt", "tt"])
+@pytest.mark.parametrize("n_features,n", [(28, 9000), (28, 20_000), (50_000, 37)])
+def test_vector_leaf_forest_routes(n_features, n, strategy):
+    """Random forests with probability-vector leaves take the row-parallel
+    general kernel at large batches when the rows fit its LDS tile, the
+    trees-across-lanes kernel at small ones, and the general kernel reading
+    features from global memory when a single row does not fit in LDS."""
+    m, rng = _vector_forest(n_features, 100, 7, 21)
+    X = np.ascontiguousarray(rng.standard_normal((n, n_features)).astype(np.float32))
+    say("vector forest", strategy, n_features, n)
+    h = hb.compile(m, device=0)
+    scores, ids = run(h, X, strategy)
+    check(m, X, scores, ids, f"vecRF F{n_features} n{n}/{strategy}")
+
+
 @pytest.mark.parametrize("strategy", STRATEGIES)
 def test_empty_batch_enqueues_nothing(strategy):
     model, h = handle(1)
