@@ -60,8 +60,8 @@ __device__ __forceinline__ void finish_row(const OutArgs &a, const double (&acc)
 // banks) so that every store instruction writes G*4-byte segments of 64*16/G
 // rows instead of one 16-byte piece of 64 rows.
 template <int G>
-__device__ __forceinline__ void flush_ids(int32_t *leaf_ids, int64_t n_rows, int T, bool ids_vec, int4 *stage,
-                                          const int32_t (&ids)[G], int64_t r0w, int t0) {
+__device__ __forceinline__ void flush_ids(int32_t *leaf_ids, int64_t n_rows, int T, bool ids_vec, bool ids_nt,
+                                          int4 *stage, const int32_t (&ids)[G], int64_t r0w, int t0) {
   constexpr int NB = G / 4;  // 16-byte blocks per row segment
   const int lane = threadIdx.x & 63;
   const int ntrees = min(G, T - t0);
@@ -83,7 +83,14 @@ __device__ __forceinline__ void flush_ids(int32_t *leaf_ids, int64_t n_rows, int
         const int64_t grow = r0w + 16 * p + r;
         if (q < 16 * NB && grow < n_rows && 4 * b < ntrees) {
           const int4 v = stage[r * NB + (b ^ (r & (NB - 1)))];
-          *reinterpret_cast<int4 *>(leaf_ids + grow * T + t0 + 4 * b) = v;
+          int32_t *dst = leaf_ids + grow * T + t0 + 4 * b;
+          if (ids_nt) {  // streaming: two 8-byte stores that do not allocate in L2
+            typedef int i32x2 __attribute__((ext_vector_type(2)));
+            __builtin_nontemporal_store(i32x2{v.x, v.y}, reinterpret_cast<i32x2 *>(dst));
+            __builtin_nontemporal_store(i32x2{v.z, v.w}, reinterpret_cast<i32x2 *>(dst + 2));
+          } else {
+            *reinterpret_cast<int4 *>(dst) = v;
+          }
         }
       }
       __builtin_amdgcn_wave_barrier();
@@ -100,10 +107,11 @@ __device__ __forceinline__ void flush_ids(int32_t *leaf_ids, int64_t n_rows, int
 
 // ---- fast traversal kernels (instantiated in hb_fast_ptt.hip / hb_fast_tt.hip)
 
-// Rows (= threads) per workgroup: 512 when the row tile fits next to the
-// tree chunks (eight waves share each staged chunk), else 256. The LDS stride
-// of one feature column of the row tile is exactly the row count, so a lane's
-// gather x[f] hits bank (lane mod 32) whatever feature each lane needs.
+// Rows (= threads) per workgroup: 256, 512 or 768, with a 64 KiB or 32 KiB
+// tree-chunk budget; the launcher takes the shape that puts the most waves on
+// a CU within the LDS (the row tile grows with the feature count). The LDS
+// stride of one feature column of the row tile is exactly the row count, so a
+// lane's gather x[f] hits bank (lane mod 32) whatever feature each lane needs.
 
 struct FastArgs {
   const float *X;
@@ -116,6 +124,7 @@ struct FastArgs {
   const int32_t *tree_depth;  // TT: [T]
   int32_t n_chunks;
   int32_t ids_vec;            // leaf_ids rows start 16-byte aligned (T % 4 == 0, aligned base)
+  int32_t ids_nt;             // leaf-id stores bypass L2 allocation (streaming)
 };
 
 using FastFn = void (*)(FastArgs);
@@ -123,6 +132,8 @@ using FastFn = void (*)(FastArgs);
 // The kernel for (mode, lg, multi-output) or nullptr; lg in [1, kFastMaxLg].
 FastFn fast_ptt_kernel_256(int lg, bool multi);
 FastFn fast_ptt_kernel_512(int lg, bool multi);
+FastFn fast_ptt_kernel_512s(int lg, bool multi);
+FastFn fast_ptt_kernel_768(int lg, bool multi);
 FastFn fast_tt_kernel_256(int lg, bool multi);
 FastFn fast_tt_kernel_512(int lg, bool multi);
 

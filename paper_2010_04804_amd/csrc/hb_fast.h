@@ -1,5 +1,5 @@
 // hb_fast.h -- the fast traversal kernel template (see the comment below);
-// included by hb_fast_ptt.hip and hb_fast_tt.hip, which instantiate it.
+// included by the hb_fast_{ptt,tt}_<rows>.hip units, which instantiate it.
 #pragma once
 
 #include "hb_device.h"
@@ -21,7 +21,10 @@ namespace {
 //     after D steps, s is exactly the offset of the leaf record (leaves follow
 //     the 2^D node slots);
 //   * TT: a node record {threshold, feature, left offset, right offset}
-//     makes a step one select; leaves point to themselves.
+//     makes a step one select; leaves point to themselves;
+//   * multi-output: the output column of each tree is uniform across a wave,
+//     so the per-row double accumulators are updated by register index (the
+//     columns of a chunk are loaded one chunk ahead, lane g holding tree g's).
 
 // Barrier for LDS traffic only: orders this workgroup's LDS accesses across
 // the barrier without waiting for outstanding global stores (the leaf-id
@@ -60,22 +63,22 @@ struct ChunkPrefetch {
 template <int MODE>
 constexpr int kFastMaxLgFor = MODE == 0 ? 10 : 11;
 
-template <int MODE, int LG, bool MULTI>
+template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET>
 struct FastCfg {
   static constexpr int TB = fast_tree_bytes(MODE, LG);
-  static constexpr int TC = fast_tc(TB);
-  static constexpr int BUFS = fast_bufs(TB);
+  static constexpr int TC = fast_tc(TB, BUDGET);
+  static constexpr int BUFS = fast_bufs(TB, BUDGET);
   static constexpr int CPF = kFastIdGroup / TC;  // chunks per leaf-id flush
   static constexpr int CHUNK16 = TC * TB / 16;
   static constexpr int KMAX = MULTI ? HB_MAX_OUTPUTS : 1;
 };
 
-template <int MODE, int LG, bool MULTI, int ROWS, int B, int Q>
-__device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI>::CHUNK16],
+template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET, int B, int Q>
+__device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
-                                           double (&acc)[FastCfg<MODE, LG, MULTI>::KMAX],
-                                           int32_t (&ids)[kFastIdGroup]) {
-  using C = FastCfg<MODE, LG, MULTI>;
+                                           double (&acc)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::KMAX],
+                                           int32_t (&ids)[kFastIdGroup], int &cls) {
+  using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
   constexpr int TC = C::TC;
   constexpr int TB = C::TB;
   // chunk c is in tbuf[B] (the barrier that ended the previous chunk made it
@@ -83,23 +86,42 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   ChunkPrefetch<ROWS, C::CHUNK16> next;
   const bool more = c + 1 < a.n_chunks;
   next.load(a.blocks + (size_t)(more ? c + 1 : c) * C::CHUNK16);
+  // multi-output: lane g of every wave holds the output column of tree g of
+  // the chunk (loaded one chunk ahead, like the blocks)
+  int cls_next = 0;
+  if (MULTI)
+    cls_next = a.tree_class[min((more ? c + 1 : c) * TC + ((int)threadIdx.x & (TC - 1)), a.out.T - 1)];
   __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the walk
   const unsigned char *base = reinterpret_cast<const unsigned char *>(tbuf[B]);
   const unsigned char *xb = reinterpret_cast<const unsigned char *>(xs);
   const int t0 = c * TC;
   uint32_t s[TC];
   if (MODE == 0) {
+    // Software-pipelined in issue order: LDS reads complete in order, so the
+    // node reads of all TC trees go first, then their feature reads, then
+    // each tree's step immediately issues its next node read; every wait is
+    // for the oldest read and about TC reads stay in flight per wave.
+    uint2 rec[TC];
+    float xv[TC];
 #pragma unroll
-    for (int g = 0; g < TC; ++g) s[g] = 8u;  // heap index 1
+    for (int g = 0; g < TC; ++g) {
+      s[g] = 8u;  // heap index 1
+      rec[g] = *reinterpret_cast<const uint2 *>(base + g * TB + 8u);
+    }
 #pragma unroll
     for (int lvl = 0; lvl < LG; ++lvl) {
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int g = 0; g < TC; ++g)
+        xv[g] = *reinterpret_cast<const float *>(xb + __umul24(rec[g].y, ROWS * 4u) + lane4);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int g = 0; g < TC; ++g) {
-        const uint2 rec = *reinterpret_cast<const uint2 *>(base + g * TB + s[g]);
-        const float x = *reinterpret_cast<const float *>(xb + __umul24(rec.y, ROWS * 4u) + lane4);
-        s[g] = 2u * s[g] + (x < as_float(rec.x) ? 0u : 8u);  // Algorithm 3's heap step, in bytes
+        s[g] = 2u * s[g] + (xv[g] < as_float(rec[g].x) ? 0u : 8u);  // Algorithm 3's heap step, in bytes
+        if (lvl + 1 < LG) rec[g] = *reinterpret_cast<const uint2 *>(base + g * TB + s[g]);
       }
     }
+    __builtin_amdgcn_sched_barrier(0);
   } else {
     int levels = 0;
 #pragma unroll
@@ -124,15 +146,15 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
     if (t < a.out.T) {
       const double v = (double)as_float(lr.x);
       if (MULTI) {
-        const int cls = __builtin_amdgcn_readfirstlane(a.tree_class[t]);
-#pragma unroll
-        for (int k = 0; k < C::KMAX; ++k)
-          if (k == cls) acc[k] += v;
+        // the column is uniform across the wave: one register-indexed update
+        const int k = __builtin_amdgcn_readlane(cls, g) & (C::KMAX - 1);
+        acc[k] += v;
       } else {
         acc[0] += v;
       }
     }
   }
+  cls = cls_next;
   if (C::BUFS == 2) {
     if (more) next.store(tbuf[B ^ 1]);  // nobody reads tbuf[B^1] during chunk c
     lds_barrier();
@@ -145,21 +167,22 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
 
 // The CPF chunks between two leaf-id flushes, unrolled so that buffer
 // indices and id slots are compile-time constants.
-template <int MODE, int LG, bool MULTI, int ROWS, int Q>
-__device__ __forceinline__ void fast_group(const FastArgs &a, int c0, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI>::CHUNK16],
+template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET, int Q>
+__device__ __forceinline__ void fast_group(const FastArgs &a, int c0, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
-                                           double (&acc)[FastCfg<MODE, LG, MULTI>::KMAX],
-                                           int32_t (&ids)[kFastIdGroup]) {
-  using C = FastCfg<MODE, LG, MULTI>;
+                                           double (&acc)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::KMAX],
+                                           int32_t (&ids)[kFastIdGroup], int &cls) {
+  using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
   if constexpr (Q < C::CPF) {
-    fast_chunk<MODE, LG, MULTI, ROWS, C::BUFS == 2 ? (Q & 1) : 0, Q>(a, c0 + Q, tbuf, xs, lane4, acc, ids);
-    fast_group<MODE, LG, MULTI, ROWS, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids);
+    fast_chunk<MODE, LG, MULTI, ROWS, BUDGET, C::BUFS == 2 ? (Q & 1) : 0, Q>(a, c0 + Q, tbuf, xs, lane4, acc, ids,
+                                                                           cls);
+    fast_group<MODE, LG, MULTI, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls);
   }
 }
 
-template <int MODE, int LG, bool MULTI, int ROWS>
+template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET>
 __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
-  using C = FastCfg<MODE, LG, MULTI>;
+  using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
   constexpr int G = kFastIdGroup;
   __shared__ __align__(16) uint4 tbuf[C::BUFS][C::CHUNK16];
   __shared__ __align__(16) int4 idstage[ROWS / 64][16 * (G / 4)];
@@ -194,11 +217,12 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
 #pragma unroll
   for (int k = 0; k < C::KMAX; ++k) acc[k] = 0.0;
   int32_t ids[G];
+  int cls = MULTI ? a.tree_class[min(tid & (C::TC - 1), a.out.T - 1)] : 0;
   const int64_t r0w = r0 + (tid & ~63);
   for (int c = 0; c < a.n_chunks; c += C::CPF) {  // chunk count is a multiple of CPF
-    fast_group<MODE, LG, MULTI, ROWS, 0>(a, c, tbuf, fxs, lane4, acc, ids);
+    fast_group<MODE, LG, MULTI, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls);
     if (a.leaf_ids)
-      flush_ids<G>(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, idstage[tid >> 6], ids, r0w, c * C::TC);
+      flush_ids<G>(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, a.ids_nt, idstage[tid >> 6], ids, r0w, c * C::TC);
   }
   if (valid) {
     finish_row<C::KMAX>(a.out, acc, row);
@@ -206,13 +230,13 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
 }
 
 
-template <int MODE, bool MULTI, int ROWS, int LG = 1>
+template <int MODE, bool MULTI, int ROWS, int BUDGET, int LG = 1>
 FastFn pick_fast(int lg) {
   if constexpr (LG > kFastMaxLgFor<MODE>) {
     return nullptr;
   } else {
-    if (lg == LG) return fast_kernel<MODE, LG, MULTI, ROWS>;
-    return pick_fast<MODE, MULTI, ROWS, LG + 1>(lg);
+    if (lg == LG) return fast_kernel<MODE, LG, MULTI, ROWS, BUDGET>;
+    return pick_fast<MODE, MULTI, ROWS, BUDGET, LG + 1>(lg);
   }
 }
 

@@ -5,7 +5,7 @@
 namespace hb {
 
 FastFn fast_ptt_kernel_256(int lg, bool multi) {
-  return multi ? pick_fast<0, true, 256>(lg) : pick_fast<0, false, 256>(lg);
+  return multi ? pick_fast<0, true, 256, kFastTableLds>(lg) : pick_fast<0, false, 256, kFastTableLds>(lg);
 }
 
 }  // namespace hb

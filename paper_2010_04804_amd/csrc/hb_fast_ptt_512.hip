@@ -5,7 +5,7 @@
 namespace hb {
 
 FastFn fast_ptt_kernel_512(int lg, bool multi) {
-  return multi ? pick_fast<0, true, 512>(lg) : pick_fast<0, false, 512>(lg);
+  return multi ? pick_fast<0, true, 512, kFastTableLds>(lg) : pick_fast<0, false, 512, kFastTableLds>(lg);
 }
 
 }  // namespace hb

@@ -5,7 +5,7 @@
 namespace hb {
 
 FastFn fast_tt_kernel_256(int lg, bool multi) {
-  return multi ? pick_fast<1, true, 256>(lg) : pick_fast<1, false, 256>(lg);
+  return multi ? pick_fast<1, true, 256, kFastTableLds>(lg) : pick_fast<1, false, 256, kFastTableLds>(lg);
 }
 
 }  // namespace hb

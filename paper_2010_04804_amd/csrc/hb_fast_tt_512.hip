@@ -5,7 +5,7 @@
 namespace hb {
 
 FastFn fast_tt_kernel_512(int lg, bool multi) {
-  return multi ? pick_fast<1, true, 512>(lg) : pick_fast<1, false, 512>(lg);
+  return multi ? pick_fast<1, true, 512, kFastTableLds>(lg) : pick_fast<1, false, 512, kFastTableLds>(lg);
 }
 
 }  // namespace hb

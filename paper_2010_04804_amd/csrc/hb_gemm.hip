@@ -262,7 +262,7 @@ __global__ __launch_bounds__(ROWS) void gemm_kernel(GemmArgs a) {
       for (int q = 0; q < kIdGroup; ++q)
         if (q == slot) ids[q] = a.leaf_id[lrec];
       if (a.leaf_ids && (slot == kIdGroup - 1 || t == a.out.T - 1))
-        flush_ids<kIdGroup>(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, idstage[wave], ids, r0w, t - slot);
+        flush_ids<kIdGroup>(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, false, idstage[wave], ids, r0w, t - slot);
     }
     // the other buffer held chunk c - 1, which every wave finished before the
     // barrier that ended it

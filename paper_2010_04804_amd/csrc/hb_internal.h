@@ -40,11 +40,18 @@ constexpr int fast_pow2_fit(int budget, int tree_bytes) {
   while (t > 1 && t * tree_bytes > budget) t >>= 1;
   return t;
 }
-constexpr bool fast_single(int tree_bytes) {
-  return fast_pow2_fit(kFastTableLds, tree_bytes) > fast_pow2_fit(kFastTableLds / 2, tree_bytes);
+constexpr bool fast_single(int tree_bytes, int budget = kFastTableLds) {
+  return fast_pow2_fit(budget, tree_bytes) > fast_pow2_fit(budget / 2, tree_bytes);
 }
-constexpr int fast_bufs(int tree_bytes) { return fast_single(tree_bytes) ? 1 : 2; }
-constexpr int fast_tc(int tree_bytes) { return fast_pow2_fit(kFastTableLds / fast_bufs(tree_bytes), tree_bytes); }
+constexpr int fast_bufs(int tree_bytes, int budget = kFastTableLds) { return fast_single(tree_bytes, budget) ? 1 : 2; }
+constexpr int fast_tc(int tree_bytes, int budget = kFastTableLds) {
+  return fast_pow2_fit(budget / fast_bufs(tree_bytes, budget), tree_bytes);
+}
+// Kernels with the half budget trade chunk size for occupancy: wider
+// workgroups, or wider feature tiles, leave room for half the chunk. Blocks
+// are contiguous per tree, so a kernel with a smaller chunk walks the same
+// packed buffer (the padded tree count is a multiple of every chunk size).
+constexpr int kFastTableSmall = kFastTableLds / 2;
 constexpr int kFastMaxLg = 12;
 
 // Ensemble-wide parameters every kernel needs.

@@ -391,19 +391,45 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
   const int lds_max = max_dynamic_lds(err);
   if (lds_max <= 0) return HB_ERR_HIP;
   const int tb = fast_tree_bytes(mode, lg);
-  const size_t table = (size_t)fast_bufs(tb) * fast_tc(tb) * tb;
-  // static LDS: the chunk buffer(s) and the leaf-id staging;
-  // dynamic LDS: the feature tile (F x rows floats)
-  auto fits = [&](int rows) {  // + leaf-id staging: rows x kFastIdGroup int32
-    return table + (size_t)rows * kFastIdGroup + (size_t)e.n_features * rows * 4 <= (size_t)lds_max;
-  };
-  int rows = 512;
-  if (!fits(rows) || n_rows < 64 * 512) rows = 256;
-  if (!fits(rows)) return kNotApplicable;
-  const size_t xbytes = (size_t)e.n_features * rows * 4;
   const bool multi = e.n_outputs > 1;
-  FastFn fn = mode == 0 ? (rows == 512 ? fast_ptt_kernel_512(lg, multi) : fast_ptt_kernel_256(lg, multi))
-                        : (rows == 512 ? fast_tt_kernel_512(lg, multi) : fast_tt_kernel_256(lg, multi));
+  // Workgroup shapes (rows, chunk budget); the one with the most waves per CU
+  // that fits in LDS wins (the walk is bound by the latency of its dependent
+  // LDS reads), the larger chunk on a tie (fewer hand-overs). Wide workgroups
+  // only when the batch gives every CU several of them.
+  struct Shape {
+    int rows, budget;
+    FastFn (*get)(int, bool);
+  };
+  static const Shape kPtt[] = {{768, kFastTableSmall, fast_ptt_kernel_768},
+                               {512, kFastTableLds, fast_ptt_kernel_512},
+                               {512, kFastTableSmall, fast_ptt_kernel_512s},
+                               {256, kFastTableLds, fast_ptt_kernel_256}};
+  static const Shape kTt[] = {{512, kFastTableLds, fast_tt_kernel_512}, {256, kFastTableLds, fast_tt_kernel_256}};
+  const Shape *shapes = mode == 0 ? kPtt : kTt;
+  const int n_shapes = mode == 0 ? 4 : 2;
+  // static LDS: the chunk buffer(s) and the leaf-id staging (rows x
+  // kFastIdGroup int32); dynamic LDS: the feature tile (F x rows floats)
+  auto lds_of = [&](const Shape &sh) {
+    const size_t table = (size_t)fast_bufs(tb, sh.budget) * fast_tc(tb, sh.budget) * tb;
+    return table + (size_t)sh.rows * kFastIdGroup + (size_t)e.n_features * sh.rows * 4;
+  };
+  int best = -1;
+  long best_waves = 0;
+  for (int i = 0; i < n_shapes; ++i) {
+    const Shape &sh = shapes[i];
+    const size_t lds = lds_of(sh);
+    if (lds > (size_t)lds_max) continue;
+    if (sh.rows > 256 && n_rows < 64 * (int64_t)sh.rows) continue;
+    const long waves = (long)(sh.rows / 64) * (long)((size_t)lds_max / lds);
+    if (waves > best_waves) {
+      best = i;
+      best_waves = waves;
+    }
+  }
+  if (best < 0) return kNotApplicable;
+  const int rows = shapes[best].rows;
+  const size_t xbytes = (size_t)e.n_features * rows * 4;
+  FastFn fn = shapes[best].get(lg, multi);
   if (!fn) return kNotApplicable;
   FastArgs a{};
   a.X = X;
@@ -414,8 +440,14 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
   a.tree_class = e.tree_class;
   a.blocks = blocks;
   a.tree_depth = depth;
-  a.n_chunks = chunks;
+  a.n_chunks = (int)((int64_t)chunks * fast_tc(tb) / fast_tc(tb, shapes[best].budget));
   a.ids_vec = (e.n_trees % 4 == 0) && ((reinterpret_cast<uintptr_t>(leaf_ids) & 15) == 0);
+  // Streaming id stores once the tables outgrow an XCD's 4 MB L2: write
+  // allocation would evict the chunks other workgroups are about to stage.
+  // Below that, allocating lets the two halves of a row segment that
+  // straddles a line merge in L2 (measured: multiclass 3500 trees 3% faster
+  // streaming, the 500-tree model 20% slower).
+  a.ids_nt = (int64_t)chunks * fast_tc(tb) * tb > (int64_t)4 << 20;
   hipError_t rc = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)xbytes);
   if (rc != hipSuccess) {
