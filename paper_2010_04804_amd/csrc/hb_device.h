@@ -58,49 +58,87 @@ __device__ __forceinline__ void finish_row(const OutArgs &a, const double (&acc)
 // lane) as whole row segments: each wave passes its rows through a
 // 16-row LDS staging area (16-byte blocks XOR-swizzled by row to spread
 // banks) so that every store instruction writes G*4-byte segments of 64*16/G
-// rows instead of one 16-byte piece of 64 rows.
+// rows instead of one 16-byte piece of 64 rows. The four 16-row passes are
+// split in two halves (flush_stage: lanes of the pass write their rows to the
+// staging area; flush_store: the wave reads them back as row segments and
+// stores them) so that a caller can put other work between the two.
+// Leaf ids of a group, one row per lane, either as G scalars or as G/4
+// native 4-vectors (whole VGPR quads, which a 16-byte LDS write takes as is).
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 template <int G>
-__device__ __forceinline__ void flush_ids(int32_t *leaf_ids, int64_t n_rows, int T, bool ids_vec, bool ids_nt,
-                                          int4 *stage, const int32_t (&ids)[G], int64_t r0w, int t0) {
+__device__ __forceinline__ i32x4 id_block(const int32_t (&ids)[G], int b) {
+  return i32x4{ids[4 * b], ids[4 * b + 1], ids[4 * b + 2], ids[4 * b + 3]};
+}
+template <int NB>
+__device__ __forceinline__ i32x4 id_block(const i32x4 (&ids)[NB], int b) {
+  return ids[b];
+}
+template <int G>
+__device__ __forceinline__ int id_at(const int32_t (&ids)[G], int g) {
+  return ids[g];
+}
+template <int NB>
+__device__ __forceinline__ int id_at(const i32x4 (&ids)[NB], int g) {
+  return ids[g >> 2][g & 3];
+}
+
+template <int G, class IDS>
+__device__ __forceinline__ void flush_stage(int4 *stage, const IDS &ids, int p) {
   constexpr int NB = G / 4;  // 16-byte blocks per row segment
   const int lane = threadIdx.x & 63;
+  if ((lane >> 4) == p) {
+    const int r = lane & 15;
+    i32x4 *st = reinterpret_cast<i32x4 *>(stage);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) st[r * NB + (b ^ (r & (NB - 1)))] = id_block(ids, b);
+  }
+}
+
+template <int G>
+__device__ __forceinline__ void flush_store(int32_t *leaf_ids, int64_t n_rows, int T, bool ids_nt,
+                                            const int4 *stage, int64_t r0w, int t0, int p) {
+  constexpr int NB = G / 4;
+  const int lane = threadIdx.x & 63;
   const int ntrees = min(G, T - t0);
+#pragma unroll
+  for (int i = 0; i < (16 * NB + 63) / 64; ++i) {
+    const int q = i * 64 + lane;
+    const int r = q / NB;
+    const int b = q % NB;
+    const int64_t grow = r0w + 16 * p + r;
+    if (q < 16 * NB && grow < n_rows && 4 * b < ntrees) {
+      const int4 v = stage[r * NB + (b ^ (r & (NB - 1)))];
+      int32_t *dst = leaf_ids + grow * T + t0 + 4 * b;
+      if (ids_nt) {  // streaming: two 8-byte stores that do not allocate in L2
+        typedef int i32x2 __attribute__((ext_vector_type(2)));
+        __builtin_nontemporal_store(i32x2{v.x, v.y}, reinterpret_cast<i32x2 *>(dst));
+        __builtin_nontemporal_store(i32x2{v.z, v.w}, reinterpret_cast<i32x2 *>(dst + 2));
+      } else {
+        *reinterpret_cast<int4 *>(dst) = v;
+      }
+    }
+  }
+}
+
+template <int G, class IDS>
+__device__ __forceinline__ void flush_ids(int32_t *leaf_ids, int64_t n_rows, int T, bool ids_vec, bool ids_nt,
+                                          int4 *stage, const IDS &ids, int64_t r0w, int t0) {
+  const int lane = threadIdx.x & 63;
   if (ids_vec) {
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
-      if ((lane >> 4) == p) {
-        const int r = lane & 15;
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-          stage[r * NB + (b ^ (r & (NB - 1)))] = make_int4(ids[4 * b], ids[4 * b + 1], ids[4 * b + 2], ids[4 * b + 3]);
-      }
+      flush_stage<G>(stage, ids, p);
       __builtin_amdgcn_wave_barrier();
-#pragma unroll
-      for (int i = 0; i < (16 * NB + 63) / 64; ++i) {
-        const int q = i * 64 + lane;
-        const int r = q / NB;
-        const int b = q % NB;
-        const int64_t grow = r0w + 16 * p + r;
-        if (q < 16 * NB && grow < n_rows && 4 * b < ntrees) {
-          const int4 v = stage[r * NB + (b ^ (r & (NB - 1)))];
-          int32_t *dst = leaf_ids + grow * T + t0 + 4 * b;
-          if (ids_nt) {  // streaming: two 8-byte stores that do not allocate in L2
-            typedef int i32x2 __attribute__((ext_vector_type(2)));
-            __builtin_nontemporal_store(i32x2{v.x, v.y}, reinterpret_cast<i32x2 *>(dst));
-            __builtin_nontemporal_store(i32x2{v.z, v.w}, reinterpret_cast<i32x2 *>(dst + 2));
-          } else {
-            *reinterpret_cast<int4 *>(dst) = v;
-          }
-        }
-      }
+      flush_store<G>(leaf_ids, n_rows, T, ids_nt, stage, r0w, t0, p);
       __builtin_amdgcn_wave_barrier();
     }
   } else {
+    const int ntrees = min(G, T - t0);
     const int64_t row = r0w + lane;
     if (row < n_rows) {
 #pragma unroll
       for (int g = 0; g < G; ++g)
-        if (g < ntrees) leaf_ids[row * T + t0 + g] = ids[g];
+        if (g < ntrees) leaf_ids[row * T + t0 + g] = id_at(ids, g);
     }
   }
 }

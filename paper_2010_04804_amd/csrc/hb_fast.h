@@ -73,14 +73,28 @@ struct FastCfg {
   static constexpr int KMAX = MULTI ? HB_MAX_OUTPUTS : 1;
 };
 
+// A group of leaf ids waiting to be written while the next group is walked.
+struct IdLag {
+  bool on;                                  // a group is pending (uniform)
+  const i32x4 (*ids)[kFastIdGroup / 4];     // its ids, one row per lane
+  int4 *stage;                              // this wave's staging area
+  int64_t r0w;                              // first row of the wave
+  int t0;                                   // first tree of the group
+};
+
 template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET, int B, int Q>
 __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
                                            double (&acc)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::KMAX],
-                                           int32_t (&ids)[kFastIdGroup], int &cls) {
+                                           i32x4 (&ids)[kFastIdGroup / 4], int &cls, const IdLag &lag) {
   using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
   constexpr int TC = C::TC;
   constexpr int TB = C::TB;
+  // the previous group's leaf ids leave in four 16-row passes spread over
+  // this group's chunks: the staging write before the walk, the read-back
+  // and stores after it, so the LDS round trip hides behind the walk
+  constexpr int PPC = C::CPF >= 4 ? 1 : 4 / C::CPF;  // passes in this chunk
+  constexpr int P0 = Q * PPC;
   // chunk c is in tbuf[B] (the barrier that ended the previous chunk made it
   // visible); fetch chunk c+1 into registers while walking chunk c
   ChunkPrefetch<ROWS, C::CHUNK16> next;
@@ -91,6 +105,7 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   int cls_next = 0;
   if (MULTI)
     cls_next = a.tree_class[min((more ? c + 1 : c) * TC + ((int)threadIdx.x & (TC - 1)), a.out.T - 1)];
+  if (P0 < 4 && lag.on) flush_stage<kFastIdGroup>(lag.stage, *lag.ids, P0);
   __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the walk
   const unsigned char *base = reinterpret_cast<const unsigned char *>(tbuf[B]);
   const unsigned char *xb = reinterpret_cast<const unsigned char *>(xs);
@@ -142,7 +157,7 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
     const int t = t0 + g;
     const uint32_t loff = MODE == 0 ? s[g] : (1u << LG) * 16u + (s[g] >> 1);
     const uint2 lr = *reinterpret_cast<const uint2 *>(base + g * TB + loff);
-    ids[Q * TC + g] = (int32_t)lr.y;
+    ids[(Q * TC + g) / 4][(Q * TC + g) % 4] = (int)lr.y;
     if (t < a.out.T) {
       const double v = (double)as_float(lr.x);
       if (MULTI) {
@@ -153,6 +168,18 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
         acc[0] += v;
       }
     }
+  }
+  if (P0 < 4 && lag.on) {
+    __builtin_amdgcn_wave_barrier();
+    flush_store<kFastIdGroup>(a.leaf_ids, a.n_rows, a.out.T, a.ids_nt, lag.stage, lag.r0w, lag.t0, P0);
+#pragma unroll
+    for (int pp = 1; pp < PPC; ++pp) {
+      __builtin_amdgcn_wave_barrier();
+      flush_stage<kFastIdGroup>(lag.stage, *lag.ids, P0 + pp);
+      __builtin_amdgcn_wave_barrier();
+      flush_store<kFastIdGroup>(a.leaf_ids, a.n_rows, a.out.T, a.ids_nt, lag.stage, lag.r0w, lag.t0, P0 + pp);
+    }
+    __builtin_amdgcn_wave_barrier();
   }
   cls = cls_next;
   if (C::BUFS == 2) {
@@ -171,12 +198,12 @@ template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET, int Q>
 __device__ __forceinline__ void fast_group(const FastArgs &a, int c0, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
                                            double (&acc)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::KMAX],
-                                           int32_t (&ids)[kFastIdGroup], int &cls) {
+                                           i32x4 (&ids)[kFastIdGroup / 4], int &cls, const IdLag &lag) {
   using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
   if constexpr (Q < C::CPF) {
     fast_chunk<MODE, LG, MULTI, ROWS, BUDGET, C::BUFS == 2 ? (Q & 1) : 0, Q>(a, c0 + Q, tbuf, xs, lane4, acc, ids,
-                                                                           cls);
-    fast_group<MODE, LG, MULTI, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls);
+                                                                           cls, lag);
+    fast_group<MODE, LG, MULTI, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls, lag);
   }
 }
 
@@ -216,14 +243,26 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   double acc[C::KMAX];
 #pragma unroll
   for (int k = 0; k < C::KMAX; ++k) acc[k] = 0.0;
-  int32_t ids[G];
+  i32x4 ids[G / 4], prev[G / 4];
   int cls = MULTI ? a.tree_class[min(tid & (C::TC - 1), a.out.T - 1)] : 0;
   const int64_t r0w = r0 + (tid & ~63);
+  // row-segment flushes of one group overlap the next group's walk; the
+  // unaligned (scalar) store path flushes each group right away
+  const bool lagged = a.leaf_ids && a.ids_vec;
+  IdLag lag{false, &prev, idstage[tid >> 6], r0w, 0};
   for (int c = 0; c < a.n_chunks; c += C::CPF) {  // chunk count is a multiple of CPF
-    fast_group<MODE, LG, MULTI, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls);
-    if (a.leaf_ids)
+    fast_group<MODE, LG, MULTI, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, lag);
+    if (lagged) {
+#pragma unroll
+      for (int b = 0; b < G / 4; ++b) prev[b] = ids[b];
+      lag.on = true;
+      lag.t0 = c * C::TC;
+    } else if (a.leaf_ids) {
       flush_ids<G>(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, a.ids_nt, idstage[tid >> 6], ids, r0w, c * C::TC);
+    }
   }
+  if (lag.on)  // the last group
+    flush_ids<G>(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, a.ids_nt, lag.stage, prev, r0w, lag.t0);
   if (valid) {
     finish_row<C::KMAX>(a.out, acc, row);
   }

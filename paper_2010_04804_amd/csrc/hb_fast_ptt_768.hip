@@ -4,8 +4,10 @@
 
 namespace hb {
 
+// Single-output only: the multi-output accumulators do not fit in the
+// registers three waves per SIMD leave.
 FastFn fast_ptt_kernel_768(int lg, bool multi) {
-  return multi ? pick_fast<0, true, 768, kFastTableSmall>(lg) : pick_fast<0, false, 768, kFastTableSmall>(lg);
+  return multi ? nullptr : pick_fast<0, false, 768, kFastTableSmall>(lg);
 }
 
 }  // namespace hb

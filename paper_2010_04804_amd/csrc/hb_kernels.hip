@@ -418,7 +418,7 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
   for (int i = 0; i < n_shapes; ++i) {
     const Shape &sh = shapes[i];
     const size_t lds = lds_of(sh);
-    if (lds > (size_t)lds_max) continue;
+    if (lds > (size_t)lds_max || !sh.get(lg, multi)) continue;
     if (sh.rows > 256 && n_rows < 64 * (int64_t)sh.rows) continue;
     const long waves = (long)(sh.rows / 64) * (long)((size_t)lds_max / lds);
     if (waves > best_waves) {
