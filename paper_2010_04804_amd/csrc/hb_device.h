@@ -145,7 +145,7 @@ __device__ __forceinline__ void flush_ids(int32_t *leaf_ids, int64_t n_rows, int
 
 // ---- fast traversal kernels (instantiated in hb_fast_ptt.hip / hb_fast_tt.hip)
 
-// Rows (= threads) per workgroup: 256, 512 or 768, with a 64 KiB or 32 KiB
+// Rows (= threads) per workgroup: 256, 512, 768 or 1024, with a 64, 32 or 16 KiB
 // tree-chunk budget; the launcher takes the shape that puts the most waves on
 // a CU within the LDS (the row tile grows with the feature count). The LDS
 // stride of one feature column of the row tile is exactly the row count, so a
@@ -172,6 +172,7 @@ FastFn fast_ptt_kernel_256(int lg, bool multi);
 FastFn fast_ptt_kernel_512(int lg, bool multi);
 FastFn fast_ptt_kernel_512s(int lg, bool multi);
 FastFn fast_ptt_kernel_768(int lg, bool multi);
+FastFn fast_ptt_kernel_1024(int lg, bool multi);
 FastFn fast_tt_kernel_256(int lg, bool multi);
 FastFn fast_tt_kernel_512(int lg, bool multi);
 

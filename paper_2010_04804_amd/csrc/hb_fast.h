@@ -73,20 +73,94 @@ struct FastCfg {
   static constexpr int KMAX = MULTI ? HB_MAX_OUTPUTS : 1;
 };
 
+// Leaf ids of a 32-tree group, one row per lane, as 16-bit halves: tree q of
+// the group sits in bits 16 (q & 1) of dword (q >> 1) & 3 of quad q >> 3.
+constexpr int kIdQuads = kFastIdGroup / 8;
+using IdPack = u32x4[kIdQuads];
+
+// q is a constant once the chunk loop is unrolled
+__device__ __forceinline__ void put_id(IdPack &ids, int q, uint32_t id) {
+  if (q & 1)
+    ids[q >> 3][(q >> 1) & 3] |= id << 16;
+  else
+    ids[q >> 3][(q >> 1) & 3] = id;
+}
+
+// The staging area of a wave: 16 rows x 64 bytes (the rows of one of the four
+// 16-row passes); quad j of row r sits at slot (j + r / 2) mod 4, so the 16
+// lanes that write a quad each touch 2 lanes per bank group.
+__device__ __forceinline__ void stage_ids(u32x4 *stage, const IdPack &ids, int p) {
+  const int lane = threadIdx.x & 63;
+  if ((lane >> 4) == p) {
+    const int r = lane & 15;
+#pragma unroll
+    for (int j = 0; j < kIdQuads; ++j) stage[r * kIdQuads + ((j + (r >> 1)) & 3)] = ids[j];
+  }
+}
+
+// Reads pass p back as row segments (eight lanes per row, four ids each, so
+// a store instruction writes whole 128-byte segments of eight rows), widens
+// the ids to int32 and stores them.
+__device__ __forceinline__ void store_ids(int32_t *leaf_ids, int64_t n_rows, int T, bool ids_nt,
+                                          const u32x4 *stage, int64_t r0w, int t0, int p) {
+  const int lane = threadIdx.x & 63;
+  const int ntrees = min(kFastIdGroup, T - t0);  // a multiple of 4 on this path
+  const uint2 *st = reinterpret_cast<const uint2 *>(stage);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int r = h * 8 + (lane >> 3), k = lane & 7;  // row of the pass, block of 4 ids
+    const int64_t grow = r0w + 16 * p + r;
+    const uint2 v = st[(r * kIdQuads + (((k >> 1) + (r >> 1)) & 3)) * 2 + (k & 1)];
+    if (grow < n_rows && 4 * k < ntrees) {
+      int32_t *dst = leaf_ids + grow * T + t0 + 4 * k;
+      const i32x4 o{(int)(v.x & 0xffffu), (int)(v.x >> 16), (int)(v.y & 0xffffu), (int)(v.y >> 16)};
+      if (ids_nt) {  // streaming: 8-byte stores that do not allocate in L2
+        typedef int i32x2 __attribute__((ext_vector_type(2)));
+        __builtin_nontemporal_store(i32x2{o.x, o.y}, reinterpret_cast<i32x2 *>(dst));
+        __builtin_nontemporal_store(i32x2{o.z, o.w}, reinterpret_cast<i32x2 *>(dst + 2));
+      } else {
+        *reinterpret_cast<i32x4 *>(dst) = o;
+      }
+    }
+  }
+}
+
+// All four passes at once, or (rows not 16-byte aligned) one int32 per store.
+__device__ __forceinline__ void flush_packed(int32_t *leaf_ids, int64_t n_rows, int T, bool ids_vec, bool ids_nt,
+                                             u32x4 *stage, const IdPack &ids, int64_t r0w, int t0) {
+  if (ids_vec) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      stage_ids(stage, ids, p);
+      __builtin_amdgcn_wave_barrier();
+      store_ids(leaf_ids, n_rows, T, ids_nt, stage, r0w, t0, p);
+      __builtin_amdgcn_wave_barrier();
+    }
+  } else {
+    const int ntrees = min(kFastIdGroup, T - t0);
+    const int64_t row = r0w + (threadIdx.x & 63);
+    if (row < n_rows) {
+#pragma unroll
+      for (int g = 0; g < kFastIdGroup; ++g)
+        if (g < ntrees) leaf_ids[row * T + t0 + g] = (int)((ids[g >> 3][(g >> 1) & 3] >> (16 * (g & 1))) & 0xffffu);
+    }
+  }
+}
+
 // A group of leaf ids waiting to be written while the next group is walked.
 struct IdLag {
-  bool on;                                  // a group is pending (uniform)
-  const i32x4 (*ids)[kFastIdGroup / 4];     // its ids, one row per lane
-  int4 *stage;                              // this wave's staging area
-  int64_t r0w;                              // first row of the wave
-  int t0;                                   // first tree of the group
+  bool on;               // a group is pending (uniform)
+  const IdPack *ids;     // its ids
+  u32x4 *stage;          // this wave's staging area
+  int64_t r0w;           // first row of the wave
+  int t0;                // first tree of the group
 };
 
 template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET, int B, int Q>
 __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
                                            double (&acc)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::KMAX],
-                                           i32x4 (&ids)[kFastIdGroup / 4], int &cls, const IdLag &lag) {
+                                           IdPack &ids, int &cls, const IdLag &lag) {
   using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
   constexpr int TC = C::TC;
   constexpr int TB = C::TB;
@@ -105,7 +179,7 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   int cls_next = 0;
   if (MULTI)
     cls_next = a.tree_class[min((more ? c + 1 : c) * TC + ((int)threadIdx.x & (TC - 1)), a.out.T - 1)];
-  if (P0 < 4 && lag.on) flush_stage<kFastIdGroup>(lag.stage, *lag.ids, P0);
+  if (P0 < 4 && lag.on) stage_ids(lag.stage, *lag.ids, P0);
   __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the walk
   const unsigned char *base = reinterpret_cast<const unsigned char *>(tbuf[B]);
   const unsigned char *xb = reinterpret_cast<const unsigned char *>(xs);
@@ -157,7 +231,7 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
     const int t = t0 + g;
     const uint32_t loff = MODE == 0 ? s[g] : (1u << LG) * 16u + (s[g] >> 1);
     const uint2 lr = *reinterpret_cast<const uint2 *>(base + g * TB + loff);
-    ids[(Q * TC + g) / 4][(Q * TC + g) % 4] = (int)lr.y;
+    put_id(ids, Q * TC + g, lr.y);
     if (t < a.out.T) {
       const double v = (double)as_float(lr.x);
       if (MULTI) {
@@ -171,13 +245,13 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   }
   if (P0 < 4 && lag.on) {
     __builtin_amdgcn_wave_barrier();
-    flush_store<kFastIdGroup>(a.leaf_ids, a.n_rows, a.out.T, a.ids_nt, lag.stage, lag.r0w, lag.t0, P0);
+    store_ids(a.leaf_ids, a.n_rows, a.out.T, a.ids_nt, lag.stage, lag.r0w, lag.t0, P0);
 #pragma unroll
     for (int pp = 1; pp < PPC; ++pp) {
       __builtin_amdgcn_wave_barrier();
-      flush_stage<kFastIdGroup>(lag.stage, *lag.ids, P0 + pp);
+      stage_ids(lag.stage, *lag.ids, P0 + pp);
       __builtin_amdgcn_wave_barrier();
-      flush_store<kFastIdGroup>(a.leaf_ids, a.n_rows, a.out.T, a.ids_nt, lag.stage, lag.r0w, lag.t0, P0 + pp);
+      store_ids(a.leaf_ids, a.n_rows, a.out.T, a.ids_nt, lag.stage, lag.r0w, lag.t0, P0 + pp);
     }
     __builtin_amdgcn_wave_barrier();
   }
@@ -198,7 +272,7 @@ template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET, int Q>
 __device__ __forceinline__ void fast_group(const FastArgs &a, int c0, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
                                            double (&acc)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::KMAX],
-                                           i32x4 (&ids)[kFastIdGroup / 4], int &cls, const IdLag &lag) {
+                                           IdPack &ids, int &cls, const IdLag &lag) {
   using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
   if constexpr (Q < C::CPF) {
     fast_chunk<MODE, LG, MULTI, ROWS, BUDGET, C::BUFS == 2 ? (Q & 1) : 0, Q>(a, c0 + Q, tbuf, xs, lane4, acc, ids,
@@ -212,7 +286,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
   constexpr int G = kFastIdGroup;
   __shared__ __align__(16) uint4 tbuf[C::BUFS][C::CHUNK16];
-  __shared__ __align__(16) int4 idstage[ROWS / 64][16 * (G / 4)];
+  __shared__ __align__(16) u32x4 idstage[ROWS / 64][16 * kIdQuads];
   extern __shared__ __align__(16) float fxs[];  // [F][ROWS]
   const int tid = threadIdx.x;
   const int64_t r0 = (int64_t)blockIdx.x * ROWS;
@@ -243,26 +317,28 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   double acc[C::KMAX];
 #pragma unroll
   for (int k = 0; k < C::KMAX; ++k) acc[k] = 0.0;
-  i32x4 ids[G / 4], prev[G / 4];
+  IdPack ids, prev;
   int cls = MULTI ? a.tree_class[min(tid & (C::TC - 1), a.out.T - 1)] : 0;
   const int64_t r0w = r0 + (tid & ~63);
   // row-segment flushes of one group overlap the next group's walk; the
-  // unaligned (scalar) store path flushes each group right away
-  const bool lagged = a.leaf_ids && a.ids_vec;
+  // unaligned (scalar) store path, and 1024-row workgroups (whose registers
+  // cannot hold a second group of ids), flush each group right away
+  constexpr bool kLag = ROWS < 1024;
+  const bool lagged = kLag && a.leaf_ids && a.ids_vec;
   IdLag lag{false, &prev, idstage[tid >> 6], r0w, 0};
   for (int c = 0; c < a.n_chunks; c += C::CPF) {  // chunk count is a multiple of CPF
     fast_group<MODE, LG, MULTI, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, lag);
     if (lagged) {
 #pragma unroll
-      for (int b = 0; b < G / 4; ++b) prev[b] = ids[b];
+      for (int b = 0; b < kIdQuads; ++b) prev[b] = ids[b];
       lag.on = true;
       lag.t0 = c * C::TC;
     } else if (a.leaf_ids) {
-      flush_ids<G>(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, a.ids_nt, idstage[tid >> 6], ids, r0w, c * C::TC);
+      flush_packed(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, a.ids_nt, idstage[tid >> 6], ids, r0w, c * C::TC);
     }
   }
   if (lag.on)  // the last group
-    flush_ids<G>(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, a.ids_nt, lag.stage, prev, r0w, lag.t0);
+    flush_packed(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, a.ids_nt, lag.stage, prev, r0w, lag.t0);
   if (valid) {
     finish_row<C::KMAX>(a.out, acc, row);
   }

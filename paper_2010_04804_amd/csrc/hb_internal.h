@@ -33,6 +33,11 @@ constexpr int64_t kTreeLdsLimit = 160 * 1024 - 4 * 1024;
 // tree count is padded with zero blocks to a multiple of kFastIdGroup.
 constexpr int kFastTableLds = 64 * 1024;
 constexpr int kFastIdGroup = 32;
+// The fast kernels hold and stage leaf ids as 16-bit halves: every caller id
+// they report is a local node id of a tree with at most 2^(kFastMaxLg + 1)
+// nodes. Each wave stages 16 of its 64 rows at a time (a 32-tree group of
+// 16-bit ids per row), so the staging costs 16 bytes per row of a workgroup.
+constexpr int kFastIdStageBytes = 16 * kFastIdGroup * 2 / 64;
 constexpr int fast_node_bytes(int mode) { return mode == 0 ? 8 : 16; }
 constexpr int fast_tree_bytes(int mode, int lg) { return (1 << lg) * (fast_node_bytes(mode) + 8); }
 constexpr int fast_pow2_fit(int budget, int tree_bytes) {
@@ -53,6 +58,7 @@ constexpr int fast_tc(int tree_bytes, int budget = kFastTableLds) {
 // packed buffer (the padded tree count is a multiple of every chunk size).
 constexpr int kFastTableSmall = kFastTableLds / 2;
 constexpr int kFastMaxLg = 12;
+static_assert(kFastMaxLg < 15, "fast-kernel leaf ids must fit in 16 bits");
 
 // Ensemble-wide parameters every kernel needs.
 struct EnsembleDev {

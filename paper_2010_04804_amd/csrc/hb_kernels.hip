@@ -400,18 +400,19 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
     int rows, budget;
     FastFn (*get)(int, bool);
   };
-  static const Shape kPtt[] = {{768, kFastTableSmall, fast_ptt_kernel_768},
+  static const Shape kPtt[] = {{1024, kFastTableSmall, fast_ptt_kernel_1024},
+                               {768, kFastTableSmall, fast_ptt_kernel_768},
                                {512, kFastTableLds, fast_ptt_kernel_512},
                                {512, kFastTableSmall, fast_ptt_kernel_512s},
                                {256, kFastTableLds, fast_ptt_kernel_256}};
   static const Shape kTt[] = {{512, kFastTableLds, fast_tt_kernel_512}, {256, kFastTableLds, fast_tt_kernel_256}};
   const Shape *shapes = mode == 0 ? kPtt : kTt;
-  const int n_shapes = mode == 0 ? 4 : 2;
-  // static LDS: the chunk buffer(s) and the leaf-id staging (rows x
-  // kFastIdGroup int32); dynamic LDS: the feature tile (F x rows floats)
+  const int n_shapes = mode == 0 ? 5 : 2;
+  // static LDS: the chunk buffer(s) and the leaf-id staging (16-bit ids of a
+  // 32-tree group per row); dynamic LDS: the feature tile (F x rows floats)
   auto lds_of = [&](const Shape &sh) {
     const size_t table = (size_t)fast_bufs(tb, sh.budget) * fast_tc(tb, sh.budget) * tb;
-    return table + (size_t)sh.rows * kFastIdGroup + (size_t)e.n_features * sh.rows * 4;
+    return table + (size_t)sh.rows * kFastIdStageBytes + (size_t)e.n_features * sh.rows * 4;
   };
   int best = -1;
   long best_waves = 0;
