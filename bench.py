@@ -223,6 +223,38 @@ def run_latency(config):
           flush=True)
 
 
+def run_pruning():
+    """Feature selection injection on wide inputs: 500 perfect trees of depth
+    8 over 2000-column rows whose decision nodes test 40, 120, 200 or all
+    2000 columns, 100,000 rows, PTT with and without leaf ids. The kernels
+    stage only the tested columns, so narrower use reaches the row-parallel
+    kernel; rows are read whole from HBM either way (the algorithmic bytes)."""
+    import torch
+
+    import paper_2010_04804_amd as hb
+    from paper_2010_04804_amd import synth
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    n = 100_000
+    X = torch.from_numpy(synth.narrow_use_rows(2000, n, seed=3)).to(dev)
+    scores = torch.empty((n, 1), dtype=torch.float32, device=dev)
+    ids = torch.empty((n, 500), dtype=torch.int32, device=dev)
+    for used in (40, 120, 200, 2000):
+        h = hb.compile(synth.narrow_use_model(2000, used, 500, 8, seed=3), device=0)
+        for leaves in (True, False):
+            fn = lambda: hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(),
+                                        ids.data_ptr() if leaves else None, "ptt", stream.cuda_stream)
+            fn()
+            torch.cuda.synchronize()
+            ms = _event_ms(stream, fn, 10)
+            b = n * 2000 * 4 + n * 4 + (n * 500 * 4 if leaves else 0)
+            print(json.dumps({"pruning": used, "n_used_features": h.info()["n_used_features"],
+                              "leaf_ids": leaves, "ms": round(ms, 4), "rows_per_s": n / (ms * 1e-3),
+                              "hbm_frac": b / (ms * 1e-3) / HBM_PEAK}), flush=True)
+        h.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -240,6 +272,8 @@ def main():
                     help="strategy crossover sweep (depth 3/7/12, batch 1..1M) instead of the bench line")
     ap.add_argument("--latency", action="store_true",
                     help="small-batch latency (eager and graph-replayed) instead of the bench line")
+    ap.add_argument("--pruning", action="store_true",
+                    help="wide inputs whose trees test few columns, instead of the bench line")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": f"--gpus {args.gpus}: this build runs on one GPU only. Rows are "
@@ -251,6 +285,8 @@ def main():
         return run_sweep()
     if args.latency:
         return run_latency(args.config)
+    if args.pruning:
+        return run_pruning()
 
     import torch
 

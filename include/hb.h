@@ -105,6 +105,9 @@ typedef struct hb_info {
   int64_t table_bytes[4];          /* bytes of compiled tensors per strategy */
   int32_t gemm_shapes;             /* distinct tree shapes (C/D matrices)    */
   int32_t ptt_depth;               /* D used by PTT (= max_depth)            */
+  int32_t n_used_features;         /* input columns some decision node tests
+                                      (the kernels stage only these; equals
+                                      n_features when every column is used) */
 } hb_info;
 
 /*
@@ -160,6 +163,9 @@ int hb_query(const hb_handle *h, hb_info *info);
  *         "shape" (int32 [T]), "ct" (int8 [S][l_pad][k_pad], 4*C^T),
  *         "bias" (int32 [S][l_pad]), "leaf_value" (float [T][l_pad][leaf_dim]),
  *         "leaf_id" (int32 [T][l_pad]), "dims" (int32 {k_pad, l_pad, S})
+ *   any : "features" (int32 [n_used_features]: the input column of each
+ *         feature index the tables above use; when n_used_features <
+ *         n_features the tables hold these ranks instead of input columns)
  * Returns HB_ERR_INVALID_ARG for an unknown name or an infeasible strategy.
  */
 int hb_table(const hb_handle *h, int strategy, const char *name, const void **data, int64_t *bytes);

@@ -49,6 +49,7 @@ class hb_info(ctypes.Structure):
         ("balance", ctypes.c_double), ("default_strategy", ctypes.c_int32),
         ("feasible", ctypes.c_int32 * 4), ("table_bytes", ctypes.c_int64 * 4),
         ("gemm_shapes", ctypes.c_int32), ("ptt_depth", ctypes.c_int32),
+        ("n_used_features", ctypes.c_int32),
     ]
 
 

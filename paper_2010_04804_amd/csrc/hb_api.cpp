@@ -115,6 +115,9 @@ int canonicalise(const hb_ensemble_desc *d, int32_t t, CanonTree *ct) {
 struct hb_handle {
   hb_info info{};
   int32_t device = -1;
+  // input column of each feature-tile column (sorted features the trees test)
+  std::vector<int32_t> cols;
+  bool pruned = false;  // cols is not the identity
   // host copies of the compiled tensors
   std::vector<int32_t> tree_class;
   std::vector<float> base_score;
@@ -477,6 +480,29 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
   }
   hb_handle *h = new (std::nothrow) hb_handle();
   if (!h) return fail(HB_ERR_OOM, "out of host memory");
+  // Feature selection injection for trees (Sec. 5.2): features no decision
+  // node tests are pruned and the decision variables re-indexed. The kernels
+  // then stage only the columns some node tests (a narrower LDS tile, so
+  // wide inputs reach the faster kernels), and the tables address a column by
+  // its rank among those.
+  {
+    std::vector<int32_t> rank(d->n_features, -1);
+    for (const CanonTree &ct : trees)
+      for (int32_t f : ct.feat)
+        if (f >= 0) rank[f] = 0;
+    for (int32_t f = 0; f < d->n_features; ++f)
+      if (rank[f] == 0) {
+        rank[f] = (int32_t)h->cols.size();
+        h->cols.push_back(f);
+      }
+    if (h->cols.empty()) h->cols.push_back(0);  // only single-leaf trees: one dummy column
+    h->pruned = (int32_t)h->cols.size() < d->n_features;
+    if (h->pruned)
+      for (CanonTree &ct : trees)
+        for (int32_t &f : ct.feat)
+          if (f >= 0) f = rank[f];
+  }
+  const int32_t n_cols = h->pruned ? (int32_t)h->cols.size() : d->n_features;
   hb_info &I = h->info;
   I.n_trees = T;
   I.n_features = d->n_features;
@@ -490,12 +516,13 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
   I.balance = n_int > 0 ? (double)T * (double)((int64_t(1) << D) - 1) / (double)n_int : 1.0;
   I.default_strategy = hint;
   I.ptt_depth = D;
+  I.n_used_features = n_cols;
   // The traversal kernels stage at least one tree's tables in LDS.
   const int64_t per_slot = 12 + 4 * (int64_t)d->leaf_dim;
   const int64_t ptt_tree_bytes = per_slot * std::max<int64_t>(int64_t(1) << std::min(D, 30), 2);
   const int64_t tt_tree_bytes = per_slot * (max_nodes + 1);
   I.feasible[HB_STRATEGY_PTT] = D <= HB_PTT_MAX_DEPTH && ptt_tree_bytes <= hb::kTreeLdsLimit;
-  I.feasible[HB_STRATEGY_TT] = max_nodes <= HB_TT_MAX_NODES && d->n_features <= HB_MAX_FEATURES &&
+  I.feasible[HB_STRATEGY_TT] = max_nodes <= HB_TT_MAX_NODES && n_cols <= HB_MAX_FEATURES &&
                                tt_tree_bytes <= hb::kTreeLdsLimit;
   I.feasible[HB_STRATEGY_GEMM] = max_leaves <= HB_GEMM_MAX_LEAVES;
   I.feasible[HB_STRATEGY_AUTO] =
@@ -532,6 +559,8 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
   hb::EnsembleDev &E = h->ens;
   E.n_trees = T;
   E.n_features = d->n_features;
+  E.n_cols = n_cols;
+  E.cols = nullptr;
   E.n_outputs = d->n_outputs;
   E.leaf_dim = d->leaf_dim;
   E.aggregation = d->aggregation;
@@ -550,6 +579,7 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
     }
     const uint32_t *pn = nullptr;
     rc = upload(h, h->tree_class, &E.tree_class);
+    if (!rc && h->pruned) rc = upload(h, h->cols, &E.cols);
     if (!rc && h->has_base) rc = upload(h, h->base_score, &E.base_score);
     if (!rc && I.feasible[HB_STRATEGY_PTT]) {
       rc = upload(h, h->ptt_node, &pn);
@@ -674,6 +704,7 @@ int hb_table(const hb_handle *h, int strategy, const char *name, const void **da
     *bytes = (int64_t)(v.size() * sizeof(v[0]));
     return HB_OK;
   };
+  if (n == "features") return give(h->cols);
   if (strategy == HB_STRATEGY_PTT) {
     if (n == "node") return give(h->ptt_node);
     if (n == "leaf_value") return give(h->ptt_leaf_value);

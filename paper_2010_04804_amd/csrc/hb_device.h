@@ -145,16 +145,22 @@ __device__ __forceinline__ void flush_ids(int32_t *leaf_ids, int64_t n_rows, int
 
 // ---- fast traversal kernels (instantiated in hb_fast_ptt.hip / hb_fast_tt.hip)
 
-// Rows (= threads) per workgroup: 256, 512, 768 or 1024, with a 64, 32 or 16 KiB
+// Rows (= threads) per workgroup: 128, 256, 512, 768 or 1024, with a 64 or 32 KiB
 // tree-chunk budget; the launcher takes the shape that puts the most waves on
 // a CU within the LDS (the row tile grows with the feature count). The LDS
 // stride of one feature column of the row tile is exactly the row count, so a
 // lane's gather x[f] hits bank (lane mod 32) whatever feature each lane needs.
 
+// Input column of feature-tile column f (the ensemble's used features, or the
+// identity when cols is null).
+__device__ __forceinline__ int xcol(const int32_t *cols, int f) { return cols ? cols[f] : f; }
+
 struct FastArgs {
   const float *X;
   int64_t n_rows;
-  int32_t F;
+  int32_t F;                  // feature-tile columns
+  int32_t Fs;                 // row stride of X (input columns)
+  const int32_t *cols;        // tile column -> input column, or nullptr
   int32_t *leaf_ids;
   OutArgs out;
   const int32_t *tree_class;
@@ -168,7 +174,9 @@ struct FastArgs {
 using FastFn = void (*)(FastArgs);
 
 // The kernel for (mode, lg, multi-output) or nullptr; lg in [1, kFastMaxLg].
+FastFn fast_ptt_kernel_128(int lg, bool multi);
 FastFn fast_ptt_kernel_256(int lg, bool multi);
+FastFn fast_ptt_kernel_256s(int lg, bool multi);
 FastFn fast_ptt_kernel_512(int lg, bool multi);
 FastFn fast_ptt_kernel_512s(int lg, bool multi);
 FastFn fast_ptt_kernel_768(int lg, bool multi);

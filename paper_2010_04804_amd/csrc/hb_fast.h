@@ -299,8 +299,8 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   }
   {  // each lane copies its own row into column tid of the tile (and only
      // ever reads that column back, so the tile needs no barrier)
-    const float *src = a.X + (valid ? row : r0) * a.F;
-    if ((a.F & 3) == 0 && (reinterpret_cast<uintptr_t>(a.X) & 15) == 0) {
+    const float *src = a.X + (valid ? row : r0) * a.Fs;
+    if (!a.cols && (a.F & 3) == 0 && (reinterpret_cast<uintptr_t>(a.X) & 15) == 0) {
       for (int f = 0; f < a.F; f += 4) {
         const float4 v = valid ? *reinterpret_cast<const float4 *>(src + f) : make_float4(0, 0, 0, 0);
         fxs[(f + 0) * ROWS + tid] = v.x;
@@ -309,7 +309,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
         fxs[(f + 3) * ROWS + tid] = v.w;
       }
     } else {
-      for (int f = 0; f < a.F; ++f) fxs[f * ROWS + tid] = valid ? src[f] : 0.0f;
+      for (int f = 0; f < a.F; ++f) fxs[f * ROWS + tid] = valid ? src[xcol(a.cols, f)] : 0.0f;
     }
   }
   lds_barrier();

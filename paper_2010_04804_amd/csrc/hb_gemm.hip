@@ -44,7 +44,9 @@ constexpr int kIdGroup = 32;               // trees per leaf-id flush
 struct GemmArgs {
   const float *X;
   int64_t n_rows;
-  int32_t F;
+  int32_t F;                // feature-tile columns
+  int32_t Fs;               // row stride of X (input columns)
+  const int32_t *cols;      // tile column -> input column, or nullptr
   int32_t *leaf_ids;
   OutArgs out;
   const int32_t *tree_class;
@@ -142,7 +144,7 @@ __global__ __launch_bounds__(ROWS) void gemm_kernel(GemmArgs a) {
 
   if (X_LDS) {
     for (int f = 0; f < a.F; ++f)
-      xs[f * XS + tid] = (r0 + tid < a.n_rows) ? a.X[(r0 + tid) * a.F + f] : 0.0f;
+      xs[f * XS + tid] = (r0 + tid < a.n_rows) ? a.X[(r0 + tid) * a.Fs + xcol(a.cols, f)] : 0.0f;
   }
   if (CT_LDS) {
     const int row16 = a.k_pad / 16;
@@ -172,7 +174,7 @@ __global__ __launch_bounds__(ROWS) void gemm_kernel(GemmArgs a) {
 #pragma unroll
   for (int rt = 0; rt < 4; ++rt) {
     const int64_t rr = r0w + rt * 16 + r16;
-    xrow[rt] = a.X + (rr < a.n_rows ? rr : a.n_rows - 1) * a.F;
+    xrow[rt] = a.X + (rr < a.n_rows ? rr : a.n_rows - 1) * a.Fs;
   }
 
   const int n_chunks = (a.out.T + kTG - 1) / kTG;
@@ -202,7 +204,7 @@ __global__ __launch_bounds__(ROWS) void gemm_kernel(GemmArgs a) {
             uint32_t w = 0;
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
-              const float x = X_LDS ? xs[rec[b].y * XS + wave * 64 + rt * 16 + r16] : xrow[rt][rec[b].y];
+              const float x = X_LDS ? xs[rec[b].y * XS + wave * 64 + rt * 16 + r16] : xrow[rt][xcol(a.cols, rec[b].y)];
               w |= (x < as_float(rec[b].x) ? 0x40u : 0u) << (8 * b);
             }
             bop[rt][kb][q] = (int)w;
@@ -401,7 +403,8 @@ __global__ __launch_bounds__(ROWS) void gemm_pipe_kernel(GemmArgs a) {
   const size_t xbytes = ((size_t)a.F * XS * 4 + 15) / 16 * 16;
   int8_t *cts = reinterpret_cast<int8_t *>(smem + xbytes);
   int32_t *bias_s = reinterpret_cast<int32_t *>(smem + xbytes + (size_t)a.l_pad * ct_stride);
-  for (int f = 0; f < a.F; ++f) xs[f * XS + tid] = (r0 + tid < a.n_rows) ? a.X[(r0 + tid) * a.F + f] : 0.0f;
+  for (int f = 0; f < a.F; ++f)
+    xs[f * XS + tid] = (r0 + tid < a.n_rows) ? a.X[(r0 + tid) * a.Fs + xcol(a.cols, f)] : 0.0f;
   {
     const int row16 = a.k_pad / 16;
     for (int u = tid; u < a.l_pad * row16; u += ROWS) {
@@ -480,7 +483,7 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
   }
   const size_t nodes = 2 * (size_t)kTG * node_lds_bytes(t.k_pad);
   const size_t ct_bytes = (size_t)t.l_pad * (t.k_pad + kCtPad) + (size_t)t.l_pad * 4;
-  auto x_bytes = [&](int rows) { return ((size_t)e.n_features * (rows + 8) * 4 + 15) / 16 * 16; };
+  auto x_bytes = [&](int rows) { return ((size_t)e.n_cols * (rows + 8) * 4 + 15) / 16 * 16; };
   auto stage_bytes = [&](int rows) { return (size_t)(rows / 64) * 16 * (kIdGroup / 4) * 16; };
   const bool ct = t.n_shapes == 1 && ct_bytes + nodes + stage_bytes(256) <= (size_t)lds_max;
   int rows = 256;
@@ -512,7 +515,9 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
   GemmArgs a{};
   a.X = X;
   a.n_rows = n_rows;
-  a.F = e.n_features;
+  a.F = e.n_cols;
+  a.Fs = e.n_features;
+  a.cols = e.cols;
   a.leaf_ids = leaf_ids;
   a.out = OutArgs{scores, e.n_trees, e.n_outputs, e.aggregation, e.transform, e.base_score};
   a.tree_class = e.tree_class;

@@ -63,6 +63,11 @@ static_assert(kFastMaxLg < 15, "fast-kernel leaf ids must fit in 16 bits");
 // Ensemble-wide parameters every kernel needs.
 struct EnsembleDev {
   int32_t n_trees, n_features, n_outputs, leaf_dim;
+  // Feature tile: the kernels stage n_cols columns per row; column i is input
+  // column cols[i] (cols == nullptr: the identity, n_cols == n_features).
+  // n_features stays the row stride of X.
+  int32_t n_cols;
+  const int32_t *cols;
   int32_t aggregation, transform;
   const int32_t *tree_class;  // [T] device; output column of a scalar-leaf tree
   const float *base_score;    // [K] device, or nullptr

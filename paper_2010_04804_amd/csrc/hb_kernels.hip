@@ -36,7 +36,9 @@ constexpr size_t xtile_bytes(int F) { return ((size_t)F * kXStride * 4 + 15) / 1
 struct TravArgs {
   const float *X;
   int64_t n_rows;
-  int32_t F;
+  int32_t F;                  // feature-tile columns
+  int32_t Fs;                 // row stride of X (input columns)
+  const int32_t *cols;        // tile column -> input column, or nullptr
   float *scores;
   int32_t *leaf_ids;
   int32_t T, K, LD, aggregation, transform;
@@ -77,16 +79,16 @@ __global__ __launch_bounds__(kRows) void traverse_kernel(TravArgs a) {
   const int stage_stride = tc_full + ((tc_full & 1) ? 0 : 1);
 
   if (X_LDS) {
-    const float *src = a.X + r0 * a.F;
+    const float *src = a.X + r0 * a.Fs;
     const int total = kRows * a.F;
     for (int i = tid; i < total; i += kRows) {
       const int r = i / a.F;
       const int f = i - r * a.F;
-      xs[f * kXStride + r] = r < nblk ? src[i] : 0.0f;
+      xs[f * kXStride + r] = r < nblk ? src[(size_t)r * a.Fs + xcol(a.cols, f)] : 0.0f;
     }
   }
   // rows past the end read row n-1 (in bounds) and are never written
-  const float *xrow = a.X + (valid ? row : a.n_rows - 1) * a.F;
+  const float *xrow = a.X + (valid ? row : a.n_rows - 1) * a.Fs;
 
   double acc[KMAX];
 #pragma unroll
@@ -130,7 +132,7 @@ __global__ __launch_bounds__(kRows) void traverse_kernel(TravArgs a) {
         for (int g = 0; g < kGroup; ++g) {
           const uint2 rec = nodes[jj[g] * a.slots + idx[g]];
           const uint32_t f = PERFECT ? rec.y : (rec.y & 0xffffu);
-          const float x = X_LDS ? xs[f * kXStride + tid] : xrow[f];
+          const float x = X_LDS ? xs[f * kXStride + tid] : xrow[xcol(a.cols, f)];
           const bool go_left = x < as_float(rec.x);
           if (PERFECT)
             idx[g] = 2u * idx[g] + (go_left ? 0u : 1u);  // Algorithm 3's heap step
@@ -293,7 +295,7 @@ __global__ __launch_bounds__(kLaneThreads) void lanes_kernel(TravArgs a) {
   const int nr = (int)min((int64_t)R, a.n_rows - r0);
   for (int i = tid; i < R * a.F; i += kLaneThreads) {
     const int r = i / a.F;
-    xs[i] = r < nr ? a.X[r0 * a.F + i] : 0.0f;
+    xs[i] = r < nr ? a.X[(r0 + r) * a.Fs + xcol(a.cols, i - r * a.F)] : 0.0f;
   }
   __syncthreads();
   const int LD = LEAF_VEC ? a.LD : 1;
@@ -404,15 +406,17 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
                                {768, kFastTableSmall, fast_ptt_kernel_768},
                                {512, kFastTableLds, fast_ptt_kernel_512},
                                {512, kFastTableSmall, fast_ptt_kernel_512s},
-                               {256, kFastTableLds, fast_ptt_kernel_256}};
+                               {256, kFastTableLds, fast_ptt_kernel_256},
+                               {256, kFastTableSmall, fast_ptt_kernel_256s},
+                               {128, kFastTableSmall, fast_ptt_kernel_128}};
   static const Shape kTt[] = {{512, kFastTableLds, fast_tt_kernel_512}, {256, kFastTableLds, fast_tt_kernel_256}};
   const Shape *shapes = mode == 0 ? kPtt : kTt;
-  const int n_shapes = mode == 0 ? 5 : 2;
+  const int n_shapes = mode == 0 ? 7 : 2;
   // static LDS: the chunk buffer(s) and the leaf-id staging (16-bit ids of a
   // 32-tree group per row); dynamic LDS: the feature tile (F x rows floats)
   auto lds_of = [&](const Shape &sh) {
     const size_t table = (size_t)fast_bufs(tb, sh.budget) * fast_tc(tb, sh.budget) * tb;
-    return table + (size_t)sh.rows * kFastIdStageBytes + (size_t)e.n_features * sh.rows * 4;
+    return table + (size_t)sh.rows * kFastIdStageBytes + (size_t)e.n_cols * sh.rows * 4;
   };
   int best = -1;
   long best_waves = 0;
@@ -429,13 +433,15 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
   }
   if (best < 0) return kNotApplicable;
   const int rows = shapes[best].rows;
-  const size_t xbytes = (size_t)e.n_features * rows * 4;
+  const size_t xbytes = (size_t)e.n_cols * rows * 4;
   FastFn fn = shapes[best].get(lg, multi);
   if (!fn) return kNotApplicable;
   FastArgs a{};
   a.X = X;
   a.n_rows = n_rows;
-  a.F = e.n_features;
+  a.F = e.n_cols;
+  a.Fs = e.n_features;
+  a.cols = e.cols;
   a.leaf_ids = leaf_ids;
   a.out = OutArgs{scores, e.n_trees, e.n_outputs, e.aggregation, e.transform, e.base_score};
   a.tree_class = e.tree_class;
@@ -510,7 +516,9 @@ TravArgs common_args(const EnsembleDev &e, const float *X, int64_t n, float *sco
   TravArgs a{};
   a.X = X;
   a.n_rows = n;
-  a.F = e.n_features;
+  a.F = e.n_cols;
+  a.Fs = e.n_features;
+  a.cols = e.cols;
   a.scores = scores;
   a.leaf_ids = ids;
   a.T = e.n_trees;

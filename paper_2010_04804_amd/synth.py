@@ -42,6 +42,8 @@ __all__ = [
     "SWEEP",
     "sweep_model",
     "sweep_rows",
+    "narrow_use_model",
+    "narrow_use_rows",
 ]
 
 
@@ -247,6 +249,38 @@ def sweep_rows(n_rows: int) -> np.ndarray:
     """Input rows of the crossover sweep: N(0,1) over 200 features."""
     _, rng = _streams(SWEEP["seed"])
     return np.ascontiguousarray(_f32(rng.standard_normal((n_rows, SWEEP["n_features"]))))
+
+
+def narrow_use_model(n_features: int, n_used: int, n_trees: int, depth: int, seed: int,
+                     leaf_dim: int = 1) -> dict:
+    """Perfect trees over a wide input whose decision nodes test only
+    ``n_used`` of its ``n_features`` columns (a seeded random subset), the
+    case feature pruning serves. Thresholds N(0,1); scalar leaves N(0, 0.05)
+    summed, or (leaf_dim 2) probability pairs averaged."""
+    rng, _ = _streams(seed)
+    cols = np.sort(rng.choice(n_features, size=n_used, replace=False)).astype(np.int32)
+    if leaf_dim == 1:
+        leaves = lambda r, n: r.normal(0.0, 0.05, n)
+    else:
+        def leaves(r, n):
+            p = r.random(n)
+            return np.stack([1.0 - p, p], axis=1)
+    m = perfect_forest(rng, n_trees, depth, n_used, lambda r, f: r.standard_normal(f.size), leaves,
+                       leaf_dim=leaf_dim)
+    f = m["feature"]
+    m["feature"] = np.where(f >= 0, cols[np.maximum(f, 0)], -1).astype(np.int32)
+    m["n_features"] = n_features
+    if leaf_dim == 1:
+        m.update(n_outputs=1, tree_class=None, aggregation="sum", transform="none", base_score=None)
+    else:
+        m.update(n_outputs=leaf_dim, tree_class=None, aggregation="mean", transform="none", base_score=None)
+    return m
+
+
+def narrow_use_rows(n_features: int, n_rows: int, seed: int) -> np.ndarray:
+    """Rows for ``narrow_use_model``: N(0,1) in every column."""
+    _, rng = _streams(seed)
+    return np.ascontiguousarray(_f32(rng.standard_normal((n_rows, n_features))))
 
 
 def make_rows(cfg: int, n_rows: int) -> np.ndarray:

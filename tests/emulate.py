@@ -34,8 +34,16 @@ def _aggregate(model, values):
     return raw
 
 
+def _tile(h, X, strategy):
+    """The feature tile the kernels stage: the input columns some decision node
+    tests, in the order the compiled tables index them."""
+    cols = h.table(strategy, "features", np.int32).astype(np.int64)
+    return X[:, cols]
+
+
 def ptt(h, model, X):
     """Algorithm 3 (PerfectTreeTraversal) on the compiled heap tables."""
+    X = _tile(h, X, "ptt")
     info = h.info()
     T, D, ld = info["n_trees"], info["ptt_depth"], info["leaf_dim"]
     S = 1 << D
@@ -55,6 +63,7 @@ def ptt(h, model, X):
 
 def tt(h, model, X):
     """Algorithm 2 (TreeTraversal) on the compiled child tables."""
+    X = _tile(h, X, "tt")
     info = h.info()
     T, ld = info["n_trees"], info["leaf_dim"]
     n_pad = int(h.table("tt", "dims", np.int32)[0])
@@ -76,6 +85,7 @@ def tt(h, model, X):
 
 def gemm(h, model, X, check_unique=True):
     """Algorithm 1 (GEMM) on the compiled A/B (node), C^T, D (bias) and E tables."""
+    X = _tile(h, X, "gemm")
     info = h.info()
     T, ld = info["n_trees"], info["leaf_dim"]
     k_pad, l_pad, S = (int(v) for v in h.table("gemm", "dims", np.int32))

@@ -143,3 +143,32 @@ def test_selector_choices():
     assert host(synth.sweep_model("leafwise-d12")).select(1000) == "tt"
     assert host(synth.sweep_model("perfect-d7")).select(1) == "ptt"
     assert hb.compile(synth.make_model(2), strategy="tt", device=-1).select(10) == "tt"
+
+
+@pytest.mark.parametrize("leaf_dim", [1, 2])
+def test_feature_pruning_tables_and_emulation(leaf_dim):
+    """Feature selection injection (Sec. 5.2): a 3000-column input whose trees
+    test 37 columns compiles to tables indexed by rank among those 37; the
+    exported column list is exactly the tested set, and all three algorithms
+    run on the compact tables give the oracle's leaves and margins."""
+    m = synth.narrow_use_model(3000, 37, 12, 5, seed=31, leaf_dim=leaf_dim)
+    used = np.unique(m["feature"][m["feature"] >= 0])
+    h = host(m)
+    info = h.info()
+    assert info["n_features"] == 3000 and info["n_used_features"] == used.size
+    for s in ("ptt", "tt", "gemm"):
+        assert np.array_equal(h.table(s, "features", np.int32), used)
+    ptt_node = h.table("ptt", "node", np.uint32).reshape(-1, 2)
+    assert ptt_node[:, 1].max() < used.size
+    X = synth.narrow_use_rows(3000, 300, seed=31)
+    o_raw, _, o_ids = oracle.predict(m, X)
+    for s in ("ptt", "tt", "gemm"):
+        ids, raw = getattr(emulate, s)(h, m, X)
+        assert np.array_equal(ids, o_ids), s
+        assert np.allclose(raw, o_raw, rtol=1e-12, atol=1e-12), s
+
+
+def test_no_pruning_when_every_feature_is_tested():
+    h = host(synth.make_model(2))
+    assert h.info()["n_used_features"] == 28
+    assert np.array_equal(h.table("ptt", "features", np.int32), np.arange(28))

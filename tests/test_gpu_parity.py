@@ -122,6 +122,24 @@ def test_vector_leaf_forest_routes(n_features, n, strategy):
 
 
 @pytest.mark.parametrize("strategy", STRATEGIES)
+@pytest.mark.parametrize("used,leaf_dim,n", [(40, 1, 700), (40, 1, 20_000), (40, 1, 40_000), (40, 2, 9000),
+                                             (120, 1, 30_000), (200, 1, 20_001)])
+def test_pruned_wide_inputs(used, leaf_dim, n, strategy):
+    """2000-column rows whose trees test 40 (or 200) columns: the kernels
+    stage only those (gathered through the compiled column list), which puts
+    these batches on the row-parallel fast kernel (128, 256 and 512 rows)
+    instead of the wide-row path; small batches and vector leaves take the
+    other kernels."""
+    m = synth.narrow_use_model(2000, used, 64, 8, seed=41, leaf_dim=leaf_dim)
+    X = synth.narrow_use_rows(2000, n, seed=41)
+    say("pruned", strategy, used, leaf_dim, n)
+    h = hb.compile(m, device=0)
+    assert h.info()["n_used_features"] == used
+    scores, ids = run(h, X, strategy)
+    check(m, X, scores, ids, f"pruned ld{leaf_dim} n{n}/{strategy}")
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES)
 def test_empty_batch_enqueues_nothing(strategy):
     model, h = handle(1)
     say("empty", strategy)
