@@ -46,8 +46,8 @@ def load(path: str = _LIB):
     P = ctypes.c_void_p
     i32, i64 = ctypes.c_int32, ctypes.c_int64
     lib.oracle_predict.restype = ctypes.c_int
-    lib.oracle_predict.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P, P, i32, i32, P, P, i64,
-                                   P, P, P, i32]
+    lib.oracle_predict.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P, P, i32, i32, P, P, P,
+                                   i64, P, P, P, i32]
     if path == _LIB:
         _lib = lib
     return lib
@@ -83,6 +83,8 @@ def predict(model: dict, X: np.ndarray, leaves: bool = True, n_threads: int | No
     tc = None if tc is None else np.ascontiguousarray(tc, np.int32)
     bs = model.get("base_score")
     bs = None if bs is None else np.ascontiguousarray(bs, np.float32)
+    dl = model.get("default_left")
+    dl = None if dl is None else np.ascontiguousarray(dl, np.uint8)
     raw = np.empty((n, K), np.float64)
     out = np.empty((n, K), np.float64)
     ids = np.empty((n, T), np.int32) if leaves else None
@@ -91,7 +93,7 @@ def predict(model: dict, X: np.ndarray, leaves: bool = True, n_threads: int | No
     rc = lib.oracle_predict(T, F, K, int(model["leaf_dim"]), _ptr(arr["off"]), _ptr(arr["feature"]),
                             _ptr(arr["threshold"]), _ptr(arr["left"]), _ptr(arr["right"]),
                             _ptr(arr["value"]), _ptr(tc), AGG[model["aggregation"]],
-                            POST[model["transform"]], _ptr(bs), _ptr(X), n, _ptr(raw), _ptr(out),
+                            POST[model["transform"]], _ptr(bs), _ptr(dl), _ptr(X), n, _ptr(raw), _ptr(out),
                             _ptr(ids), int(n_threads))
     if rc != 0:
         raise ValueError(f"oracle: {ERRORS.get(rc, rc)}")

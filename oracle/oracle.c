@@ -17,7 +17,11 @@
  * decision node performs a strict < comparison) until a leaf is reached.
  *
  * Readings of the paper used here (each listed in the design notes):
- *  - ties x == t go right (strict <), NaN goes right (IEEE: NaN < t is false);
+ *  - ties x == t go right (strict <), NaN goes right (IEEE: NaN < t is false)
+ *    unless the caller gives the node a default direction: the paper leaves
+ *    missing values to future work (Sec. 4.1 notes they are not supported
+ *    yet), and this extension follows the common per-node "missing values go
+ *    left" flag of tree learners;
  *  - the reported leaf index is the caller's local node id of the leaf;
  *  - ensemble aggregation is SUM or MEAN (the paper's ReduceMean) over
  *    trees, per output column, plus an optional base score; the paper's
@@ -58,6 +62,7 @@ typedef struct {
   const int32_t *tree_class;       /* [n_trees] or NULL */
   int32_t aggregation, transform;
   const float *base_score;         /* [n_outputs] or NULL */
+  const uint8_t *default_left;     /* [nodes] or NULL: NaN goes left where 1 */
   const float *X;                  /* [n_rows, n_features] row-major */
   int64_t n_rows;
   double *raw;                     /* [n_rows, n_outputs] before transform */
@@ -75,8 +80,11 @@ static int64_t walk(const oracle_job *J, int32_t t, const float *x) {
     int32_t f = J->feature[base + v];
     if (f >= J->n_features) return ORACLE_ERR_FEATURE;
     if (++steps > count) return ORACLE_ERR_CYCLE;
-    /* Sec. 4.1: every decision node performs a strict < comparison. */
-    if (x[f] < J->threshold[base + v])
+    /* Sec. 4.1: every decision node performs a strict < comparison; a
+       missing (NaN) value follows the node's default direction if given. */
+    if (J->default_left && isnan(x[f]))
+      v = J->default_left[base + v] ? J->left[base + v] : J->right[base + v];
+    else if (x[f] < J->threshold[base + v])
       v = J->left[base + v];
     else
       v = J->right[base + v];
@@ -160,7 +168,8 @@ int oracle_predict(int32_t n_trees, int32_t n_features, int32_t n_outputs,
                    const int32_t *left, const int32_t *right,
                    const float *leaf_value, const int32_t *tree_class,
                    int32_t aggregation, int32_t transform,
-                   const float *base_score, const float *X, int64_t n_rows,
+                   const float *base_score, const uint8_t *default_left,
+                   const float *X, int64_t n_rows,
                    double *raw, double *out, int32_t *leaf_ids,
                    int32_t n_threads) {
   if (n_trees < 1 || n_features < 1 || n_outputs < 1 || n_rows < 0) return ORACLE_ERR_ARG;
@@ -180,8 +189,8 @@ int oracle_predict(int32_t n_trees, int32_t n_features, int32_t n_outputs,
 
   oracle_job J = {n_trees, n_features, n_outputs, leaf_dim, tree_node_offset,
                   feature, threshold, left, right, leaf_value, tree_class,
-                  aggregation, transform, base_score, X, n_rows, raw, out,
-                  leaf_ids};
+                  aggregation, transform, base_score, default_left, X, n_rows,
+                  raw, out, leaf_ids};
   if (n_threads < 1) n_threads = 1;
   if ((int64_t)n_threads > n_rows) n_threads = (int32_t)n_rows;
   oracle_slice *slices = (oracle_slice *)calloc((size_t)n_threads, sizeof(oracle_slice));

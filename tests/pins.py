@@ -39,15 +39,18 @@ def model_from_trees(trees, n_features, n_outputs=1, leaf_dim=1, tree_class=None
                      aggregation="sum", transform="none", base_score=None):
     """trees: list of lists of (feature, threshold, left, right, value or [values])."""
     off = [0]
-    f, t, l, r, v = [], [], [], [], []
+    f, t, l, r, v, dl = [], [], [], [], [], []
     for tr in trees:
-        for (ff, tt, ll, rr, vv) in tr:
+        for node in tr:
+            ff, tt, ll, rr, vv = node[:5]
             f.append(ff)
             t.append(tt)
             l.append(ll)
             r.append(rr)
+            dl.append(node[5] if len(node) > 5 else 0)
             v.extend(np.atleast_1d(np.asarray(vv, np.float64)).tolist() if leaf_dim > 1 else [vv])
         off.append(off[-1] + len(tr))
+    with_dl = any(len(node) > 5 for tr in trees for node in tr)
     return {
         "n_trees": len(trees), "n_features": n_features, "n_outputs": n_outputs,
         "leaf_dim": leaf_dim,
@@ -58,6 +61,7 @@ def model_from_trees(trees, n_features, n_outputs=1, leaf_dim=1, tree_class=None
         "tree_class": None if tree_class is None else np.asarray(tree_class, np.int32),
         "aggregation": aggregation, "transform": transform,
         "base_score": None if base_score is None else np.asarray(base_score, np.float32),
+        "default_left": np.asarray(dl, np.uint8) if with_dl else None,
     }
 
 
@@ -72,7 +76,8 @@ def load_golden(name="hand_traced_two_trees.txt"):
             if parts[0] == "node":
                 name_, nid = parts[1], int(parts[2])
                 ff, tt, ll, rr, vv = int(parts[3]), float(parts[4]), int(parts[5]), int(parts[6]), float(parts[7])
-                trees.setdefault(name_, {})[nid] = (ff, tt, ll, rr, vv)
+                node = (ff, tt, ll, rr, vv) if len(parts) < 9 else (ff, tt, ll, rr, vv, int(parts[8]))
+                trees.setdefault(name_, {})[nid] = node
             elif parts[0] == "row":
                 arrow = parts.index("->")
                 x = [float(s) for s in parts[1:arrow]]
@@ -106,11 +111,17 @@ def root_to_leaf_paths(feat, left, right):
 def brute_force_leaf(model, t, x):
     """The unique leaf whose every path predicate holds (asserts uniqueness)."""
     feat, thr, left, right = tree_view(model, t)
+    dl = model.get("default_left")
+    a = int(model["tree_node_offset"][t])
     hits = []
     for leaf, path in root_to_leaf_paths(feat, left, right).items():
         ok = True
         for node, went_left in path:
-            pred = bool(np.float32(x[feat[node]]) < np.float32(thr[node]))
+            xv = np.float32(x[feat[node]])
+            if dl is not None and np.isnan(xv):
+                pred = bool(dl[a + node])
+            else:
+                pred = bool(xv < np.float32(thr[node]))
             if pred != went_left:
                 ok = False
                 break
@@ -199,7 +210,24 @@ def ptt_leaf(feat, thr, left, right, x):
 # ---------------------------------------------------------------------------
 # pins
 
+def pin_golden_default_left(lib):
+    """Hand-traced missing values with per-node default directions."""
+    trees, rows = load_golden("hand_traced_default_left.txt")
+    m = model_from_trees(trees, 3)
+    X = np.asarray([r[0] for r in rows], np.float32)
+    raw, _, ids = oracle.predict(m, X, lib=lib, n_threads=2)
+    assert np.array_equal(ids, np.asarray([r[1] for r in rows], np.int32)), ids
+    assert np.array_equal(raw[:, 0], np.asarray([r[2] for r in rows]))
+    # no flags: the same rows follow the IEEE rule (NaN goes right everywhere)
+    m0 = dict(m, default_left=None)
+    _, _, ids0 = oracle.predict(m0, X, lib=lib)
+    m1 = dict(m, default_left=np.zeros_like(m["default_left"]))
+    _, _, ids1 = oracle.predict(m1, X, lib=lib)
+    assert np.array_equal(ids0, ids1)
+
+
 def pin_golden(lib):
+    pin_golden_default_left(lib)
     trees, rows = load_golden()
     m = model_from_trees(trees, 3)
     X = np.asarray([r[0] for r in rows], np.float32)
@@ -263,6 +291,8 @@ def pin_brute_force(lib, seeds=range(6), n_rows=60):
     for seed in seeds:
         m = random_small_ensemble(seed)
         rng = np.random.Generator(np.random.PCG64(seed + 77))
+        if seed % 2:  # per-node default directions for missing values
+            m["default_left"] = (rng.random(m["feature"].size) < 0.5).astype(np.uint8)
         X = tricky_rows(rng, m, n_rows)
         raw, _, ids = oracle.predict(m, X, lib=lib, n_threads=3)
         for r in range(n_rows):

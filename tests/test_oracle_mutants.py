@@ -27,6 +27,9 @@ MUTANTS = {
     "last_tree_skipped": ("for (int32_t t = 0; t < J->n_trees; ++t) {\n      int64_t leaf",
                           "for (int32_t t = 0; t < J->n_trees - 1; ++t) {\n      int64_t leaf"),
     "feature_off_by_one": ("if (x[f] < J->threshold", "if (x[f == 0 ? 0 : f - 1] < J->threshold"),
+    "default_left_ignored": ("if (J->default_left && isnan(x[f]))", "if (0)"),
+    "default_left_inverted": ("J->default_left[base + v] ? J->left[base + v] : J->right[base + v]",
+                              "J->default_left[base + v] ? J->right[base + v] : J->left[base + v]"),
 }
 
 PINS = [pins.pin_golden, pins.pin_brute_force, pins.pin_gemm_closed_form, pins.pin_closed_forms,
