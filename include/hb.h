@@ -90,6 +90,17 @@ typedef struct hb_ensemble_desc {
   int32_t aggregation;             /* enum hb_aggregation                    */
   int32_t transform;               /* enum hb_transform                      */
   const float *base_score;         /* [n_outputs] added after aggregation, or NULL */
+  const uint8_t *default_left;     /* [nodes] or NULL; read at internal nodes only.
+                                      Missing values: a NaN feature value goes to
+                                      the left child where this is 1 and to the
+                                      right child where it is 0 (NULL: right
+                                      everywhere, which is also what x < t gives
+                                      for NaN). Values other than 0/1 are
+                                      HB_ERR_INVALID_MODEL; a 1 on a node whose
+                                      threshold is -inf is HB_ERR_UNSUPPORTED.
+                                      The paper leaves missing values to future
+                                      work (Sec. 4.1); this is the per-node
+                                      default direction of common tree learners. */
 } hb_ensemble_desc;
 
 typedef struct hb_handle hb_handle;
@@ -105,9 +116,12 @@ typedef struct hb_info {
   int64_t table_bytes[4];          /* bytes of compiled tensors per strategy */
   int32_t gemm_shapes;             /* distinct tree shapes (C/D matrices)    */
   int32_t ptt_depth;               /* D used by PTT (= max_depth)            */
-  int32_t n_used_features;         /* input columns some decision node tests
-                                      (the kernels stage only these; equals
-                                      n_features when every column is used) */
+  int32_t n_used_features;         /* feature columns the kernels stage: the
+                                      input columns some decision node tests,
+                                      one more for each column that nodes with
+                                      default_left = 1 test (n_features when
+                                      every column is tested and no node sends
+                                      missing values left) */
 } hb_info;
 
 /*
@@ -164,8 +178,10 @@ int hb_query(const hb_handle *h, hb_info *info);
  *         "bias" (int32 [S][l_pad]), "leaf_value" (float [T][l_pad][leaf_dim]),
  *         "leaf_id" (int32 [T][l_pad]), "dims" (int32 {k_pad, l_pad, S})
  *   any : "features" (int32 [n_used_features]: the input column of each
- *         feature index the tables above use; when n_used_features <
- *         n_features the tables hold these ranks instead of input columns)
+ *         feature index the tables above use, in bits 0-29; bit 30 set
+ *         means that index reads a NaN input as -inf, for the nodes that
+ *         send missing values left. Unless this is the identity, the tables
+ *         hold these indices instead of input columns)
  * Returns HB_ERR_INVALID_ARG for an unknown name or an infeasible strategy.
  */
 int hb_table(const hb_handle *h, int strategy, const char *name, const void **data, int64_t *bytes);

@@ -37,6 +37,7 @@ class hb_ensemble_desc(ctypes.Structure):
         ("tree_node_offset", _P), ("feature", _P), ("threshold", _P), ("left", _P),
         ("right", _P), ("leaf_value", _P), ("tree_class", _P),
         ("aggregation", ctypes.c_int32), ("transform", ctypes.c_int32), ("base_score", _P),
+        ("default_left", _P),
     ]
 
 
@@ -164,6 +165,7 @@ def compile(model: dict, strategy="auto", device: int = 0) -> Handle:
         "value": _arr(model["leaf_value"], np.float32),
         "tree_class": _arr(model.get("tree_class"), np.int32),
         "base": _arr(model.get("base_score"), np.float32),
+        "default_left": _arr(model.get("default_left"), np.uint8),
     }
 
     def p(a):
@@ -173,7 +175,7 @@ def compile(model: dict, strategy="auto", device: int = 0) -> Handle:
         int(model["n_trees"]), int(model["n_features"]), int(model["n_outputs"]),
         int(model["leaf_dim"]), p(keep["off"]), p(keep["feature"]), p(keep["threshold"]),
         p(keep["left"]), p(keep["right"]), p(keep["value"]), p(keep["tree_class"]),
-        AGG[model["aggregation"]], POST[model["transform"]], p(keep["base"]))
+        AGG[model["aggregation"]], POST[model["transform"]], p(keep["base"]), p(keep["default_left"]))
     h = _P()
     _check(lib.hb_compile(ctypes.byref(d), _strategy(strategy), int(device), ctypes.byref(h)))
     return Handle(h.value, device)

@@ -36,6 +36,7 @@ uint32_t fbits(float f) {
 struct CanonTree {
   std::vector<int32_t> caller;  // canonical -> caller-local id
   std::vector<int32_t> feat;    // -1 at leaves
+  std::vector<uint8_t> dleft;   // 1: a missing (NaN) value goes left at this node
   std::vector<float> thr;
   std::vector<int32_t> left;    // canonical left child (right = left + 1), -1 at leaves
   std::vector<int32_t> parent;  // -1 at the root
@@ -66,6 +67,12 @@ int canonicalise(const hb_ensemble_desc *d, int32_t t, CanonTree *ct) {
     if (std::isnan(d->threshold[base + v]))
       return fail(HB_ERR_INVALID_MODEL, "tree " + std::to_string(t) + " node " +
                                             std::to_string(v) + ": NaN threshold");
+    if (d->default_left && d->default_left[base + v] > 1)
+      return fail(HB_ERR_INVALID_MODEL, "tree " + std::to_string(t) + " node " +
+                                            std::to_string(v) + ": default_left must be 0 or 1");
+    if (d->default_left && d->default_left[base + v] && d->threshold[base + v] == -INFINITY)
+      return fail(HB_ERR_UNSUPPORTED, "tree " + std::to_string(t) + " node " + std::to_string(v) +
+                                          ": a node that sends missing values left cannot have threshold -inf");
     const int32_t kids[2] = {d->left[base + v], d->right[base + v]};
     for (int32_t c : kids) {
       if (c < 0 || c >= n)
@@ -83,6 +90,7 @@ int canonicalise(const hb_ensemble_desc *d, int32_t t, CanonTree *ct) {
                                           std::to_string(n - (int32_t)ct->caller.size()) +
                                           " node(s) unreachable from the root");
   ct->feat.assign(n, -1);
+  ct->dleft.assign(n, 0);
   ct->thr.assign(n, 0.0f);
   ct->left.assign(n, -1);
   ct->parent.assign(n, -1);
@@ -99,6 +107,7 @@ int canonicalise(const hb_ensemble_desc *d, int32_t t, CanonTree *ct) {
     }
     ++ct->n_internal;
     ct->feat[c] = f;
+    ct->dleft[c] = d->default_left ? d->default_left[base + v] : 0;
     ct->thr[c] = d->threshold[base + v];
     const int32_t l = canon_of[d->left[base + v]];
     const int32_t r = canon_of[d->right[base + v]];
@@ -484,23 +493,29 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
   // node tests are pruned and the decision variables re-indexed. The kernels
   // then stage only the columns some node tests (a narrower LDS tile, so
   // wide inputs reach the faster kernels), and the tables address a column by
-  // its rank among those.
+  // its rank among those. Missing values: a column that nodes with the
+  // default-left flag test gets a second tile column that reads NaN as -inf
+  // (then x < t holds for every finite or +inf threshold, so NaN goes left),
+  // and those nodes test that column; every other node sees NaN, which no
+  // x < t accepts, so NaN goes right. The walk itself is unchanged.
   {
-    std::vector<int32_t> rank(d->n_features, -1);
+    std::vector<int32_t> rank(2 * (size_t)d->n_features, -1);  // [column][default-left]
     for (const CanonTree &ct : trees)
-      for (int32_t f : ct.feat)
-        if (f >= 0) rank[f] = 0;
-    for (int32_t f = 0; f < d->n_features; ++f)
-      if (rank[f] == 0) {
-        rank[f] = (int32_t)h->cols.size();
-        h->cols.push_back(f);
+      for (int32_t c = 0; c < ct.size(); ++c)
+        if (ct.feat[c] >= 0) rank[2 * (size_t)ct.feat[c] + ct.dleft[c]] = 0;
+    bool variant = false;
+    for (size_t k = 0; k < rank.size(); ++k)
+      if (rank[k] == 0) {
+        rank[k] = (int32_t)h->cols.size();
+        h->cols.push_back((int32_t)(k >> 1) | ((k & 1) ? hb::kColNanLeft : 0));
+        variant |= (k & 1) != 0;
       }
     if (h->cols.empty()) h->cols.push_back(0);  // only single-leaf trees: one dummy column
-    h->pruned = (int32_t)h->cols.size() < d->n_features;
+    h->pruned = variant || (int32_t)h->cols.size() < d->n_features;
     if (h->pruned)
       for (CanonTree &ct : trees)
-        for (int32_t &f : ct.feat)
-          if (f >= 0) f = rank[f];
+        for (int32_t c = 0; c < ct.size(); ++c)
+          if (ct.feat[c] >= 0) ct.feat[c] = rank[2 * (size_t)ct.feat[c] + ct.dleft[c]];
   }
   const int32_t n_cols = h->pruned ? (int32_t)h->cols.size() : d->n_features;
   hb_info &I = h->info;

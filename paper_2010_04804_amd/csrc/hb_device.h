@@ -151,9 +151,15 @@ __device__ __forceinline__ void flush_ids(int32_t *leaf_ids, int64_t n_rows, int
 // stride of one feature column of the row tile is exactly the row count, so a
 // lane's gather x[f] hits bank (lane mod 32) whatever feature each lane needs.
 
-// Input column of feature-tile column f (the ensemble's used features, or the
-// identity when cols is null).
-__device__ __forceinline__ int xcol(const int32_t *cols, int f) { return cols ? cols[f] : f; }
+// Feature-tile column f of an input row: the identity when cols is null, else
+// input column cols[f] & kColMask, with a NaN read as -inf when the column
+// serves nodes that send missing values left.
+__device__ __forceinline__ float xval(const float *row, const int32_t *cols, int f) {
+  if (!cols) return row[f];
+  const int c = cols[f];
+  const float v = row[c & kColMask];
+  return ((c & kColNanLeft) && __builtin_isnan(v)) ? -__builtin_inff() : v;
+}
 
 struct FastArgs {
   const float *X;

@@ -309,7 +309,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
         fxs[(f + 3) * ROWS + tid] = v.w;
       }
     } else {
-      for (int f = 0; f < a.F; ++f) fxs[f * ROWS + tid] = valid ? src[xcol(a.cols, f)] : 0.0f;
+      for (int f = 0; f < a.F; ++f) fxs[f * ROWS + tid] = valid ? xval(src, a.cols, f) : 0.0f;
     }
   }
   lds_barrier();

@@ -144,7 +144,7 @@ __global__ __launch_bounds__(ROWS) void gemm_kernel(GemmArgs a) {
 
   if (X_LDS) {
     for (int f = 0; f < a.F; ++f)
-      xs[f * XS + tid] = (r0 + tid < a.n_rows) ? a.X[(r0 + tid) * a.Fs + xcol(a.cols, f)] : 0.0f;
+      xs[f * XS + tid] = (r0 + tid < a.n_rows) ? xval(a.X + (r0 + tid) * a.Fs, a.cols, f) : 0.0f;
   }
   if (CT_LDS) {
     const int row16 = a.k_pad / 16;
@@ -204,7 +204,7 @@ __global__ __launch_bounds__(ROWS) void gemm_kernel(GemmArgs a) {
             uint32_t w = 0;
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
-              const float x = X_LDS ? xs[rec[b].y * XS + wave * 64 + rt * 16 + r16] : xrow[rt][xcol(a.cols, rec[b].y)];
+              const float x = X_LDS ? xs[rec[b].y * XS + wave * 64 + rt * 16 + r16] : xval(xrow[rt], a.cols, rec[b].y);
               w |= (x < as_float(rec[b].x) ? 0x40u : 0u) << (8 * b);
             }
             bop[rt][kb][q] = (int)w;
@@ -404,7 +404,7 @@ __global__ __launch_bounds__(ROWS) void gemm_pipe_kernel(GemmArgs a) {
   int8_t *cts = reinterpret_cast<int8_t *>(smem + xbytes);
   int32_t *bias_s = reinterpret_cast<int32_t *>(smem + xbytes + (size_t)a.l_pad * ct_stride);
   for (int f = 0; f < a.F; ++f)
-    xs[f * XS + tid] = (r0 + tid < a.n_rows) ? a.X[(r0 + tid) * a.Fs + xcol(a.cols, f)] : 0.0f;
+    xs[f * XS + tid] = (r0 + tid < a.n_rows) ? xval(a.X + (r0 + tid) * a.Fs, a.cols, f) : 0.0f;
   {
     const int row16 = a.k_pad / 16;
     for (int u = tid; u < a.l_pad * row16; u += ROWS) {

@@ -84,7 +84,7 @@ __global__ __launch_bounds__(kRows) void traverse_kernel(TravArgs a) {
     for (int i = tid; i < total; i += kRows) {
       const int r = i / a.F;
       const int f = i - r * a.F;
-      xs[f * kXStride + r] = r < nblk ? src[(size_t)r * a.Fs + xcol(a.cols, f)] : 0.0f;
+      xs[f * kXStride + r] = r < nblk ? xval(src + (size_t)r * a.Fs, a.cols, f) : 0.0f;
     }
   }
   // rows past the end read row n-1 (in bounds) and are never written
@@ -132,7 +132,7 @@ __global__ __launch_bounds__(kRows) void traverse_kernel(TravArgs a) {
         for (int g = 0; g < kGroup; ++g) {
           const uint2 rec = nodes[jj[g] * a.slots + idx[g]];
           const uint32_t f = PERFECT ? rec.y : (rec.y & 0xffffu);
-          const float x = X_LDS ? xs[f * kXStride + tid] : xrow[xcol(a.cols, f)];
+          const float x = X_LDS ? xs[f * kXStride + tid] : xval(xrow, a.cols, f);
           const bool go_left = x < as_float(rec.x);
           if (PERFECT)
             idx[g] = 2u * idx[g] + (go_left ? 0u : 1u);  // Algorithm 3's heap step
@@ -295,7 +295,7 @@ __global__ __launch_bounds__(kLaneThreads) void lanes_kernel(TravArgs a) {
   const int nr = (int)min((int64_t)R, a.n_rows - r0);
   for (int i = tid; i < R * a.F; i += kLaneThreads) {
     const int r = i / a.F;
-    xs[i] = r < nr ? a.X[(r0 + r) * a.Fs + xcol(a.cols, i - r * a.F)] : 0.0f;
+    xs[i] = r < nr ? xval(a.X + (r0 + r) * a.Fs, a.cols, i - r * a.F) : 0.0f;
   }
   __syncthreads();
   const int LD = LEAF_VEC ? a.LD : 1;

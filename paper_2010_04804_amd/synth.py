@@ -44,6 +44,7 @@ __all__ = [
     "sweep_rows",
     "narrow_use_model",
     "narrow_use_rows",
+    "with_missing",
 ]
 
 
@@ -281,6 +282,20 @@ def narrow_use_rows(n_features: int, n_rows: int, seed: int) -> np.ndarray:
     """Rows for ``narrow_use_model``: N(0,1) in every column."""
     _, rng = _streams(seed)
     return np.ascontiguousarray(_f32(rng.standard_normal((n_rows, n_features))))
+
+
+def with_missing(model: dict, X: np.ndarray, seed: int, p_left: float = 0.5, p_missing: float = 0.1):
+    """The same model with a random default direction per node (left with
+    probability ``p_left``) and a copy of ``X`` with a fraction ``p_missing``
+    of its values replaced by NaN; returns ``(model, X)``."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    m = dict(model)
+    m["default_left"] = (rng.random(model["feature"].size) < p_left).astype(np.uint8)
+    # a default-left node may not test against -inf
+    m["default_left"][(model["feature"] >= 0) & (model["threshold"] == -np.inf)] = 0
+    Xm = np.array(X, np.float32, copy=True)
+    Xm[rng.random(Xm.shape) < p_missing] = np.nan
+    return m, Xm
 
 
 def make_rows(cfg: int, n_rows: int) -> np.ndarray:

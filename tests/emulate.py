@@ -36,9 +36,15 @@ def _aggregate(model, values):
 
 def _tile(h, X, strategy):
     """The feature tile the kernels stage: the input columns some decision node
-    tests, in the order the compiled tables index them."""
+    tests, in the order the compiled tables index them; a column flagged for
+    nodes that send missing values left reads NaN as -inf."""
     cols = h.table(strategy, "features", np.int32).astype(np.int64)
-    return X[:, cols]
+    tile = X[:, cols & ((1 << 30) - 1)].copy()
+    nan_left = (cols >> 30) & 1 == 1
+    sub = tile[:, nan_left]
+    sub[np.isnan(sub)] = -np.inf
+    tile[:, nan_left] = sub
+    return tile
 
 
 def ptt(h, model, X):

@@ -93,3 +93,18 @@ def test_destroy_twice_via_close_is_safe():
     h.close()
     with pytest.raises(RuntimeError):
         h.info()
+
+
+def test_default_left_validation():
+    trees, rows = pins.load_golden("hand_traced_default_left.txt")
+    m = pins.model_from_trees(trees, 3)
+    hb.compile(m, device=-1).close()
+    bad = dict(m, default_left=np.where(m["default_left"] > 0, 2, 0).astype(np.uint8))
+    with pytest.raises(hb.HBError) as e:
+        hb.compile(bad, device=-1)
+    assert e.value.code == -2  # HB_ERR_INVALID_MODEL
+    ninf = dict(m, threshold=m["threshold"].copy())
+    ninf["threshold"][0] = -np.inf  # tree A's root sends missing values left
+    with pytest.raises(hb.HBError) as e:
+        hb.compile(ninf, device=-1)
+    assert e.value.code == -3  # HB_ERR_UNSUPPORTED

@@ -172,3 +172,32 @@ def test_no_pruning_when_every_feature_is_tested():
     h = host(synth.make_model(2))
     assert h.info()["n_used_features"] == 28
     assert np.array_equal(h.table("ptt", "features", np.int32), np.arange(28))
+
+
+@pytest.mark.parametrize("strategy", ["ptt", "tt", "gemm"])
+@pytest.mark.parametrize("cfg", [1, 5])
+def test_missing_values_default_directions(cfg, strategy):
+    """Per-node default directions for NaN: the compiled tables send a node's
+    missing values through a tile column that reads NaN as -inf (left) or
+    through the plain column (right); emulating the algorithms on them gives
+    the oracle's leaves."""
+    m, X = synth.with_missing(synth.make_model(cfg), synth.make_rows(cfg, 300), seed=cfg)
+    h = host(m)
+    cols = h.table(strategy, "features", np.int32)
+    assert ((cols >> 30) & 1).any() and ((cols >> 30) & 1 == 0).any()
+    ids, raw = getattr(emulate, strategy)(h, m, X)
+    o_raw, _, o_ids = oracle.predict(m, X)
+    assert np.array_equal(ids, o_ids)
+    assert np.allclose(raw, o_raw, rtol=1e-12, atol=1e-12)
+
+
+def test_missing_values_tricky_ensembles():
+    for seed in range(4):
+        m = pins.random_small_ensemble(seed)
+        X = pins.tricky_rows(np.random.Generator(np.random.PCG64(seed)), m, 200)
+        m, _ = synth.with_missing(m, X[:1], seed=seed)
+        h = host(m)
+        o_raw, _, o_ids = oracle.predict(m, X)
+        for s in ("ptt", "tt", "gemm"):
+            ids, raw = getattr(emulate, s)(h, m, X)
+            assert np.array_equal(ids, o_ids), (seed, s)

@@ -140,6 +140,32 @@ def test_pruned_wide_inputs(used, leaf_dim, n, strategy):
 
 
 @pytest.mark.parametrize("strategy", STRATEGIES)
+@pytest.mark.parametrize("cfg,n", [(2, 1000), (2, 12_000), (2, 40_000), (3, 2000), (4, 3000), (4, 40_000),
+                                   (5, 20_000)])
+def test_missing_values_parity(cfg, n, strategy):
+    """Per-node default directions for NaN (half the nodes send missing values
+    left, 10% of the inputs missing) on every kernel path: tree-parallel,
+    row-parallel fast shapes, general, GEMM."""
+    model, _ = handle(cfg)
+    m, X = synth.with_missing(model, synth.make_rows(cfg, n), seed=cfg + n)
+    say("missing", cfg, n, strategy)
+    h = hb.compile(m, device=0)
+    scores, ids = run(h, X, strategy)
+    check(m, X, scores, ids, f"missing cfg{cfg}/{n}/{strategy}")
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES)
+def test_hand_traced_default_left(strategy):
+    trees, rows = pins.load_golden("hand_traced_default_left.txt")
+    m = pins.model_from_trees(trees, 3)
+    X = np.asarray([r[0] for r in rows], np.float32)
+    say("hand-traced default-left", strategy)
+    scores, ids = run(hb.compile(m, device=0), X, strategy)
+    assert np.array_equal(ids, np.asarray([r[1] for r in rows], np.int32))
+    assert np.allclose(scores[:, 0], [r[2] for r in rows], rtol=1e-6, atol=0)
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES)
 def test_empty_batch_enqueues_nothing(strategy):
     model, h = handle(1)
     say("empty", strategy)
