@@ -255,6 +255,50 @@ def run_pruning():
         h.close()
 
 
+def run_configs():
+    """Every workload (1-5) at its batch size, every feasible strategy, with
+    and without leaf ids: ms per call (HIP events), rows/s, and the fraction
+    of the roofline that bounds it (HBM for the traversals, int8 MFMA for
+    GEMM). One JSON line per point."""
+    import torch
+
+    import paper_2010_04804_amd as hb
+    from paper_2010_04804_amd import synth
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    for cfg in sorted(synth.CONFIGS):
+        n = synth.CONFIGS[cfg]["n_rows"]
+        model = synth.make_model(cfg)
+        h = hb.compile(model, device=0)
+        info = h.info()
+        X = torch.from_numpy(synth.make_rows(cfg, n)).to(dev)
+        scores = torch.empty((n, info["n_outputs"]), dtype=torch.float32, device=dev)
+        ids = torch.empty((n, info["n_trees"]), dtype=torch.int32, device=dev)
+        auto = h.select(n)
+        for s in ("ptt", "tt", "gemm"):
+            if not info["feasible"][s]:
+                continue
+            for leaves in (True, False):
+                fn = lambda: hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(),
+                                            ids.data_ptr() if leaves else None, s, stream.cuda_stream)
+                fn()
+                torch.cuda.synchronize()
+                probe = _event_ms(stream, fn, 1)
+                ms = _event_ms(stream, fn, int(min(20, max(2, 300.0 / max(probe, 1e-3)))))
+                if s == "gemm":
+                    frac = gemm_ops(model, n) / (ms * 1e-3) / INT8_PEAK
+                else:
+                    frac = algorithmic_bytes(info, n, leaves, s) / (ms * 1e-3) / HBM_PEAK
+                print(json.dumps({"workload": cfg, "name": synth.CONFIGS[cfg]["name"], "rows": n,
+                                  "strategy": s, "auto": s == auto, "leaf_ids": leaves,
+                                  "ms": round(ms, 4), "rows_per_s": n / (ms * 1e-3),
+                                  "bound": "mfma" if s == "gemm" else "hbm", "frac": frac}), flush=True)
+        del X, scores, ids
+        h.close()
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -274,6 +318,8 @@ def main():
                     help="small-batch latency (eager and graph-replayed) instead of the bench line")
     ap.add_argument("--pruning", action="store_true",
                     help="wide inputs whose trees test few columns, instead of the bench line")
+    ap.add_argument("--configs", action="store_true",
+                    help="every workload and strategy against its roofline, instead of the bench line")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": f"--gpus {args.gpus}: this build runs on one GPU only. Rows are "
@@ -287,6 +333,8 @@ def main():
         return run_latency(args.config)
     if args.pruning:
         return run_pruning()
+    if args.configs:
+        return run_configs()
 
     import torch
 
