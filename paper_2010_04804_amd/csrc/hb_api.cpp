@@ -303,17 +303,17 @@ void build_fast(hb_handle *h, const hb_ensemble_desc *d, const std::vector<Canon
       const CanonTree &ct = trees[t];
       const int64_t base = d->tree_node_offset[t];
       uint32_t *blk = &h->tt_fast[(size_t)t * words];
+      const uint32_t ninf = fbits(-std::numeric_limits<float>::infinity());
       for (size_t c = 0; c < NP; ++c) {
-        uint32_t *rec = blk + 4 * c;
+        uint32_t *rec = blk + 2 * c;
         if (c < (size_t)ct.size() && ct.feat[c] >= 0) {
           rec[0] = fbits(ct.thr[c]);
-          rec[1] = (uint32_t)ct.feat[c];
-          rec[2] = 16u * (uint32_t)ct.left[c];
-          rec[3] = 16u * (uint32_t)(ct.left[c] + 1);
-        } else {
-          rec[2] = rec[3] = 16u * (uint32_t)c;  // leaves (and padding) stay put
+          rec[1] = (uint32_t)ct.feat[c] | (8u * (uint32_t)(ct.left[c] + 1)) << 16;
+        } else {  // leaves (and padding) stay put: no x is below -inf
+          rec[0] = ninf;
+          rec[1] = (8u * (uint32_t)c) << 16;
         }
-        uint32_t *lr = blk + 4 * NP + 2 * c;
+        uint32_t *lr = blk + 2 * NP + 2 * c;
         if (c < (size_t)ct.size()) {
           const int32_t v = ct.caller[c];
           lr[0] = ct.feat[c] < 0 ? fbits(d->leaf_value[base + v]) : 0u;

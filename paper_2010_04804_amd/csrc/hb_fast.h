@@ -20,8 +20,9 @@ namespace {
 //   * PTT: heap index a lives as s = 8a; the child is 2s + 8*(x >= t) and,
 //     after D steps, s is exactly the offset of the leaf record (leaves follow
 //     the 2^D node slots);
-//   * TT: a node record {threshold, feature, left offset, right offset}
-//     makes a step one select; leaves point to themselves;
+//   * TT: a node record {threshold, feature | 8 * right << 16} (children are
+//     adjacent, left = right - 1) makes a step one shift and one subtract of
+//     8 or 0; a leaf holds threshold -inf and points to itself;
 //   * multi-output: the output column of each tree is uniform across a wave,
 //     so the per-row double accumulators are updated by register index (the
 //     columns of a chunk are loaded one chunk ahead, lane g holding tree g's).
@@ -220,16 +221,16 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
     for (int lvl = 0; lvl < levels; ++lvl) {
 #pragma unroll
       for (int g = 0; g < TC; ++g) {
-        const uint4 rec = *reinterpret_cast<const uint4 *>(base + g * TB + s[g]);
-        const float x = *reinterpret_cast<const float *>(xb + __umul24(rec.y, ROWS * 4u) + lane4);
-        s[g] = x < as_float(rec.x) ? rec.z : rec.w;  // Algorithm 2's step: left or right child
+        const uint2 rec = *reinterpret_cast<const uint2 *>(base + g * TB + s[g]);
+        const float x = *reinterpret_cast<const float *>(xb + __umul24(rec.y & 0xffffu, ROWS * 4u) + lane4);
+        s[g] = (rec.y >> 16) - (x < as_float(rec.x) ? 8u : 0u);  // Algorithm 2's step: left or right child
       }
     }
   }
 #pragma unroll
   for (int g = 0; g < TC; ++g) {
     const int t = t0 + g;
-    const uint32_t loff = MODE == 0 ? s[g] : (1u << LG) * 16u + (s[g] >> 1);
+    const uint32_t loff = MODE == 0 ? s[g] : (1u << LG) * 8u + s[g];
     const uint2 lr = *reinterpret_cast<const uint2 *>(base + g * TB + loff);
     put_id(ids, Q * TC + g, lr.y);
     if (t < a.out.T) {

@@ -38,7 +38,7 @@ constexpr int kFastIdGroup = 32;
 // nodes. Each wave stages 16 of its 64 rows at a time (a 32-tree group of
 // 16-bit ids per row), so the staging costs 16 bytes per row of a workgroup.
 constexpr int kFastIdStageBytes = 16 * kFastIdGroup * 2 / 64;
-constexpr int fast_node_bytes(int mode) { return mode == 0 ? 8 : 16; }
+constexpr int fast_node_bytes(int mode) { return (void)mode, 8; }
 constexpr int fast_tree_bytes(int mode, int lg) { return (1 << lg) * (fast_node_bytes(mode) + 8); }
 constexpr int fast_pow2_fit(int budget, int tree_bytes) {
   int t = 16;

@@ -409,9 +409,13 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
                                {256, kFastTableLds, fast_ptt_kernel_256},
                                {256, kFastTableSmall, fast_ptt_kernel_256s},
                                {128, kFastTableSmall, fast_ptt_kernel_128}};
-  static const Shape kTt[] = {{512, kFastTableLds, fast_tt_kernel_512}, {256, kFastTableLds, fast_tt_kernel_256}};
+  static const Shape kTt[] = {{512, kFastTableLds, fast_tt_kernel_512},
+                              {512, kFastTableSmall, fast_tt_kernel_512s},
+                              {256, kFastTableLds, fast_tt_kernel_256},
+                              {256, kFastTableSmall, fast_tt_kernel_256s},
+                              {128, kFastTableSmall, fast_tt_kernel_128}};
   const Shape *shapes = mode == 0 ? kPtt : kTt;
-  const int n_shapes = mode == 0 ? 7 : 2;
+  const int n_shapes = mode == 0 ? 7 : 5;
   // static LDS: the chunk buffer(s) and the leaf-id staging (16-bit ids of a
   // 32-tree group per row); dynamic LDS: the feature tile (F x rows floats)
   auto lds_of = [&](const Shape &sh) {
