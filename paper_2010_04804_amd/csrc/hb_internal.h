@@ -22,15 +22,17 @@ constexpr int64_t kTreeLdsLimit = 160 * 1024 - 4 * 1024;
 //   PTT (mode 0, lg = D): node record p = {threshold bits, feature} for heap
 //     index p in [1, 2^D) (slot 0 unused); the leaf record of heap index
 //     a in [2^D, 2^(D+1)) sits at byte 8a of the block.
-//   TT (mode 1, 2^lg >= nodes): node record c = {threshold bits, feature,
-//     16 * left child, 16 * right child} (16 bytes; a leaf points to itself
-//     on both sides); the leaf record of node c sits at 16 * 2^lg + 8c.
+//   TT (mode 1, 2^lg >= nodes): node record c = {threshold bits, feature |
+//     8 * right child << 16} (children adjacent: left = right - 1; a leaf
+//     holds threshold -inf and points to itself); the leaf record of node c
+//     sits at 8 * 2^lg + 8c.
 // Blocks are grouped in chunks of fast_tc() trees staged through LDS, either
 // double-buffered (the next chunk is stored while nobody reads its buffer) or
 // single-buffered with twice as many trees per chunk (more independent walks
 // per wave, one extra barrier per chunk), whichever fits more trees in the
-// 64 KiB table budget. Leaf ids are flushed every kFastIdGroup trees, and the
-// tree count is padded with zero blocks to a multiple of kFastIdGroup.
+// kernel's table budget (64 or 32 KiB). Leaf ids are flushed every
+// kFastIdGroup trees, and the tree count is padded with zero blocks to a
+// multiple of kFastIdGroup (so every chunk size divides it).
 constexpr int kFastTableLds = 64 * 1024;
 constexpr int kFastIdGroup = 32;
 // The fast kernels hold and stage leaf ids as 16-bit halves: every caller id
