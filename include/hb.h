@@ -119,9 +119,10 @@ typedef struct hb_info {
   int32_t n_used_features;         /* feature columns the kernels stage: the
                                       input columns some decision node tests,
                                       one more for each column that nodes with
-                                      default_left = 1 test (n_features when
-                                      every column is tested and no node sends
-                                      missing values left) */
+                                      default_left = 1 test; n_features (all
+                                      columns, in order) when no node sends
+                                      missing values left and pruning would
+                                      drop less than a quarter of them */
 } hb_info;
 
 /*

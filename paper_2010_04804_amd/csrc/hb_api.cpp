@@ -511,7 +511,14 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
         variant |= (k & 1) != 0;
       }
     if (h->cols.empty()) h->cols.push_back(0);  // only single-leaf trees: one dummy column
-    h->pruned = variant || (int32_t)h->cols.size() < d->n_features;
+    // Pruning costs the kernels a gather through the column list instead of
+    // whole-row loads, so it is applied when it removes at least a quarter of
+    // the columns (or when missing values need NaN-as--inf columns).
+    h->pruned = variant || (int64_t)h->cols.size() * 4 <= (int64_t)d->n_features * 3;
+    if (!h->pruned) {
+      h->cols.resize(d->n_features);
+      for (int32_t f = 0; f < d->n_features; ++f) h->cols[f] = f;
+    }
     if (h->pruned)
       for (CanonTree &ct : trees)
         for (int32_t c = 0; c < ct.size(); ++c)

@@ -161,6 +161,16 @@ __device__ __forceinline__ float xval(const float *row, const int32_t *cols, int
   return ((c & kColNanLeft) && __builtin_isnan(v)) ? -__builtin_inff() : v;
 }
 
+// xval for reads straight from an input row inside a hot loop: COLS is a
+// compile-time choice, so a model without a column list pays nothing.
+template <bool COLS>
+__device__ __forceinline__ float xget(const float *row, const int32_t *cols, int f) {
+  if constexpr (COLS)
+    return xval(row, cols, f);
+  else
+    return row[f];
+}
+
 struct FastArgs {
   const float *X;
   int64_t n_rows;

@@ -110,7 +110,7 @@ struct NodePrefetch {
 
 // KB: 64-node slices of the decision-node dimension; KMODE: 0 scalar leaves
 // and one output, 1 scalar leaves with a class per tree, 2 vector leaves.
-template <int KB, bool CT_LDS, bool X_LDS, int KMODE, int ROWS>
+template <int KB, bool CT_LDS, bool X_LDS, int KMODE, int ROWS, bool COLS = false>
 __global__ __launch_bounds__(ROWS) void gemm_kernel(GemmArgs a) {
   constexpr int KMAX = KMODE == 0 ? 1 : HB_MAX_OUTPUTS;
   constexpr int XS = ROWS + 8;
@@ -204,7 +204,7 @@ __global__ __launch_bounds__(ROWS) void gemm_kernel(GemmArgs a) {
             uint32_t w = 0;
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
-              const float x = X_LDS ? xs[rec[b].y * XS + wave * 64 + rt * 16 + r16] : xval(xrow[rt], a.cols, rec[b].y);
+              const float x = X_LDS ? xs[rec[b].y * XS + wave * 64 + rt * 16 + r16] : xget<COLS>(xrow[rt], a.cols, rec[b].y);
               w |= (x < as_float(rec[b].x) ? 0x40u : 0u) << (8 * b);
             }
             bop[rt][kb][q] = (int)w;
@@ -448,18 +448,20 @@ __global__ __launch_bounds__(ROWS) void gemm_pipe_kernel(GemmArgs a) {
 
 using GemmFn = void (*)(GemmArgs);
 
-template <int KB, bool CT, bool XL, int ROWS>
+template <int KB, bool CT, bool XL, int ROWS, bool COLS = false>
 GemmFn pick_mode(int kmode) {
-  if (kmode == 0) return gemm_kernel<KB, CT, XL, 0, ROWS>;
-  if (kmode == 1) return gemm_kernel<KB, CT, XL, 1, ROWS>;
-  return gemm_kernel<KB, CT, XL, 2, ROWS>;
+  if (kmode == 0) return gemm_kernel<KB, CT, XL, 0, ROWS, COLS>;
+  if (kmode == 1) return gemm_kernel<KB, CT, XL, 1, ROWS, COLS>;
+  return gemm_kernel<KB, CT, XL, 2, ROWS, COLS>;
 }
 
+// cols: features read straight from global memory go through the column list
 template <int KB>
-GemmFn pick_gemm(bool ct, bool xl, int kmode, int rows) {
+GemmFn pick_gemm(bool ct, bool xl, int kmode, int rows, bool cols) {
   if (rows == 512) return ct && xl ? pick_mode<KB, true, true, 512>(kmode) : nullptr;
-  if (ct) return xl ? pick_mode<KB, true, true, 256>(kmode) : pick_mode<KB, true, false, 256>(kmode);
-  return xl ? pick_mode<KB, false, true, 256>(kmode) : pick_mode<KB, false, false, 256>(kmode);
+  if (xl) return ct ? pick_mode<KB, true, true, 256>(kmode) : pick_mode<KB, false, true, 256>(kmode);
+  if (ct) return cols ? pick_mode<KB, true, false, 256, true>(kmode) : pick_mode<KB, true, false, 256>(kmode);
+  return cols ? pick_mode<KB, false, false, 256, true>(kmode) : pick_mode<KB, false, false, 256>(kmode);
 }
 
 }  // namespace
@@ -496,10 +498,11 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
   }
   const int kmode = e.leaf_dim > 1 ? 2 : (e.n_outputs > 1 ? 1 : 0);
   const int kb = t.k_pad / 64;
-  GemmFn fn = kb == 1 ? pick_gemm<1>(ct, xl, kmode, rows)
-              : kb == 2 ? pick_gemm<2>(ct, xl, kmode, rows)
-              : kb == 3 ? pick_gemm<3>(ct, xl, kmode, rows)
-                        : pick_gemm<4>(ct, xl, kmode, rows);
+  const bool cols = e.cols != nullptr;
+  GemmFn fn = kb == 1 ? pick_gemm<1>(ct, xl, kmode, rows, cols)
+              : kb == 2 ? pick_gemm<2>(ct, xl, kmode, rows, cols)
+              : kb == 3 ? pick_gemm<3>(ct, xl, kmode, rows, cols)
+                        : pick_gemm<4>(ct, xl, kmode, rows, cols);
   if (ct && xl && kb == 4 && t.l_pad == 256) {  // the software-pipelined kernel needs no node chunks
     const size_t need = x_bytes(rows) + ct_bytes;
     if (need + stage_bytes(rows) <= (size_t)lds_max) {

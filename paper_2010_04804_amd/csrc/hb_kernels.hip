@@ -55,7 +55,7 @@ struct TravArgs {
   int32_t x_in_lds;           // informational; the template decides
 };
 
-template <bool PERFECT, bool X_LDS, int KMAX, bool LEAF_VEC>
+template <bool PERFECT, bool X_LDS, int KMAX, bool LEAF_VEC, bool COLS = false>
 __global__ __launch_bounds__(kRows) void traverse_kernel(TravArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x;
@@ -132,7 +132,7 @@ __global__ __launch_bounds__(kRows) void traverse_kernel(TravArgs a) {
         for (int g = 0; g < kGroup; ++g) {
           const uint2 rec = nodes[jj[g] * a.slots + idx[g]];
           const uint32_t f = PERFECT ? rec.y : (rec.y & 0xffffu);
-          const float x = X_LDS ? xs[f * kXStride + tid] : xval(xrow, a.cols, f);
+          const float x = X_LDS ? xs[f * kXStride + tid] : xget<COLS>(xrow, a.cols, f);
           const bool go_left = x < as_float(rec.x);
           if (PERFECT)
             idx[g] = 2u * idx[g] + (go_left ? 0u : 1u);  // Algorithm 3's heap step
@@ -178,20 +178,20 @@ __global__ __launch_bounds__(kRows) void traverse_kernel(TravArgs a) {
 
 using KernelFn = void (*)(TravArgs);
 
-template <bool PERFECT, bool X_LDS>
+template <bool PERFECT, bool X_LDS, bool COLS = false>
 KernelFn pick_k(int kmax, bool vec) {
   if (vec) {
     switch (kmax) {
-      case 2: return traverse_kernel<PERFECT, X_LDS, 2, true>;
-      case 8: return traverse_kernel<PERFECT, X_LDS, 8, true>;
-      default: return traverse_kernel<PERFECT, X_LDS, 16, true>;
+      case 2: return traverse_kernel<PERFECT, X_LDS, 2, true, COLS>;
+      case 8: return traverse_kernel<PERFECT, X_LDS, 8, true, COLS>;
+      default: return traverse_kernel<PERFECT, X_LDS, 16, true, COLS>;
     }
   }
   switch (kmax) {
-    case 1: return traverse_kernel<PERFECT, X_LDS, 1, false>;
-    case 2: return traverse_kernel<PERFECT, X_LDS, 2, false>;
-    case 8: return traverse_kernel<PERFECT, X_LDS, 8, false>;
-    default: return traverse_kernel<PERFECT, X_LDS, 16, false>;
+    case 1: return traverse_kernel<PERFECT, X_LDS, 1, false, COLS>;
+    case 2: return traverse_kernel<PERFECT, X_LDS, 2, false, COLS>;
+    case 8: return traverse_kernel<PERFECT, X_LDS, 8, false, COLS>;
+    default: return traverse_kernel<PERFECT, X_LDS, 16, false, COLS>;
   }
 }
 
@@ -250,8 +250,11 @@ int launch_traverse(bool perfect, TravArgs a, hipStream_t stream, std::string *e
   const size_t lds = traverse_lds(a, x_lds, tc);
   const bool vec = LD > 1;
   const int kmax = kmax_for(vec ? LD : a.K);
-  KernelFn fn = perfect ? (x_lds ? pick_k<true, true>(kmax, vec) : pick_k<true, false>(kmax, vec))
-                        : (x_lds ? pick_k<false, true>(kmax, vec) : pick_k<false, false>(kmax, vec));
+  const bool cols = a.cols != nullptr;  // only the global-memory reads need the column list per visit
+  KernelFn fn = perfect ? (x_lds ? pick_k<true, true>(kmax, vec)
+                                 : cols ? pick_k<true, false, true>(kmax, vec) : pick_k<true, false>(kmax, vec))
+                        : (x_lds ? pick_k<false, true>(kmax, vec)
+                                 : cols ? pick_k<false, false, true>(kmax, vec) : pick_k<false, false>(kmax, vec));
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) {
@@ -383,6 +386,7 @@ constexpr int64_t kLanesMaxRowsPtt = 8192;
 constexpr int64_t kLanesMaxRowsTt = 16384;
 
 constexpr int kNotApplicable = 1;
+constexpr int kPreferLanes = 2;  // launch_fast: the trees-across-lanes kernel is the better fit
 
 // Launches the fast kernel when its layout exists and its LDS fits; returns
 // kNotApplicable to fall back to traverse_kernel.
@@ -436,6 +440,10 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
     }
   }
   if (best < 0) return kNotApplicable;
+  // Below four waves per CU the row-parallel walk is latency-bound; the
+  // trees-across-lanes kernel then wins when the node tables are small
+  // enough to stay in L1 (depth-3 forests: 0.9 vs 1.5 ms at 1M rows).
+  if (best_waves < 4 && (int64_t)chunks * fast_tc(tb) * tb <= (int64_t)64 << 10) return kPreferLanes;
   const int rows = shapes[best].rows;
   const size_t xbytes = (size_t)e.n_cols * rows * 4;
   FastFn fn = shapes[best].get(lg, multi);
@@ -556,7 +564,7 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
   if (n_rows <= kLanesMaxRowsPtt) rc = launch_lanes(true, a, stream, err);
   if (rc == kNotApplicable)
     rc = launch_fast(0, t.depth, t.fast, t.fast_chunks, nullptr, e, X, n_rows, scores, leaf_ids, stream, err);
-  if (rc == kNotApplicable && rows_too_wide(a, err)) rc = launch_lanes(true, a, stream, err);
+  if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(true, a, stream, err);
   if (rc != kNotApplicable) return rc;
   return launch_traverse(true, a, stream, err);
 }
@@ -583,7 +591,7 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
   if (n_rows <= kLanesMaxRowsTt) rc = launch_lanes(false, a, stream, err);
   if (rc == kNotApplicable)
     rc = launch_fast(1, t.fast_lg, t.fast, t.fast_chunks, t.depth, e, X, n_rows, scores, leaf_ids, stream, err);
-  if (rc == kNotApplicable && rows_too_wide(a, err)) rc = launch_lanes(false, a, stream, err);
+  if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(false, a, stream, err);
   if (rc != kNotApplicable) return rc;
   return launch_traverse(false, a, stream, err);
 }
