@@ -154,11 +154,13 @@ def run_sweep():
     print(json.dumps({"sweep_summary": table}), flush=True)
 
 
-def run_latency(config):
-    """Request-response latency on one workload's model at batch sizes 1 to
-    10K (scores only): back-to-back launches timed with HIP events, and one
-    call plus a stream synchronisation timed on the host, both for the eager
-    call and for a replay of it captured in a HIP graph."""
+def run_latency(config, batches=(1, 10, 100, 1_000, 10_000, 30_000)):
+    """Request-response latency on one workload's model at small batch sizes
+    (scores only): back-to-back launches timed with HIP events, and one call
+    plus a stream synchronisation timed on the host, both for the eager call
+    and for a replay of it captured in a HIP graph. The selector's strategy
+    runs with and without a tree-split workspace (hb_predict_ws), and GEMM
+    beside it."""
     import statistics
 
     import torch
@@ -171,19 +173,23 @@ def run_latency(config):
     h = hb.compile(model, device=0)
     info = h.info()
     K = info["n_outputs"]
-    batches = (1, 10, 100, 1_000, 10_000)
     X = torch.from_numpy(synth.make_rows(config, max(batches))).to(dev)
     side = torch.cuda.Stream(dev)
     out = {}
     for n in batches:
-        for strat in ("auto", "gemm"):
+        for strat, use_ws in (("auto", False), ("auto", True), ("gemm", False)):
             s_name = h.select(n) if strat == "auto" else strat
             if not info["feasible"][s_name]:
                 continue
+            nws = hb.workspace_bytes(h, n, s_name) if use_ws else 0
+            if use_ws and not nws:
+                continue
+            ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+            ws_ptr = ws.data_ptr() if nws else None
             scores = torch.empty((n, K), dtype=torch.float32, device=dev)
             with torch.cuda.stream(side):
                 fn = lambda: hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), None, s_name,
-                                            torch.cuda.current_stream(dev).cuda_stream)
+                                            torch.cuda.current_stream(dev).cuda_stream, ws_ptr, nws)
                 for _ in range(3):
                     fn()
                 torch.cuda.synchronize()
@@ -199,7 +205,7 @@ def run_latency(config):
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=side):
                 hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), None, s_name,
-                               side.cuda_stream)
+                               side.cuda_stream, ws_ptr, nws)
             grt = []
             for i in range(reps):
                 scores.fill_(float("nan"))
@@ -210,7 +216,7 @@ def run_latency(config):
                 grt.append(time.perf_counter() - t0)
                 if i < 3 and not torch.equal(scores, ref):
                     raise RuntimeError(f"graph replay {i} differs from the eager call (batch {n})")
-            key = f"{n}/{s_name}"
+            key = f"{n}/{s_name}" + ("+ws" if nws else "")
             out[key] = {"pipelined_us": round(pipelined * 1e3, 2),
                         "roundtrip_us_median": round(statistics.median(rt) * 1e6, 2),
                         "roundtrip_us_min": round(min(rt) * 1e6, 2),
@@ -316,6 +322,8 @@ def main():
                     help="strategy crossover sweep (depth 3/7/12, batch 1..1M) instead of the bench line")
     ap.add_argument("--latency", action="store_true",
                     help="small-batch latency (eager and graph-replayed) instead of the bench line")
+    ap.add_argument("--batches", default="",
+                    help="comma-separated batch sizes for --latency")
     ap.add_argument("--pruning", action="store_true",
                     help="wide inputs whose trees test few columns, instead of the bench line")
     ap.add_argument("--configs", action="store_true",
@@ -330,6 +338,8 @@ def main():
     if args.sweep:
         return run_sweep()
     if args.latency:
+        if args.batches:
+            return run_latency(args.config, tuple(int(b) for b in args.batches.split(",")))
         return run_latency(args.config)
     if args.pruning:
         return run_pruning()

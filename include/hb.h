@@ -156,6 +156,28 @@ int hb_compile(const hb_ensemble_desc *desc, int strategy_hint, int device, hb_h
 int hb_predict(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
                int strategy, void *stream);
 
+/*
+ * hb_predict with an optional device workspace (8-byte aligned, on the
+ * handle's device, owned by the caller, not shared with any call that may
+ * run concurrently). With a workspace of at least
+ * hb_workspace_bytes(h, n_rows, strategy) bytes, batches of up to 65,536
+ * rows on PTT or TT divide the trees of each row tile among several
+ * workgroups (the walk of a small batch otherwise occupies few compute
+ * units) and add the partial sums in a fixed order in a second kernel, so
+ * results are reproducible run to run. A NULL workspace (or 0 bytes) is
+ * exactly hb_predict; a smaller one is used only where it suffices. The
+ * workspace holds nothing between calls. Errors as hb_predict, plus
+ * HB_ERR_INVALID_ARG for workspace_bytes < 0, a NULL workspace with
+ * workspace_bytes > 0, or a misaligned workspace.
+ */
+int hb_predict_ws(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
+                  int strategy, void *stream, void *workspace, int64_t workspace_bytes);
+
+/* Workspace bytes that let hb_predict_ws split the trees of a batch of
+ * n_rows rows under `strategy` (AUTO: the selector's choice); 0 when that
+ * batch never splits. A negative value is an error code. */
+int64_t hb_workspace_bytes(const hb_handle *h, int64_t n_rows, int strategy);
+
 /* The strategy hb_predict would run for this batch size under AUTO. */
 int hb_select_strategy(const hb_handle *h, int64_t n_rows);
 

@@ -1,8 +1,9 @@
 """Batched tree-ensemble inference on MI355X: Python binding of libhb.
 
 This module only marshals arguments into the C-ABI declared in
-``include/hb.h`` (``hb_compile``, ``hb_predict``, ``hb_query``, ``hb_table``,
-``hb_select_strategy``, ``hb_destroy``, ``hb_last_error``). Every step of
+``include/hb.h`` (``hb_compile``, ``hb_predict``, ``hb_predict_ws``,
+``hb_workspace_bytes``, ``hb_query``, ``hb_table``, ``hb_select_strategy``,
+``hb_destroy``, ``hb_last_error``). Every step of
 scoring runs in the library's HIP kernels; PyTorch only supplies device
 memory and the current stream. If ``libhb.so`` has not been built, importing
 works but every call raises.
@@ -16,7 +17,7 @@ import os
 
 import numpy as np
 
-__all__ = ["compile", "predict", "predict_ptr", "Handle", "HBError", "STRATEGY", "load_library",
+__all__ = ["compile", "predict", "predict_ptr", "workspace_bytes", "Handle", "HBError", "STRATEGY", "load_library",
            "LIB_PATH"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhb.so")
@@ -77,6 +78,10 @@ def load_library(path: str = LIB_PATH):
                                ctypes.POINTER(_P)]
     lib.hb_predict.restype = ctypes.c_int
     lib.hb_predict.argtypes = [_P, _P, ctypes.c_int64, _P, _P, ctypes.c_int, _P]
+    lib.hb_predict_ws.restype = ctypes.c_int
+    lib.hb_predict_ws.argtypes = [_P, _P, ctypes.c_int64, _P, _P, ctypes.c_int, _P, _P, ctypes.c_int64]
+    lib.hb_workspace_bytes.restype = ctypes.c_int64
+    lib.hb_workspace_bytes.argtypes = [_P, ctypes.c_int64, ctypes.c_int]
     lib.hb_select_strategy.restype = ctypes.c_int
     lib.hb_select_strategy.argtypes = [_P, ctypes.c_int64]
     lib.hb_query.restype = ctypes.c_int
@@ -181,19 +186,34 @@ def compile(model: dict, strategy="auto", device: int = 0) -> Handle:
     return Handle(h.value, device)
 
 
+def workspace_bytes(h: Handle, n_rows: int, strategy="auto") -> int:
+    """Device workspace bytes that let a batch of ``n_rows`` split its trees."""
+    v = load_library().hb_workspace_bytes(h.ptr, int(n_rows), _strategy(strategy))
+    _check(int(v) if v < 0 else 0)
+    return int(v)
+
+
 def predict_ptr(h: Handle, x_ptr: int, n_rows: int, scores_ptr: int, ids_ptr: int | None,
-                strategy="auto", stream: int | None = None):
-    """hb_predict on raw device pointers (no allocation, no synchronisation)."""
-    _check(load_library().hb_predict(h.ptr, x_ptr, int(n_rows), scores_ptr, ids_ptr or None,
-                                     _strategy(strategy), stream or None))
+                strategy="auto", stream: int | None = None, ws_ptr: int | None = None, ws_bytes: int = 0):
+    """hb_predict (hb_predict_ws with a workspace) on raw device pointers
+    (no allocation, no synchronisation)."""
+    if ws_ptr:
+        _check(load_library().hb_predict_ws(h.ptr, x_ptr, int(n_rows), scores_ptr, ids_ptr or None,
+                                            _strategy(strategy), stream or None, ws_ptr, int(ws_bytes)))
+    else:
+        _check(load_library().hb_predict(h.ptr, x_ptr, int(n_rows), scores_ptr, ids_ptr or None,
+                                         _strategy(strategy), stream or None))
 
 
-def predict(h: Handle, X, strategy="auto", leaves: bool = True, out=None, stream=None):
+def predict(h: Handle, X, strategy="auto", leaves: bool = True, out=None, stream=None,
+            workspace: bool = True):
     """Score a float32 CUDA tensor ``X`` [n, F].
 
     Returns ``(scores [n, K] float32, leaf_ids [n, T] int32 or None)`` as torch
     tensors on X's device, enqueued on ``stream`` (default: torch's current
-    stream) without synchronising.
+    stream) without synchronising. With ``workspace`` (the default) a small
+    batch gets a torch-allocated workspace so that its trees can be split
+    across workgroups (hb_predict_ws); ``workspace=False`` calls hb_predict.
     """
     import torch
 
@@ -211,8 +231,14 @@ def predict(h: Handle, X, strategy="auto", leaves: bool = True, out=None, stream
         ids = torch.empty((n, info["n_trees"]), dtype=torch.int32, device=X.device) if leaves else None
     else:
         scores, ids = out
+    current = torch.cuda.current_stream(X.device).cuda_stream
     if stream is None:
-        stream = torch.cuda.current_stream(X.device).cuda_stream
+        stream = current
+    nws = workspace_bytes(h, n, strategy) if workspace else 0
+    ws = torch.empty(nws, dtype=torch.uint8, device=X.device) if nws else None
     predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), ids.data_ptr() if ids is not None else None,
-                strategy, stream)
+                strategy, stream, ws.data_ptr() if ws is not None else None, nws)
+    if ws is not None and stream != current:
+        # torch's allocator must not reuse the workspace before `stream` is done with it.
+        ws.record_stream(torch.cuda.ExternalStream(stream, device=X.device))
     return scores, ids

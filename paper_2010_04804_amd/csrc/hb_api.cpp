@@ -676,9 +676,28 @@ int hb_select_strategy(const hb_handle *h, int64_t n_rows) {
   return select_strategy(h, n_rows);
 }
 
+int64_t hb_workspace_bytes(const hb_handle *h, int64_t n_rows, int strategy) {
+  if (!h) return fail(HB_ERR_INVALID_ARG, "handle is NULL");
+  if (n_rows < 0) return fail(HB_ERR_INVALID_ARG, "n_rows < 0");
+  if (strategy < HB_STRATEGY_AUTO || strategy > HB_STRATEGY_PTT) return fail(HB_ERR_INVALID_ARG, "bad strategy");
+  if (strategy == HB_STRATEGY_AUTO) strategy = hb_select_strategy(h, n_rows);
+  const bool fast = (strategy == HB_STRATEGY_PTT && !h->ptt_fast.empty()) ||
+                    (strategy == HB_STRATEGY_TT && !h->tt_fast.empty());
+  return fast ? hb::split_workspace_bytes(n_rows, h->info.n_trees, h->info.n_outputs) : 0;
+}
+
 int hb_predict(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
                int strategy, void *stream) {
+  return hb_predict_ws(h, X, n_rows, scores, leaf_ids, strategy, stream, nullptr, 0);
+}
+
+int hb_predict_ws(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
+                  int strategy, void *stream, void *workspace, int64_t workspace_bytes) {
   if (!h) return fail(HB_ERR_INVALID_ARG, "handle is NULL");
+  if (workspace_bytes < 0 || (workspace_bytes > 0 && !workspace))
+    return fail(HB_ERR_INVALID_ARG, "workspace_bytes > 0 needs a workspace");
+  if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 7))
+    return fail(HB_ERR_INVALID_ARG, "workspace must be 8-byte aligned");
   if (h->device < 0) return fail(HB_ERR_INVALID_ARG, "host-only handle: compile with a device to predict");
   if (n_rows < 0) return fail(HB_ERR_INVALID_ARG, "n_rows < 0");
   if (strategy < HB_STRATEGY_AUTO || strategy > HB_STRATEGY_PTT) return fail(HB_ERR_INVALID_ARG, "bad strategy");
@@ -694,11 +713,16 @@ int hb_predict(hb_handle *h, const float *X, int64_t n_rows, float *scores, int3
   std::string err;
   int rc = HB_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  hb::Workspace ws;
+  if (workspace && workspace_bytes > 0) {
+    ws.ptr = workspace;
+    ws.bytes = workspace_bytes;
+  }
   try {
     if (strategy == HB_STRATEGY_PTT)
-      rc = hb::launch_ptt(h->ens, h->ptt, X, n_rows, scores, leaf_ids, s, &err);
+      rc = hb::launch_ptt(h->ens, h->ptt, X, n_rows, scores, leaf_ids, ws, s, &err);
     else if (strategy == HB_STRATEGY_TT)
-      rc = hb::launch_tt(h->ens, h->tt, X, n_rows, scores, leaf_ids, s, &err);
+      rc = hb::launch_tt(h->ens, h->tt, X, n_rows, scores, leaf_ids, ws, s, &err);
     else
       rc = hb::launch_gemm(h->ens, h->gemm, X, n_rows, scores, leaf_ids, s, &err);
   } catch (...) {

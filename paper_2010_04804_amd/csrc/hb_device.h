@@ -183,6 +183,11 @@ struct FastArgs {
   const uint4 *blocks;        // [chunks * TC][tree bytes / 16]
   const int32_t *tree_depth;  // TT: [T]
   int32_t n_chunks;
+  // Tree split (small batches): workgroup (x, y) walks chunks [y * split,
+  // min((y + 1) * split, n_chunks)) of row tile x and stores its raw sums in
+  // partial[y][row][K]; 0 = one workgroup walks every tree and finishes rows.
+  int32_t split;
+  double *partial;
   int32_t ids_vec;            // leaf_ids rows start 16-byte aligned (T % 4 == 0, aligned base)
   int32_t ids_nt;             // leaf-id stores bypass L2 allocation (streaming)
 };

@@ -286,6 +286,9 @@ template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET>
 __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
   constexpr int G = kFastIdGroup;
+  // this workgroup's chunks (all of them unless the trees are split)
+  const int c_begin = a.split ? (int)blockIdx.y * a.split : 0;
+  if (a.split) a.n_chunks = min(c_begin + a.split, a.n_chunks);
   __shared__ __align__(16) uint4 tbuf[C::BUFS][C::CHUNK16];
   __shared__ __align__(16) u32x4 idstage[ROWS / 64][16 * kIdQuads];
   extern __shared__ __align__(16) float fxs[];  // [F][ROWS]
@@ -295,7 +298,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   const bool valid = row < a.n_rows;
   {
     ChunkPrefetch<ROWS, C::CHUNK16> first;
-    first.load(a.blocks);
+    first.load(a.blocks + (size_t)c_begin * C::CHUNK16);
     first.store(tbuf[0]);
   }
   {  // each lane copies its own row into column tid of the tile (and only
@@ -319,7 +322,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
 #pragma unroll
   for (int k = 0; k < C::KMAX; ++k) acc[k] = 0.0;
   IdPack ids, prev;
-  int cls = MULTI ? a.tree_class[min(tid & (C::TC - 1), a.out.T - 1)] : 0;
+  int cls = MULTI ? a.tree_class[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
   const int64_t r0w = r0 + (tid & ~63);
   // row-segment flushes of one group overlap the next group's walk; the
   // unaligned (scalar) store path, and 1024-row workgroups (whose registers
@@ -327,7 +330,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   constexpr bool kLag = ROWS < 1024;
   const bool lagged = kLag && a.leaf_ids && a.ids_vec;
   IdLag lag{false, &prev, idstage[tid >> 6], r0w, 0};
-  for (int c = 0; c < a.n_chunks; c += C::CPF) {  // chunk count is a multiple of CPF
+  for (int c = c_begin; c < a.n_chunks; c += C::CPF) {  // chunk counts are multiples of CPF
     fast_group<MODE, LG, MULTI, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, lag);
     if (lagged) {
 #pragma unroll
@@ -341,7 +344,14 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   if (lag.on)  // the last group
     flush_packed(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, a.ids_nt, lag.stage, prev, r0w, lag.t0);
   if (valid) {
-    finish_row<C::KMAX>(a.out, acc, row);
+    if (a.split) {
+      double *dst = a.partial + ((size_t)blockIdx.y * a.n_rows + row) * a.out.K;
+#pragma unroll
+      for (int k = 0; k < C::KMAX; ++k)
+        if (k < a.out.K) dst[k] = acc[k];
+    } else {
+      finish_row<C::KMAX>(a.out, acc, row);
+    }
   }
 }
 

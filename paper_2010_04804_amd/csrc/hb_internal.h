@@ -123,13 +123,31 @@ struct GemmDev {
   int32_t k_pad, l_pad, n_shapes;
 };
 
+// Caller-provided device scratch for the tree split of small batches.
+struct Workspace {
+  void *ptr = nullptr;
+  int64_t bytes = 0;
+};
+
+// Tree split: batches up to kSplitMaxRows rows may have their trees divided
+// among up to one workgroup per 32-tree group of each row tile, so that a
+// small batch still fills the chip; the workgroups leave double partial sums
+// (split x rows x outputs) that a second kernel adds in a fixed order.
+constexpr int64_t kSplitMaxRows = 65536;
+// Largest workspace a split of n_rows rows can use (0: never split).
+inline int64_t split_workspace_bytes(int64_t n_rows, int32_t n_trees, int32_t n_outputs) {
+  if (n_rows < 1 || n_rows > kSplitMaxRows) return 0;
+  const int64_t groups = (n_trees + kFastIdGroup - 1) / kFastIdGroup;
+  return groups < 2 ? 0 : groups * n_rows * n_outputs * 8;
+}
+
 // Each launcher checks its arguments against what the kernel and its grid
 // assume, enqueues on `stream`, and returns HB_OK or an error code with a
 // message in *err.
 int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_rows,
-               float *scores, int32_t *leaf_ids, hipStream_t stream, std::string *err);
+               float *scores, int32_t *leaf_ids, const Workspace &ws, hipStream_t stream, std::string *err);
 int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_rows,
-              float *scores, int32_t *leaf_ids, hipStream_t stream, std::string *err);
+              float *scores, int32_t *leaf_ids, const Workspace &ws, hipStream_t stream, std::string *err);
 int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t n_rows,
                 float *scores, int32_t *leaf_ids, hipStream_t stream, std::string *err);
 

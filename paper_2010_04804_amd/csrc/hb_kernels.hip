@@ -384,15 +384,56 @@ LanesFn pick_lanes_r(int kmax, bool vec) {
 // for TT, whose row-parallel walk is slower.
 constexpr int64_t kLanesMaxRowsPtt = 8192;
 constexpr int64_t kLanesMaxRowsTt = 16384;
+// With a workspace the tree-split row-parallel kernel takes over from here
+// (measured on the three models above: the split wins from 1,000 to 1,200 rows).
+constexpr int64_t kLanesMaxRowsSplit = 1024;
 
 constexpr int kNotApplicable = 1;
 constexpr int kPreferLanes = 2;  // launch_fast: the trees-across-lanes kernel is the better fit
+
+// Adds the split workgroups' partial sums of each row, then applies the
+// aggregation and transform. A workgroup takes 64 rows; wave j adds parts
+// j, j + J, j + 2J, ... in turn (J waves keep J loads of every row in
+// flight), and the first wave adds the J sums in wave order: a fixed order,
+// so the result does not vary from run to run.
+template <int KMAX, int J>
+__global__ __launch_bounds__(64 * J) void split_finish_kernel(const double *partial, int split, int64_t n_rows,
+                                                              OutArgs out) {
+  extern __shared__ double red[];  // [J][K][64]
+  const int lane = threadIdx.x & 63, j = threadIdx.x >> 6;
+  const int64_t row = (int64_t)blockIdx.x * 64 + lane;
+  const bool valid = row < n_rows;
+  double tot[KMAX];
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) tot[k] = 0.0;
+  if (valid) {
+#pragma unroll 4
+    for (int s = j; s < split; s += J) {
+      const double *p = partial + ((size_t)s * n_rows + row) * out.K;
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k)
+        if (k < out.K) tot[k] += p[k];
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k)
+    if (k < out.K) red[(j * out.K + k) * 64 + lane] = tot[k];
+  __syncthreads();
+  if (j != 0 || !valid) return;
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    tot[k] = 0.0;
+    if (k < out.K)
+      for (int w = 0; w < J; ++w) tot[k] += red[(w * out.K + k) * 64 + lane];
+  }
+  finish_row<KMAX>(out, tot, row);
+}
 
 // Launches the fast kernel when its layout exists and its LDS fits; returns
 // kNotApplicable to fall back to traverse_kernel.
 int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t *depth,
                 const EnsembleDev &e, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
-                hipStream_t stream, std::string *err) {
+                const Workspace &ws, hipStream_t stream, std::string *err) {
   if (!blocks || lg < 1 || lg > kFastMaxLg || e.leaf_dim != 1) return kNotApplicable;
   const int lds_max = max_dynamic_lds(err);
   if (lds_max <= 0) return HB_ERR_HIP;
@@ -474,8 +515,58 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
     return HB_ERR_HIP;
   }
   const int64_t blocks_n = (n_rows + rows - 1) / rows;
-  hipLaunchKernelGGL(fn, dim3((unsigned)blocks_n), dim3(rows), xbytes, stream, a);
+  // Small batch with a workspace: divide the 32-tree groups among `parts`
+  // workgroups per row tile. With `resident` workgroups of this shape running
+  // at once, the walk takes about ceil(parts * tiles / resident) rounds of
+  // `per` groups each plus a fixed cost per workgroup (feature tile, partial
+  // sums) worth about kSplitOverheadGroups groups; take the fewest parts that
+  // reach the least such time (no split when that is the unsplit launch).
+  // Measured against forced part counts on the 500-tree depth-8, leaf-wise
+  // depth-12 and 7-class models from 10K to 64K rows, this picks the fastest
+  // count or one within 3% of it.
+  int split = 1;
+  const int cpf = kFastIdGroup / fast_tc(tb, shapes[best].budget);  // chunks per 32 trees
+  const int64_t groups = a.n_chunks / cpf;
+  if (ws.ptr && n_rows <= kSplitMaxRows && groups >= 2) {
+    int cus = 0, dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) {
+      *err = "hipDeviceGetAttribute(MultiprocessorCount) failed";
+      return HB_ERR_HIP;
+    }
+    const int64_t resident = (int64_t)cus * (int64_t)((size_t)lds_max / lds_of(shapes[best]));
+    const int64_t row_bytes = n_rows * e.n_outputs * 8;
+    constexpr int64_t kSplitOverheadGroups = 4;
+    int64_t best_cost = (blocks_n + resident - 1) / resident * (groups + kSplitOverheadGroups), best_per = groups;
+    for (int64_t p = 2; p <= groups; ++p) {
+      const int64_t per = (groups + p - 1) / p, parts = (groups + per - 1) / per;
+      if (parts * row_bytes > ws.bytes) break;
+      const int64_t cost = (parts * blocks_n + resident - 1) / resident * (per + kSplitOverheadGroups);
+      if (cost < best_cost) {
+        best_cost = cost;
+        best_per = per;
+      }
+    }
+    if (best_per < groups) {
+      split = (int)((groups + best_per - 1) / best_per);
+      a.split = (int)best_per * cpf;
+      a.partial = static_cast<double *>(ws.ptr);
+    }
+  }
+  hipLaunchKernelGGL(fn, dim3((unsigned)blocks_n, (unsigned)split), dim3(rows), xbytes, stream, a);
   rc = hipGetLastError();
+  if (rc == hipSuccess && split > 1) {
+    // 16 waves per 64 rows for scalar outputs, 8 for several (their sums
+    // take K times the LDS: at most 64 KiB)
+    const unsigned fin_rows = (unsigned)((n_rows + 63) / 64);
+    if (multi)
+      hipLaunchKernelGGL((split_finish_kernel<HB_MAX_OUTPUTS, 8>), dim3(fin_rows), dim3(64 * 8),
+                         (size_t)8 * e.n_outputs * 64 * sizeof(double), stream, a.partial, split, n_rows, a.out);
+    else
+      hipLaunchKernelGGL((split_finish_kernel<1, 16>), dim3(fin_rows), dim3(64 * 16),
+                         (size_t)16 * 64 * sizeof(double), stream, a.partial, split, n_rows, a.out);
+    rc = hipGetLastError();
+  }
   if (rc != hipSuccess) {
     *err = std::string("kernel launch: ") + hipGetErrorString(rc);
     return HB_ERR_HIP;
@@ -546,7 +637,7 @@ TravArgs common_args(const EnsembleDev &e, const float *X, int64_t n, float *sco
 }  // namespace
 
 int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_rows, float *scores,
-               int32_t *leaf_ids, hipStream_t stream, std::string *err) {
+               int32_t *leaf_ids, const Workspace &ws, hipStream_t stream, std::string *err) {
   if (!t.node || !t.leaf_value || !t.leaf_id || t.depth < 0 || t.depth > HB_PTT_MAX_DEPTH) {
     *err = "PTT tables missing";
     return HB_ERR_INVALID_ARG;
@@ -561,16 +652,16 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
   a.leaf_slots = 1 << t.depth;
   if (a.slots < 2) a.slots = 2;  // depth 0 still stores two (unused) records per tree
   int rc = kNotApplicable;
-  if (n_rows <= kLanesMaxRowsPtt) rc = launch_lanes(true, a, stream, err);
+  if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsPtt)) rc = launch_lanes(true, a, stream, err);
   if (rc == kNotApplicable)
-    rc = launch_fast(0, t.depth, t.fast, t.fast_chunks, nullptr, e, X, n_rows, scores, leaf_ids, stream, err);
+    rc = launch_fast(0, t.depth, t.fast, t.fast_chunks, nullptr, e, X, n_rows, scores, leaf_ids, ws, stream, err);
   if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(true, a, stream, err);
   if (rc != kNotApplicable) return rc;
   return launch_traverse(true, a, stream, err);
 }
 
 int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_rows, float *scores,
-              int32_t *leaf_ids, hipStream_t stream, std::string *err) {
+              int32_t *leaf_ids, const Workspace &ws, hipStream_t stream, std::string *err) {
   if (!t.node || !t.leaf_value || !t.leaf_id || !t.depth || t.n_pad < 1) {
     *err = "TT tables missing";
     return HB_ERR_INVALID_ARG;
@@ -588,9 +679,9 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
   a.slots = t.n_pad;
   a.leaf_slots = t.n_pad;
   int rc = kNotApplicable;
-  if (n_rows <= kLanesMaxRowsTt) rc = launch_lanes(false, a, stream, err);
+  if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsTt)) rc = launch_lanes(false, a, stream, err);
   if (rc == kNotApplicable)
-    rc = launch_fast(1, t.fast_lg, t.fast, t.fast_chunks, t.depth, e, X, n_rows, scores, leaf_ids, stream, err);
+    rc = launch_fast(1, t.fast_lg, t.fast, t.fast_chunks, t.depth, e, X, n_rows, scores, leaf_ids, ws, stream, err);
   if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(false, a, stream, err);
   if (rc != kNotApplicable) return rc;
   return launch_traverse(false, a, stream, err);

@@ -108,3 +108,28 @@ def test_default_left_validation():
     with pytest.raises(hb.HBError) as e:
         hb.compile(ninf, device=-1)
     assert e.value.code == -3  # HB_ERR_UNSUPPORTED
+
+
+def test_workspace_bytes_and_errors():
+    lib = hb.load_library()
+    h = hb.compile(synth.make_model(2), device=-1)  # 500 trees: 16 groups of 32
+    assert hb.workspace_bytes(h, 1000, "ptt") == 16 * 1000 * 1 * 8
+    assert hb.workspace_bytes(h, 65536, "tt") == 16 * 65536 * 8
+    assert hb.workspace_bytes(h, 65537, "ptt") == 0  # large batches never split
+    assert hb.workspace_bytes(h, 0, "ptt") == 0
+    assert hb.workspace_bytes(h, 1000, "gemm") == 0
+    assert lib.hb_workspace_bytes(h.ptr, -1, 0) == -1
+    assert lib.hb_workspace_bytes(None, 10, 0) == -1
+    assert lib.hb_workspace_bytes(h.ptr, 10, 9) == -1
+    one = hb.compile(synth.make_model(1), device=-1)
+    info = one.info()
+    groups = (info["n_trees"] + 31) // 32
+    want = groups * 100 * info["n_outputs"] * 8 if groups >= 2 else 0
+    assert hb.workspace_bytes(one, 100, "tt") == want
+    for ws, nbytes, match in [(None, 64, "needs a workspace"), (8, -1, "needs a workspace"),
+                              (12, 64, "8-byte aligned")]:
+        rc = lib.hb_predict_ws(h.ptr, 1, 10, 1, None, 0, None, ws, nbytes)
+        assert rc == -1 and match in lib.hb_last_error().decode()
+    # a valid workspace on a host-only handle reaches the device check
+    assert lib.hb_predict_ws(h.ptr, 1, 10, 1, None, 0, None, 64, 64) == -1
+    assert "host-only" in lib.hb_last_error().decode()

@@ -39,9 +39,9 @@ def handle(cfg):
     return _handles[cfg]
 
 
-def run(h, X, strategy, leaves=True, stream=None):
+def run(h, X, strategy, leaves=True, stream=None, workspace=True):
     Xd = torch.from_numpy(X).cuda()
-    s, ids = hb.predict(h, Xd, strategy=strategy, leaves=leaves, stream=stream)
+    s, ids = hb.predict(h, Xd, strategy=strategy, leaves=leaves, stream=stream, workspace=workspace)
     torch.cuda.synchronize()
     return s.cpu().numpy(), (ids.cpu().numpy() if ids is not None else None)
 
@@ -91,6 +91,47 @@ def test_tree_parallel_boundaries(cfg, n, strategy):
     X = synth.make_rows(cfg, n)
     scores, ids = run(h, X, strategy)
     check(model, X, scores, ids, f"lanes cfg{cfg}/{n}/{strategy}")
+
+
+@pytest.mark.parametrize("strategy", ["ptt", "tt"])
+@pytest.mark.parametrize("cfg,n", [(2, 513), (2, 1000), (2, 4097), (2, 30_000), (2, 65_536), (4, 700), (4, 9000),
+                                   (5, 600), (5, 20_001), (3, 1000)])
+def test_tree_split_parity(cfg, n, strategy):
+    """With a workspace (hb_predict_ws), batches of up to 65,536 rows divide
+    their trees among workgroups and add the partial sums in a second kernel:
+    the result meets the oracle bar and its leaf ids equal the unsplit call's."""
+    model, h = handle(cfg)
+    say("tree split", cfg, strategy, n)
+    X = synth.make_rows(cfg, n)
+    s_ws, i_ws = run(h, X, strategy)
+    s_no, i_no = run(h, X, strategy, workspace=False)
+    check(model, X, s_ws, i_ws, f"split cfg{cfg}/{n}/{strategy}")
+    check(model, X, s_no, i_no, f"unsplit cfg{cfg}/{n}/{strategy}")
+    assert np.array_equal(i_ws, i_no)
+
+
+@pytest.mark.parametrize("strategy", ["ptt", "tt"])
+def test_tree_split_uses_and_reuses_the_workspace(strategy):
+    """The split writes its partial sums into the caller's workspace; one
+    workspace serves successive calls (the second one smaller), and a
+    workspace smaller than hb_workspace_bytes still gives correct results."""
+    model, h = handle(2)
+    nbytes = hb.workspace_bytes(h, 4000, strategy)
+    assert nbytes == 16 * 4000 * 8
+    ws = torch.full((nbytes,), 0xFF, dtype=torch.uint8, device="cuda")
+    rows = synth.make_rows(2, 8500)
+    for lo, n, avail in [(0, 4000, nbytes), (4000, 1500, nbytes), (5500, 3000, nbytes // 3)]:
+        say("workspace reuse", strategy, n, avail)
+        X = np.ascontiguousarray(rows[lo:lo + n])
+        Xd = torch.from_numpy(X).cuda()
+        scores = torch.empty((n, 1), dtype=torch.float32, device="cuda")
+        ids = torch.empty((n, 500), dtype=torch.int32, device="cuda")
+        hb.predict_ptr(h, Xd.data_ptr(), n, scores.data_ptr(), ids.data_ptr(), strategy,
+                       torch.cuda.current_stream().cuda_stream, ws.data_ptr(), avail)
+        torch.cuda.synchronize()
+        if n == 4000:
+            assert int((ws != 0xFF).sum()) > 0, "the split did not write the workspace"
+        check(model, X, scores.cpu().numpy(), ids.cpu().numpy(), f"ws {strategy}/{n}/{avail}")
 
 
 def _vector_forest(n_features, n_trees, depth, seed):
@@ -241,24 +282,32 @@ def test_non_default_stream():
     check(model, X, s.cpu().numpy(), ids.cpu().numpy(), "stream")
 
 
-@pytest.mark.parametrize("strategy,n", [("ptt", 100), ("ptt", 20_000), ("tt", 3000), ("gemm", 600)])
-def test_graph_capture_replays_match_eager(strategy, n):
-    """hb_predict captured into a HIP graph: every replay, with eager work and
-    synchronisations between replays, equals the eager call bit for bit."""
+@pytest.mark.parametrize("strategy,n,use_ws", [("ptt", 100, False), ("ptt", 20_000, False), ("tt", 3000, False),
+                                              ("gemm", 600, False), ("ptt", 2000, True), ("tt", 3000, True)])
+def test_graph_capture_replays_match_eager(strategy, n, use_ws):
+    """hb_predict (or hb_predict_ws with a workspace) captured into a HIP
+    graph: every replay, with eager work and synchronisations between
+    replays, equals the eager call bit for bit."""
     model, h = handle(2)
-    say("graph capture", strategy, n)
+    say("graph capture", strategy, n, "workspace" if use_ws else "")
     X = torch.from_numpy(synth.make_rows(2, n)).cuda()
-    s_ref, i_ref = hb.predict(h, X, strategy=strategy)
+    s_ref, i_ref = hb.predict(h, X, strategy=strategy, workspace=use_ws)
     torch.cuda.synchronize()
     scores = torch.empty_like(s_ref)
     ids = torch.empty_like(i_ref)
+    nws = hb.workspace_bytes(h, n, strategy) if use_ws else 0
+    assert nws > 0 or not use_ws
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda")
+    ws_ptr = ws.data_ptr() if nws else None
     side = torch.cuda.Stream()
     with torch.cuda.stream(side):  # warm up on the capture stream
-        hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), ids.data_ptr(), strategy, side.cuda_stream)
+        hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), ids.data_ptr(), strategy, side.cuda_stream,
+                       ws_ptr, nws)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=side):
-        hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), ids.data_ptr(), strategy, side.cuda_stream)
+        hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), ids.data_ptr(), strategy, side.cuda_stream,
+                       ws_ptr, nws)
     for rep in range(4):
         scores.fill_(float("nan"))
         ids.fill_(-7)
