@@ -95,9 +95,24 @@ def cpu_baseline(model, cfg, seconds_target=15.0):
     t0 = time.perf_counter()
     oracle.predict(model, X, leaves=True, n_threads=cores)
     dt = time.perf_counter() - t0
+    # one thread on a 10,000-row slice, for a per-core figure
+    t1 = time.perf_counter()
+    oracle.predict(model, X[:10_000], leaves=True, n_threads=1)
+    dt1 = time.perf_counter() - t1
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": n / dt, "unit": "rows/s", "cores": cores, "kind": "oracle",
             "sample": f"first {n} rows of the same workload (scores and leaf ids), "
-                      f"{dt:.1f} s on {cores} threads"}
+                      f"{dt:.1f} s on {cores} threads",
+            "single_thread_rows_per_s": min(10_000, n) / dt1, "cpu_model": cpu_model,
+            "host_cpus": os.cpu_count()}
 
 
 def _event_ms(stream, fn, reps):
@@ -425,6 +440,16 @@ def main():
             others[s] = {"rows_per_s": n / (mss * 1e-3), "ms": mss, "bound": r["bound"],
                          "achieved": r["achieved"], "unit": r["unit"], "frac": r["frac"]}
         out["other_strategies"] = others
+    if strategy != "gemm" and not args.copy_calibration:
+        # HBM fraction also against what a plain 1 GiB device copy reaches here
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        copy_ms = _event_ms(stream, lambda: dst.copy_(src), 5)
+        copy_gbs = 2.0 * (1 << 30) / (copy_ms * 1e-3) / 1e9
+        out["roofline"]["copy_GBps_measured"] = copy_gbs
+        out["roofline"]["frac_of_copy"] = out["roofline"]["achieved"] / copy_gbs
+        del src, dst
     if args.copy_calibration:
         # a plain device copy of exactly 1 GiB, to scale FETCH_SIZE / WRITE_SIZE
         src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
