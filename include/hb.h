@@ -195,7 +195,14 @@ int hb_query(const hb_handle *h, hb_info *info);
  *         tree, n_pad slots, n_pad even; a leaf holds {-inf, own id << 16}),
  *         "depth" (int32 [T]), "leaf_value"
  *         (float [T][n_pad][leaf_dim]), "leaf_id" (int32 [T][n_pad]),
- *         "dims" (int32 {n_pad})
+ *         "dims" (int32 {n_pad}), and the row-parallel kernels' packed form:
+ *         "fast_node" (uint32 pairs per tree, trees padded to a multiple of
+ *         32, 2^lg records each: {threshold bits, feature | 8 * right << 16};
+ *         leaves and padding trees hold {-inf, 8 * own index << 16}),
+ *         "fast_leaf" (uint32 pairs {value bits, caller id} per record of
+ *         "fast_node"); empty when the model has vector leaves or lg > 11.
+ *         On the device the leaf records stay a separate array while they
+ *         take at most 4 MB, and follow each tree's node records otherwise
  *   GEMM: "node" (uint32 pairs {threshold bits, feature} [T][k_pad]),
  *         "shape" (int32 [T]), "ct" (int8 [S][l_pad][k_pad], 4*C^T),
  *         "bias" (int32 [S][l_pad]), "leaf_value" (float [T][l_pad][leaf_dim]),

@@ -13,7 +13,8 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["hb_api.cpp", "hb_kernels.hip", "hb_gemm.hip", "hb_fast_ptt_128.hip", "hb_fast_ptt_256.hip", "hb_fast_ptt_256s.hip", "hb_fast_ptt_512.hip",
            "hb_fast_ptt_512s.hip", "hb_fast_ptt_768.hip", "hb_fast_ptt_1024.hip",
            "hb_fast_tt_128.hip", "hb_fast_tt_256.hip", "hb_fast_tt_256s.hip",
-           "hb_fast_tt_512.hip", "hb_fast_tt_512s.hip"]
+           "hb_fast_tt_512.hip", "hb_fast_tt_512s.hip", "hb_fast_ttg_128.hip", "hb_fast_ttg_256.hip",
+           "hb_fast_ttg_256s.hip", "hb_fast_ttg_512.hip", "hb_fast_ttg_512s.hip"]
 
 # -packed-fp32-ops: no packed fp32 instructions in device code (the host pass
 # warns that it does not know the feature; that is harmless).

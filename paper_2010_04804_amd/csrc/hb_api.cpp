@@ -149,8 +149,8 @@ struct hb_handle {
   std::vector<int32_t> gemm_leaf_id;
   int32_t gemm_k_pad = 0, gemm_l_pad = 0, gemm_n_shapes = 0;
   // packed blocks of the fast traversal kernels (device layout only)
-  std::vector<uint32_t> ptt_fast, tt_fast;
-  int32_t ptt_fast_chunks = 0, tt_fast_lg = 0, tt_fast_chunks = 0;
+  std::vector<uint32_t> ptt_fast, tt_fast, tt_fast_leaf;
+  int32_t ptt_fast_chunks = 0, tt_fast_lg = 0, tt_fast_chunks = 0, tt_fast_mode = 1;
   // device
   std::vector<void *> allocations;
   hb::EnsembleDev ens{};
@@ -293,16 +293,26 @@ void build_fast(hb_handle *h, const hb_ensemble_desc *d, const std::vector<Canon
   int lg = 1;
   while ((1 << lg) < max_nodes) ++lg;
   if (h->info.feasible[HB_STRATEGY_TT] && lg <= hb::kFastMaxLg) {
-    const int tb = hb::fast_tree_bytes(1, lg);
-    const int tc = hb::fast_tc(tb);
-    const int chunks = (T + hb::kFastIdGroup - 1) / hb::kFastIdGroup * (hb::kFastIdGroup / tc);
-    const size_t words = (size_t)tb / 4;
+    // node records and leaf records per tree, 2^lg of each; the tree count
+    // is padded to a multiple of the leaf-id group (so of every chunk size)
     const size_t NP = (size_t)1 << lg;
-    h->tt_fast.assign((size_t)chunks * tc * words, 0u);
+    const size_t words = 2 * NP;
+    const size_t padded = (size_t)(T + hb::kFastIdGroup - 1) / hb::kFastIdGroup * hb::kFastIdGroup;
+    h->tt_fast.assign(padded * words, 0u);
+    h->tt_fast_leaf.assign(padded * words, 0u);
+    // padding trees: every node a leaf that loops to itself, so a walk over
+    // them stays at the root
+    const uint32_t ninf_pad = fbits(-std::numeric_limits<float>::infinity());
+    for (size_t t = (size_t)T; t < padded; ++t)
+      for (size_t c = 0; c < NP; ++c) {
+        h->tt_fast[t * words + 2 * c] = ninf_pad;
+        h->tt_fast[t * words + 2 * c + 1] = (8u * (uint32_t)c) << 16;
+      }
     for (int32_t t = 0; t < T; ++t) {
       const CanonTree &ct = trees[t];
       const int64_t base = d->tree_node_offset[t];
       uint32_t *blk = &h->tt_fast[(size_t)t * words];
+      uint32_t *leaf = &h->tt_fast_leaf[(size_t)t * words];
       const uint32_t ninf = fbits(-std::numeric_limits<float>::infinity());
       for (size_t c = 0; c < NP; ++c) {
         uint32_t *rec = blk + 2 * c;
@@ -313,7 +323,7 @@ void build_fast(hb_handle *h, const hb_ensemble_desc *d, const std::vector<Canon
           rec[0] = ninf;
           rec[1] = (8u * (uint32_t)c) << 16;
         }
-        uint32_t *lr = blk + 2 * NP + 2 * c;
+        uint32_t *lr = leaf + 2 * c;
         if (c < (size_t)ct.size()) {
           const int32_t v = ct.caller[c];
           lr[0] = ct.feat[c] < 0 ? fbits(d->leaf_value[base + v]) : 0u;
@@ -321,8 +331,9 @@ void build_fast(hb_handle *h, const hb_ensemble_desc *d, const std::vector<Canon
         }
       }
     }
+    h->tt_fast_mode = (int64_t)(padded * NP * 8) <= hb::kTtLeafGlobalMax ? 2 : 1;
     h->tt_fast_lg = lg;
-    h->tt_fast_chunks = chunks;
+    h->tt_fast_chunks = (int)(padded / hb::fast_tc(hb::fast_tree_bytes(h->tt_fast_mode, lg)));
   }
 }
 
@@ -624,8 +635,23 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
       h->tt.n_pad = h->tt_n_pad;
       h->tt.max_depth = D;
       if (!rc && !h->tt_fast.empty()) {
-        rc = upload(h, h->tt_fast, &pn);
-        h->tt.fast = reinterpret_cast<const uint4 *>(pn);
+        if (h->tt_fast_mode == 2) {  // node blocks, leaf records apart
+          rc = upload(h, h->tt_fast, &pn);
+          h->tt.fast = reinterpret_cast<const uint4 *>(pn);
+          if (!rc) rc = upload(h, h->tt_fast_leaf, &pn);
+          h->tt.fast_leaf = reinterpret_cast<const uint2 *>(pn);
+        } else {  // each tree's node records, then its leaf records
+          const size_t w = (size_t)2 << h->tt_fast_lg;
+          std::vector<uint32_t> blocks(2 * h->tt_fast.size());
+          for (size_t t = 0; t < h->tt_fast.size() / w; ++t) {
+            std::copy_n(&h->tt_fast[t * w], w, &blocks[2 * t * w]);
+            std::copy_n(&h->tt_fast_leaf[t * w], w, &blocks[2 * t * w + w]);
+          }
+          rc = upload(h, blocks, &pn);
+          h->tt.fast = reinterpret_cast<const uint4 *>(pn);
+          h->tt.fast_leaf = nullptr;
+        }
+        h->tt.fast_mode = h->tt_fast_mode;
         h->tt.fast_lg = h->tt_fast_lg;
         h->tt.fast_chunks = h->tt_fast_chunks;
       }
@@ -761,6 +787,8 @@ int hb_table(const hb_handle *h, int strategy, const char *name, const void **da
     if (n == "leaf_value") return give(h->tt_leaf_value);
     if (n == "leaf_id") return give(h->tt_leaf_id);
     if (n == "dims") return give(h->tt_dims);
+    if (n == "fast_node") return give(h->tt_fast);
+    if (n == "fast_leaf") return give(h->tt_fast_leaf);
   } else {
     if (n == "node") return give(h->gemm_node);
     if (n == "shape") return give(h->gemm_shape);

@@ -181,6 +181,7 @@ struct FastArgs {
   OutArgs out;
   const int32_t *tree_class;
   const uint4 *blocks;        // [chunks * TC][tree bytes / 16]
+  const uint2 *leaf;          // TT mode 2: [chunks * TC][2^lg] leaf records (global memory)
   const int32_t *tree_depth;  // TT: [T]
   int32_t n_chunks;
   // Tree split (small batches): workgroup (x, y) walks chunks [y * split,
@@ -207,5 +208,11 @@ FastFn fast_tt_kernel_512(int lg, bool multi);
 FastFn fast_tt_kernel_512s(int lg, bool multi);
 FastFn fast_tt_kernel_256s(int lg, bool multi);
 FastFn fast_tt_kernel_128(int lg, bool multi);
+// TT with leaf records in global memory (mode 2)
+FastFn fast_ttg_kernel_256(int lg, bool multi);
+FastFn fast_ttg_kernel_512(int lg, bool multi);
+FastFn fast_ttg_kernel_512s(int lg, bool multi);
+FastFn fast_ttg_kernel_256s(int lg, bool multi);
+FastFn fast_ttg_kernel_128(int lg, bool multi);
 
 }  // namespace hb

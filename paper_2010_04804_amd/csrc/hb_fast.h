@@ -230,8 +230,14 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
 #pragma unroll
   for (int g = 0; g < TC; ++g) {
     const int t = t0 + g;
-    const uint32_t loff = MODE == 0 ? s[g] : (1u << LG) * 8u + s[g];
-    const uint2 lr = *reinterpret_cast<const uint2 *>(base + g * TB + loff);
+    // PTT: leaf record at the heap index; TT mode 1: after the node records;
+    // TT mode 2: from global memory (the index is masked to the tree's 2^LG
+    // records, so even a malformed table cannot read outside them)
+    uint2 lr;
+    if (MODE == 2)
+      lr = a.leaf[(size_t)t * (1u << LG) + ((s[g] >> 3) & ((1u << LG) - 1u))];
+    else
+      lr = *reinterpret_cast<const uint2 *>(base + g * TB + (MODE == 0 ? 0u : (1u << LG) * 8u) + s[g]);
     put_id(ids, Q * TC + g, lr.y);
     if (t < a.out.T) {
       const double v = (double)as_float(lr.x);

@@ -1,0 +1,11 @@
+// hb_fast_ttg_512.hip -- instantiations of the fast TreeTraversal kernel with
+// leaf records in global memory, for 512-row workgroups.
+#include "hb_fast.h"
+
+namespace hb {
+
+FastFn fast_ttg_kernel_512(int lg, bool multi) {
+  return multi ? pick_fast<2, true, 512, kFastTableLds>(lg) : pick_fast<2, false, 512, kFastTableLds>(lg);
+}
+
+}  // namespace hb

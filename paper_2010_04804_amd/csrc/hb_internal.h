@@ -17,15 +17,19 @@ namespace hb {
 constexpr int64_t kTreeLdsLimit = 160 * 1024 - 4 * 1024;
 
 // Packed per-tree blocks for the fast traversal kernels (scalar leaves).
-// A tree's block holds 2^lg node records followed by 2^lg leaf records
-// {value bits, caller id} (8 bytes each):
-//   PTT (mode 0, lg = D): node record p = {threshold bits, feature} for heap
-//     index p in [1, 2^D) (slot 0 unused); the leaf record of heap index
-//     a in [2^D, 2^(D+1)) sits at byte 8a of the block.
-//   TT (mode 1, 2^lg >= nodes): node record c = {threshold bits, feature |
-//     8 * right child << 16} (children adjacent: left = right - 1; a leaf
-//     holds threshold -inf and points to itself); the leaf record of node c
-//     sits at 8 * 2^lg + 8c.
+// Node and leaf records are 8 bytes; a leaf record is {value bits, caller id}.
+//   PTT (mode 0, lg = D): the block holds 2^D node records followed by 2^D
+//     leaf records: node record p = {threshold bits, feature} for heap index
+//     p in [1, 2^D) (slot 0 unused); the leaf record of heap index a in
+//     [2^D, 2^(D+1)) sits at byte 8a of the block.
+//   TT (2^lg >= nodes): node record c = {threshold bits, feature | 8 * right
+//     child << 16} (children adjacent: left = right - 1; a leaf holds
+//     threshold -inf and points to itself), leaf record c for node c.
+//     Mode 1: the block holds the 2^lg node records followed by the 2^lg
+//     leaf records, all staged through LDS. Mode 2: the block holds the node
+//     records only, and the leaf records live in a separate array
+//     [trees][2^lg] read from global memory once per walk, so a chunk holds
+//     twice the trees; used while that array fits in an XCD's L2.
 // Blocks are grouped in chunks of fast_tc() trees staged through LDS, either
 // double-buffered (the next chunk is stored while nobody reads its buffer) or
 // single-buffered with twice as many trees per chunk (more independent walks
@@ -41,7 +45,11 @@ constexpr int kFastIdGroup = 32;
 // 16-bit ids per row), so the staging costs 16 bytes per row of a workgroup.
 constexpr int kFastIdStageBytes = 16 * kFastIdGroup * 2 / 64;
 constexpr int fast_node_bytes(int mode) { return (void)mode, 8; }
-constexpr int fast_tree_bytes(int mode, int lg) { return (1 << lg) * (fast_node_bytes(mode) + 8); }
+constexpr int fast_tree_bytes(int mode, int lg) { return (1 << lg) * (fast_node_bytes(mode) + (mode == 2 ? 0 : 8)); }
+// TT leaf records up to this size stay in global memory (mode 2); measured
+// on 1M rows: leaf-wise 500 trees (2 MB) 5.1 -> 3.9 ms, 3500 depth-8 trees
+// (14 MB, L2 misses on every leaf read) 16.6 -> 21.6 ms.
+constexpr int64_t kTtLeafGlobalMax = (int64_t)4 << 20;
 constexpr int fast_pow2_fit(int budget, int tree_bytes) {
   int t = 16;
   while (t > 1 && t * tree_bytes > budget) t >>= 1;
@@ -103,7 +111,9 @@ struct TtDev {
   const int32_t *leaf_id;   // [T][n_pad] caller-local node id
   int32_t n_pad;
   int32_t max_depth;
-  const uint4 *fast;        // packed blocks (mode 1), or nullptr
+  const uint4 *fast;        // packed blocks (mode 1 or 2), or nullptr
+  const uint2 *fast_leaf;   // mode 2: [padded T][2^fast_lg] leaf records; else nullptr
+  int32_t fast_mode;
   int32_t fast_lg;
   int32_t fast_chunks;
 };

@@ -431,10 +431,10 @@ __global__ __launch_bounds__(64 * J) void split_finish_kernel(const double *part
 
 // Launches the fast kernel when its layout exists and its LDS fits; returns
 // kNotApplicable to fall back to traverse_kernel.
-int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t *depth,
+int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int chunks, const int32_t *depth,
                 const EnsembleDev &e, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
                 const Workspace &ws, hipStream_t stream, std::string *err) {
-  if (!blocks || lg < 1 || lg > kFastMaxLg || e.leaf_dim != 1) return kNotApplicable;
+  if (!blocks || (mode == 2 && !leaf) || lg < 1 || lg > kFastMaxLg || e.leaf_dim != 1) return kNotApplicable;
   const int lds_max = max_dynamic_lds(err);
   if (lds_max <= 0) return HB_ERR_HIP;
   const int tb = fast_tree_bytes(mode, lg);
@@ -459,7 +459,12 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
                               {256, kFastTableLds, fast_tt_kernel_256},
                               {256, kFastTableSmall, fast_tt_kernel_256s},
                               {128, kFastTableSmall, fast_tt_kernel_128}};
-  const Shape *shapes = mode == 0 ? kPtt : kTt;
+  static const Shape kTtg[] = {{512, kFastTableLds, fast_ttg_kernel_512},
+                               {512, kFastTableSmall, fast_ttg_kernel_512s},
+                               {256, kFastTableLds, fast_ttg_kernel_256},
+                               {256, kFastTableSmall, fast_ttg_kernel_256s},
+                               {128, kFastTableSmall, fast_ttg_kernel_128}};
+  const Shape *shapes = mode == 0 ? kPtt : mode == 1 ? kTt : kTtg;
   const int n_shapes = mode == 0 ? 7 : 5;
   // static LDS: the chunk buffer(s) and the leaf-id staging (16-bit ids of a
   // 32-tree group per row); dynamic LDS: the feature tile (F x rows floats)
@@ -484,7 +489,8 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
   // Below four waves per CU the row-parallel walk is latency-bound; the
   // trees-across-lanes kernel then wins when the node tables are small
   // enough to stay in L1 (depth-3 forests: 0.9 vs 1.5 ms at 1M rows).
-  if (best_waves < 4 && (int64_t)chunks * fast_tc(tb) * tb <= (int64_t)64 << 10) return kPreferLanes;
+  const int64_t table_bytes = (int64_t)chunks * fast_tc(tb) * (tb + (mode == 2 ? (8 << lg) : 0));
+  if (best_waves < 4 && table_bytes <= (int64_t)64 << 10) return kPreferLanes;
   const int rows = shapes[best].rows;
   const size_t xbytes = (size_t)e.n_cols * rows * 4;
   FastFn fn = shapes[best].get(lg, multi);
@@ -499,6 +505,7 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
   a.out = OutArgs{scores, e.n_trees, e.n_outputs, e.aggregation, e.transform, e.base_score};
   a.tree_class = e.tree_class;
   a.blocks = blocks;
+  a.leaf = leaf;
   a.tree_depth = depth;
   a.n_chunks = (int)((int64_t)chunks * fast_tc(tb) / fast_tc(tb, shapes[best].budget));
   a.ids_vec = (e.n_trees % 4 == 0) && ((reinterpret_cast<uintptr_t>(leaf_ids) & 15) == 0);
@@ -507,7 +514,7 @@ int launch_fast(int mode, int lg, const uint4 *blocks, int chunks, const int32_t
   // Below that, allocating lets the two halves of a row segment that
   // straddles a line merge in L2 (measured: multiclass 3500 trees 3% faster
   // streaming, the 500-tree model 20% slower).
-  a.ids_nt = (int64_t)chunks * fast_tc(tb) * tb > (int64_t)4 << 20;
+  a.ids_nt = table_bytes > (int64_t)4 << 20;
   hipError_t rc = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)xbytes);
   if (rc != hipSuccess) {
@@ -654,7 +661,8 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
   int rc = kNotApplicable;
   if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsPtt)) rc = launch_lanes(true, a, stream, err);
   if (rc == kNotApplicable)
-    rc = launch_fast(0, t.depth, t.fast, t.fast_chunks, nullptr, e, X, n_rows, scores, leaf_ids, ws, stream, err);
+    rc = launch_fast(0, t.depth, t.fast, nullptr, t.fast_chunks, nullptr, e, X, n_rows, scores, leaf_ids, ws, stream,
+                     err);
   if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(true, a, stream, err);
   if (rc != kNotApplicable) return rc;
   return launch_traverse(true, a, stream, err);
@@ -681,7 +689,8 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
   int rc = kNotApplicable;
   if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsTt)) rc = launch_lanes(false, a, stream, err);
   if (rc == kNotApplicable)
-    rc = launch_fast(1, t.fast_lg, t.fast, t.fast_chunks, t.depth, e, X, n_rows, scores, leaf_ids, ws, stream, err);
+    rc = launch_fast(t.fast_mode, t.fast_lg, t.fast, t.fast_leaf, t.fast_chunks, t.depth, e, X, n_rows, scores,
+                     leaf_ids, ws, stream, err);
   if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(false, a, stream, err);
   if (rc != kNotApplicable) return rc;
   return launch_traverse(false, a, stream, err);

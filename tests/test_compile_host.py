@@ -201,3 +201,41 @@ def test_missing_values_tricky_ensembles():
         for s in ("ptt", "tt", "gemm"):
             ids, raw = getattr(emulate, s)(h, m, X)
             assert np.array_equal(ids, o_ids), (seed, s)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 4, 5])
+def test_tt_packed_tables_walk_in_bounds(cfg):
+    """The row-parallel TT kernels' packed tables ("fast_node", "fast_leaf"),
+    walked in numpy the way the kernel walks them, for every tree of the
+    padded count (a multiple of 32): the state never leaves its tree, the
+    padding trees stay at their root, and the leaf ids are the oracle's.
+    Rows include negative values, which a zero record would send to child
+    offset -8."""
+    model = synth.make_model(cfg)
+    h = hb.compile(model, device=-1)
+    info = h.info()
+    T = info["n_trees"]
+    node = h.table("tt", "fast_node", np.uint32).reshape(-1, 2)
+    leaf = h.table("tt", "fast_leaf", np.uint32).reshape(-1, 2)
+    Tp = -(-T // 32) * 32
+    NP = node.shape[0] // Tp
+    assert node.shape[0] == Tp * NP and NP & (NP - 1) == 0 and leaf.shape == node.shape
+    X = synth.make_rows(cfg, 256).astype(np.float32)
+    X[::2] = -X[::2]
+    cols = h.table("tt", "features", np.int32) & ((1 << 30) - 1)
+    Xt = X[:, cols]
+    thr = node[:, 0].view(np.float32)
+    feat = (node[:, 1] & 0xFFFF).astype(np.int64)
+    right = (node[:, 1] >> 16).astype(np.int64)
+    base = (np.arange(Tp, dtype=np.int64) * NP)[None, :]
+    rows = np.arange(X.shape[0])[:, None]
+    s = np.zeros((X.shape[0], Tp), dtype=np.int64)
+    for _ in range(int(h.table("tt", "depth", np.int32).max()) + 2):
+        idx = base + s // 8
+        f = feat[idx]
+        assert (f < Xt.shape[1]).all()
+        s = right[idx] - 8 * (Xt[rows, f] < thr[idx])
+        assert ((s >= 0) & (s < 8 * NP) & (s % 8 == 0)).all()
+    assert (s[:, T:] == 0).all()
+    _, _, o_ids = oracle.predict(model, X)
+    assert np.array_equal(leaf[base + s // 8, 1][:, :T].astype(np.int32), o_ids)
