@@ -424,6 +424,33 @@ void build_gemm(hb_handle *h, const hb_ensemble_desc *d, const std::vector<Canon
   h->gemm_dims = {k_pad, l_pad, h->gemm_n_shapes};
 }
 
+// Node records [T][slots] (two words each) regrouped as [ceil(T/64)][slots][64]
+// for the trees-across-lanes kernel; records of padding trees stay zero and
+// are never read (lanes past the last tree do not walk).
+std::vector<uint32_t> interleave64(const std::vector<uint32_t> &node, int64_t T, int64_t slots) {
+  const int64_t groups = (T + 63) / 64;
+  std::vector<uint32_t> il((size_t)(groups * slots * 64 * 2), 0u);
+  for (int64_t t = 0; t < T; ++t)
+    for (int64_t p = 0; p < slots; ++p) {
+      const size_t dst = (size_t)(((t / 64) * slots + p) * 64 + t % 64) * 2;
+      il[dst] = node[(size_t)(t * slots + p) * 2];
+      il[dst + 1] = node[(size_t)(t * slots + p) * 2 + 1];
+    }
+  return il;
+}
+
+// Leaf values [T * slots][ld] and caller ids [T * slots] as one record per
+// leaf: ld value words, the id, zero padding to leaf_pk_words(ld).
+std::vector<uint32_t> pack_leaves(const std::vector<float> &value, const std::vector<int32_t> &id, int32_t ld) {
+  const size_t w = (size_t)hb::leaf_pk_words(ld);
+  std::vector<uint32_t> pk(id.size() * w, 0u);
+  for (size_t i = 0; i < id.size(); ++i) {
+    for (int32_t k = 0; k < ld; ++k) pk[i * w + k] = fbits(value[i * ld + k]);
+    pk[i * w + ld] = (uint32_t)id[i];
+  }
+  return pk;
+}
+
 template <class T>
 int upload(hb_handle *h, const std::vector<T> &src, const T **dst) {
   if (src.empty()) {
@@ -620,6 +647,12 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
       if (!rc) rc = upload(h, h->ptt_leaf_value, &h->ptt.leaf_value);
       if (!rc) rc = upload(h, h->ptt_leaf_id, &h->ptt.leaf_id);
       h->ptt.depth = D;
+      if (!rc) {
+        const int64_t slots = (int64_t)h->ptt_node.size() / 2 / h->info.n_trees;
+        rc = upload(h, interleave64(h->ptt_node, h->info.n_trees, slots), &pn);
+        h->ptt.node_il = reinterpret_cast<const uint2 *>(pn);
+      }
+      if (!rc) rc = upload(h, pack_leaves(h->ptt_leaf_value, h->ptt_leaf_id, d->leaf_dim), &h->ptt.leaf_pk);
       if (!rc && !h->ptt_fast.empty()) {
         rc = upload(h, h->ptt_fast, &pn);
         h->ptt.fast = reinterpret_cast<const uint4 *>(pn);
@@ -634,6 +667,11 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
       if (!rc) rc = upload(h, h->tt_leaf_id, &h->tt.leaf_id);
       h->tt.n_pad = h->tt_n_pad;
       h->tt.max_depth = D;
+      if (!rc) {
+        rc = upload(h, interleave64(h->tt_node, h->info.n_trees, h->tt_n_pad), &pn);
+        h->tt.node_il = reinterpret_cast<const uint2 *>(pn);
+      }
+      if (!rc) rc = upload(h, pack_leaves(h->tt_leaf_value, h->tt_leaf_id, d->leaf_dim), &h->tt.leaf_pk);
       if (!rc && !h->tt_fast.empty()) {
         if (h->tt_fast_mode == 2) {  // node blocks, leaf records apart
           rc = upload(h, h->tt_fast, &pn);

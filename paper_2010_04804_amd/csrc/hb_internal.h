@@ -89,6 +89,20 @@ struct EnsembleDev {
   const float *base_score;    // [K] device, or nullptr
 };
 
+// Interleaved node records (node_il) serve the trees-across-lanes kernel, in
+// which lane l of a wave walks tree 64 g + l: slot p of the 64 trees of group
+// g is 64 consecutive records, so lanes at the same slot share cache lines
+// (the paper batches the trees' tensors level by level in the same spirit).
+// The same kernel reads a leaf through one packed record (leaf_pk):
+// [T][leaf slots][leaf_pk_words(leaf_dim)] 32-bit words, the leaf_dim values
+// then the caller id, padded to a power of two so a record never straddles a
+// 128-byte line.
+constexpr int leaf_pk_words(int leaf_dim) {
+  int w = 2;
+  while (w < leaf_dim + 1) w *= 2;
+  return w;
+}
+
 // PerfectTreeTraversal tensors (Table 6, Algorithm 3), 1-based heap per tree:
 // slot p in [1, 2^D) is a decision node, the children of p are 2p and 2p+1,
 // and after D steps the index lies in [2^D, 2^(D+1)); leaf slot = index - 2^D.
@@ -97,6 +111,9 @@ struct PttDev {
   const float *leaf_value;  // [T][2^D][leaf_dim]
   const int32_t *leaf_id;   // [T][2^D] caller-local node id
   int32_t depth;            // D
+  const uint2 *node_il;     // [ceil(T/64)][2^D][64]: the node records of 64
+                            // consecutive trees interleaved slot by slot
+  const uint32_t *leaf_pk;  // [T][2^D][leaf_pk_words]: values, then caller id
   const uint4 *fast;        // packed blocks (mode 0, lg = D), or nullptr
   int32_t fast_chunks;
 };
@@ -111,6 +128,8 @@ struct TtDev {
   const int32_t *leaf_id;   // [T][n_pad] caller-local node id
   int32_t n_pad;
   int32_t max_depth;
+  const uint2 *node_il;     // [ceil(T/64)][n_pad][64], as PttDev::node_il
+  const uint32_t *leaf_pk;  // [T][n_pad][leaf_pk_words], as PttDev::leaf_pk
   const uint4 *fast;        // packed blocks (mode 1 or 2), or nullptr
   const uint2 *fast_leaf;   // mode 2: [padded T][2^fast_lg] leaf records; else nullptr
   int32_t fast_mode;

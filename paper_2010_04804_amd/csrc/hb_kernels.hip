@@ -45,6 +45,8 @@ struct TravArgs {
   const int32_t *tree_class;
   const float *base_score;
   const uint2 *node;          // [T][slots]
+  const uint2 *node_il;       // [ceil(T/64)][slots][64] (trees-across-lanes kernel)
+  const uint32_t *leaf_pk;    // [T][leaf_slots][leaf_pk_words(LD)] (trees-across-lanes kernel)
   const float *leaf_value;    // [T][leaf_slots][LD]
   const int32_t *leaf_id;     // [T][leaf_slots]
   const int32_t *tree_depth;  // TT: [T]
@@ -308,31 +310,49 @@ __global__ __launch_bounds__(kLaneThreads) void lanes_kernel(TravArgs a) {
 #pragma unroll
     for (int k = 0; k < KMAX; ++k) acc[r][k] = 0.0;
   for (int t = tid; t < a.T; t += kLaneThreads) {
-    const uint2 *node = a.node + (size_t)t * a.slots;
+    // the wave's 64 trees are interleaved slot by slot: this lane's tree
+    // has slot p at record 64 p of its group
+    const uint2 *node = a.node_il + (size_t)(t >> 6) * a.slots * 64 + (t & 63);
     const int levels = PERFECT ? a.depth : a.tree_depth[t];
     const int cls = (!LEAF_VEC && KMAX > 1) ? a.tree_class[t] : 0;
+    // the R walks of a tree are independent: advance them level by level
+    // together so that R node reads are in flight at once
+    uint32_t idx[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) idx[r] = PERFECT ? 1u : 0u;
+    for (int lvl = 0; lvl < levels; ++lvl) {
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const uint2 rec = node[idx[r] * 64u];
+        const uint32_t f = PERFECT ? rec.y : (rec.y & 0xffffu);
+        const bool go_left = xs[r * a.F + f] < as_float(rec.x);
+        idx[r] = PERFECT ? 2u * idx[r] + (go_left ? 0u : 1u) : (rec.y >> 16) - (go_left ? 1u : 0u);
+      }
+    }
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      const float *x = xs + r * a.F;
-      uint32_t idx = PERFECT ? 1u : 0u;
-      for (int lvl = 0; lvl < levels; ++lvl) {
-        const uint2 rec = node[idx];
-        const uint32_t f = PERFECT ? rec.y : (rec.y & 0xffffu);
-        const bool go_left = x[f] < as_float(rec.x);
-        idx = PERFECT ? 2u * idx + (go_left ? 0u : 1u) : (rec.y >> 16) - (go_left ? 1u : 0u);
-      }
-      const uint32_t slot = PERFECT ? idx - (uint32_t)a.leaf_slots : idx;
-      const size_t lrec = (size_t)t * a.leaf_slots + slot;
-      if (LEAF_VEC) {
+      const uint32_t slot = PERFECT ? idx[r] - (uint32_t)a.leaf_slots : idx[r];
+      // one packed record per leaf: the values, then the caller id
+      const uint32_t *lrec = a.leaf_pk + ((size_t)t * a.leaf_slots + slot) * leaf_pk_words(LD);
+      uint32_t id;
+      if (!LEAF_VEC) {
+        const uint2 v = *reinterpret_cast<const uint2 *>(lrec);
+        const double d = (double)as_float(v.x);
+#pragma unroll
+        for (int k = 0; k < KMAX; ++k) acc[r][k] += (k == cls) ? d : 0.0;
+        id = v.y;
+      } else if (KMAX == 2) {  // leaf_dim 2: {v0, v1, id, 0}
+        const uint4 v = *reinterpret_cast<const uint4 *>(lrec);
+        acc[r][0] += (double)as_float(v.x);
+        acc[r][1] += (double)as_float(v.y);
+        id = v.z;
+      } else {
 #pragma unroll
         for (int k = 0; k < KMAX; ++k)
-          if (k < LD) acc[r][k] += (double)a.leaf_value[lrec * LD + k];
-      } else {
-        const double v = (double)a.leaf_value[lrec];
-#pragma unroll
-        for (int k = 0; k < KMAX; ++k) acc[r][k] += (k == cls) ? v : 0.0;
+          if (k < LD) acc[r][k] += (double)as_float(lrec[k]);
+        id = lrec[LD];
       }
-      if (a.leaf_ids && r < nr) a.leaf_ids[(r0 + r) * a.T + t] = a.leaf_id[lrec];
+      if (a.leaf_ids && r < nr) a.leaf_ids[(r0 + r) * a.T + t] = (int32_t)id;
     }
   }
 #pragma unroll
@@ -645,13 +665,15 @@ TravArgs common_args(const EnsembleDev &e, const float *X, int64_t n, float *sco
 
 int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_rows, float *scores,
                int32_t *leaf_ids, const Workspace &ws, hipStream_t stream, std::string *err) {
-  if (!t.node || !t.leaf_value || !t.leaf_id || t.depth < 0 || t.depth > HB_PTT_MAX_DEPTH) {
+  if (!t.node || !t.node_il || !t.leaf_pk || !t.leaf_value || !t.leaf_id || t.depth < 0 || t.depth > HB_PTT_MAX_DEPTH) {
     *err = "PTT tables missing";
     return HB_ERR_INVALID_ARG;
   }
   if (n_rows <= 0) return HB_OK;
   TravArgs a = common_args(e, X, n_rows, scores, leaf_ids);
   a.node = t.node;
+  a.node_il = t.node_il;
+  a.leaf_pk = t.leaf_pk;
   a.leaf_value = t.leaf_value;
   a.leaf_id = t.leaf_id;
   a.depth = t.depth;
@@ -670,7 +692,7 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
 
 int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_rows, float *scores,
               int32_t *leaf_ids, const Workspace &ws, hipStream_t stream, std::string *err) {
-  if (!t.node || !t.leaf_value || !t.leaf_id || !t.depth || t.n_pad < 1) {
+  if (!t.node || !t.node_il || !t.leaf_pk || !t.leaf_value || !t.leaf_id || !t.depth || t.n_pad < 1) {
     *err = "TT tables missing";
     return HB_ERR_INVALID_ARG;
   }
@@ -681,6 +703,8 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
   if (n_rows <= 0) return HB_OK;
   TravArgs a = common_args(e, X, n_rows, scores, leaf_ids);
   a.node = t.node;
+  a.node_il = t.node_il;
+  a.leaf_pk = t.leaf_pk;
   a.leaf_value = t.leaf_value;
   a.leaf_id = t.leaf_id;
   a.tree_depth = t.depth;
