@@ -399,13 +399,16 @@ LanesFn pick_lanes_r(int kmax, bool vec) {
 // row-parallel ones. The row-parallel kernels cost a near-constant time until
 // the batch fills the chip (one workgroup walks every tree in sequence), the
 // tree-parallel one a time proportional to the batch; both scale with
-// trees x depth, so the crossing is a batch size, measured on the 500-tree
-// depth-8 and the leaf-wise depth-12 models: about 8K rows for PTT and 16K
-// for TT, whose row-parallel walk is slower.
-constexpr int64_t kLanesMaxRowsPtt = 8192;
+// trees x depth, so the crossing is a batch size. Measured (scores only):
+// 500 perfect depth-8 trees cross at about 16K rows, 7 x 500 such trees with
+// seven outputs at 12K-14K, and the leaf-wise depth-12 trees (TT, whose
+// row-parallel walk is slower) at about 20K.
+constexpr int64_t kLanesMaxRowsPtt = 12288;
 constexpr int64_t kLanesMaxRowsTt = 16384;
 // With a workspace the tree-split row-parallel kernel takes over from here
-// (measured on the three models above: the split wins from 1,000 to 1,200 rows).
+// (measured: the split wins from 1,500 to 2,000 rows on the single-output
+// models, while the seven-output model gains from splitting at any size
+// measured, 512 rows up).
 constexpr int64_t kLanesMaxRowsSplit = 1024;
 
 constexpr int kNotApplicable = 1;
@@ -618,8 +621,9 @@ int launch_lanes(bool perfect, const TravArgs &a, hipStream_t stream, std::strin
   if (lds_max <= 0) return HB_ERR_HIP;
   const bool vec = a.LD > 1;
   const int kmax = kmax_for(vec ? a.LD : a.K);
-  // four rows per workgroup when the batch is large enough and the sums are few
-  int R = (a.n_rows > 4 * 256 && kmax <= 2) ? 4 : 1;
+  // four rows per workgroup (four walks in flight per lane) when the batch is
+  // large enough and the 4 x kmax double sums fit in registers
+  int R = (a.n_rows > 4 * 256 && kmax <= 8) ? 4 : 1;
   auto need = [&](int r) { return ((size_t)r * a.F * 4 + 15) / 16 * 16 + (size_t)4 * r * kmax * 8; };
   if (need(R) > (size_t)lds_max) R = 1;
   if (need(R) > (size_t)lds_max) return kNotApplicable;

@@ -84,18 +84,21 @@ def test_ragged_batches(strategy, n):
     check(model, X, scores, ids, f"ragged{n}/{strategy}")
 
 
+@pytest.mark.parametrize("workspace", [False, True])
 @pytest.mark.parametrize("strategy", ["ptt", "tt"])
-@pytest.mark.parametrize("cfg,n", [(2, 1025), (2, 1027), (2, 4096), (2, 8192), (2, 8193), (5, 16384), (5, 16385), (4, 4095),
-                                   (3, 4093), (3, 20_001)])
-def test_tree_parallel_boundaries(cfg, n, strategy):
-    """Batch sizes around the switch between the trees-across-lanes kernel and
-    the row-parallel one, and its four-rows-per-workgroup form with a ragged
-    last workgroup; config 3's 2000-feature rows take it at every size."""
+@pytest.mark.parametrize("cfg,n", [(2, 1024), (2, 1025), (2, 1027), (2, 4096), (2, 12288), (2, 12289), (5, 16384),
+                                   (5, 16385), (4, 1025), (4, 4095), (3, 4093), (3, 20_001)])
+def test_tree_parallel_boundaries(cfg, n, strategy, workspace):
+    """Batch sizes around the switches between the trees-across-lanes kernel
+    and the row-parallel ones (1,024 rows with a workspace; 12,288 rows for
+    PTT and 16,384 for TT without), and its four-rows-per-workgroup form with
+    a ragged last workgroup, also with seven outputs; config 3's 2000-feature
+    rows take it at every size."""
     model, h = handle(cfg)
-    say("tree-parallel", cfg, strategy, n)
+    say("tree-parallel", cfg, strategy, n, "workspace" if workspace else "no workspace")
     X = synth.make_rows(cfg, n)
-    scores, ids = run(h, X, strategy)
-    check(model, X, scores, ids, f"lanes cfg{cfg}/{n}/{strategy}")
+    scores, ids = run(h, X, strategy, workspace=workspace)
+    check(model, X, scores, ids, f"lanes cfg{cfg}/{n}/{strategy}/ws={workspace}")
 
 
 @pytest.mark.parametrize("strategy", ["ptt", "tt"])
