@@ -148,6 +148,20 @@ __device__ __forceinline__ void flush_packed(int32_t *leaf_ids, int64_t n_rows, 
   }
 }
 
+typedef __attribute__((address_space(3))) const float lds_f32;
+
+// LDS byte address of a TT node's feature in this lane's column of the tile:
+// xlane + (w & 0xffff) * ROWS * 4 in one v_mad_u32_u16, which multiplies the
+// low 16 bits of the record word (the feature) as they are, so the child
+// offset in the high half needs no mask.
+template <int ROWS>
+__device__ __forceinline__ uint32_t tt_xaddr(uint32_t w, uint32_t xlane) {
+  static_assert(ROWS * 4 < 65536, "the row stride must fit the 16-bit multiplier");
+  uint32_t r;
+  asm("v_mad_u32_u16 %0, %1, %2, %3" : "=v"(r) : "v"(w), "s"((uint32_t)ROWS * 4u), "v"(xlane));
+  return r;
+}
+
 // A group of leaf ids waiting to be written while the next group is walked.
 struct IdLag {
   bool on;               // a group is pending (uniform)
@@ -216,16 +230,32 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
     int levels = 0;
 #pragma unroll
     for (int g = 0; g < TC; ++g) levels = max(levels, a.tree_depth[min(t0 + g, a.out.T - 1)]);
+    // Pipelined like the PTT walk: all feature reads of a level are issued
+    // before the first is used, and each tree's next node read right after
+    // its step (the read after the last level is unused but in bounds: every
+    // record's children lie in its own tree).
+    const uint32_t xlane = (uint32_t)(uintptr_t)xs + lane4;
+    uint64_t rec[TC];  // {threshold bits, feature | 8 * right << 16}, one 8-byte read
+    float xv[TC];
 #pragma unroll
-    for (int g = 0; g < TC; ++g) s[g] = 0u;  // root record
+    for (int g = 0; g < TC; ++g) {
+      s[g] = 0u;  // root record
+      rec[g] = *reinterpret_cast<const uint64_t *>(base + g * TB);
+    }
     for (int lvl = 0; lvl < levels; ++lvl) {
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int g = 0; g < TC; ++g)
+        xv[g] = *reinterpret_cast<lds_f32 *>((uintptr_t)tt_xaddr<ROWS>((uint32_t)(rec[g] >> 32), xlane));
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int g = 0; g < TC; ++g) {
-        const uint2 rec = *reinterpret_cast<const uint2 *>(base + g * TB + s[g]);
-        const float x = *reinterpret_cast<const float *>(xb + __umul24(rec.y & 0xffffu, ROWS * 4u) + lane4);
-        s[g] = (rec.y >> 16) - (x < as_float(rec.x) ? 8u : 0u);  // Algorithm 2's step: left or right child
+        // Algorithm 2's step: left or right child
+        s[g] = (uint32_t)(rec[g] >> 48) - (xv[g] < as_float((uint32_t)rec[g]) ? 8u : 0u);
+        rec[g] = *reinterpret_cast<const uint64_t *>(base + g * TB + s[g]);
       }
     }
+    __builtin_amdgcn_sched_barrier(0);
   }
 #pragma unroll
   for (int g = 0; g < TC; ++g) {
