@@ -451,6 +451,28 @@ std::vector<uint32_t> pack_leaves(const std::vector<float> &value, const std::ve
   return pk;
 }
 
+// The PTT last decision level with its leaves, trees interleaved by 64 (the
+// layout of PttDev::last_il); D >= 1 and leaf_dim <= 2.
+std::vector<uint32_t> ptt_last_level(const hb_handle *h, int32_t D, int32_t ld) {
+  const int64_t T = h->info.n_trees, S = int64_t(1) << D, half = S / 2;
+  const int64_t groups = (T + 63) / 64;
+  std::vector<uint32_t> out((size_t)(groups * half * 64 * hb::kLastWords), 0u);
+  for (int64_t t = 0; t < T; ++t)
+    for (int64_t q = 0; q < half; ++q) {
+      uint32_t *w = &out[(size_t)(((t / 64) * half + q) * 64 + t % 64) * hb::kLastWords];
+      const size_t node = (size_t)(t * S + half + q) * 2;
+      w[0] = h->ptt_node[node];
+      w[1] = h->ptt_node[node + 1];
+      for (int side = 0; side < 2; ++side) {
+        const size_t leaf = (size_t)(t * S + 2 * q + side);
+        uint32_t *lw = w + 2 + side * (ld + 1);
+        for (int32_t k = 0; k < ld; ++k) lw[k] = fbits(h->ptt_leaf_value[leaf * ld + k]);
+        lw[ld] = (uint32_t)h->ptt_leaf_id[leaf];
+      }
+    }
+  return out;
+}
+
 template <class T>
 int upload(hb_handle *h, const std::vector<T> &src, const T **dst) {
   if (src.empty()) {
@@ -653,6 +675,10 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
         h->ptt.node_il = reinterpret_cast<const uint2 *>(pn);
       }
       if (!rc) rc = upload(h, pack_leaves(h->ptt_leaf_value, h->ptt_leaf_id, d->leaf_dim), &h->ptt.leaf_pk);
+      if (!rc && D >= 1 && d->leaf_dim <= 2) {
+        rc = upload(h, ptt_last_level(h, D, d->leaf_dim), &pn);
+        h->ptt.last_il = reinterpret_cast<const uint4 *>(pn);
+      }
       if (!rc && !h->ptt_fast.empty()) {
         rc = upload(h, h->ptt_fast, &pn);
         h->ptt.fast = reinterpret_cast<const uint4 *>(pn);

@@ -97,6 +97,13 @@ struct EnsembleDev {
 // [T][leaf slots][leaf_pk_words(leaf_dim)] 32-bit words, the leaf_dim values
 // then the caller id, padded to a power of two so a record never straddles a
 // 128-byte line.
+// For perfect trees with leaf_dim <= 2 the last decision level and the two
+// leaves under each of its nodes form one 32-byte record (last_il), so the
+// final step and the leaf read are one access:
+// [ceil(T/64)][2^(D-1)][64][8 words] = {threshold bits, feature, left leaf,
+// right leaf}, a leaf being {value, caller id} (leaf_dim 1, then two zero
+// words) or {value 0, value 1, caller id} (leaf_dim 2).
+constexpr int kLastWords = 8;
 constexpr int leaf_pk_words(int leaf_dim) {
   int w = 2;
   while (w < leaf_dim + 1) w *= 2;
@@ -114,6 +121,7 @@ struct PttDev {
   const uint2 *node_il;     // [ceil(T/64)][2^D][64]: the node records of 64
                             // consecutive trees interleaved slot by slot
   const uint32_t *leaf_pk;  // [T][2^D][leaf_pk_words]: values, then caller id
+  const uint4 *last_il;     // D >= 1 and leaf_dim <= 2: the last level with its leaves, else nullptr
   const uint4 *fast;        // packed blocks (mode 0, lg = D), or nullptr
   int32_t fast_chunks;
 };

@@ -47,6 +47,7 @@ struct TravArgs {
   const uint2 *node;          // [T][slots]
   const uint2 *node_il;       // [ceil(T/64)][slots][64] (trees-across-lanes kernel)
   const uint32_t *leaf_pk;    // [T][leaf_slots][leaf_pk_words(LD)] (trees-across-lanes kernel)
+  const uint4 *last_il;       // PTT: last level with its leaves (PttDev::last_il), or nullptr
   const float *leaf_value;    // [T][leaf_slots][LD]
   const int32_t *leaf_id;     // [T][leaf_slots]
   const int32_t *tree_depth;  // TT: [T]
@@ -320,7 +321,11 @@ __global__ __launch_bounds__(kLaneThreads) void lanes_kernel(TravArgs a) {
     uint32_t idx[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) idx[r] = PERFECT ? 1u : 0u;
-    for (int lvl = 0; lvl < levels; ++lvl) {
+    // perfect trees with at most two leaf values take their last level and
+    // the leaf from one 32-byte record (LAST is uniform)
+    const bool LAST = PERFECT && (LEAF_VEC ? KMAX == 2 : true) && a.last_il != nullptr;
+    const int node_levels = LAST ? levels - 1 : levels;
+    for (int lvl = 0; lvl < node_levels; ++lvl) {
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         const uint2 rec = node[idx[r] * 64u];
@@ -328,6 +333,29 @@ __global__ __launch_bounds__(kLaneThreads) void lanes_kernel(TravArgs a) {
         const bool go_left = xs[r * a.F + f] < as_float(rec.x);
         idx[r] = PERFECT ? 2u * idx[r] + (go_left ? 0u : 1u) : (rec.y >> 16) - (go_left ? 1u : 0u);
       }
+    }
+    if (LAST) {
+      const uint32_t half = (uint32_t)a.leaf_slots >> 1;
+      const uint4 *last = a.last_il + ((size_t)(t >> 6) * half * 64 + (t & 63)) * 2;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const uint4 q0 = last[(idx[r] - half) * 128u];      // {threshold, feature, leaf words}
+        const uint4 q1 = last[(idx[r] - half) * 128u + 1];  // more leaf words
+        const bool go_left = xs[r * a.F + q0.y] < as_float(q0.x);
+        uint32_t id;
+        if (!LEAF_VEC) {  // {value, id} left, then right
+          const double d = (double)as_float(go_left ? q0.z : q1.x);
+#pragma unroll
+          for (int k = 0; k < KMAX; ++k) acc[r][k] += (k == cls) ? d : 0.0;
+          id = go_left ? q0.w : q1.y;
+        } else {  // {value 0, value 1, id} left, then right
+          acc[r][0] += (double)as_float(go_left ? q0.z : q1.y);
+          acc[r][1] += (double)as_float(go_left ? q0.w : q1.z);
+          id = go_left ? q1.x : q1.w;
+        }
+        if (a.leaf_ids && r < nr) a.leaf_ids[(r0 + r) * a.T + t] = (int32_t)id;
+      }
+      continue;
     }
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -678,6 +706,7 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
   a.node = t.node;
   a.node_il = t.node_il;
   a.leaf_pk = t.leaf_pk;
+  a.last_il = t.last_il;
   a.leaf_value = t.leaf_value;
   a.leaf_id = t.leaf_id;
   a.depth = t.depth;
