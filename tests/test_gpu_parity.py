@@ -170,6 +170,34 @@ def test_vector_leaf_forest_routes(n_features, n, strategy):
     check(m, X, scores, ids, f"vecRF F{n_features} n{n}/{strategy}")
 
 
+def _layout_forest(n_trees, depth, leaf_dim, seed, n_features=12):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    m = synth.perfect_forest(rng, n_trees, depth, n_features, lambda r, f: r.standard_normal(f.size),
+                             lambda r, n: r.standard_normal(n * leaf_dim), leaf_dim=leaf_dim)
+    m.update(n_outputs=leaf_dim, tree_class=None, aggregation="mean" if leaf_dim > 1 else "sum",
+             transform="none", base_score=None)
+    return m, rng
+
+
+@pytest.mark.parametrize("strategy", ["ptt", "tt"])
+@pytest.mark.parametrize("n", [37, 3000])
+@pytest.mark.parametrize("n_trees,depth,leaf_dim", [(70, 0, 1), (300, 1, 1), (300, 5, 1), (100, 1, 2), (130, 4, 3),
+                                                    (65, 3, 9)])
+def test_lanes_layouts(n_trees, depth, leaf_dim, n, strategy):
+    """The trees-across-lanes kernel's layouts at their edges: node records
+    interleaved by 64 trees with a partial last group and a second round of
+    trees per lane (300 trees), the 32-byte last-level record at depth 1 and
+    with two leaf values, packed leaf records of 4 and 16 words (3 and 9
+    values), single-leaf trees (no last level); one row per workgroup (37
+    rows, and 9 values at any size) and four."""
+    m, rng = _layout_forest(n_trees, depth, leaf_dim, seed=500 + 7 * depth + leaf_dim)
+    X = np.ascontiguousarray(rng.standard_normal((n, 12)).astype(np.float32))
+    say("lanes layouts", strategy, n_trees, depth, leaf_dim, n)
+    h = hb.compile(m, device=0)
+    scores, ids = run(h, X, strategy, workspace=False)
+    check(m, X, scores, ids, f"lanes T{n_trees} D{depth} ld{leaf_dim} n{n}/{strategy}")
+
+
 @pytest.mark.parametrize("strategy", STRATEGIES)
 @pytest.mark.parametrize("used,leaf_dim,n", [(40, 1, 700), (40, 1, 20_000), (40, 1, 40_000), (40, 2, 9000),
                                              (120, 1, 30_000), (200, 1, 20_001)])
