@@ -368,7 +368,7 @@ def main():
                     help="every workload and strategy against its roofline, instead of the bench line")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": f"--gpus {args.gpus}: this build runs on one GPU only. Rows are "
+        print(json.dumps({"error": f"--gpus {args.gpus}: this benchmark runs on one GPU only. Rows are "
                                    "independent, so N GPUs would each score n/N rows with a "
                                    "replica of the compiled tables and no exchange step."}))
         sys.exit(2)
