@@ -203,12 +203,14 @@ FastFn fast_ptt_kernel_512(int lg, bool multi);
 FastFn fast_ptt_kernel_512s(int lg, bool multi);
 FastFn fast_ptt_kernel_768(int lg, bool multi);
 FastFn fast_ptt_kernel_1024(int lg, bool multi);
+FastFn fast_tt_kernel_1024(int lg, bool multi);
 FastFn fast_tt_kernel_256(int lg, bool multi);
 FastFn fast_tt_kernel_512(int lg, bool multi);
 FastFn fast_tt_kernel_512s(int lg, bool multi);
 FastFn fast_tt_kernel_256s(int lg, bool multi);
 FastFn fast_tt_kernel_128(int lg, bool multi);
 // TT with leaf records in global memory (mode 2)
+FastFn fast_ttg_kernel_1024(int lg, bool multi);
 FastFn fast_ttg_kernel_256(int lg, bool multi);
 FastFn fast_ttg_kernel_512(int lg, bool multi);
 FastFn fast_ttg_kernel_512s(int lg, bool multi);

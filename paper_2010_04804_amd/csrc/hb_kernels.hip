@@ -505,18 +505,20 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int ch
                                {256, kFastTableLds, fast_ptt_kernel_256},
                                {256, kFastTableSmall, fast_ptt_kernel_256s},
                                {128, kFastTableSmall, fast_ptt_kernel_128}};
-  static const Shape kTt[] = {{512, kFastTableLds, fast_tt_kernel_512},
+  static const Shape kTt[] = {{1024, kFastTableSmall, fast_tt_kernel_1024},
+                              {512, kFastTableLds, fast_tt_kernel_512},
                               {512, kFastTableSmall, fast_tt_kernel_512s},
                               {256, kFastTableLds, fast_tt_kernel_256},
                               {256, kFastTableSmall, fast_tt_kernel_256s},
                               {128, kFastTableSmall, fast_tt_kernel_128}};
-  static const Shape kTtg[] = {{512, kFastTableLds, fast_ttg_kernel_512},
+  static const Shape kTtg[] = {{1024, kFastTableSmall, fast_ttg_kernel_1024},
+                               {512, kFastTableLds, fast_ttg_kernel_512},
                                {512, kFastTableSmall, fast_ttg_kernel_512s},
                                {256, kFastTableLds, fast_ttg_kernel_256},
                                {256, kFastTableSmall, fast_ttg_kernel_256s},
                                {128, kFastTableSmall, fast_ttg_kernel_128}};
   const Shape *shapes = mode == 0 ? kPtt : mode == 1 ? kTt : kTtg;
-  const int n_shapes = mode == 0 ? 7 : 5;
+  const int n_shapes = mode == 0 ? 7 : 6;
   // static LDS: the chunk buffer(s) and the leaf-id staging (16-bit ids of a
   // 32-tree group per row); dynamic LDS: the feature tile (F x rows floats)
   auto lds_of = [&](const Shape &sh) {

@@ -170,6 +170,22 @@ def test_vector_leaf_forest_routes(n_features, n, strategy):
     check(m, X, scores, ids, f"vecRF F{n_features} n{n}/{strategy}")
 
 
+@pytest.mark.parametrize("missing", [False, True])
+def test_tt_widest_workgroups(missing):
+    """TreeTraversal in 1024-row workgroups (batches of 65,536 rows and more
+    with a narrow feature tile), with a ragged last workgroup, and with
+    default directions for missing values."""
+    model, h = handle(2)
+    n = 70_001
+    X = synth.make_rows(2, n)
+    if missing:
+        model, X = synth.with_missing(model, X, seed=77)
+        h = hb.compile(model, device=0)
+    say("tt 1024-row workgroups", n, "missing" if missing else "")
+    scores, ids = run(h, X, "tt", workspace=False)
+    check(model, X, scores, ids, f"tt1024 missing={missing}")
+
+
 def _layout_forest(n_trees, depth, leaf_dim, seed, n_features=12):
     rng = np.random.Generator(np.random.PCG64(seed))
     m = synth.perfect_forest(rng, n_trees, depth, n_features, lambda r, f: r.standard_normal(f.size),
