@@ -31,12 +31,6 @@ uint32_t fbits(float f) {
   return u;
 }
 
-float as_float_bits(uint32_t u) {
-  float f;
-  std::memcpy(&f, &u, 4);
-  return f;
-}
-
 // One tree renumbered breadth-first: canonical node 0 is the root and the two
 // children of an internal node get consecutive ids (left, then right).
 struct CanonTree {
@@ -156,15 +150,6 @@ struct hb_handle {
   int32_t gemm_k_pad = 0, gemm_l_pad = 0, gemm_n_shapes = 0;
   // packed blocks of the fast traversal kernels (device layout only)
   std::vector<uint32_t> ptt_fast, tt_fast, tt_fast_leaf;
-  // Exact 16-bit feature ranks for the fast kernels: per feature-tile column
-  // the sorted distinct thresholds its node records hold (rank_thr, column c
-  // at [rank_off[c], rank_off[c+1])), and the fast blocks with each node
-  // record's threshold replaced by j = 1 + its index among them, so that
-  // x < t exactly when rank(x) = #{thresholds <= x} < j (NaN: rank = count).
-  // Empty when a column holds more than 65535 distinct thresholds.
-  std::vector<int32_t> rank_off;
-  std::vector<float> rank_thr;
-  std::vector<uint32_t> ptt_fast_rank, tt_fast_rank;
   int32_t ptt_fast_chunks = 0, tt_fast_lg = 0, tt_fast_chunks = 0, tt_fast_mode = 1;
   // device
   std::vector<void *> allocations;
@@ -350,55 +335,6 @@ void build_fast(hb_handle *h, const hb_ensemble_desc *d, const std::vector<Canon
     h->tt_fast_lg = lg;
     h->tt_fast_chunks = (int)(padded / hb::fast_tc(hb::fast_tree_bytes(h->tt_fast_mode, lg)));
   }
-}
-
-// The rank tables of the fast blocks (see hb_handle::rank_off). A record's
-// threshold word and tile column are read from the blocks themselves, padding
-// and leaf records included (their thresholds then also get ranks, which
-// keeps every conversion exact without special cases).
-void build_rank(hb_handle *h, int32_t n_cols) {
-  if ((h->ptt_fast.empty() && h->tt_fast.empty()) || n_cols < 1) return;
-  const size_t ptt_words = h->ptt_fast.empty() ? 0 : (size_t)4 << h->info.max_depth;  // per tree
-  const size_t ptt_slots = ptt_words / 4;                                             // 2^D node slots
-  const size_t tt_words = h->tt_fast.empty() ? 0 : (size_t)2 << h->tt_fast_lg;        // per tree
-  // visits every node record as (threshold word, tile column, record pointer)
-  auto each_record = [&](auto &&fn) {
-    for (size_t t = 0; ptt_words && t < h->ptt_fast.size() / ptt_words; ++t)
-      for (size_t p = 1; p < ptt_slots; ++p) {
-        uint32_t *rec = &h->ptt_fast[t * ptt_words + 2 * p];
-        fn(rec, rec[1]);
-      }
-    for (size_t i = 0; tt_words && i < h->tt_fast.size(); i += 2) fn(&h->tt_fast[i], h->tt_fast[i + 1] & 0xffffu);
-  };
-  std::vector<std::vector<float>> thr(n_cols);
-  bool ok = true;
-  each_record([&](const uint32_t *rec, uint32_t col) {
-    if (col >= (uint32_t)n_cols) ok = false;
-    else thr[col].push_back(as_float_bits(rec[0]));
-  });
-  if (!ok) return;
-  h->rank_off.assign(n_cols + 1, 0);
-  for (int32_t c = 0; c < n_cols; ++c) {
-    std::sort(thr[c].begin(), thr[c].end());
-    thr[c].erase(std::unique(thr[c].begin(), thr[c].end()), thr[c].end());  // -0 == +0: one entry
-    if (thr[c].size() > 65535) return;
-    h->rank_off[c + 1] = h->rank_off[c] + (int32_t)thr[c].size();
-  }
-  h->rank_thr.reserve(h->rank_off[n_cols]);
-  for (int32_t c = 0; c < n_cols; ++c) h->rank_thr.insert(h->rank_thr.end(), thr[c].begin(), thr[c].end());
-  h->ptt_fast_rank = h->ptt_fast;
-  h->tt_fast_rank = h->tt_fast;
-  auto rank_of = [&](uint32_t bits, uint32_t col) {
-    const std::vector<float> &v = thr[col];
-    return (uint32_t)(std::lower_bound(v.begin(), v.end(), as_float_bits(bits)) - v.begin()) + 1u;
-  };
-  for (size_t t = 0; ptt_words && t < h->ptt_fast.size() / ptt_words; ++t)
-    for (size_t p = 1; p < ptt_slots; ++p) {
-      const size_t i = t * ptt_words + 2 * p;
-      h->ptt_fast_rank[i] = rank_of(h->ptt_fast[i], h->ptt_fast[i + 1]);
-    }
-  for (size_t i = 0; tt_words && i < h->tt_fast.size(); i += 2)
-    h->tt_fast_rank[i] = rank_of(h->tt_fast[i], h->tt_fast[i + 1] & 0xffffu);
 }
 
 void build_gemm(hb_handle *h, const hb_ensemble_desc *d, const std::vector<CanonTree> &trees) {
@@ -683,7 +619,6 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
     if (I.feasible[HB_STRATEGY_TT]) build_tt(h, d, trees);
     if (I.feasible[HB_STRATEGY_GEMM]) build_gemm(h, d, trees);
     build_fast(h, d, trees);
-    build_rank(h, n_cols);
   } catch (const std::bad_alloc &) {
     delete h;
     return fail(HB_ERR_OOM, "out of host memory building tables");
@@ -906,14 +841,10 @@ int hb_table(const hb_handle *h, int strategy, const char *name, const void **da
     return HB_OK;
   };
   if (n == "features") return give(h->cols);
-  if (n == "rank_off") return give(h->rank_off);
-  if (n == "rank_thr") return give(h->rank_thr);
   if (strategy == HB_STRATEGY_PTT) {
     if (n == "node") return give(h->ptt_node);
     if (n == "leaf_value") return give(h->ptt_leaf_value);
     if (n == "leaf_id") return give(h->ptt_leaf_id);
-    if (n == "fast") return give(h->ptt_fast);
-    if (n == "fast_rank") return give(h->ptt_fast_rank);
   } else if (strategy == HB_STRATEGY_TT) {
     if (n == "node") return give(h->tt_node);
     if (n == "depth") return give(h->tt_depth);
@@ -922,7 +853,6 @@ int hb_table(const hb_handle *h, int strategy, const char *name, const void **da
     if (n == "dims") return give(h->tt_dims);
     if (n == "fast_node") return give(h->tt_fast);
     if (n == "fast_leaf") return give(h->tt_fast_leaf);
-    if (n == "fast_rank") return give(h->tt_fast_rank);
   } else {
     if (n == "node") return give(h->gemm_node);
     if (n == "shape") return give(h->gemm_shape);

@@ -114,58 +114,3 @@ def gemm(h, model, X, check_unique=True):
         cols[:, t] = c
     tix = np.arange(T)[None, :]
     return lid[tix, cols], _aggregate(model, lv[tix, cols])
-
-
-def _ranks(h, X, strategy):
-    """The fast kernels' 16-bit feature ranks: per tile column, the number of
-    the column's sorted distinct thresholds that are <= x (all of them for a
-    NaN, which no threshold is above)."""
-    tile = _tile(h, X, strategy)
-    off = h.table(strategy, "rank_off", np.int32)
-    thr = h.table(strategy, "rank_thr", np.float32)
-    R = np.empty(tile.shape, np.int64)
-    for c in range(tile.shape[1]):
-        t = thr[off[c]:off[c + 1]]
-        assert np.all(t[1:] > t[:-1]), "thresholds sorted and distinct"
-        r = np.searchsorted(t, tile[:, c], side="right")
-        r[np.isnan(tile[:, c])] = len(t)
-        R[:, c] = r
-    assert R.max(initial=0) < 65536
-    return R
-
-
-def ptt_ranked(h, model, X):
-    """Algorithm 3 on the rank-form fast blocks: a node holds j = 1 + the index
-    of its threshold among its column's, and x < t is rank(x) < j."""
-    R = _ranks(h, X, "ptt")
-    info = h.info()
-    T, D = info["n_trees"], info["ptt_depth"]
-    blk = h.table("ptt", "fast_rank", np.uint32).reshape(-1, 4 << D)[:T]
-    n = X.shape[0]
-    tix = np.arange(T)[None, :]
-    rows = np.arange(n)[:, None]
-    a = np.ones((n, T), np.int64)
-    for _ in range(D):
-        j = blk[tix, 2 * a].astype(np.int64)
-        r = R[rows, blk[tix, 2 * a + 1].astype(np.int64)]
-        a = 2 * a + (r >= j)
-    vals = _f32(blk[tix, 2 * a])
-    return blk[tix, 2 * a + 1].astype(np.int32), _aggregate(model, vals[..., None])
-
-
-def tt_ranked(h, model, X):
-    """Algorithm 2 on the rank-form fast node records and the fast leaf records."""
-    R = _ranks(h, X, "tt")
-    T = h.info()["n_trees"]
-    node = h.table("tt", "fast_rank", np.uint32).reshape(-1, 2)
-    leaf = h.table("tt", "fast_leaf", np.uint32).reshape(-1, 2)
-    NP = node.shape[0] // (-(-T // 32) * 32)
-    base = (np.arange(T, dtype=np.int64) * NP)[None, :]
-    rows = np.arange(X.shape[0])[:, None]
-    s = np.zeros((X.shape[0], T), np.int64)
-    for _ in range(int(h.table("tt", "depth", np.int32).max(initial=0))):
-        rec = node[base + s]
-        r = R[rows, (rec[..., 1] & 0xFFFF).astype(np.int64)]
-        s = (rec[..., 1] >> 19).astype(np.int64) - (r < rec[..., 0]).astype(np.int64)
-    lr = leaf[base + s]
-    return lr[..., 1].astype(np.int32), _aggregate(model, _f32(lr[..., 0])[..., None])

@@ -239,29 +239,3 @@ def test_tt_packed_tables_walk_in_bounds(cfg):
     assert (s[:, T:] == 0).all()
     _, _, o_ids = oracle.predict(model, X)
     assert np.array_equal(leaf[base + s // 8, 1][:, :T].astype(np.int32), o_ids)
-
-
-@pytest.mark.parametrize("strategy", ["ptt", "tt"])
-@pytest.mark.parametrize("case", ["cfg1", "cfg2", "cfg4", "cfg5", "missing5", "tricky0", "tricky1", "tricky2",
-                                  "tricky3"])
-def test_rank_form_tables_are_exact(case, strategy):
-    """The fast kernels' rank form: each tile column's sorted distinct
-    thresholds, rows ranked against them and every node threshold replaced by
-    its 1-based index; walking the rank-form blocks must reach the oracle's
-    leaves on ties, -0.0, +-inf, NaN and missing-value directions too."""
-    if case.startswith("tricky"):
-        seed = int(case[-1])
-        m = pins.random_small_ensemble(seed)
-        X = pins.tricky_rows(np.random.Generator(np.random.PCG64(seed)), m, 300)
-    else:
-        cfg = int(case[-1])
-        m, X = synth.make_model(cfg), synth.make_rows(cfg, 24 if cfg == 4 else 64)
-        if case.startswith("missing"):
-            m, X = synth.with_missing(m, X, seed=cfg)
-    h = host(m)
-    if h.info()["feasible"][strategy] is False:
-        pytest.skip("strategy infeasible")
-    ids, raw = getattr(emulate, strategy + "_ranked")(h, m, X)
-    o_raw, _, o_ids = oracle.predict(m, X)
-    assert np.array_equal(ids, o_ids)
-    assert np.allclose(raw, o_raw, rtol=1e-12, atol=1e-12)
