@@ -186,6 +186,55 @@ def test_tt_widest_workgroups(missing):
     check(model, X, scores, ids, f"tt1024 missing={missing}")
 
 
+def _random_model(seed):
+    """A seeded random ensemble: perfect or leaf-wise trees, 1 to 700 trees,
+    depth 1 to 12, 1 to 300 features, scalar leaves with 1 to 9 output
+    columns or vector leaves of 2 to 5 values, any aggregation and transform,
+    numbering permuted; plus a batch size and rows that include ties."""
+    rng = np.random.Generator(np.random.PCG64(9000 + seed))
+    T = int(rng.choice([1, 3, 31, 64, 65, 130, 257, 700]))
+    F = int(rng.choice([1, 2, 7, 28, 64, 150, 300]))
+    thr = lambda r, f: r.standard_normal(f.size)
+    if rng.random() < 0.5:
+        depth = int(rng.integers(1, 13))
+        ld = int(rng.choice([1, 1, 1, 2, 5]))
+        m = synth.perfect_forest(rng, T, depth, F, thr, lambda r, n: r.standard_normal(n * ld), leaf_dim=ld)
+    else:
+        ld = 1
+        max_depth = int(rng.integers(2, 12))
+        n_leaves = int(rng.integers(2, min(200, 2 ** max_depth) + 1))
+        m = synth.leafwise_forest(rng, T, n_leaves, max_depth, 0.7, F, thr, lambda r, n: r.standard_normal(n))
+    K = ld if ld > 1 else int(rng.choice([1, 1, 3, 9]))
+    m.update(n_outputs=K, aggregation=str(rng.choice(["sum", "mean"])),
+             transform="softmax" if K > 1 and rng.random() < 0.5 else str(rng.choice(["none", "sigmoid"])),
+             base_score=rng.standard_normal(K).astype(np.float32) if rng.random() < 0.3 else None,
+             tree_class=rng.integers(0, K, T).astype(np.int32) if ld == 1 and K > 1 else None)
+    m = synth.permute_nodes(m, seed)
+    n = int(rng.choice([1, 5, 700, 3000, 40_000]))
+    X = pins.tricky_rows(rng, m, n) if rng.random() < 0.5 else rng.standard_normal((n, F)).astype(np.float32)
+    return m, np.ascontiguousarray(X)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_ensembles(seed):
+    """Seeded random shapes through every feasible strategy, with and without
+    a workspace, with and without leaf ids."""
+    m, X = _random_model(seed)
+    h = hb.compile(m, device=0)
+    info = h.info()
+    o_raw, o_out, o_ids = oracle.predict(m, X, n_threads=ORACLE_THREADS)
+    for strategy in ("ptt", "tt", "gemm"):
+        if not info["feasible"][strategy]:
+            continue
+        for ws in (False, True):
+            say("random", seed, strategy, "ws" if ws else "no ws", m["n_trees"], X.shape)
+            scores, ids = run(h, X, strategy, workspace=ws, leaves=ws)
+            if ids is not None:
+                assert np.array_equal(ids, o_ids), f"random{seed}/{strategy}/ws={ws}: leaf ids differ"
+            err = np.abs(scores.astype(np.float64) - o_out)
+            assert np.all(err <= TOL * (1.0 + np.abs(o_out))), f"random{seed}/{strategy}/ws={ws}: scores"
+
+
 def _layout_forest(n_trees, depth, leaf_dim, seed, n_features=12):
     rng = np.random.Generator(np.random.PCG64(seed))
     m = synth.perfect_forest(rng, n_trees, depth, n_features, lambda r, f: r.standard_normal(f.size),
