@@ -190,7 +190,9 @@ struct FastArgs {
   int32_t split;
   double *partial;
   int32_t ids_vec;            // leaf_ids rows start 16-byte aligned (T % 4 == 0, aligned base)
-  int32_t ids_nt;             // leaf-id stores bypass L2 allocation (streaming)
+  // with ids_vec: byte k = the residues r mod 8 of the rows whose 128-byte
+  // lines of leaf ids begin at trees congruent to 4k mod 32
+  uint64_t id_phase;
 };
 
 using FastFn = void (*)(FastArgs);

@@ -87,64 +87,66 @@ __device__ __forceinline__ void put_id(IdPack &ids, int q, uint32_t id) {
     ids[q >> 3][(q >> 1) & 3] = id;
 }
 
-// The staging area of a wave: 16 rows x 64 bytes (the rows of one of the four
-// 16-row passes); quad j of row r sits at slot (j + r / 2) mod 4, so the 16
-// lanes that write a quad each touch 2 lanes per bank group.
-__device__ __forceinline__ void stage_ids(u32x4 *stage, const IdPack &ids, int p) {
+// Leaf ids leave in whole 128-byte lines of the output, each as soon as its
+// last tree is walked. Row r's ids start at int offset b + r T (b: the
+// output's offset within a line, in ints), so row r's lines begin at trees
+// congruent to phi(r) = -(b + r T) mod 32; with T a multiple of 4 and a
+// 16-byte aligned output, phi is a multiple of 4 that depends on r mod 8
+// only, and byte k of id_phase lists the residues r mod 8 whose lines begin
+// at trees congruent to 4k. After every fourth tree the lanes of the rows
+// whose line just ended hand its 32 ids (the last 32 slots of their IdPack)
+// to the whole wave through a 512-byte staging area, and one store
+// instruction writes the eight lines (lines that end with a chunk leave at
+// the start of the next one, once its prefetch is issued, since a load
+// issued behind a store is only usable once the store is acknowledged:
+// vmcnt retires both in issue order). For the usual tree counts only one
+// residue in eight has a line ending at a given tree, so the stores spread
+// evenly over the walk instead of leaving in bursts, and each line reaches
+// memory whole.
+struct IdOut {
+  bool on;         // leaf ids requested and the row layout allows vector stores (uniform)
+  u32x4 *stage;    // this wave's staging area: 8 rows x 64 bytes
+  int64_t r0w;     // first row of the wave
+  int t_begin;     // first tree of this workgroup's part
+};
+
+// Writes, for the rows of residue rho in this wave, the ids of trees
+// [max(lo, t_end - 31), min(t_end, T - 1)]; c = (t_end + 1) mod 32 is the
+// slot of tree t_end - 31. lo and T are multiples of 4, and so is t_end + 1.
+__device__ __forceinline__ void id_pass(int32_t *leaf_ids, int64_t n_rows, int T, const IdOut &io,
+                                        const IdPack &ids, int rho, int t_end, int c, int lo) {
   const int lane = threadIdx.x & 63;
-  if ((lane >> 4) == p) {
-    const int r = lane & 15;
+  const int i = lane >> 3, k = lane & 7;  // row of the pass, block of 4 ids
+  if (k == rho) {
+    // quad j of row i at slot (j + i / 2) mod 4: the eight writers touch distinct banks
 #pragma unroll
-    for (int j = 0; j < kIdQuads; ++j) stage[r * kIdQuads + ((j + (r >> 1)) & 3)] = ids[j];
+    for (int j = 0; j < kIdQuads; ++j) io.stage[i * kIdQuads + ((j + (i >> 1)) & 3)] = ids[j];
   }
+  __builtin_amdgcn_wave_barrier();
+  const int slot = (c + 4 * k) & 31;
+  const uint2 v = reinterpret_cast<const uint2 *>(io.stage)[(i * kIdQuads + (((slot >> 3) + (i >> 1)) & 3)) * 2 +
+                                                            ((slot >> 2) & 1)];
+  const int64_t row = io.r0w + rho + 8 * i;
+  const int t0 = t_end - 31 + 4 * k;
+  if (row < n_rows && t0 >= lo && t0 < T) {
+    int32_t *dst = leaf_ids + row * T + t0;
+    const i32x4 o{(int)(v.x & 0xffffu), (int)(v.x >> 16), (int)(v.y & 0xffffu), (int)(v.y >> 16)};
+    // streaming: whole lines need no merging in L2, and allocating them
+    // there would evict the blocks other workgroups are about to stage
+    __builtin_nontemporal_store(o, reinterpret_cast<i32x4 *>(dst));
+  }
+  __builtin_amdgcn_wave_barrier();
 }
 
-// Reads pass p back as row segments (eight lanes per row, four ids each, so
-// a store instruction writes whole 128-byte segments of eight rows), widens
-// the ids to int32 and stores them.
-__device__ __forceinline__ void store_ids(int32_t *leaf_ids, int64_t n_rows, int T, bool ids_nt,
-                                          const u32x4 *stage, int64_t r0w, int t0, int p) {
-  const int lane = threadIdx.x & 63;
-  const int ntrees = min(kFastIdGroup, T - t0);  // a multiple of 4 on this path
-  const uint2 *st = reinterpret_cast<const uint2 *>(stage);
+// Rows not 16-byte aligned: one int32 per store, a 32-tree group at a time.
+__device__ __forceinline__ void flush_scalar(int32_t *leaf_ids, int64_t n_rows, int T, const IdPack &ids, int64_t r0w,
+                                             int t0) {
+  const int ntrees = min(kFastIdGroup, T - t0);
+  const int64_t row = r0w + (threadIdx.x & 63);
+  if (row < n_rows) {
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int r = h * 8 + (lane >> 3), k = lane & 7;  // row of the pass, block of 4 ids
-    const int64_t grow = r0w + 16 * p + r;
-    const uint2 v = st[(r * kIdQuads + (((k >> 1) + (r >> 1)) & 3)) * 2 + (k & 1)];
-    if (grow < n_rows && 4 * k < ntrees) {
-      int32_t *dst = leaf_ids + grow * T + t0 + 4 * k;
-      const i32x4 o{(int)(v.x & 0xffffu), (int)(v.x >> 16), (int)(v.y & 0xffffu), (int)(v.y >> 16)};
-      if (ids_nt) {  // streaming: 8-byte stores that do not allocate in L2
-        typedef int i32x2 __attribute__((ext_vector_type(2)));
-        __builtin_nontemporal_store(i32x2{o.x, o.y}, reinterpret_cast<i32x2 *>(dst));
-        __builtin_nontemporal_store(i32x2{o.z, o.w}, reinterpret_cast<i32x2 *>(dst + 2));
-      } else {
-        *reinterpret_cast<i32x4 *>(dst) = o;
-      }
-    }
-  }
-}
-
-// All four passes at once, or (rows not 16-byte aligned) one int32 per store.
-__device__ __forceinline__ void flush_packed(int32_t *leaf_ids, int64_t n_rows, int T, bool ids_vec, bool ids_nt,
-                                             u32x4 *stage, const IdPack &ids, int64_t r0w, int t0) {
-  if (ids_vec) {
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      stage_ids(stage, ids, p);
-      __builtin_amdgcn_wave_barrier();
-      store_ids(leaf_ids, n_rows, T, ids_nt, stage, r0w, t0, p);
-      __builtin_amdgcn_wave_barrier();
-    }
-  } else {
-    const int ntrees = min(kFastIdGroup, T - t0);
-    const int64_t row = r0w + (threadIdx.x & 63);
-    if (row < n_rows) {
-#pragma unroll
-      for (int g = 0; g < kFastIdGroup; ++g)
-        if (g < ntrees) leaf_ids[row * T + t0 + g] = (int)((ids[g >> 3][(g >> 1) & 3] >> (16 * (g & 1))) & 0xffffu);
-    }
+    for (int g = 0; g < kFastIdGroup; ++g)
+      if (g < ntrees) leaf_ids[row * T + t0 + g] = (int)((ids[g >> 3][(g >> 1) & 3] >> (16 * (g & 1))) & 0xffffu);
   }
 }
 
@@ -162,43 +164,45 @@ __device__ __forceinline__ uint32_t tt_xaddr(uint32_t w, uint32_t xlane) {
   return r;
 }
 
-// A group of leaf ids waiting to be written while the next group is walked.
-struct IdLag {
-  bool on;               // a group is pending (uniform)
-  const IdPack *ids;     // its ids
-  u32x4 *stage;          // this wave's staging area
-  int64_t r0w;           // first row of the wave
-  int t0;                // first tree of the group
-};
-
 template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET, int B, int Q>
 __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
                                            double (&acc)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::KMAX],
-                                           IdPack &ids, int &cls, const IdLag &lag) {
+                                           IdPack &ids, int &cls, int &dep, const IdOut &io) {
   using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
   constexpr int TC = C::TC;
   constexpr int TB = C::TB;
-  // the previous group's leaf ids leave in four 16-row passes spread over
-  // this group's chunks: the staging write before the walk, the read-back
-  // and stores after it, so the LDS round trip hides behind the walk
-  constexpr int PPC = C::CPF >= 4 ? 1 : 4 / C::CPF;  // passes in this chunk
-  constexpr int P0 = Q * PPC;
   // chunk c is in tbuf[B] (the barrier that ended the previous chunk made it
   // visible); fetch chunk c+1 into registers while walking chunk c
-  ChunkPrefetch<ROWS, C::CHUNK16> next;
   const bool more = c + 1 < a.n_chunks;
+  // TT: lane g holds the depth of tree g of the chunk, loaded one chunk ahead
+  // and before the blocks (waiting for a load issued behind the prefetch
+  // would mean waiting for the whole prefetch)
+  int dep_next = 0;
+  if (MODE != 0) dep_next = a.tree_depth[min((more ? c + 1 : c) * TC + ((int)threadIdx.x & (TC - 1)), a.out.T - 1)];
+  __builtin_amdgcn_sched_barrier(0);
+  ChunkPrefetch<ROWS, C::CHUNK16> next;
   next.load(a.blocks + (size_t)(more ? c + 1 : c) * C::CHUNK16);
   // multi-output: lane g of every wave holds the output column of tree g of
   // the chunk (loaded one chunk ahead, like the blocks)
   int cls_next = 0;
   if (MULTI)
     cls_next = a.tree_class[min((more ? c + 1 : c) * TC + ((int)threadIdx.x & (TC - 1)), a.out.T - 1)];
-  if (P0 < 4 && lag.on) stage_ids(lag.stage, *lag.ids, P0);
+  const int t0 = c * TC;
+  // the lines that ended with the previous chunk leave now, behind the
+  // prefetch: a wait for the prefetch then never waits for their stores
+  if (((Q * TC) & 3) == 0 && io.on && t0 > io.t_begin) {
+    constexpr int kC = (Q * TC) & 31;
+    uint32_t m = (uint32_t)(a.id_phase >> (8 * (kC >> 2))) & 0xffu;
+    while (m) {
+      const int rho = __builtin_ctz(m);
+      m &= m - 1;
+      id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, rho, t0 - 1, kC, io.t_begin);
+    }
+  }
   __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the walk
   const unsigned char *base = reinterpret_cast<const unsigned char *>(tbuf[B]);
   const unsigned char *xb = reinterpret_cast<const unsigned char *>(xs);
-  const int t0 = c * TC;
   uint32_t s[TC];
   if (MODE == 0) {
     // Software-pipelined in issue order: LDS reads complete in order, so the
@@ -229,7 +233,7 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   } else {
     int levels = 0;
 #pragma unroll
-    for (int g = 0; g < TC; ++g) levels = max(levels, a.tree_depth[min(t0 + g, a.out.T - 1)]);
+    for (int g = 0; g < TC; ++g) levels = max(levels, __builtin_amdgcn_readlane(dep, g));
     // Pipelined like the PTT walk: all feature reads of a level are issued
     // before the first is used, and each tree's next node read right after
     // its step (the read after the last level is unused but in bounds: every
@@ -257,18 +261,33 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
     }
     __builtin_amdgcn_sched_barrier(0);
   }
+  // PTT: leaf record at the heap index; TT mode 1: after the node records;
+  // TT mode 2: from global memory (the index is masked to the tree's 2^LG
+  // records, so even a malformed table cannot read outside them). All are
+  // read before the first leaf-id store: a load issued behind a store would
+  // also wait for the store to complete.
+  uint2 lrs[TC];
+#pragma unroll
+  for (int g = 0; g < TC; ++g) {
+    if (MODE == 2)
+      lrs[g] = a.leaf[(size_t)(t0 + g) * (1u << LG) + ((s[g] >> 3) & ((1u << LG) - 1u))];
+    else
+      lrs[g] = *reinterpret_cast<const uint2 *>(base + g * TB + (MODE == 0 ? 0u : (1u << LG) * 8u) + s[g]);
+  }
 #pragma unroll
   for (int g = 0; g < TC; ++g) {
     const int t = t0 + g;
-    // PTT: leaf record at the heap index; TT mode 1: after the node records;
-    // TT mode 2: from global memory (the index is masked to the tree's 2^LG
-    // records, so even a malformed table cannot read outside them)
-    uint2 lr;
-    if (MODE == 2)
-      lr = a.leaf[(size_t)t * (1u << LG) + ((s[g] >> 3) & ((1u << LG) - 1u))];
-    else
-      lr = *reinterpret_cast<const uint2 *>(base + g * TB + (MODE == 0 ? 0u : (1u << LG) * 8u) + s[g]);
+    const uint2 lr = lrs[g];
     put_id(ids, Q * TC + g, lr.y);
+    if (((Q * TC + g) & 3) == 3 && g < TC - 1 && io.on) {  // lines that end at tree t, within the chunk
+      const int c = (Q * TC + g + 1) & 31;
+      uint32_t m = (uint32_t)(a.id_phase >> (8 * (c >> 2))) & 0xffu;
+      while (m) {
+        const int rho = __builtin_ctz(m);
+        m &= m - 1;
+        id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, rho, t, c, io.t_begin);
+      }
+    }
     if (t < a.out.T) {
       const double v = (double)as_float(lr.x);
       if (MULTI) {
@@ -280,19 +299,8 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
       }
     }
   }
-  if (P0 < 4 && lag.on) {
-    __builtin_amdgcn_wave_barrier();
-    store_ids(a.leaf_ids, a.n_rows, a.out.T, a.ids_nt, lag.stage, lag.r0w, lag.t0, P0);
-#pragma unroll
-    for (int pp = 1; pp < PPC; ++pp) {
-      __builtin_amdgcn_wave_barrier();
-      stage_ids(lag.stage, *lag.ids, P0 + pp);
-      __builtin_amdgcn_wave_barrier();
-      store_ids(a.leaf_ids, a.n_rows, a.out.T, a.ids_nt, lag.stage, lag.r0w, lag.t0, P0 + pp);
-    }
-    __builtin_amdgcn_wave_barrier();
-  }
   cls = cls_next;
+  dep = dep_next;
   if (C::BUFS == 2) {
     if (more) next.store(tbuf[B ^ 1]);  // nobody reads tbuf[B^1] during chunk c
     lds_barrier();
@@ -309,12 +317,12 @@ template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET, int Q>
 __device__ __forceinline__ void fast_group(const FastArgs &a, int c0, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
                                            double (&acc)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::KMAX],
-                                           IdPack &ids, int &cls, const IdLag &lag) {
+                                           IdPack &ids, int &cls, int &dep, const IdOut &io) {
   using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
   if constexpr (Q < C::CPF) {
     fast_chunk<MODE, LG, MULTI, ROWS, BUDGET, C::BUFS == 2 ? (Q & 1) : 0, Q>(a, c0 + Q, tbuf, xs, lane4, acc, ids,
-                                                                           cls, lag);
-    fast_group<MODE, LG, MULTI, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls, lag);
+                                                                           cls, dep, io);
+    fast_group<MODE, LG, MULTI, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls, dep, io);
   }
 }
 
@@ -326,7 +334,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   const int c_begin = a.split ? (int)blockIdx.y * a.split : 0;
   if (a.split) a.n_chunks = min(c_begin + a.split, a.n_chunks);
   __shared__ __align__(16) uint4 tbuf[C::BUFS][C::CHUNK16];
-  __shared__ __align__(16) u32x4 idstage[ROWS / 64][16 * kIdQuads];
+  __shared__ __align__(16) u32x4 idstage[ROWS / 64][8 * kIdQuads];
   extern __shared__ __align__(16) float fxs[];  // [F][ROWS]
   const int tid = threadIdx.x;
   const int64_t r0 = (int64_t)blockIdx.x * ROWS;
@@ -357,28 +365,28 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   double acc[C::KMAX];
 #pragma unroll
   for (int k = 0; k < C::KMAX; ++k) acc[k] = 0.0;
-  IdPack ids, prev;
+  IdPack ids;
   int cls = MULTI ? a.tree_class[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
+  int dep = MODE != 0 ? a.tree_depth[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
   const int64_t r0w = r0 + (tid & ~63);
-  // row-segment flushes of one group overlap the next group's walk; the
-  // unaligned (scalar) store path, and 1024-row workgroups (whose registers
-  // cannot hold a second group of ids), flush each group right away
-  constexpr bool kLag = ROWS < 1024;
-  const bool lagged = kLag && a.leaf_ids && a.ids_vec;
-  IdLag lag{false, &prev, idstage[tid >> 6], r0w, 0};
+  const IdOut io{a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], r0w, c_begin * C::TC};
   for (int c = c_begin; c < a.n_chunks; c += C::CPF) {  // chunk counts are multiples of CPF
-    fast_group<MODE, LG, MULTI, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, lag);
-    if (lagged) {
-#pragma unroll
-      for (int b = 0; b < kIdQuads; ++b) prev[b] = ids[b];
-      lag.on = true;
-      lag.t0 = c * C::TC;
-    } else if (a.leaf_ids) {
-      flush_packed(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, a.ids_nt, idstage[tid >> 6], ids, r0w, c * C::TC);
+    fast_group<MODE, LG, MULTI, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, io);
+    if (a.leaf_ids && !a.ids_vec) flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, r0w, c * C::TC);
+  }
+  if (io.on) {
+    // the rest of every row's last line: from its start (tree t_pad - 32 + 4k)
+    // to the end (k = 0: the lines that ended with the last chunk)
+    const int t_pad = a.n_chunks * C::TC;
+    for (int k = 0; k < 8; ++k) {
+      uint32_t m = (uint32_t)(a.id_phase >> (8 * k)) & 0xffu;
+      while (m) {
+        const int rho = __builtin_ctz(m);
+        m &= m - 1;
+        id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, rho, t_pad - 1, 0, max(io.t_begin, t_pad - 32 + 4 * k));
+      }
     }
   }
-  if (lag.on)  // the last group
-    flush_packed(a.leaf_ids, a.n_rows, a.out.T, a.ids_vec, a.ids_nt, lag.stage, prev, r0w, lag.t0);
   if (valid) {
     if (a.split) {
       double *dst = a.partial + ((size_t)blockIdx.y * a.n_rows + row) * a.out.K;

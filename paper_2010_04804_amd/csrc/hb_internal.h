@@ -34,16 +34,17 @@ constexpr int64_t kTreeLdsLimit = 160 * 1024 - 4 * 1024;
 // double-buffered (the next chunk is stored while nobody reads its buffer) or
 // single-buffered with twice as many trees per chunk (more independent walks
 // per wave, one extra barrier per chunk), whichever fits more trees in the
-// kernel's table budget (64 or 32 KiB). Leaf ids are flushed every
+// kernel's table budget (64 or 32 KiB). Leaf ids are held for the last
 // kFastIdGroup trees, and the tree count is padded with zero blocks to a
 // multiple of kFastIdGroup (so every chunk size divides it).
 constexpr int kFastTableLds = 64 * 1024;
 constexpr int kFastIdGroup = 32;
 // The fast kernels hold and stage leaf ids as 16-bit halves: every caller id
 // they report is a local node id of a tree with at most 2^(kFastMaxLg + 1)
-// nodes. Each wave stages 16 of its 64 rows at a time (a 32-tree group of
-// 16-bit ids per row), so the staging costs 16 bytes per row of a workgroup.
-constexpr int kFastIdStageBytes = 16 * kFastIdGroup * 2 / 64;
+// nodes. Each wave stages 8 of its 64 rows at a time (the 32 ids of one
+// 128-byte output line per row), so the staging costs 8 bytes per row of a
+// workgroup.
+constexpr int kFastIdStageBytes = 8 * kFastIdGroup * 2 / 64;
 constexpr int fast_node_bytes(int mode) { return (void)mode, 8; }
 constexpr int fast_tree_bytes(int mode, int lg) { return (1 << lg) * (fast_node_bytes(mode) + (mode == 2 ? 0 : 8)); }
 // TT leaf records up to this size stay in global memory (mode 2); measured

@@ -562,12 +562,16 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int ch
   a.tree_depth = depth;
   a.n_chunks = (int)((int64_t)chunks * fast_tc(tb) / fast_tc(tb, shapes[best].budget));
   a.ids_vec = (e.n_trees % 4 == 0) && ((reinterpret_cast<uintptr_t>(leaf_ids) & 15) == 0);
-  // Streaming id stores once the tables outgrow an XCD's 4 MB L2: write
-  // allocation would evict the chunks other workgroups are about to stage.
-  // Below that, allocating lets the two halves of a row segment that
-  // straddles a line merge in L2 (measured: multiclass 3500 trees 3% faster
-  // streaming, the 500-tree model 20% slower).
-  a.ids_nt = table_bytes > (int64_t)4 << 20;
+  if (a.ids_vec) {
+    // row r's ids begin at int b + r T of a line (b the output's offset in
+    // its line), so its lines begin at trees -(b + r T) mod 32: a multiple
+    // of 4 that depends on r mod 8
+    const int64_t b = (int64_t)((reinterpret_cast<uintptr_t>(leaf_ids) >> 2) & 31);
+    for (int rho = 0; rho < 8; ++rho) {
+      const int phi = (int)((32 - (b + (int64_t)e.n_trees * rho) % 32) % 32);
+      a.id_phase |= (uint64_t)1 << (8 * (phi / 4) + rho);
+    }
+  }
   hipError_t rc = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)xbytes);
   if (rc != hipSuccess) {

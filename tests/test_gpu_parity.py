@@ -142,6 +142,45 @@ def test_tree_split_uses_and_reuses_the_workspace(strategy):
         check(model, X, scores.cpu().numpy(), ids.cpu().numpy(), f"ws {strategy}/{n}/{avail}")
 
 
+@pytest.mark.parametrize("n_trees", [500, 64, 48, 40, 36, 3500])
+def test_leaf_id_lines_at_any_offset(n_trees):
+    """Leaf ids leave as whole 128-byte lines whose first tree depends on the
+    output's offset within a line and on the row (tree counts with 1, 2, 4 or
+    8 line phases); every offset gives the oracle's ids, and nothing outside
+    the output changes. Offsets of 1 and 2 ints take the unaligned path."""
+    if n_trees == 500:
+        model, h = handle(2)
+    else:
+        rng = np.random.Generator(np.random.PCG64(700 + n_trees))
+        depth = 8 if n_trees == 3500 else 6
+        model = synth.perfect_forest(rng, n_trees, depth, 28, lambda r, f: r.standard_normal(f.size),
+                                     lambda r, n: r.normal(0.0, 0.05, n))
+        model.update(n_outputs=1, tree_class=None, aggregation="sum", transform="none", base_score=None)
+        model = synth.permute_nodes(model, n_trees)
+        h = hb.compile(model, device=0)
+    sizes = [3001] if n_trees == 3500 else [3001, 20_000]
+    for n in sizes:
+        X = synth.make_rows(2, n)
+        Xd = torch.from_numpy(X).cuda()
+        _, _, o_ids = oracle.predict(model, X, n_threads=ORACLE_THREADS)
+        for strategy in ("ptt", "tt"):
+            for off in (0, 4, 12, 28, 1, 2):
+                for ws in (False, True):
+                    say("id lines", n_trees, n, strategy, "offset", off, "ws" if ws else "no ws")
+                    buf = torch.full((n * n_trees + 64,), -7, dtype=torch.int32, device="cuda")
+                    scores = torch.empty((n, 1), dtype=torch.float32, device="cuda")
+                    nws = hb.workspace_bytes(h, n, strategy) if ws else 0
+                    wsb = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda")
+                    hb.predict_ptr(h, Xd.data_ptr(), n, scores.data_ptr(), buf.data_ptr() + 4 * off, strategy,
+                                   torch.cuda.current_stream().cuda_stream, wsb.data_ptr() if nws else None, nws)
+                    torch.cuda.synchronize()
+                    b = buf.cpu().numpy()
+                    got = b[off:off + n * n_trees].reshape(n, n_trees)
+                    bad = np.argwhere(got != o_ids)
+                    assert bad.size == 0, f"offset {off}/{strategy}/ws={ws}: {len(bad)} ids differ, first {bad[:4].tolist()}"
+                    assert np.all(b[:off] == -7) and np.all(b[off + n * n_trees:] == -7), "write outside the output"
+
+
 def _vector_forest(n_features, n_trees, depth, seed):
     rng = np.random.Generator(np.random.PCG64(seed))
 
