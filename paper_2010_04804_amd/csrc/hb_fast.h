@@ -104,32 +104,47 @@ __device__ __forceinline__ void put_id(IdPack &ids, int q, uint32_t id) {
 // evenly over the walk instead of leaving in bursts, and each line reaches
 // memory whole.
 struct IdOut {
-  bool on;         // leaf ids requested and the row layout allows vector stores (uniform)
-  u32x4 *stage;    // this wave's staging area: 8 rows x 64 bytes
-  int64_t r0w;     // first row of the wave
-  int t_begin;     // first tree of this workgroup's part
+  bool on;            // leaf ids requested and the row layout allows vector stores (uniform)
+  u32x4 *stage;       // this wave's staging area: 8 rows x 64 bytes
+  int64_t r0w;        // first row of the wave
+  int t_begin;        // first tree of this workgroup's part
+  // per lane (i = lane / 8: row of a pass, k = lane % 8: block of 4 ids)
+  uint32_t lane_off;  // 8 i T + 4 k: the lane's piece, in ints from the pass's first row and tree
+  int rd;             // 8 k + 16 (i / 2): byte offset of that piece in staged row i, before the rotation
+  int k4;             // 4 k
+  int row8;           // 8 i
 };
+
+template <int ROWS>
+__device__ __forceinline__ IdOut make_id_out(bool on, u32x4 *stage, int t_begin, int T) {
+  const int lane = threadIdx.x & 63;
+  const int i = lane >> 3, k = lane & 7;
+  // the wave's first row is uniform: keep it (and the per-pass row and tree
+  // offsets computed from it) in scalar registers
+  const int64_t r0w = (int64_t)blockIdx.x * ROWS + 64 * __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  return IdOut{on, stage, r0w, t_begin, (uint32_t)(8 * i) * (uint32_t)T + 4u * k, 8 * k + 16 * (i >> 1), 4 * k, 8 * i};
+}
 
 // Writes, for the rows of residue rho in this wave, the ids of trees
 // [max(lo, t_end - 31), min(t_end, T - 1)]; c = (t_end + 1) mod 32 is the
 // slot of tree t_end - 31. lo and T are multiples of 4, and so is t_end + 1.
 __device__ __forceinline__ void id_pass(int32_t *leaf_ids, int64_t n_rows, int T, const IdOut &io,
                                         const IdPack &ids, int rho, int t_end, int c, int lo) {
-  const int lane = threadIdx.x & 63;
-  const int i = lane >> 3, k = lane & 7;  // row of the pass, block of 4 ids
-  if (k == rho) {
+  if (io.k4 == 4 * rho) {
     // quad j of row i at slot (j + i / 2) mod 4: the eight writers touch distinct banks
+    const int i = (threadIdx.x & 63) >> 3;
 #pragma unroll
     for (int j = 0; j < kIdQuads; ++j) io.stage[i * kIdQuads + ((j + (i >> 1)) & 3)] = ids[j];
   }
   __builtin_amdgcn_wave_barrier();
-  const int slot = (c + 4 * k) & 31;
-  const uint2 v = reinterpret_cast<const uint2 *>(io.stage)[(i * kIdQuads + (((slot >> 3) + (i >> 1)) & 3)) * 2 +
-                                                            ((slot >> 2) & 1)];
-  const int64_t row = io.r0w + rho + 8 * i;
-  const int t0 = t_end - 31 + 4 * k;
-  if (row < n_rows && t0 >= lo && t0 < T) {
-    int32_t *dst = leaf_ids + row * T + t0;
+  // ids 2 slot .. of row i sit at byte 2 slot of its staged row, rotated by 16 (i / 2)
+  const uint2 v = *reinterpret_cast<const uint2 *>(reinterpret_cast<const unsigned char *>(io.stage) + 8 * io.row8 +
+                                                   ((2 * c + io.rd) & 63));
+  const int64_t row0 = io.r0w + rho;
+  const int rem = (int)min(n_rows - row0, (int64_t)64);
+  const int tb = t_end - 31;
+  if (io.row8 < rem && io.k4 >= lo - tb && io.k4 < T - tb) {
+    int32_t *dst = leaf_ids + (row0 * T + tb) + io.lane_off;
     const i32x4 o{(int)(v.x & 0xffffu), (int)(v.x >> 16), (int)(v.y & 0xffffu), (int)(v.y >> 16)};
     // streaming: whole lines need no merging in L2, and allocating them
     // there would evict the blocks other workgroups are about to stage
@@ -369,7 +384,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   int cls = MULTI ? a.tree_class[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
   int dep = MODE != 0 ? a.tree_depth[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
   const int64_t r0w = r0 + (tid & ~63);
-  const IdOut io{a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], r0w, c_begin * C::TC};
+  const IdOut io = make_id_out<ROWS>(a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], c_begin * C::TC, a.out.T);
   for (int c = c_begin; c < a.n_chunks; c += C::CPF) {  // chunk counts are multiples of CPF
     fast_group<MODE, LG, MULTI, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, io);
     if (a.leaf_ids && !a.ids_vec) flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, r0w, c * C::TC);
