@@ -23,6 +23,7 @@
 // and receives D[4(l/16) + i][n = l%16], i = 0..3.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <climits>
 #include <string>
 
@@ -446,6 +447,227 @@ __global__ __launch_bounds__(ROWS) void gemm_pipe_kernel(GemmArgs a) {
   if (row < a.n_rows) finish_row<PipeState<KMODE, ROWS>::KMAX>(a.out, st.acc, row);
 }
 
+// ---------------------------------------------------------------------------
+// Wide rows: when 256 rows of features do not fit in LDS next to C^T (a few
+// thousand input columns), a workgroup takes 16 rows, the N dimension of one
+// v_mfma_i32_16x16x64_i8, and keeps C^T in registers instead of LDS: wave w
+// holds the A operands of leaves 64w .. 64w + 63 (4 leaf tiles x 4 slices,
+// 64 VGPRs). Per tree the four waves build the shared predicate operand
+// (256 decision nodes x 16 rows, bytes 0/64) together, one 16-node block of
+// one row per thread, into a double-buffered LDS tile; each wave then runs
+// its 16 matrix instructions and reduces its leaves to four maxima per row
+// (one per lane group), and the sixteen maxima meet in LDS. Trees go in
+// pairs, one barrier per pair, so that the latencies of two trees' LDS round
+// trips overlap (a 16-row tile of 2000 features leaves room for one
+// workgroup per CU only). Node records pass through LDS one pair ahead
+// (loaded two pairs ahead); the leaf of tree t is looked up by wave t mod 4,
+// whose loads are consumed when that wave's turn comes again, and the four
+// waves' partial sums are added in wave order at the end.
+constexpr int kTileRows = 16;
+constexpr int kTileBStride = 256 + 16;  // bytes per row of the predicate tile (spreads the 16 rows over banks)
+
+// Row stride of the feature tile in floats: a multiple of 4 whose quotient by
+// 4 is odd, so the 16 rows of one feature fall in 16 different banks.
+__host__ __device__ inline int gemm_tile_xs(int F) {
+  const int xs = (F + 3) & ~3;
+  return (xs & 7) ? xs : xs + 4;
+}
+
+template <int KMODE>
+struct TileLeaf {
+  static constexpr int KMAX = KMODE == 0 ? 1 : HB_MAX_OUTPUTS;
+  int t = -1;  // tree of the pending lookup, -1 none
+  int cls = 0;
+  int32_t id = 0;
+  float v[KMODE == 2 ? KMAX : 1];
+};
+
+template <int KMODE>
+__device__ __forceinline__ void tile_leaf_issue(const GemmArgs &a, TileLeaf<KMODE> &p, int t, int col) {
+  const size_t lrec = (size_t)t * a.l_pad + (size_t)col;
+  p.t = t;
+  p.id = a.leaf_id[lrec];
+  if (KMODE == 2) {
+#pragma unroll
+    for (int k = 0; k < TileLeaf<KMODE>::KMAX; ++k) p.v[k] = k < a.LD ? a.leaf_value[lrec * a.LD + k] : 0.0f;
+  } else {
+    p.v[0] = a.leaf_value[lrec];
+    if (KMODE == 1) p.cls = a.tree_class[t];
+  }
+}
+
+template <int KMODE>
+__device__ __forceinline__ void tile_leaf_consume(const GemmArgs &a, TileLeaf<KMODE> &p, double (&acc)[TileLeaf<KMODE>::KMAX],
+                                                  int64_t row) {
+  if (p.t < 0) return;
+  if (KMODE == 2) {
+#pragma unroll
+    for (int k = 0; k < TileLeaf<KMODE>::KMAX; ++k) acc[k] += (double)p.v[k];
+  } else if (KMODE == 0) {
+    acc[0] += (double)p.v[0];
+  } else {
+#pragma unroll
+    for (int k = 0; k < TileLeaf<KMODE>::KMAX; ++k)
+      if (k == p.cls) acc[k] += (double)p.v[0];
+  }
+  if (a.leaf_ids && row < a.n_rows) a.leaf_ids[row * a.out.T + p.t] = p.id;
+  p.t = -1;
+}
+
+// Predicate operand of one tree: thread (row tid % 16, nodes 16 (tid / 16)
+// .. + 15) compares its row's features with the 16 records and writes the
+// 16 outcome bytes to the tile.
+__device__ __forceinline__ void tile_build(const float *xs, int XS, const uint2 *rtab, unsigned char *bt) {
+  const int tid = threadIdx.x;
+  const int r = tid & 15, nb = tid >> 4;
+  const uint2 *rec = rtab + nb * 16;
+  u32x4 w;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    uint32_t word = 0;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const uint2 nr = rec[q * 4 + b];
+      word |= (xs[r * XS + (int)nr.y] < as_float(nr.x) ? 0x40u : 0u) << (8 * b);
+    }
+    w[q] = word;
+  }
+  *reinterpret_cast<u32x4 *>(bt + r * kTileBStride + nb * 16) = w;
+}
+
+// The path product of one tree for this wave's 64 leaves: the largest
+// biased accumulator per row, per lane group.
+__device__ __forceinline__ int tile_product(const unsigned char *bt, const v4i (&ctr)[4][4], const v4i (&b4)[4]) {
+  const int lane = threadIdx.x & 63, g4 = lane >> 4, r16 = lane & 15;
+  v4i bop[4];
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) bop[kb] = *reinterpret_cast<const v4i *>(bt + r16 * kTileBStride + kb * 64 + 16 * g4);
+  int best = INT_MIN;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v4i d = b4[j];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) d = __builtin_amdgcn_mfma_i32_16x16x64_i8(ctr[j][kb], bop[kb], d, 0, 0, 0);
+    best = max(best, hmax4(d));
+  }
+  return best;
+}
+
+// Trees t and t+1 (t even); P = (t / 2) & 1 selects the buffers and the
+// record registers. Records of trees t+4, t+5 (loaded two pairs ago) go to
+// LDS for the build one pair ahead, and trees t+8, t+9 are loaded.
+template <int KMODE, int P>
+__device__ __forceinline__ void tile_pair(const GemmArgs &a, int t, const float *xs, int XS,
+                                          unsigned char (*bt)[2][kTileRows * kTileBStride], uint2 (*rtab)[2][256],
+                                          int (*red)[2][16][kTileRows], uint2 (&rset)[2][2], const v4i (&ctr)[4][4],
+                                          const v4i (&b4)[4], TileLeaf<KMODE> &pend,
+                                          double (&acc)[TileLeaf<KMODE>::KMAX], int64_t r0) {
+  const int T = a.out.T;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, r16 = lane & 15;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    rtab[P][u][tid] = rset[P][u];
+    rset[P][u] = a.node[(size_t)min(t + 8 + u, T - 1) * 256 + tid];
+  }
+  const bool second = t + 1 < T;  // uniform
+  const int best0 = tile_product(bt[P][0], ctr, b4);
+  const int best1 = second ? tile_product(bt[P][1], ctr, b4) : INT_MIN;
+  if (t + 2 < T) tile_build(xs, XS, rtab[P ^ 1][0], bt[P ^ 1][0]);
+  if (t + 3 < T) tile_build(xs, XS, rtab[P ^ 1][1], bt[P ^ 1][1]);
+  red[P][0][wave * 4 + g4][r16] = best0;  // 16 partial maxima per row, combined by the leaf's wave
+  red[P][1][wave * 4 + g4][r16] = best1;
+  lds_sync();
+  // the leaves of trees t and t+1, by waves t mod 4 and t+1 mod 4 (a wave's
+  // previous lookup is consumed first)
+  const int u = wave - (t & 3);
+  if ((u == 0 || (u == 1 && second)) && lane < kTileRows) {
+    tile_leaf_consume<KMODE>(a, pend, acc, r0 + lane);
+    int col = red[P][u][0][lane];
+#pragma unroll
+    for (int q = 1; q < 16; ++q) col = max(col, red[P][u][q][lane]);
+    col = min(max(col, 0), a.l_pad - 1);  // a valid tree always yields a column in range
+    tile_leaf_issue<KMODE>(a, pend, t + u, col);
+  }
+}
+
+template <int KMODE>
+__global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
+  constexpr int KMAX = TileLeaf<KMODE>::KMAX;
+  extern __shared__ __align__(16) unsigned char smem[];  // feature tile [16][XS], then the waves' partial sums
+  __shared__ __align__(16) unsigned char bt[2][2][kTileRows * kTileBStride];
+  __shared__ __align__(16) uint2 rtab[2][2][256];
+  __shared__ int red[2][2][16][kTileRows];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, r16 = lane & 15;
+  const int T = a.out.T;
+  const int XS = gemm_tile_xs(a.F);
+  float *xs = reinterpret_cast<float *>(smem);
+  const int64_t r0 = (int64_t)blockIdx.x * kTileRows;
+  if (!a.cols && (a.F & 3) == 0 && (a.Fs & 3) == 0 && (reinterpret_cast<uintptr_t>(a.X) & 15) == 0) {
+    // 16-byte loads, four rows' worth in flight before their LDS stores
+    const int F4 = a.F >> 2;
+#pragma unroll 4
+    for (int r = 0; r < kTileRows; ++r) {
+      const bool ok = r0 + r < a.n_rows;
+      const float4 *src = reinterpret_cast<const float4 *>(a.X + (ok ? r0 + r : (int64_t)0) * a.Fs);
+      for (int f = tid; f < F4; f += 256)
+        *reinterpret_cast<float4 *>(xs + r * XS + 4 * f) = ok ? src[f] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  } else {
+    for (int r = 0; r < kTileRows; ++r) {
+      const bool ok = r0 + r < a.n_rows;
+      const float *src = a.X + (ok ? r0 + r : (int64_t)0) * a.Fs;
+      for (int f = tid; f < a.F; f += 256) xs[r * XS + f] = ok ? xval(src, a.cols, f) : 0.0f;
+    }
+  }
+  // this wave's leaves: A operands (4 C^T) and accumulator biases
+  v4i ctr[4][4], b4[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int lt = wave * 4 + j;
+    b4[j] = *reinterpret_cast<const v4i *>(a.bias + lt * 16 + 4 * g4);
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+      ctr[j][kb] = *reinterpret_cast<const v4i *>(a.ct + (size_t)(lt * 16 + r16) * 256 + kb * 64 + 16 * g4);
+  }
+  // records of trees 0-3 in LDS, 4-7 in registers
+  uint2 rset[2][2];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    rtab[u >> 1][u & 1][tid] = a.node[(size_t)min(u, T - 1) * 256 + tid];
+    rset[u >> 1][u & 1] = a.node[(size_t)min(u + 4, T - 1) * 256 + tid];
+  }
+  lds_sync();
+  tile_build(xs, XS, rtab[0][0], bt[0][0]);
+  if (T > 1) tile_build(xs, XS, rtab[0][1], bt[0][1]);
+  lds_sync();
+  double acc[KMAX];
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) acc[k] = 0.0;
+  TileLeaf<KMODE> pend;
+  for (int t = 0; t < T; t += 4) {
+    tile_pair<KMODE, 0>(a, t, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0);
+    if (t + 2 < T) tile_pair<KMODE, 1>(a, t + 2, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0);
+  }
+  if (lane < kTileRows) tile_leaf_consume<KMODE>(a, pend, acc, r0 + lane);
+  // partial sums in wave order (the feature tile is no longer read)
+  double *part = reinterpret_cast<double *>(smem);
+  if (lane < kTileRows) {
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) part[(wave * kTileRows + lane) * KMAX + k] = acc[k];
+  }
+  lds_sync();
+  if (wave == 0 && lane < kTileRows && r0 + lane < a.n_rows) {
+    double s[KMAX];
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) s[k] = 0.0;
+    for (int w = 0; w < 4; ++w) {
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k) s[k] += part[(w * kTileRows + lane) * KMAX + k];
+    }
+    finish_row<KMAX>(a.out, s, r0 + lane);
+  }
+}
+
 using GemmFn = void (*)(GemmArgs);
 
 template <int KB, bool CT, bool XL, int ROWS, bool COLS = false>
@@ -503,12 +725,28 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
               : kb == 2 ? pick_gemm<2>(ct, xl, kmode, rows, cols)
               : kb == 3 ? pick_gemm<3>(ct, xl, kmode, rows, cols)
                         : pick_gemm<4>(ct, xl, kmode, rows, cols);
+  int threads = rows;
+  bool piped = false;
   if (ct && xl && kb == 4 && t.l_pad == 256) {  // the software-pipelined kernel needs no node chunks
     const size_t need = x_bytes(rows) + ct_bytes;
     if (need + stage_bytes(rows) <= (size_t)lds_max) {
       fn = rows == 512 ? (kmode == 0 ? gemm_pipe_kernel<0, 512> : kmode == 1 ? gemm_pipe_kernel<1, 512> : gemm_pipe_kernel<2, 512>)
                        : (kmode == 0 ? gemm_pipe_kernel<0, 256> : kmode == 1 ? gemm_pipe_kernel<1, 256> : gemm_pipe_kernel<2, 256>);
       dyn = need;
+      piped = true;
+    }
+  }
+  if (!piped && t.n_shapes == 1 && kb == 4 && t.l_pad == 256) {
+    // wide rows (the pipelined kernel's 256-row feature tile does not fit):
+    // 16-row tiles with C^T in registers
+    const int kmax = kmode == 0 ? 1 : HB_MAX_OUTPUTS;
+    const size_t tile_dyn = std::max((size_t)kTileRows * gemm_tile_xs(e.n_cols) * 4, (size_t)4 * kTileRows * kmax * 8);
+    const size_t tile_static = (size_t)4 * kTileRows * kTileBStride + 4 * 256 * 8 + 4 * 16 * kTileRows * 4;
+    if (tile_dyn + tile_static <= (size_t)lds_max) {
+      fn = kmode == 0 ? gemm_tile_kernel<0> : kmode == 1 ? gemm_tile_kernel<1> : gemm_tile_kernel<2>;
+      dyn = tile_dyn;
+      rows = kTileRows;
+      threads = 256;
     }
   }
   if (!fn) {
@@ -541,7 +779,7 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
     return HB_ERR_HIP;
   }
   const int64_t blocks = (n_rows + rows - 1) / rows;
-  hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(rows), dyn, stream, a);
+  hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(threads), dyn, stream, a);
   rc = hipGetLastError();
   if (rc != hipSuccess) {
     *err = std::string("kernel launch: ") + hipGetErrorString(rc);

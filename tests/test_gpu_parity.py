@@ -181,6 +181,30 @@ def test_leaf_id_lines_at_any_offset(n_trees):
                     assert np.all(b[:off] == -7) and np.all(b[off + n * n_trees:] == -7), "write outside the output"
 
 
+@pytest.mark.parametrize("kind", ["scalar", "classes", "vector"])
+@pytest.mark.parametrize("n_trees,n", [(1, 17), (2, 16), (3, 33), (37, 1007), (64, 4099)])
+def test_gemm_wide_rows(kind, n_trees, n):
+    """Depth-8 trees over 1,500 features: the GEMM tables' 256-row feature
+    tile does not fit in LDS, so 16-row tiles with C^T in registers take
+    the batch (tree counts of 1 to 3 exercise the two-tree software
+    pipeline's start; rows hold ties, NaN and infinities)."""
+    rng = np.random.Generator(np.random.PCG64(4200 + n_trees + n))
+    F = 1500
+    ld = 2 if kind == "vector" else 1
+    model = synth.perfect_forest(rng, n_trees, 8, F, lambda r, f: r.standard_normal(f.size),
+                                 lambda r, k: r.standard_normal(k * ld), leaf_dim=ld)
+    K = {"scalar": 1, "classes": 3, "vector": 2}[kind]
+    model.update(n_outputs=K, aggregation="mean" if kind == "vector" else "sum",
+                 transform="softmax" if kind == "classes" else "none", base_score=None,
+                 tree_class=(np.arange(n_trees) % 3).astype(np.int32) if kind == "classes" else None)
+    model = synth.permute_nodes(model, n_trees + n)
+    X = np.ascontiguousarray(pins.tricky_rows(rng, model, n))
+    h = hb.compile(model, device=0)
+    say("gemm wide rows", kind, n_trees, n)
+    scores, ids = run(h, X, "gemm")
+    check(model, X, scores, ids, f"gemm wide {kind}/{n_trees}/{n}")
+
+
 def _vector_forest(n_features, n_trees, depth, seed):
     rng = np.random.Generator(np.random.PCG64(seed))
 
