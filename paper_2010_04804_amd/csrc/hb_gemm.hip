@@ -736,9 +736,12 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
       piped = true;
     }
   }
-  if (!piped && t.n_shapes == 1 && kb == 4 && t.l_pad == 256) {
-    // wide rows (the pipelined kernel's 256-row feature tile does not fit):
-    // 16-row tiles with C^T in registers
+  if (!(piped && rows == 512) && t.n_shapes == 1 && kb == 4 && t.l_pad == 256) {
+    // 16-row tiles with C^T in registers, unless the pipelined kernel gets
+    // 512-row workgroups (two waves per SIMD): wide rows, where its feature
+    // tile does not fit, and 256-row workgroups, one wave per SIMD (measured:
+    // 7 x 500 trees over 54 features at 1M rows 413 -> 361 ms; the 500-tree
+    // 28-feature model stays on 512-row pipelined workgroups, 28 against 39 ms)
     const int kmax = kmode == 0 ? 1 : HB_MAX_OUTPUTS;
     const size_t tile_dyn = std::max((size_t)kTileRows * gemm_tile_xs(e.n_cols) * 4, (size_t)4 * kTileRows * kmax * 8);
     const size_t tile_static = (size_t)4 * kTileRows * kTileBStride + 4 * 256 * 8 + 4 * 16 * kTileRows * 4;
