@@ -514,10 +514,41 @@ __device__ __forceinline__ void tile_leaf_consume(const GemmArgs &a, TileLeaf<KM
   p.t = -1;
 }
 
-// Predicate operand of one tree: thread (row tid % 16, nodes 16 (tid / 16)
-// .. + 15) compares its row's features with the 16 records and writes the
-// 16 outcome bytes to the tile.
-__device__ __forceinline__ void tile_build(const float *xs, int XS, const uint2 *rtab, unsigned char *bt) {
+// Predicate operands of two trees: thread (row tid % 16, nodes 16 (tid / 16)
+// .. + 15) compares its row's features with the 16 records of each tree and
+// writes the 16 outcome bytes per tree to the tiles. All record reads go
+// first, then all feature reads, so that the LDS round trips overlap.
+__device__ __forceinline__ void tile_build2(const float *xs, int XS, const uint2 (*rtab)[256],
+                                            unsigned char (*bt)[kTileRows * kTileBStride]) {
+  const int tid = threadIdx.x;
+  const int r = tid & 15, nb = tid >> 4;
+  uint2 rec[2][16];
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) rec[u][q] = rtab[u][nb * 16 + q];
+  float x[2][16];
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) x[u][q] = xs[r * XS + (int)rec[u][q].y];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    u32x4 w;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t word = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) word |= (x[u][q * 4 + b] < as_float(rec[u][q * 4 + b].x) ? 0x40u : 0u) << (8 * b);
+      w[q] = word;
+    }
+    *reinterpret_cast<u32x4 *>(bt[u] + r * kTileBStride + nb * 16) = w;
+  }
+}
+
+// The same for one tree, with a quarter of the registers: where LDS leaves
+// room for two or more workgroups per CU, occupancy hides the round trips.
+__device__ __forceinline__ void tile_build1(const float *xs, int XS, const uint2 *rtab, unsigned char *bt) {
   const int tid = threadIdx.x;
   const int r = tid & 15, nb = tid >> 4;
   const uint2 *rec = rtab + nb * 16;
@@ -535,28 +566,34 @@ __device__ __forceinline__ void tile_build(const float *xs, int XS, const uint2 
   *reinterpret_cast<u32x4 *>(bt + r * kTileBStride + nb * 16) = w;
 }
 
-// The path product of one tree for this wave's 64 leaves: the largest
-// biased accumulator per row, per lane group.
-__device__ __forceinline__ int tile_product(const unsigned char *bt, const v4i (&ctr)[4][4], const v4i (&b4)[4]) {
+// The path product of one tree for this wave's 64 leaves (4 leaf tiles),
+// accumulators started at the biases.
+__device__ __forceinline__ void tile_product(const unsigned char *bt, const v4i (&ctr)[4][4], const v4i (&b4)[4],
+                                             v4i (&d)[4]) {
   const int lane = threadIdx.x & 63, g4 = lane >> 4, r16 = lane & 15;
   v4i bop[4];
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) bop[kb] = *reinterpret_cast<const v4i *>(bt + r16 * kTileBStride + kb * 64 + 16 * g4);
-  int best = INT_MIN;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    v4i d = b4[j];
+    d[j] = b4[j];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) d = __builtin_amdgcn_mfma_i32_16x16x64_i8(ctr[j][kb], bop[kb], d, 0, 0, 0);
-    best = max(best, hmax4(d));
+    for (int kb = 0; kb < 4; ++kb) d[j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ctr[j][kb], bop[kb], d[j], 0, 0, 0);
   }
-  return best;
+}
+
+__device__ __forceinline__ int tile_best(const v4i (&d)[4]) {
+  return max(max(hmax4(d[0]), hmax4(d[1])), max(hmax4(d[2]), hmax4(d[3])));
 }
 
 // Trees t and t+1 (t even); P = (t / 2) & 1 selects the buffers and the
 // record registers. Records of trees t+4, t+5 (loaded two pairs ago) go to
-// LDS for the build one pair ahead, and trees t+8, t+9 are loaded.
-template <int KMODE, int P>
+// LDS for the build one pair ahead, and trees t+8, t+9 are loaded. Past the
+// last tree the products and builds run on the last tree's records (clamped
+// loads) and are discarded, so the pair is one straight block: the builds
+// are issued while the matrix instructions execute, and only then are the
+// accumulators read.
+template <int KMODE, bool WIDE, int P>
 __device__ __forceinline__ void tile_pair(const GemmArgs &a, int t, const float *xs, int XS,
                                           unsigned char (*bt)[2][kTileRows * kTileBStride], uint2 (*rtab)[2][256],
                                           int (*red)[2][16][kTileRows], uint2 (&rset)[2][2], const v4i (&ctr)[4][4],
@@ -569,18 +606,22 @@ __device__ __forceinline__ void tile_pair(const GemmArgs &a, int t, const float 
     rtab[P][u][tid] = rset[P][u];
     rset[P][u] = a.node[(size_t)min(t + 8 + u, T - 1) * 256 + tid];
   }
-  const bool second = t + 1 < T;  // uniform
-  const int best0 = tile_product(bt[P][0], ctr, b4);
-  const int best1 = second ? tile_product(bt[P][1], ctr, b4) : INT_MIN;
-  if (t + 2 < T) tile_build(xs, XS, rtab[P ^ 1][0], bt[P ^ 1][0]);
-  if (t + 3 < T) tile_build(xs, XS, rtab[P ^ 1][1], bt[P ^ 1][1]);
-  red[P][0][wave * 4 + g4][r16] = best0;  // 16 partial maxima per row, combined by the leaf's wave
-  red[P][1][wave * 4 + g4][r16] = best1;
+  v4i d0[4], d1[4];
+  tile_product(bt[P][0], ctr, b4, d0);
+  tile_product(bt[P][1], ctr, b4, d1);
+  if (WIDE) {
+    tile_build2(xs, XS, rtab[P ^ 1], bt[P ^ 1]);
+  } else {
+    tile_build1(xs, XS, rtab[P ^ 1][0], bt[P ^ 1][0]);
+    tile_build1(xs, XS, rtab[P ^ 1][1], bt[P ^ 1][1]);
+  }
+  red[P][0][wave * 4 + g4][r16] = tile_best(d0);  // 16 partial maxima per row, combined by the leaf's wave
+  red[P][1][wave * 4 + g4][r16] = tile_best(d1);
   lds_sync();
   // the leaves of trees t and t+1, by waves t mod 4 and t+1 mod 4 (a wave's
   // previous lookup is consumed first)
   const int u = wave - (t & 3);
-  if ((u == 0 || (u == 1 && second)) && lane < kTileRows) {
+  if ((u == 0 || (u == 1 && t + 1 < T)) && lane < kTileRows) {
     tile_leaf_consume<KMODE>(a, pend, acc, r0 + lane);
     int col = red[P][u][0][lane];
 #pragma unroll
@@ -590,7 +631,10 @@ __device__ __forceinline__ void tile_pair(const GemmArgs &a, int t, const float 
   }
 }
 
-template <int KMODE>
+// WIDE: the feature tile leaves room for one workgroup per CU; both trees'
+// predicate operands are built together (more registers, overlapped LDS
+// round trips) instead of one after the other.
+template <int KMODE, bool WIDE>
 __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
   constexpr int KMAX = TileLeaf<KMODE>::KMAX;
   extern __shared__ __align__(16) unsigned char smem[];  // feature tile [16][XS], then the waves' partial sums
@@ -637,16 +681,15 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
     rset[u >> 1][u & 1] = a.node[(size_t)min(u + 4, T - 1) * 256 + tid];
   }
   lds_sync();
-  tile_build(xs, XS, rtab[0][0], bt[0][0]);
-  if (T > 1) tile_build(xs, XS, rtab[0][1], bt[0][1]);
+  tile_build2(xs, XS, rtab[0], bt[0]);
   lds_sync();
   double acc[KMAX];
 #pragma unroll
   for (int k = 0; k < KMAX; ++k) acc[k] = 0.0;
   TileLeaf<KMODE> pend;
   for (int t = 0; t < T; t += 4) {
-    tile_pair<KMODE, 0>(a, t, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0);
-    if (t + 2 < T) tile_pair<KMODE, 1>(a, t + 2, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0);
+    tile_pair<KMODE, WIDE, 0>(a, t, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0);
+    if (t + 2 < T) tile_pair<KMODE, WIDE, 1>(a, t + 2, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0);
   }
   if (lane < kTileRows) tile_leaf_consume<KMODE>(a, pend, acc, r0 + lane);
   // partial sums in wave order (the feature tile is no longer read)
@@ -746,7 +789,9 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
     const size_t tile_dyn = std::max((size_t)kTileRows * gemm_tile_xs(e.n_cols) * 4, (size_t)4 * kTileRows * kmax * 8);
     const size_t tile_static = (size_t)4 * kTileRows * kTileBStride + 4 * 256 * 8 + 4 * 16 * kTileRows * 4;
     if (tile_dyn + tile_static <= (size_t)lds_max) {
-      fn = kmode == 0 ? gemm_tile_kernel<0> : kmode == 1 ? gemm_tile_kernel<1> : gemm_tile_kernel<2>;
+      const bool wide = 2 * (tile_dyn + tile_static) > (size_t)lds_max;  // one workgroup per CU
+      fn = wide ? (kmode == 0 ? gemm_tile_kernel<0, true> : kmode == 1 ? gemm_tile_kernel<1, true> : gemm_tile_kernel<2, true>)
+                : (kmode == 0 ? gemm_tile_kernel<0, false> : kmode == 1 ? gemm_tile_kernel<1, false> : gemm_tile_kernel<2, false>);
       dyn = tile_dyn;
       rows = kTileRows;
       threads = 256;
