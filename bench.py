@@ -45,7 +45,7 @@ def kernel_label(strat, n, info, workspace=True):
     if n <= (1024 if workspace else 12288 if strat == "ptt" else 16384):
         return LANES.format(name)
     cols = info["n_used_features"]
-    fast = info["leaf_dim"] == 1 and (strat == "tt" or info["ptt_depth"] <= 10)
+    fast = strat == "tt" or info["ptt_depth"] <= 10
     if fast and cols * 128 * 4 + 34 * 1024 <= 160 * 1024:
         return KERNEL[strat]
     xtile = cols * 257 * 4

@@ -263,9 +263,12 @@ void build_tt(hb_handle *h, const hb_ensemble_desc *d, const std::vector<CanonTr
   h->tt_dims = {n_pad};
 }
 
-// Packed blocks for the fast kernels (scalar leaves only); see hb_internal.h.
+// Packed blocks for the fast kernels; see hb_internal.h. A leaf record holds
+// the leaf's value and caller id; with vector leaves the value field holds
+// the first component and the kernels read the vector from the strategy's
+// leaf-value table.
 void build_fast(hb_handle *h, const hb_ensemble_desc *d, const std::vector<CanonTree> &trees) {
-  if (d->leaf_dim != 1) return;
+  const int32_t ld = d->leaf_dim;
   const int32_t T = d->n_trees;
   const int32_t D = h->info.max_depth;
   if (h->info.feasible[HB_STRATEGY_PTT] && D >= 1 && D <= hb::kFastMaxLg) {
@@ -282,7 +285,7 @@ void build_fast(hb_handle *h, const hb_ensemble_desc *d, const std::vector<Canon
         blk[2 * p + 1] = h->ptt_node[((size_t)t * S + p) * 2 + 1];
       }
       for (size_t q = 0; q < S; ++q) {
-        blk[2 * (S + q)] = fbits(h->ptt_leaf_value[(size_t)t * S + q]);
+        blk[2 * (S + q)] = fbits(h->ptt_leaf_value[((size_t)t * S + q) * ld]);
         blk[2 * (S + q) + 1] = (uint32_t)h->ptt_leaf_id[(size_t)t * S + q];
       }
     }
@@ -326,7 +329,7 @@ void build_fast(hb_handle *h, const hb_ensemble_desc *d, const std::vector<Canon
         uint32_t *lr = leaf + 2 * c;
         if (c < (size_t)ct.size()) {
           const int32_t v = ct.caller[c];
-          lr[0] = ct.feat[c] < 0 ? fbits(d->leaf_value[base + v]) : 0u;
+          lr[0] = ct.feat[c] < 0 ? fbits(d->leaf_value[(base + v) * ld]) : 0u;
           lr[1] = (uint32_t)v;
         }
       }

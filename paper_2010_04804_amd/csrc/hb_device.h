@@ -190,6 +190,11 @@ struct FastArgs {
   int32_t split;
   double *partial;
   int32_t ids_vec;            // leaf_ids rows start 16-byte aligned (T % 4 == 0, aligned base)
+  // vector leaves: [T][vec_stride][LD] leaf values, indexed by the tree and
+  // the leaf's slot (PTT) or node (TT); nullptr for scalar leaves
+  const float *vec;
+  int32_t vec_stride;
+  int32_t LD;
   // with ids_vec: byte k = the residues r mod 8 of the rows whose 128-byte
   // lines of leaf ids begin at trees congruent to 4k mod 32
   uint64_t id_phase;

@@ -25,7 +25,9 @@ namespace {
 //     8 or 0; a leaf holds threshold -inf and points to itself;
 //   * multi-output: the output column of each tree is uniform across a wave,
 //     so the per-row double accumulators are updated by register index (the
-//     columns of a chunk are loaded one chunk ahead, lane g holding tree g's).
+//     columns of a chunk are loaded one chunk ahead, lane g holding tree g's);
+//     vector leaves add every value of the reached leaf, read from the
+//     strategy's leaf-value table in global memory (L2-resident).
 
 // Barrier for LDS traffic only: orders this workgroup's LDS accesses across
 // the barrier without waiting for outstanding global stores (the leaf-id
@@ -179,6 +181,15 @@ __device__ __forceinline__ uint32_t tt_xaddr(uint32_t w, uint32_t xlane) {
   return r;
 }
 
+// The values of tree t's leaf reached with walk state s (byte offset of
+// the record: PTT heap index 2^LG + slot, TT node index), vector leaves.
+template <int MODE, int LG>
+__device__ __forceinline__ const float *fast_vec_leaf(const FastArgs &a, int t, uint32_t s) {
+  const uint32_t idx = MODE == 0 ? (s >> 3) - (1u << LG) : ((s >> 3) & ((1u << LG) - 1u));
+  // (clamped to the table's row so that even a malformed table cannot read outside it)
+  return a.vec + ((size_t)min(t, a.out.T - 1) * a.vec_stride + min(idx, (uint32_t)a.vec_stride - 1u)) * a.LD;
+}
+
 template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET, int B, int Q>
 __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
@@ -201,7 +212,7 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   // multi-output: lane g of every wave holds the output column of tree g of
   // the chunk (loaded one chunk ahead, like the blocks)
   int cls_next = 0;
-  if (MULTI)
+  if (MULTI && !a.vec)
     cls_next = a.tree_class[min((more ? c + 1 : c) * TC + ((int)threadIdx.x & (TC - 1)), a.out.T - 1)];
   const int t0 = c * TC;
   // the lines that ended with the previous chunk leave now, behind the
@@ -289,6 +300,20 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
     else
       lrs[g] = *reinterpret_cast<const uint2 *>(base + g * TB + (MODE == 0 ? 0u : (1u << LG) * 8u) + s[g]);
   }
+  // vector leaves: every value of every tree's leaf is added here, before
+  // the first leaf-id store (a load issued behind a store would also wait
+  // for the store)
+  if (MULTI && a.vec) {
+#pragma unroll
+    for (int g = 0; g < TC; ++g) {
+      if (t0 + g < a.out.T) {
+        const float *vp = fast_vec_leaf<MODE, LG>(a, t0 + g, s[g]);
+#pragma unroll
+        for (int k = 0; k < C::KMAX; ++k)
+          if (k < a.LD) acc[k] += (double)vp[k];
+      }
+    }
+  }
 #pragma unroll
   for (int g = 0; g < TC; ++g) {
     const int t = t0 + g;
@@ -305,7 +330,9 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
     }
     if (t < a.out.T) {
       const double v = (double)as_float(lr.x);
-      if (MULTI) {
+      if (MULTI && a.vec) {
+        // added above
+      } else if (MULTI) {
         // the column is uniform across the wave: one register-indexed update
         const int k = __builtin_amdgcn_readlane(cls, g) & (C::KMAX - 1);
         acc[k] += v;
@@ -381,7 +408,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
 #pragma unroll
   for (int k = 0; k < C::KMAX; ++k) acc[k] = 0.0;
   IdPack ids;
-  int cls = MULTI ? a.tree_class[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
+  int cls = MULTI && !a.vec ? a.tree_class[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
   int dep = MODE != 0 ? a.tree_depth[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
   const int64_t r0w = r0 + (tid & ~63);
   const IdOut io = make_id_out<ROWS>(a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], c_begin * C::TC, a.out.T);

@@ -482,10 +482,13 @@ __global__ __launch_bounds__(64 * J) void split_finish_kernel(const double *part
 
 // Launches the fast kernel when its layout exists and its LDS fits; returns
 // kNotApplicable to fall back to traverse_kernel.
+// vec, vec_stride: vector leaves' values [T][vec_stride][leaf_dim] (the
+// strategy's leaf-value table), or nullptr for scalar leaves.
 int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int chunks, const int32_t *depth,
-                const EnsembleDev &e, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
-                const Workspace &ws, hipStream_t stream, std::string *err) {
-  if (!blocks || (mode == 2 && !leaf) || lg < 1 || lg > kFastMaxLg || e.leaf_dim != 1) return kNotApplicable;
+                const float *vec, int vec_stride, const EnsembleDev &e, const float *X, int64_t n_rows,
+                float *scores, int32_t *leaf_ids, const Workspace &ws, hipStream_t stream, std::string *err) {
+  if (!blocks || (mode == 2 && !leaf) || lg < 1 || lg > kFastMaxLg) return kNotApplicable;
+  if (e.leaf_dim != 1 && (!vec || e.leaf_dim != e.n_outputs || e.leaf_dim > HB_MAX_OUTPUTS)) return kNotApplicable;
   const int lds_max = max_dynamic_lds(err);
   if (lds_max <= 0) return HB_ERR_HIP;
   const int tb = fast_tree_bytes(mode, lg);
@@ -557,6 +560,11 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int ch
   a.leaf_ids = leaf_ids;
   a.out = OutArgs{scores, e.n_trees, e.n_outputs, e.aggregation, e.transform, e.base_score};
   a.tree_class = e.tree_class;
+  if (e.leaf_dim != 1) {
+    a.vec = vec;
+    a.vec_stride = vec_stride;
+    a.LD = e.leaf_dim;
+  }
   a.blocks = blocks;
   a.leaf = leaf;
   a.tree_depth = depth;
@@ -722,8 +730,8 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
   int rc = kNotApplicable;
   if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsPtt)) rc = launch_lanes(true, a, stream, err);
   if (rc == kNotApplicable)
-    rc = launch_fast(0, t.depth, t.fast, nullptr, t.fast_chunks, nullptr, e, X, n_rows, scores, leaf_ids, ws, stream,
-                     err);
+    rc = launch_fast(0, t.depth, t.fast, nullptr, t.fast_chunks, nullptr, t.leaf_value, 1 << t.depth, e, X, n_rows,
+                     scores, leaf_ids, ws, stream, err);
   if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(true, a, stream, err);
   if (rc != kNotApplicable) return rc;
   return launch_traverse(true, a, stream, err);
@@ -752,8 +760,8 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
   int rc = kNotApplicable;
   if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsTt)) rc = launch_lanes(false, a, stream, err);
   if (rc == kNotApplicable)
-    rc = launch_fast(t.fast_mode, t.fast_lg, t.fast, t.fast_leaf, t.fast_chunks, t.depth, e, X, n_rows, scores,
-                     leaf_ids, ws, stream, err);
+    rc = launch_fast(t.fast_mode, t.fast_lg, t.fast, t.fast_leaf, t.fast_chunks, t.depth, t.leaf_value, t.n_pad, e, X,
+                     n_rows, scores, leaf_ids, ws, stream, err);
   if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(false, a, stream, err);
   if (rc != kNotApplicable) return rc;
   return launch_traverse(false, a, stream, err);

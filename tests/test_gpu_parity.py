@@ -222,7 +222,7 @@ def _vector_forest(n_features, n_trees, depth, seed):
 @pytest.mark.parametrize("n_features,n", [(28, 9000), (28, 20_000), (50_000, 37)])
 def test_vector_leaf_forest_routes(n_features, n, strategy):
     """Random forests with probability-vector leaves take the row-parallel
-    general kernel at large batches when the rows fit its LDS tile, the
+    fast kernels at large batches when the rows fit their LDS tile, the
     trees-across-lanes kernel at small ones, and the general kernel reading
     features from global memory when a single row does not fit in LDS."""
     m, rng = _vector_forest(n_features, 100, 7, 21)
@@ -231,6 +231,37 @@ def test_vector_leaf_forest_routes(n_features, n, strategy):
     h = hb.compile(m, device=0)
     scores, ids = run(h, X, strategy)
     check(m, X, scores, ids, f"vecRF F{n_features} n{n}/{strategy}")
+
+
+@pytest.mark.parametrize("ld", [2, 3, 5, 16])
+@pytest.mark.parametrize("leafwise", [False, True])
+def test_vector_leaves_row_parallel(ld, leafwise):
+    """Vector leaves in the row-parallel fast kernels (leaf vectors read from
+    the leaf-value table), with and without the tree split, with leaf ids, for
+    perfect trees (PTT and TT) and leaf-wise trees (TT), 1 to 16 values."""
+    rng = np.random.Generator(np.random.PCG64(9100 + ld + 50 * leafwise))
+    T = 70
+    if leafwise:
+        m = synth.leafwise_forest(rng, T, 90, 10, 0.7, 24, lambda r, f: r.standard_normal(f.size),
+                                  lambda r, k: r.standard_normal(k))
+        m["leaf_dim"] = ld
+        m["leaf_value"] = rng.standard_normal(m["leaf_value"].size * ld).astype(np.float32)
+    else:
+        m = synth.perfect_forest(rng, T, 7, 24, lambda r, f: r.standard_normal(f.size),
+                                 lambda r, k: r.standard_normal(k * ld), leaf_dim=ld)
+    m.update(n_outputs=ld, tree_class=None, aggregation="mean", transform="softmax" if ld > 2 else "none",
+             base_score=rng.standard_normal(ld).astype(np.float32))
+    m = synth.permute_nodes(m, ld)
+    h = hb.compile(m, device=0)
+    for n in (5000, 40_001):
+        X = np.ascontiguousarray(pins.tricky_rows(rng, m, n))
+        for strategy in (("tt",) if leafwise else ("ptt", "tt")):
+            if not h.info()["feasible"][strategy]:
+                continue
+            for ws in (False, True):
+                say("vector leaves", ld, "leafwise" if leafwise else "perfect", n, strategy, ws)
+                scores, ids = run(h, X, strategy, workspace=ws)
+                check(m, X, scores, ids, f"vec{ld}/{leafwise}/{n}/{strategy}/ws={ws}")
 
 
 @pytest.mark.parametrize("missing", [False, True])
