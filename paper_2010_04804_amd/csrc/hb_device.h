@@ -202,26 +202,29 @@ struct FastArgs {
 
 using FastFn = void (*)(FastArgs);
 
+// Accumulators per row of a fast kernel: 1 (one output), 2 (two outputs,
+// e.g. binary classifiers with probability-vector leaves) or HB_MAX_OUTPUTS.
+
 // The kernel for (mode, lg, multi-output) or nullptr; lg in [1, kFastMaxLg].
-FastFn fast_ptt_kernel_128(int lg, bool multi);
-FastFn fast_ptt_kernel_256(int lg, bool multi);
-FastFn fast_ptt_kernel_256s(int lg, bool multi);
-FastFn fast_ptt_kernel_512(int lg, bool multi);
-FastFn fast_ptt_kernel_512s(int lg, bool multi);
-FastFn fast_ptt_kernel_768(int lg, bool multi);
-FastFn fast_ptt_kernel_1024(int lg, bool multi);
-FastFn fast_tt_kernel_1024(int lg, bool multi);
-FastFn fast_tt_kernel_256(int lg, bool multi);
-FastFn fast_tt_kernel_512(int lg, bool multi);
-FastFn fast_tt_kernel_512s(int lg, bool multi);
-FastFn fast_tt_kernel_256s(int lg, bool multi);
-FastFn fast_tt_kernel_128(int lg, bool multi);
+FastFn fast_ptt_kernel_128(int lg, int km);
+FastFn fast_ptt_kernel_256(int lg, int km);
+FastFn fast_ptt_kernel_256s(int lg, int km);
+FastFn fast_ptt_kernel_512(int lg, int km);
+FastFn fast_ptt_kernel_512s(int lg, int km);
+FastFn fast_ptt_kernel_768(int lg, int km);
+FastFn fast_ptt_kernel_1024(int lg, int km);
+FastFn fast_tt_kernel_1024(int lg, int km);
+FastFn fast_tt_kernel_256(int lg, int km);
+FastFn fast_tt_kernel_512(int lg, int km);
+FastFn fast_tt_kernel_512s(int lg, int km);
+FastFn fast_tt_kernel_256s(int lg, int km);
+FastFn fast_tt_kernel_128(int lg, int km);
 // TT with leaf records in global memory (mode 2)
-FastFn fast_ttg_kernel_1024(int lg, bool multi);
-FastFn fast_ttg_kernel_256(int lg, bool multi);
-FastFn fast_ttg_kernel_512(int lg, bool multi);
-FastFn fast_ttg_kernel_512s(int lg, bool multi);
-FastFn fast_ttg_kernel_256s(int lg, bool multi);
-FastFn fast_ttg_kernel_128(int lg, bool multi);
+FastFn fast_ttg_kernel_1024(int lg, int km);
+FastFn fast_ttg_kernel_256(int lg, int km);
+FastFn fast_ttg_kernel_512(int lg, int km);
+FastFn fast_ttg_kernel_512s(int lg, int km);
+FastFn fast_ttg_kernel_256s(int lg, int km);
+FastFn fast_ttg_kernel_128(int lg, int km);
 
 }  // namespace hb

@@ -66,14 +66,15 @@ struct ChunkPrefetch {
 template <int MODE>
 constexpr int kFastMaxLgFor = MODE == 0 ? 10 : 11;
 
-template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET>
+template <int MODE, int LG, int KM, int ROWS, int BUDGET>
 struct FastCfg {
   static constexpr int TB = fast_tree_bytes(MODE, LG);
   static constexpr int TC = fast_tc(TB, BUDGET);
   static constexpr int BUFS = fast_bufs(TB, BUDGET);
   static constexpr int CPF = kFastIdGroup / TC;  // chunks per leaf-id flush
   static constexpr int CHUNK16 = TC * TB / 16;
-  static constexpr int KMAX = MULTI ? HB_MAX_OUTPUTS : 1;
+  static constexpr int KMAX = KM;  // accumulators: 1, 2 or HB_MAX_OUTPUTS
+  static constexpr bool MULTI = KM > 1;
 };
 
 // Leaf ids of a 32-tree group, one row per lane, as 16-bit halves: tree q of
@@ -190,12 +191,12 @@ __device__ __forceinline__ const float *fast_vec_leaf(const FastArgs &a, int t, 
   return a.vec + ((size_t)min(t, a.out.T - 1) * a.vec_stride + min(idx, (uint32_t)a.vec_stride - 1u)) * a.LD;
 }
 
-template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET, int B, int Q>
-__device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::CHUNK16],
+template <int MODE, int LG, int KM, int ROWS, int BUDGET, int B, int Q>
+__device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbuf)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
-                                           double (&acc)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::KMAX],
+                                           double (&acc)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::KMAX],
                                            IdPack &ids, int &cls, int &dep, const IdOut &io) {
-  using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
+  using C = FastCfg<MODE, LG, KM, ROWS, BUDGET>;
   constexpr int TC = C::TC;
   constexpr int TB = C::TB;
   // chunk c is in tbuf[B] (the barrier that ended the previous chunk made it
@@ -212,7 +213,7 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   // multi-output: lane g of every wave holds the output column of tree g of
   // the chunk (loaded one chunk ahead, like the blocks)
   int cls_next = 0;
-  if (MULTI && !a.vec)
+  if (C::MULTI && !a.vec)
     cls_next = a.tree_class[min((more ? c + 1 : c) * TC + ((int)threadIdx.x & (TC - 1)), a.out.T - 1)];
   const int t0 = c * TC;
   // the lines that ended with the previous chunk leave now, behind the
@@ -303,7 +304,7 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   // vector leaves: every value of every tree's leaf is added here, before
   // the first leaf-id store (a load issued behind a store would also wait
   // for the store)
-  if (MULTI && a.vec) {
+  if (C::MULTI && a.vec) {
 #pragma unroll
     for (int g = 0; g < TC; ++g) {
       if (t0 + g < a.out.T) {
@@ -330,9 +331,9 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
     }
     if (t < a.out.T) {
       const double v = (double)as_float(lr.x);
-      if (MULTI && a.vec) {
+      if (C::MULTI && a.vec) {
         // added above
-      } else if (MULTI) {
+      } else if (C::MULTI) {
         // the column is uniform across the wave: one register-indexed update
         const int k = __builtin_amdgcn_readlane(cls, g) & (C::KMAX - 1);
         acc[k] += v;
@@ -355,22 +356,22 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
 
 // The CPF chunks between two leaf-id flushes, unrolled so that buffer
 // indices and id slots are compile-time constants.
-template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET, int Q>
-__device__ __forceinline__ void fast_group(const FastArgs &a, int c0, uint4 (*tbuf)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::CHUNK16],
+template <int MODE, int LG, int KM, int ROWS, int BUDGET, int Q>
+__device__ __forceinline__ void fast_group(const FastArgs &a, int c0, uint4 (*tbuf)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
-                                           double (&acc)[FastCfg<MODE, LG, MULTI, ROWS, BUDGET>::KMAX],
+                                           double (&acc)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::KMAX],
                                            IdPack &ids, int &cls, int &dep, const IdOut &io) {
-  using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
+  using C = FastCfg<MODE, LG, KM, ROWS, BUDGET>;
   if constexpr (Q < C::CPF) {
-    fast_chunk<MODE, LG, MULTI, ROWS, BUDGET, C::BUFS == 2 ? (Q & 1) : 0, Q>(a, c0 + Q, tbuf, xs, lane4, acc, ids,
+    fast_chunk<MODE, LG, KM, ROWS, BUDGET, C::BUFS == 2 ? (Q & 1) : 0, Q>(a, c0 + Q, tbuf, xs, lane4, acc, ids,
                                                                            cls, dep, io);
-    fast_group<MODE, LG, MULTI, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls, dep, io);
+    fast_group<MODE, LG, KM, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls, dep, io);
   }
 }
 
-template <int MODE, int LG, bool MULTI, int ROWS, int BUDGET>
+template <int MODE, int LG, int KM, int ROWS, int BUDGET>
 __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
-  using C = FastCfg<MODE, LG, MULTI, ROWS, BUDGET>;
+  using C = FastCfg<MODE, LG, KM, ROWS, BUDGET>;
   constexpr int G = kFastIdGroup;
   // this workgroup's chunks (all of them unless the trees are split)
   const int c_begin = a.split ? (int)blockIdx.y * a.split : 0;
@@ -408,12 +409,12 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
 #pragma unroll
   for (int k = 0; k < C::KMAX; ++k) acc[k] = 0.0;
   IdPack ids;
-  int cls = MULTI && !a.vec ? a.tree_class[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
+  int cls = C::MULTI && !a.vec ? a.tree_class[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
   int dep = MODE != 0 ? a.tree_depth[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
   const int64_t r0w = r0 + (tid & ~63);
   const IdOut io = make_id_out<ROWS>(a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], c_begin * C::TC, a.out.T);
   for (int c = c_begin; c < a.n_chunks; c += C::CPF) {  // chunk counts are multiples of CPF
-    fast_group<MODE, LG, MULTI, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, io);
+    fast_group<MODE, LG, KM, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, io);
     if (a.leaf_ids && !a.ids_vec) flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, r0w, c * C::TC);
   }
   if (io.on) {
@@ -442,13 +443,13 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
 }
 
 
-template <int MODE, bool MULTI, int ROWS, int BUDGET, int LG = 1>
+template <int MODE, int KM, int ROWS, int BUDGET, int LG = 1>
 FastFn pick_fast(int lg) {
   if constexpr (LG > kFastMaxLgFor<MODE>) {
     return nullptr;
   } else {
-    if (lg == LG) return fast_kernel<MODE, LG, MULTI, ROWS, BUDGET>;
-    return pick_fast<MODE, MULTI, ROWS, BUDGET, LG + 1>(lg);
+    if (lg == LG) return fast_kernel<MODE, LG, KM, ROWS, BUDGET>;
+    return pick_fast<MODE, KM, ROWS, BUDGET, LG + 1>(lg);
   }
 }
 

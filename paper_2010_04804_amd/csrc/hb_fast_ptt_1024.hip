@@ -6,8 +6,8 @@
 
 namespace hb {
 
-FastFn fast_ptt_kernel_1024(int lg, bool multi) {
-  return multi ? nullptr : pick_fast<0, false, 1024, kFastTableSmall>(lg);
+FastFn fast_ptt_kernel_1024(int lg, int km) {
+  return km == 1 ? pick_fast<0, 1, 1024, kFastTableSmall>(lg) : km == 2 ? pick_fast<0, 2, 1024, kFastTableSmall>(lg) : nullptr;
 }
 
 }  // namespace hb

@@ -5,8 +5,8 @@
 
 namespace hb {
 
-FastFn fast_ptt_kernel_128(int lg, bool multi) {
-  return multi ? pick_fast<0, true, 128, kFastTableSmall>(lg) : pick_fast<0, false, 128, kFastTableSmall>(lg);
+FastFn fast_ptt_kernel_128(int lg, int km) {
+  return km == 1 ? pick_fast<0, 1, 128, kFastTableSmall>(lg) : pick_fast<0, HB_MAX_OUTPUTS, 128, kFastTableSmall>(lg);
 }
 
 }  // namespace hb

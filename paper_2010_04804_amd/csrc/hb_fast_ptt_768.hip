@@ -6,8 +6,8 @@ namespace hb {
 
 // Single-output only: the multi-output accumulators do not fit in the
 // registers three waves per SIMD leave.
-FastFn fast_ptt_kernel_768(int lg, bool multi) {
-  return multi ? nullptr : pick_fast<0, false, 768, kFastTableSmall>(lg);
+FastFn fast_ptt_kernel_768(int lg, int km) {
+  return km == 1 ? pick_fast<0, 1, 768, kFastTableSmall>(lg) : km == 2 ? pick_fast<0, 2, 768, kFastTableSmall>(lg) : nullptr;
 }
 
 }  // namespace hb

@@ -4,8 +4,8 @@
 
 namespace hb {
 
-FastFn fast_tt_kernel_256(int lg, bool multi) {
-  return multi ? pick_fast<1, true, 256, kFastTableLds>(lg) : pick_fast<1, false, 256, kFastTableLds>(lg);
+FastFn fast_tt_kernel_256(int lg, int km) {
+  return km == 1 ? pick_fast<1, 1, 256, kFastTableLds>(lg) : pick_fast<1, HB_MAX_OUTPUTS, 256, kFastTableLds>(lg);
 }
 
 }  // namespace hb

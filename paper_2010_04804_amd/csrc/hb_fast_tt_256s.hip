@@ -4,8 +4,8 @@
 
 namespace hb {
 
-FastFn fast_tt_kernel_256s(int lg, bool multi) {
-  return multi ? pick_fast<1, true, 256, kFastTableSmall>(lg) : pick_fast<1, false, 256, kFastTableSmall>(lg);
+FastFn fast_tt_kernel_256s(int lg, int km) {
+  return km == 1 ? pick_fast<1, 1, 256, kFastTableSmall>(lg) : pick_fast<1, HB_MAX_OUTPUTS, 256, kFastTableSmall>(lg);
 }
 
 }  // namespace hb

@@ -4,8 +4,8 @@
 
 namespace hb {
 
-FastFn fast_tt_kernel_512(int lg, bool multi) {
-  return multi ? pick_fast<1, true, 512, kFastTableLds>(lg) : pick_fast<1, false, 512, kFastTableLds>(lg);
+FastFn fast_tt_kernel_512(int lg, int km) {
+  return km == 1 ? pick_fast<1, 1, 512, kFastTableLds>(lg) : pick_fast<1, HB_MAX_OUTPUTS, 512, kFastTableLds>(lg);
 }
 
 }  // namespace hb

@@ -5,8 +5,8 @@
 
 namespace hb {
 
-FastFn fast_ttg_kernel_1024(int lg, bool multi) {
-  return multi ? nullptr : pick_fast<2, false, 1024, kFastTableSmall>(lg);
+FastFn fast_ttg_kernel_1024(int lg, int km) {
+  return km == 1 ? pick_fast<2, 1, 1024, kFastTableSmall>(lg) : km == 2 ? pick_fast<2, 2, 1024, kFastTableSmall>(lg) : nullptr;
 }
 
 }  // namespace hb

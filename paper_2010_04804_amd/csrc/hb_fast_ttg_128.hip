@@ -5,8 +5,8 @@
 
 namespace hb {
 
-FastFn fast_ttg_kernel_128(int lg, bool multi) {
-  return multi ? pick_fast<2, true, 128, kFastTableSmall>(lg) : pick_fast<2, false, 128, kFastTableSmall>(lg);
+FastFn fast_ttg_kernel_128(int lg, int km) {
+  return km == 1 ? pick_fast<2, 1, 128, kFastTableSmall>(lg) : pick_fast<2, HB_MAX_OUTPUTS, 128, kFastTableSmall>(lg);
 }
 
 }  // namespace hb

@@ -4,8 +4,8 @@
 
 namespace hb {
 
-FastFn fast_ttg_kernel_256(int lg, bool multi) {
-  return multi ? pick_fast<2, true, 256, kFastTableLds>(lg) : pick_fast<2, false, 256, kFastTableLds>(lg);
+FastFn fast_ttg_kernel_256(int lg, int km) {
+  return km == 1 ? pick_fast<2, 1, 256, kFastTableLds>(lg) : pick_fast<2, HB_MAX_OUTPUTS, 256, kFastTableLds>(lg);
 }
 
 }  // namespace hb

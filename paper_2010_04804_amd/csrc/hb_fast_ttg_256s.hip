@@ -4,8 +4,8 @@
 
 namespace hb {
 
-FastFn fast_ttg_kernel_256s(int lg, bool multi) {
-  return multi ? pick_fast<2, true, 256, kFastTableSmall>(lg) : pick_fast<2, false, 256, kFastTableSmall>(lg);
+FastFn fast_ttg_kernel_256s(int lg, int km) {
+  return km == 1 ? pick_fast<2, 1, 256, kFastTableSmall>(lg) : pick_fast<2, HB_MAX_OUTPUTS, 256, kFastTableSmall>(lg);
 }
 
 }  // namespace hb

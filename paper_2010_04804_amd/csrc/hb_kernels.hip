@@ -492,14 +492,14 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int ch
   const int lds_max = max_dynamic_lds(err);
   if (lds_max <= 0) return HB_ERR_HIP;
   const int tb = fast_tree_bytes(mode, lg);
-  const bool multi = e.n_outputs > 1;
+  const int km = e.n_outputs == 1 ? 1 : e.n_outputs == 2 ? 2 : HB_MAX_OUTPUTS;
   // Workgroup shapes (rows, chunk budget); the one with the most waves per CU
   // that fits in LDS wins (the walk is bound by the latency of its dependent
   // LDS reads), the larger chunk on a tie (fewer hand-overs). Wide workgroups
   // only when the batch gives every CU several of them.
   struct Shape {
     int rows, budget;
-    FastFn (*get)(int, bool);
+    FastFn (*get)(int, int);
   };
   static const Shape kPtt[] = {{1024, kFastTableSmall, fast_ptt_kernel_1024},
                                {768, kFastTableSmall, fast_ptt_kernel_768},
@@ -533,7 +533,7 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int ch
   for (int i = 0; i < n_shapes; ++i) {
     const Shape &sh = shapes[i];
     const size_t lds = lds_of(sh);
-    if (lds > (size_t)lds_max || !sh.get(lg, multi)) continue;
+    if (lds > (size_t)lds_max || !sh.get(lg, km)) continue;
     if (sh.rows > 256 && n_rows < 64 * (int64_t)sh.rows) continue;
     const long waves = (long)(sh.rows / 64) * (long)((size_t)lds_max / lds);
     if (waves > best_waves) {
@@ -549,7 +549,7 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int ch
   if (best_waves < 4 && table_bytes <= (int64_t)64 << 10) return kPreferLanes;
   const int rows = shapes[best].rows;
   const size_t xbytes = (size_t)e.n_cols * rows * 4;
-  FastFn fn = shapes[best].get(lg, multi);
+  FastFn fn = shapes[best].get(lg, km);
   if (!fn) return kNotApplicable;
   FastArgs a{};
   a.X = X;
@@ -631,7 +631,7 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int ch
     // 16 waves per 64 rows for scalar outputs, 8 for several (their sums
     // take K times the LDS: at most 64 KiB)
     const unsigned fin_rows = (unsigned)((n_rows + 63) / 64);
-    if (multi)
+    if (km > 1)
       hipLaunchKernelGGL((split_finish_kernel<HB_MAX_OUTPUTS, 8>), dim3(fin_rows), dim3(64 * 8),
                          (size_t)8 * e.n_outputs * 64 * sizeof(double), stream, a.partial, split, n_rows, a.out);
     else

@@ -264,6 +264,22 @@ def test_vector_leaves_row_parallel(ld, leafwise):
                 check(m, X, scores, ids, f"vec{ld}/{leafwise}/{n}/{strategy}/ws={ws}")
 
 
+def test_two_class_scalar_leaves_row_parallel():
+    """Two outputs with scalar leaves and a class per tree take the
+    two-accumulator fast kernels (1024-row workgroups) like 2-vector leaves."""
+    rng = np.random.Generator(np.random.PCG64(9300))
+    m = synth.perfect_forest(rng, 90, 8, 20, lambda r, f: r.standard_normal(f.size), lambda r, k: r.standard_normal(k))
+    m.update(n_outputs=2, tree_class=(rng.random(90) < 0.5).astype(np.int32), aggregation="sum",
+             transform="softmax", base_score=None)
+    h = hb.compile(m, device=0)
+    X = np.ascontiguousarray(pins.tricky_rows(rng, m, 70_001))
+    for strategy in ("ptt", "tt"):
+        for ws in (False, True):
+            say("two classes", strategy, ws)
+            scores, ids = run(h, X, strategy, workspace=ws)
+            check(m, X, scores, ids, f"2cls/{strategy}/ws={ws}")
+
+
 @pytest.mark.parametrize("missing", [False, True])
 def test_tt_widest_workgroups(missing):
     """TreeTraversal in 1024-row workgroups (batches of 65,536 rows and more
