@@ -311,12 +311,16 @@ def run_configs():
 
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
-    for cfg in sorted(synth.CONFIGS):
-        n = synth.CONFIGS[cfg]["n_rows"]
-        model = synth.make_model(cfg)
+    for cfg in sorted(synth.CONFIGS) + ["rf2"]:
+        if cfg == "rf2":  # beside the five: a binary random forest with vector leaves over narrow rows
+            n, name = synth.RF_VECTOR["n_rows"], synth.RF_VECTOR["name"]
+            model, rows = synth.rf_vector_model(), synth.rf_vector_rows(n)
+        else:
+            n, name = synth.CONFIGS[cfg]["n_rows"], synth.CONFIGS[cfg]["name"]
+            model, rows = synth.make_model(cfg), synth.make_rows(cfg, n)
         h = hb.compile(model, device=0)
         info = h.info()
-        X = torch.from_numpy(synth.make_rows(cfg, n)).to(dev)
+        X = torch.from_numpy(rows).to(dev)
         scores = torch.empty((n, info["n_outputs"]), dtype=torch.float32, device=dev)
         ids = torch.empty((n, info["n_trees"]), dtype=torch.int32, device=dev)
         auto = h.select(n)
@@ -334,7 +338,7 @@ def run_configs():
                     frac = gemm_ops(model, n) / (ms * 1e-3) / INT8_PEAK
                 else:
                     frac = algorithmic_bytes(info, n, leaves, s) / (ms * 1e-3) / HBM_PEAK
-                print(json.dumps({"workload": cfg, "name": synth.CONFIGS[cfg]["name"], "rows": n,
+                print(json.dumps({"workload": cfg, "name": name, "rows": n,
                                   "strategy": s, "auto": s == auto, "leaf_ids": leaves,
                                   "ms": round(ms, 4), "rows_per_s": n / (ms * 1e-3),
                                   "bound": "mfma" if s == "gemm" else "hbm", "frac": frac}), flush=True)

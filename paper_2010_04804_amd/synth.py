@@ -42,6 +42,9 @@ __all__ = [
     "SWEEP",
     "sweep_model",
     "sweep_rows",
+    "RF_VECTOR",
+    "rf_vector_model",
+    "rf_vector_rows",
     "narrow_use_model",
     "narrow_use_rows",
     "with_missing",
@@ -250,6 +253,32 @@ def sweep_rows(n_rows: int) -> np.ndarray:
     """Input rows of the crossover sweep: N(0,1) over 200 features."""
     _, rng = _streams(SWEEP["seed"])
     return np.ascontiguousarray(_f32(rng.standard_normal((n_rows, SWEEP["n_features"]))))
+
+
+# A binary random-forest classifier over narrow rows (the shape of the
+# paper's RandomForest models on 28-feature data): 500 perfect trees of
+# depth 8, leaves holding class probabilities (1 - p, p), MEAN aggregation.
+RF_VECTOR = dict(name="random forest, narrow input: 500 perfect trees depth 8, 28 features, 2-vector leaves",
+                 n_trees=500, depth=8, n_features=28, seed=7, n_rows=1_000_000)
+
+
+def rf_vector_model() -> dict:
+    rng, _ = _streams(RF_VECTOR["seed"])
+
+    def leaves(r, n):
+        p = r.random(n)
+        return np.stack([1.0 - p, p], axis=1)
+
+    m = perfect_forest(rng, RF_VECTOR["n_trees"], RF_VECTOR["depth"], RF_VECTOR["n_features"],
+                       lambda r, f: r.standard_normal(f.size), leaves, leaf_dim=2)
+    m.update(n_outputs=2, tree_class=None, aggregation="mean", transform="none", base_score=None)
+    return m
+
+
+def rf_vector_rows(n_rows: int) -> np.ndarray:
+    """Input rows of the narrow random forest: N(0,1) over 28 features."""
+    _, rng = _streams(RF_VECTOR["seed"])
+    return np.ascontiguousarray(_f32(rng.standard_normal((n_rows, RF_VECTOR["n_features"]))))
 
 
 def narrow_use_model(n_features: int, n_used: int, n_trees: int, depth: int, seed: int,

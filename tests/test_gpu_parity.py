@@ -264,6 +264,18 @@ def test_vector_leaves_row_parallel(ld, leafwise):
                 check(m, X, scores, ids, f"vec{ld}/{leafwise}/{n}/{strategy}/ws={ws}")
 
 
+@pytest.mark.parametrize("strategy", STRATEGIES)
+def test_rf_vector_workload(strategy):
+    """The narrow binary random forest that the workload table reports beside
+    the five (2-vector leaves, 28 features) at 70,001 rows."""
+    m = synth.rf_vector_model()
+    h = hb.compile(m, device=0)
+    X = synth.rf_vector_rows(70_001)
+    say("rf vector workload", strategy)
+    scores, ids = run(h, X, strategy, workspace=False)
+    check(m, X, scores, ids, f"rf2/{strategy}")
+
+
 def test_two_class_scalar_leaves_row_parallel():
     """Two outputs with scalar leaves and a class per tree take the
     two-accumulator fast kernels (1024-row workgroups) like 2-vector leaves."""
