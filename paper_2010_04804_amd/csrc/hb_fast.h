@@ -75,6 +75,10 @@ struct FastCfg {
   static constexpr int CHUNK16 = TC * TB / 16;
   static constexpr int KMAX = KM;  // accumulators: 1, 2 or HB_MAX_OUTPUTS
   static constexpr bool MULTI = KM > 1;
+  // two outputs: the chunk's 2-vector leaves are held in registers for one
+  // walk (up to 8 trees per chunk; larger chunks add them at once)
+  static constexpr bool VHOLD = KM == 2 && TC <= 8;
+  static constexpr int VH = VHOLD ? TC : 1;
 };
 
 // Leaf ids of a 32-tree group, one row per lane, as 16-bit halves: tree q of
@@ -195,7 +199,8 @@ template <int MODE, int LG, int KM, int ROWS, int BUDGET, int B, int Q>
 __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbuf)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
                                            double (&acc)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::KMAX],
-                                           IdPack &ids, int &cls, int &dep, const IdOut &io) {
+                                           IdPack &ids, int &cls, int &dep, float2 (&vh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::VH],
+                                           const IdOut &io) {
   using C = FastCfg<MODE, LG, KM, ROWS, BUDGET>;
   constexpr int TC = C::TC;
   constexpr int TB = C::TB;
@@ -301,10 +306,21 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
     else
       lrs[g] = *reinterpret_cast<const uint2 *>(base + g * TB + (MODE == 0 ? 0u : (1u << LG) * 8u) + s[g]);
   }
-  // vector leaves: every value of every tree's leaf is added here, before
-  // the first leaf-id store (a load issued behind a store would also wait
-  // for the store)
-  if (C::MULTI && a.vec) {
+  // vector leaves, two values (VHOLD): the previous chunk's leaves, read
+  // a whole walk ago, are added now and this chunk's are read, before the
+  // first leaf-id store (a load issued behind a store would also wait for
+  // the store), to be added after the next walk
+  if (C::VHOLD && a.vec) {
+#pragma unroll
+    for (int g = 0; g < C::VH; ++g) {
+      acc[0] += (double)vh[g].x;
+      acc[1] += (double)vh[g].y;
+      vh[g] = t0 + g < a.out.T ? *reinterpret_cast<const float2 *>(fast_vec_leaf<MODE, LG>(a, t0 + g, s[g]))
+                               : make_float2(0.0f, 0.0f);
+    }
+  } else if (C::MULTI && a.vec) {
+    // longer vectors: every value of every tree's leaf is added here, before
+    // the first leaf-id store
 #pragma unroll
     for (int g = 0; g < TC; ++g) {
       if (t0 + g < a.out.T) {
@@ -360,12 +376,13 @@ template <int MODE, int LG, int KM, int ROWS, int BUDGET, int Q>
 __device__ __forceinline__ void fast_group(const FastArgs &a, int c0, uint4 (*tbuf)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
                                            double (&acc)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::KMAX],
-                                           IdPack &ids, int &cls, int &dep, const IdOut &io) {
+                                           IdPack &ids, int &cls, int &dep, float2 (&vh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::VH],
+                                           const IdOut &io) {
   using C = FastCfg<MODE, LG, KM, ROWS, BUDGET>;
   if constexpr (Q < C::CPF) {
     fast_chunk<MODE, LG, KM, ROWS, BUDGET, C::BUFS == 2 ? (Q & 1) : 0, Q>(a, c0 + Q, tbuf, xs, lane4, acc, ids,
-                                                                           cls, dep, io);
-    fast_group<MODE, LG, KM, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls, dep, io);
+                                                                           cls, dep, vh, io);
+    fast_group<MODE, LG, KM, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls, dep, vh, io);
   }
 }
 
@@ -411,11 +428,21 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   IdPack ids;
   int cls = C::MULTI && !a.vec ? a.tree_class[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
   int dep = MODE != 0 ? a.tree_depth[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
+  float2 vh[C::VH];
+#pragma unroll
+  for (int g = 0; g < C::VH; ++g) vh[g] = make_float2(0.0f, 0.0f);
   const int64_t r0w = r0 + (tid & ~63);
   const IdOut io = make_id_out<ROWS>(a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], c_begin * C::TC, a.out.T);
   for (int c = c_begin; c < a.n_chunks; c += C::CPF) {  // chunk counts are multiples of CPF
-    fast_group<MODE, LG, KM, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, io);
+    fast_group<MODE, LG, KM, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, vh, io);
     if (a.leaf_ids && !a.ids_vec) flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, r0w, c * C::TC);
+  }
+  if (C::VHOLD && a.vec) {  // the last chunk's 2-vector leaves
+#pragma unroll
+    for (int g = 0; g < C::VH; ++g) {
+      acc[0] += (double)vh[g].x;
+      acc[1] += (double)vh[g].y;
+    }
   }
   if (io.on) {
     // the rest of every row's last line: from its start (tree t_pad - 32 + 4k)
