@@ -79,6 +79,11 @@ struct FastCfg {
   // walk (up to 8 trees per chunk; larger chunks add them at once)
   static constexpr bool VHOLD = KM == 2 && TC <= 8;
   static constexpr int VH = VHOLD ? TC : 1;
+  // TT leaf records in global memory (mode 2), one output, chunks of up to 8
+  // trees: the records are held in registers for one walk, and the chunk's
+  // leaf ids and sums are taken one chunk late
+  static constexpr bool LAG = MODE == 2 && KM == 1 && TC <= 8;
+  static constexpr int LH = LAG ? TC : 1;
 };
 
 // Leaf ids of a 32-tree group, one row per lane, as 16-bit halves: tree q of
@@ -195,12 +200,53 @@ __device__ __forceinline__ const float *fast_vec_leaf(const FastArgs &a, int t, 
   return a.vec + ((size_t)min(t, a.out.T - 1) * a.vec_stride + min(idx, (uint32_t)a.vec_stride - 1u)) * a.LD;
 }
 
+// Leaf ids and sums of one chunk's trees tb .. tb + TC - 1 (chunk index QP
+// within its 32-tree group) from their leaf records: each id into its slot,
+// the lines that end inside the chunk out, the values into the sums.
+template <int MODE, int LG, int KM, int ROWS, int BUDGET, int QP>
+__device__ __forceinline__ void fast_leaves(const FastArgs &a, const uint2 (&lrs)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::TC],
+                                            int tb, double (&acc)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::KMAX],
+                                            IdPack &ids, int cls, const IdOut &io) {
+  using C = FastCfg<MODE, LG, KM, ROWS, BUDGET>;
+  constexpr int TC = C::TC;
+#pragma unroll
+  for (int g = 0; g < TC; ++g) {
+    const int t = tb + g;
+    const uint2 lr = lrs[g];
+    put_id(ids, QP * TC + g, lr.y);
+    if (((QP * TC + g) & 3) == 3 && g < TC - 1 && io.on) {  // lines that end at tree t, within the chunk
+      const int c = (QP * TC + g + 1) & 31;
+      uint32_t m = (uint32_t)(a.id_phase >> (8 * (c >> 2))) & 0xffu;
+      while (m) {
+        const int rho = __builtin_ctz(m);
+        m &= m - 1;
+        id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, rho, t, c, io.t_begin);
+      }
+    }
+    if (t < a.out.T) {
+      const double v = (double)as_float(lr.x);
+      if (C::MULTI && a.vec) {
+        // vector leaves are added by the caller
+      } else if (C::MULTI) {
+        // the column is uniform across the wave: one register-indexed update
+        const int k = __builtin_amdgcn_readlane(cls, g) & (C::KMAX - 1);
+        acc[k] += v;
+      } else {
+        acc[0] += v;
+      }
+    }
+  }
+  // rows not 16-byte aligned: a 32-tree group's ids leave at once, by scalar stores
+  if (QP == C::CPF - 1 && a.leaf_ids && !a.ids_vec)
+    flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, io.r0w, tb - (C::CPF - 1) * TC);
+}
+
 template <int MODE, int LG, int KM, int ROWS, int BUDGET, int B, int Q>
 __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbuf)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
                                            double (&acc)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::KMAX],
                                            IdPack &ids, int &cls, int &dep, float2 (&vh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::VH],
-                                           const IdOut &io) {
+                                           uint2 (&lh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::LH], const IdOut &io) {
   using C = FastCfg<MODE, LG, KM, ROWS, BUDGET>;
   constexpr int TC = C::TC;
   constexpr int TB = C::TB;
@@ -221,15 +267,19 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   if (C::MULTI && !a.vec)
     cls_next = a.tree_class[min((more ? c + 1 : c) * TC + ((int)threadIdx.x & (TC - 1)), a.out.T - 1)];
   const int t0 = c * TC;
-  // the lines that ended with the previous chunk leave now, behind the
-  // prefetch: a wait for the prefetch then never waits for their stores
-  if (((Q * TC) & 3) == 0 && io.on && t0 > io.t_begin) {
-    constexpr int kC = (Q * TC) & 31;
+  // the lines that ended with the previous chunk (with LAG: the one before,
+  // whose ids were taken after this chunk's predecessor's walk) leave now,
+  // behind the prefetch: a wait for the prefetch then never waits for their
+  // stores
+  constexpr int kLag = C::LAG ? 1 : 0;
+  constexpr int kQE = (Q + C::CPF - kLag) % C::CPF;  // the chunk that ended, within its group
+  if (((kQE * TC) & 3) == 0 && io.on && t0 - kLag * TC > io.t_begin) {
+    constexpr int kC = (kQE * TC) & 31;
     uint32_t m = (uint32_t)(a.id_phase >> (8 * (kC >> 2))) & 0xffu;
     while (m) {
       const int rho = __builtin_ctz(m);
       m &= m - 1;
-      id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, rho, t0 - 1, kC, io.t_begin);
+      id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, rho, t0 - kLag * TC - 1, kC, io.t_begin);
     }
   }
   __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the walk
@@ -331,32 +381,17 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
       }
     }
   }
+  if (C::LAG) {
+    // the previous chunk's records (read a walk ago), then hold this chunk's
+    uint2 prev[TC];
 #pragma unroll
-  for (int g = 0; g < TC; ++g) {
-    const int t = t0 + g;
-    const uint2 lr = lrs[g];
-    put_id(ids, Q * TC + g, lr.y);
-    if (((Q * TC + g) & 3) == 3 && g < TC - 1 && io.on) {  // lines that end at tree t, within the chunk
-      const int c = (Q * TC + g + 1) & 31;
-      uint32_t m = (uint32_t)(a.id_phase >> (8 * (c >> 2))) & 0xffu;
-      while (m) {
-        const int rho = __builtin_ctz(m);
-        m &= m - 1;
-        id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, rho, t, c, io.t_begin);
-      }
+    for (int g = 0; g < TC; ++g) {
+      prev[g] = lh[g < C::LH ? g : 0];
+      lh[g < C::LH ? g : 0] = lrs[g];
     }
-    if (t < a.out.T) {
-      const double v = (double)as_float(lr.x);
-      if (C::MULTI && a.vec) {
-        // added above
-      } else if (C::MULTI) {
-        // the column is uniform across the wave: one register-indexed update
-        const int k = __builtin_amdgcn_readlane(cls, g) & (C::KMAX - 1);
-        acc[k] += v;
-      } else {
-        acc[0] += v;
-      }
-    }
+    if (t0 > io.t_begin) fast_leaves<MODE, LG, KM, ROWS, BUDGET, (Q + C::CPF - 1) % C::CPF>(a, prev, t0 - TC, acc, ids, cls, io);
+  } else {
+    fast_leaves<MODE, LG, KM, ROWS, BUDGET, Q>(a, lrs, t0, acc, ids, cls, io);
   }
   cls = cls_next;
   dep = dep_next;
@@ -377,12 +412,12 @@ __device__ __forceinline__ void fast_group(const FastArgs &a, int c0, uint4 (*tb
                                            const float *xs, uint32_t lane4,
                                            double (&acc)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::KMAX],
                                            IdPack &ids, int &cls, int &dep, float2 (&vh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::VH],
-                                           const IdOut &io) {
+                                           uint2 (&lh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::LH], const IdOut &io) {
   using C = FastCfg<MODE, LG, KM, ROWS, BUDGET>;
   if constexpr (Q < C::CPF) {
     fast_chunk<MODE, LG, KM, ROWS, BUDGET, C::BUFS == 2 ? (Q & 1) : 0, Q>(a, c0 + Q, tbuf, xs, lane4, acc, ids,
-                                                                           cls, dep, vh, io);
-    fast_group<MODE, LG, KM, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls, dep, vh, io);
+                                                                           cls, dep, vh, lh, io);
+    fast_group<MODE, LG, KM, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls, dep, vh, lh, io);
   }
 }
 
@@ -431,11 +466,30 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   float2 vh[C::VH];
 #pragma unroll
   for (int g = 0; g < C::VH; ++g) vh[g] = make_float2(0.0f, 0.0f);
-  const int64_t r0w = r0 + (tid & ~63);
+  uint2 lh[C::LH];
+#pragma unroll
+  for (int g = 0; g < C::LH; ++g) lh[g] = make_uint2(0u, 0u);
   const IdOut io = make_id_out<ROWS>(a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], c_begin * C::TC, a.out.T);
   for (int c = c_begin; c < a.n_chunks; c += C::CPF) {  // chunk counts are multiples of CPF
-    fast_group<MODE, LG, KM, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, vh, io);
-    if (a.leaf_ids && !a.ids_vec) flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, r0w, c * C::TC);
+    fast_group<MODE, LG, KM, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, vh, lh, io);
+  }
+  if (C::LAG) {
+    // the lines that ended with the next-to-last chunk, then the last
+    // chunk's leaf ids and sums
+    const int t_last = a.n_chunks * C::TC - C::TC;  // first tree of the last chunk
+    constexpr int kC = ((C::CPF - 1) * C::TC) & 31;
+    if ((kC & 3) == 0 && io.on && t_last > io.t_begin) {
+      uint32_t m = (uint32_t)(a.id_phase >> (8 * (kC >> 2))) & 0xffu;
+      while (m) {
+        const int rho = __builtin_ctz(m);
+        m &= m - 1;
+        id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, rho, t_last - 1, kC, io.t_begin);
+      }
+    }
+    uint2 last[C::TC];
+#pragma unroll
+    for (int g = 0; g < C::TC; ++g) last[g] = lh[g < C::LH ? g : 0];
+    fast_leaves<MODE, LG, KM, ROWS, BUDGET, C::CPF - 1>(a, last, t_last, acc, ids, cls, io);
   }
   if (C::VHOLD && a.vec) {  // the last chunk's 2-vector leaves
 #pragma unroll
