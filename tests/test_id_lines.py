@@ -13,13 +13,15 @@ written exactly once, from the slot that holds that tree at that moment.
 import numpy as np
 import pytest
 
-import numpy as np
+
 def phases(T, b):
+    """Byte k lists the residues r mod 8 whose lines begin at trees 4k mod 32."""
     ph = 0
     for rho in range(8):
         phi = (32 - (b + T * rho) % 32) % 32
         ph |= 1 << (8 * (phi // 4) + rho)
     return ph
+
 
 def run_schedule(T, b, n_rows, TC, split_groups=None, lag=False):
     n_groups = (T + 31) // 32
