@@ -236,8 +236,9 @@ __device__ __forceinline__ void fast_leaves(const FastArgs &a, const uint2 (&lrs
       }
     }
   }
-  // rows not 16-byte aligned: a 32-tree group's ids leave at once, by scalar stores
-  if (QP == C::CPF - 1 && a.leaf_ids && !a.ids_vec)
+  // rows not 16-byte aligned: a 32-tree group's ids leave at once, by scalar
+  // stores (here with LAG, whose groups end one chunk late; else after the group)
+  if (C::LAG && QP == C::CPF - 1 && a.leaf_ids && !a.ids_vec)
     flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, io.r0w, tb - (C::CPF - 1) * TC);
 }
 
@@ -472,6 +473,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   const IdOut io = make_id_out<ROWS>(a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], c_begin * C::TC, a.out.T);
   for (int c = c_begin; c < a.n_chunks; c += C::CPF) {  // chunk counts are multiples of CPF
     fast_group<MODE, LG, KM, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, vh, lh, io);
+    if (!C::LAG && a.leaf_ids && !a.ids_vec) flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, io.r0w, c * C::TC);
   }
   if (C::LAG) {
     // the lines that ended with the next-to-last chunk, then the last
