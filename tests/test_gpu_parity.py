@@ -284,12 +284,13 @@ def test_two_class_scalar_leaves_row_parallel():
     m.update(n_outputs=2, tree_class=(rng.random(90) < 0.5).astype(np.int32), aggregation="sum",
              transform="softmax", base_score=None)
     h = hb.compile(m, device=0)
-    X = np.ascontiguousarray(pins.tricky_rows(rng, m, 70_001))
-    for strategy in ("ptt", "tt"):
-        for ws in (False, True):
-            say("two classes", strategy, ws)
-            scores, ids = run(h, X, strategy, workspace=ws)
-            check(m, X, scores, ids, f"2cls/{strategy}/ws={ws}")
+    for n in (70_001, 65_536):  # 65,536 rows with a workspace: 1024-row workgroups with the tree split
+        X = np.ascontiguousarray(pins.tricky_rows(rng, m, n))
+        for strategy in ("ptt", "tt"):
+            for ws in (False, True):
+                say("two classes", n, strategy, ws)
+                scores, ids = run(h, X, strategy, workspace=ws)
+                check(m, X, scores, ids, f"2cls/{n}/{strategy}/ws={ws}")
 
 
 @pytest.mark.parametrize("missing", [False, True])
