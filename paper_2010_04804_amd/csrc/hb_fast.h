@@ -120,21 +120,14 @@ struct IdOut {
   u32x4 *stage;       // this wave's staging area: 8 rows x 64 bytes
   int64_t r0w;        // first row of the wave
   int t_begin;        // first tree of this workgroup's part
-  // per lane (i = lane / 8: row of a pass, k = lane % 8: block of 4 ids)
-  uint32_t lane_off;  // 8 i T + 4 k: the lane's piece, in ints from the pass's first row and tree
-  int rd;             // 8 k + 16 (i / 2): byte offset of that piece in staged row i, before the rotation
-  int k4;             // 4 k
-  int row8;           // 8 i
 };
 
 template <int ROWS>
-__device__ __forceinline__ IdOut make_id_out(bool on, u32x4 *stage, int t_begin, int T) {
-  const int lane = threadIdx.x & 63;
-  const int i = lane >> 3, k = lane & 7;
+__device__ __forceinline__ IdOut make_id_out(bool on, u32x4 *stage, int t_begin) {
   // the wave's first row is uniform: keep it (and the per-pass row and tree
   // offsets computed from it) in scalar registers
   const int64_t r0w = (int64_t)blockIdx.x * ROWS + 64 * __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  return IdOut{on, stage, r0w, t_begin, (uint32_t)(8 * i) * (uint32_t)T + 4u * k, 8 * k + 16 * (i >> 1), 4 * k, 8 * i};
+  return IdOut{on, stage, r0w, t_begin};
 }
 
 // Writes, for the rows of residue rho in this wave, the ids of trees
@@ -142,7 +135,12 @@ __device__ __forceinline__ IdOut make_id_out(bool on, u32x4 *stage, int t_begin,
 // slot of tree t_end - 31. lo and T are multiples of 4, and so is t_end + 1.
 __device__ __forceinline__ void id_pass(int32_t *leaf_ids, int64_t n_rows, int T, const IdOut &io,
                                         const IdPack &ids, int rho, int t_end, int c, int lo) {
-  if (io.k4 == 4 * rho) {
+  // as a reader, lane (i = lane / 8, k = lane % 8) stores ids 4k .. 4k+3 of
+  // row i of the pass; the per-lane offsets are recomputed here rather than
+  // held in registers across the walk
+  const int lane = threadIdx.x & 63;
+  const int k4 = 4 * (lane & 7), row8 = lane & ~7;  // 4 k, 8 i
+  if (k4 == 4 * rho) {
     // quad j of row i at slot (j + i / 2) mod 4: the eight writers touch distinct banks
     const int i = (threadIdx.x & 63) >> 3;
 #pragma unroll
@@ -150,13 +148,14 @@ __device__ __forceinline__ void id_pass(int32_t *leaf_ids, int64_t n_rows, int T
   }
   __builtin_amdgcn_wave_barrier();
   // ids 2 slot .. of row i sit at byte 2 slot of its staged row, rotated by 16 (i / 2)
-  const uint2 v = *reinterpret_cast<const uint2 *>(reinterpret_cast<const unsigned char *>(io.stage) + 8 * io.row8 +
-                                                   ((2 * c + io.rd) & 63));
+  const int rd = 2 * k4 + (row8 & ~15);  // 8 k + 16 (i / 2)
+  const uint2 v = *reinterpret_cast<const uint2 *>(reinterpret_cast<const unsigned char *>(io.stage) + 8 * row8 +
+                                                   ((2 * c + rd) & 63));
   const int64_t row0 = io.r0w + rho;
   const int rem = (int)min(n_rows - row0, (int64_t)64);
   const int tb = t_end - 31;
-  if (io.row8 < rem && io.k4 >= lo - tb && io.k4 < T - tb) {
-    int32_t *dst = leaf_ids + (row0 * T + tb) + io.lane_off;
+  if (row8 < rem && k4 >= lo - tb && k4 < T - tb) {
+    int32_t *dst = leaf_ids + (row0 * T + tb) + ((uint32_t)row8 * (uint32_t)T + (uint32_t)k4);
     const i32x4 o{(int)(v.x & 0xffffu), (int)(v.x >> 16), (int)(v.y & 0xffffu), (int)(v.y >> 16)};
     // streaming: whole lines need no merging in L2, and allocating them
     // there would evict the blocks other workgroups are about to stage
@@ -470,7 +469,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   uint2 lh[C::LH];
 #pragma unroll
   for (int g = 0; g < C::LH; ++g) lh[g] = make_uint2(0u, 0u);
-  const IdOut io = make_id_out<ROWS>(a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], c_begin * C::TC, a.out.T);
+  const IdOut io = make_id_out<ROWS>(a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], c_begin * C::TC);
   for (int c = c_begin; c < a.n_chunks; c += C::CPF) {  // chunk counts are multiples of CPF
     fast_group<MODE, LG, KM, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, vh, lh, io);
     if (!C::LAG && a.leaf_ids && !a.ids_vec) flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, io.r0w, c * C::TC);
