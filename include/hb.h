@@ -67,6 +67,8 @@ enum hb_transform { HB_POST_NONE = 0, HB_POST_SIGMOID = 1, HB_POST_SOFTMAX = 2 }
 #define HB_TT_MAX_NODES 65535      /* nodes per tree for TT (16-bit ids)    */
 #define HB_MAX_FEATURES 65535      /* features (16-bit ids in TT records)   */
 #define HB_GEMM_MAX_LEAVES 256     /* leaves per tree for GEMM              */
+#define HB_MAX_TREES (1 << 24)     /* n_trees (kernels index eight rows of
+                                      leaf ids with 32-bit offsets)          */
 
 /*
  * The ensemble, in host memory, owned by the caller and only read (copied)
@@ -75,7 +77,7 @@ enum hb_transform { HB_POST_NONE = 0, HB_POST_SIGMOID = 1, HB_POST_SOFTMAX = 2 }
  * and local node 0 is the root. A node is a leaf iff feature < 0.
  */
 typedef struct hb_ensemble_desc {
-  int32_t n_trees;                 /* >= 1                                   */
+  int32_t n_trees;                 /* 1 .. HB_MAX_TREES                      */
   int32_t n_features;              /* >= 1, columns of X                     */
   int32_t n_outputs;               /* K: 1 .. HB_MAX_OUTPUTS                 */
   int32_t leaf_dim;                /* 1 (scalar leaves) or n_outputs         */

@@ -508,7 +508,8 @@ void release(hb_handle *h) {
 
 int validate_desc(const hb_ensemble_desc *d) {
   if (!d) return fail(HB_ERR_INVALID_ARG, "desc is NULL");
-  if (d->n_trees < 1) return fail(HB_ERR_INVALID_ARG, "n_trees must be >= 1");
+  if (d->n_trees < 1 || d->n_trees > HB_MAX_TREES)
+    return fail(HB_ERR_INVALID_ARG, "n_trees must be in [1, " + std::to_string(HB_MAX_TREES) + "]");
   if (d->n_features < 1) return fail(HB_ERR_INVALID_ARG, "n_features must be >= 1");
   if (d->n_outputs < 1 || d->n_outputs > HB_MAX_OUTPUTS)
     return fail(HB_ERR_INVALID_ARG, "n_outputs must be in [1, " + std::to_string(HB_MAX_OUTPUTS) + "]");

@@ -72,6 +72,9 @@ def test_invalid_models_are_rejected():
     _expect(bad_ld, -1, "leaf_dim")
     too_many = dict(pins.model_from_trees([[(-1, 0, -1, -1, 1.0)]], 1), n_outputs=17)
     _expect(too_many, -1, "n_outputs")
+    # rejected before any per-tree array is read
+    too_many_trees = dict(pins.model_from_trees([[(-1, 0, -1, -1, 1.0)]], 1), n_trees=(1 << 24) + 1)
+    _expect(too_many_trees, -1, "n_trees")
 
 
 def test_forced_infeasible_strategy_is_unsupported():
