@@ -27,32 +27,14 @@ sys.path.insert(0, ROOT)
 METRIC = "rows/sec scored, 500-tree depth-8 ensemble, 1M rows; % HBM / MFMA peak"
 HBM_PEAK = 8.0e12   # B/s, MI355X HBM3E
 INT8_PEAK = 5.0e15  # dense int8 MFMA ops/s, MI355X
-KERNEL = {"ptt": "fast_kernel<0, D, ...> (PerfectTreeTraversal)",
-          "tt": "fast_kernel<1, lg, ...> (TreeTraversal)",
-          "gemm": "gemm_kernel<KB, ...> (GEMM, int8 MFMA)"}
-LANES = "lanes_kernel<...> (trees across lanes, {})"
-GENERAL = "traverse_kernel<...> (general, {})"
 
 
-def kernel_label(strat, n, info, workspace=True):
-    """The kernel a call of n rows runs, for the bench line's label: the
-    launcher's routing by batch size and row width, restated (the trees-across-
-    lanes kernel up to 1,024 rows with a workspace, 12,288 (PTT) or 16,384 (TT)
-    without, and for rows too wide for the row-parallel LDS tile)."""
-    if strat == "gemm":
-        return KERNEL["gemm"]
-    name = "PerfectTreeTraversal" if strat == "ptt" else "TreeTraversal"
-    if n <= (1024 if workspace else 12288 if strat == "ptt" else 16384):
-        return LANES.format(name)
-    cols = info["n_used_features"]
-    fast = strat == "tt" or info["ptt_depth"] <= 10
-    if fast and cols * 128 * 4 + 34 * 1024 <= 160 * 1024:
-        return KERNEL[strat]
-    xtile = cols * 257 * 4
-    per_tree = info["table_bytes"][strat] / max(1, info["n_trees"])
-    if xtile > 120 * 1024 or xtile + per_tree > 160 * 1024:
-        return LANES.format(name)
-    return GENERAL.format(name)
+def kernel_label(h, strat, n, ws_bytes=0):
+    """The kernels a call of n rows launches, as the library's own launch
+    plan reports them (hb_plan): "name grid=(x,y) block=b" per launch."""
+    return "; ".join(f"{p['kernel']} grid={p['grid']} block={p['block']}" for p in h.plan(n, strat, ws_bytes))
+
+
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2010_04804_amd", "csrc")
 
@@ -431,12 +413,12 @@ def main():
             achieved = ops / (ms * 1e-3)
             return {"bound": "mfma", "achieved": achieved / 1e12, "peak": INT8_PEAK / 1e12,
                     "unit": "TOP/s", "frac": achieved / INT8_PEAK, "traffic": None,
-                    "kernel": kernel_label(strat, n, info, workspace=False), "avg_launch_ms": ms, "ops_per_launch": ops}
+                    "kernel": kernel_label(h, strat, n), "avg_launch_ms": ms, "ops_per_launch": ops}
         b = algorithmic_bytes(info, n, leaves, strat)
         achieved = b / (ms * 1e-3)
         return {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
                 "frac": achieved / HBM_PEAK, "traffic": recorded_traffic(cfg, strat, n, leaves),
-                "kernel": kernel_label(strat, n, info, workspace=False), "avg_launch_ms": ms, "bytes_per_launch": b}
+                "kernel": kernel_label(h, strat, n), "avg_launch_ms": ms, "bytes_per_launch": b}
 
     print(f"[bench] config {cfg}: {n} rows, strategy {strategy}, leaf ids {leaves}", flush=True)
     t_wall = time.perf_counter()

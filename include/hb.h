@@ -32,6 +32,10 @@
 
 #include <stdint.h>
 
+/* The library is built with hidden visibility; only these entry points are
+ * exported. */
+#define HB_API __attribute__((visibility("default")))
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -137,7 +141,7 @@ typedef struct hb_info {
  * forced hint that is infeasible returns HB_ERR_UNSUPPORTED.
  * On success *out owns all device memory; release it with hb_destroy.
  */
-int hb_compile(const hb_ensemble_desc *desc, int strategy_hint, int device, hb_handle **out);
+HB_API int hb_compile(const hb_ensemble_desc *desc, int strategy_hint, int device, hb_handle **out);
 
 /*
  * Score n_rows rows. X, scores and leaf_ids are device pointers on the
@@ -155,7 +159,7 @@ int hb_compile(const hb_ensemble_desc *desc, int strategy_hint, int device, hb_h
  * HB_OK and enqueues nothing. Concurrent calls on one handle are allowed:
  * the compiled tensors are read only and no scratch memory is shared.
  */
-int hb_predict(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
+HB_API int hb_predict(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
                int strategy, void *stream);
 
 /*
@@ -172,22 +176,35 @@ int hb_predict(hb_handle *h, const float *X, int64_t n_rows, float *scores, int3
  * HB_ERR_INVALID_ARG for workspace_bytes < 0, a NULL workspace with
  * workspace_bytes > 0, or a misaligned workspace.
  */
-int hb_predict_ws(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
+HB_API int hb_predict_ws(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
                   int strategy, void *stream, void *workspace, int64_t workspace_bytes);
 
 /* Workspace bytes that let hb_predict_ws split the trees of a batch of
  * n_rows rows under `strategy` (AUTO: the selector's choice); 0 when that
- * batch never splits. A negative value is an error code. */
-int64_t hb_workspace_bytes(const hb_handle *h, int64_t n_rows, int strategy);
+ * batch never splits. A negative value is an error code. The split serves
+ * the small batches of request-response serving, for which the paper
+ * measures latency per batch size (Sec. 6, batch-size and request-response
+ * experiments); the paper's own kernels have no such scratch. */
+HB_API int64_t hb_workspace_bytes(const hb_handle *h, int64_t n_rows, int strategy);
 
-/* The strategy hb_predict would run for this batch size under AUTO. */
-int hb_select_strategy(const hb_handle *h, int64_t n_rows);
+/* The strategy hb_predict would run for this batch size under AUTO: the
+ * selector of Sec. 5.1 ("Execution Strategy Selection"), which picks among
+ * GEMM, TreeTraversal and PerfectTreeTraversal by tree depth and batch
+ * size, with thresholds re-measured on this device. Returns the enum value,
+ * or a negative error code for a NULL handle. */
+HB_API int hb_select_strategy(const hb_handle *h, int64_t n_rows);
 
-/* Shape statistics, feasibility and table sizes of a compiled handle. */
-int hb_query(const hb_handle *h, hb_info *info);
+/* Shape statistics, feasibility and table sizes of a compiled handle: the
+ * quantities Table 4 states the strategies' costs in (trees, depth, internal
+ * and leaf node counts, the perfect-tree padding that PTT's O(2^D) memory
+ * implies) and the bytes each strategy's tensors take. Returns HB_OK or
+ * HB_ERR_INVALID_ARG for a NULL argument. */
+HB_API int hb_query(const hb_handle *h, hb_info *info);
 
 /*
- * Host copy of one compiled tensor, for inspection and testing: *data points
+ * Host copy of one compiled tensor (the tensors of Table 3 for GEMM, Table 5
+ * for TT and Table 6 for PTT, in the layouts below), for inspection and
+ * testing: *data points
  * into memory owned by the handle (valid until hb_destroy), *bytes is its
  * size. Names per strategy:
  *   PTT : "node" (uint32 pairs {threshold bits, feature} per tree, max(2^D, 2)
@@ -216,13 +233,26 @@ int hb_query(const hb_handle *h, hb_info *info);
  *         hold these indices instead of input columns)
  * Returns HB_ERR_INVALID_ARG for an unknown name or an infeasible strategy.
  */
-int hb_table(const hb_handle *h, int strategy, const char *name, const void **data, int64_t *bytes);
+HB_API int hb_table(const hb_handle *h, int strategy, const char *name, const void **data, int64_t *bytes);
+
+/*
+ * Dry run of hb_predict_ws: writes into buf (NUL-terminated, at most
+ * buf_bytes bytes including the NUL) the kernels a call with this batch size,
+ * strategy and workspace size would launch, in launch order, separated by
+ * "; ", each as "name grid=(x,y) block=b lds=bytes" with name the kernel
+ * template instantiation as a profiler prints it. Launches nothing and needs
+ * no buffers; the handle must be a device handle. Errors: those of
+ * hb_predict_ws, HB_ERR_INVALID_ARG for a NULL or too small buf. This
+ * reports the launch plan behind the selector of Sec. 5.1.
+ */
+HB_API int hb_plan(const hb_handle *h, int64_t n_rows, int strategy, int64_t workspace_bytes, char *buf,
+                   int64_t buf_bytes);
 
 /* Synchronise the handle's device and free everything it owns. NULL is a no-op. */
-void hb_destroy(hb_handle *h);
+HB_API void hb_destroy(hb_handle *h);
 
 /* Message for the last non-zero return on this thread ("" if none). */
-const char *hb_last_error(void);
+HB_API const char *hb_last_error(void);
 
 #ifdef __cplusplus
 }

@@ -3,7 +3,7 @@
 This module only marshals arguments into the C-ABI declared in
 ``include/hb.h`` (``hb_compile``, ``hb_predict``, ``hb_predict_ws``,
 ``hb_workspace_bytes``, ``hb_query``, ``hb_table``, ``hb_select_strategy``,
-``hb_destroy``, ``hb_last_error``). Every step of
+``hb_plan``, ``hb_destroy``, ``hb_last_error``). Every step of
 scoring runs in the library's HIP kernels; PyTorch only supplies device
 memory and the current stream. If ``libhb.so`` has not been built, importing
 works but every call raises.
@@ -89,6 +89,8 @@ def load_library(path: str = LIB_PATH):
     lib.hb_table.restype = ctypes.c_int
     lib.hb_table.argtypes = [_P, ctypes.c_int, ctypes.c_char_p, ctypes.POINTER(_P),
                              ctypes.POINTER(ctypes.c_int64)]
+    lib.hb_plan.restype = ctypes.c_int
+    lib.hb_plan.argtypes = [_P, ctypes.c_int64, ctypes.c_int, ctypes.c_int64, ctypes.c_char_p, ctypes.c_int64]
     lib.hb_destroy.restype = None
     lib.hb_destroy.argtypes = [_P]
     lib.hb_last_error.restype = ctypes.c_char_p
@@ -133,6 +135,21 @@ class Handle:
         if rc < 0:
             _check(rc)
         return STRATEGY_NAME[rc]
+
+    def plan(self, n_rows: int, strategy="auto", workspace_bytes: int = 0) -> list:
+        """The kernels hb_predict_ws would launch for this batch (hb_plan):
+        one dict per launch with the kernel's template name, grid, block and
+        dynamic LDS bytes."""
+        buf = ctypes.create_string_buffer(4096)
+        _check(load_library().hb_plan(self.ptr, int(n_rows), _strategy(strategy), int(workspace_bytes), buf, 4096))
+        out = []
+        for part in filter(None, buf.value.decode().split("; ")):
+            name, rest = part.split(" grid=(")
+            grid, rest = rest.split(") block=")
+            block, lds = rest.split(" lds=")
+            out.append({"kernel": name, "grid": tuple(int(g) for g in grid.split(",")), "block": int(block),
+                        "lds": int(lds)})
+        return out
 
     def table(self, strategy, name: str, dtype) -> np.ndarray:
         """A copy of one compiled tensor (see hb_table in include/hb.h)."""
@@ -231,14 +248,35 @@ def predict(h: Handle, X, strategy="auto", leaves: bool = True, out=None, stream
         ids = torch.empty((n, info["n_trees"]), dtype=torch.int32, device=X.device) if leaves else None
     else:
         scores, ids = out
-    current = torch.cuda.current_stream(X.device).cuda_stream
+        _check_out(scores, (n, info["n_outputs"]), torch.float32, X.device, "scores")
+        if ids is not None:
+            _check_out(ids, (n, info["n_trees"]), torch.int32, X.device, "leaf ids")
+    current = torch.cuda.current_stream(X.device)
+    ext = None
     if stream is None:
-        stream = current
+        stream = current.cuda_stream
+    elif stream != current.cuda_stream:
+        # X's copy and the output allocations were enqueued on the current
+        # stream: the kernel on `stream` waits for them
+        ext = torch.cuda.ExternalStream(stream, device=X.device)
+        ext.wait_stream(current)
     nws = workspace_bytes(h, n, strategy) if workspace else 0
     ws = torch.empty(nws, dtype=torch.uint8, device=X.device) if nws else None
     predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), ids.data_ptr() if ids is not None else None,
                 strategy, stream, ws.data_ptr() if ws is not None else None, nws)
-    if ws is not None and stream != current:
-        # torch's allocator must not reuse the workspace before `stream` is done with it.
-        ws.record_stream(torch.cuda.ExternalStream(stream, device=X.device))
+    if ext is not None:
+        # torch's allocator must not reuse these buffers before `stream` is done with them
+        for t in (X, scores, ids, ws):
+            if t is not None:
+                t.record_stream(ext)
     return scores, ids
+
+
+def _check_out(t, shape, dtype, device, what):
+    """An out= buffer must be exactly what the kernels write: no bigger check
+    is possible past this point, and a smaller buffer would be overrun."""
+    import torch
+
+    if not isinstance(t, torch.Tensor) or t.dtype != dtype or tuple(t.shape) != tuple(shape) \
+            or t.device != device or not t.is_contiguous():
+        raise ValueError(f"out {what} must be a contiguous {dtype} tensor of shape {tuple(shape)} on {device}")

@@ -18,8 +18,11 @@ SOURCES = ["hb_api.cpp", "hb_kernels.hip", "hb_gemm.hip", "hb_fast_ptt_128.hip",
 
 # -packed-fp32-ops: no packed fp32 instructions in device code (the host pass
 # warns that it does not know the feature; that is harmless).
-DEVICE_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
+# -fvisibility=hidden: the library exports only the C-ABI of include/hb.h
+# (declared with HB_API), none of its C++ internals.
+DEVICE_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
                 "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+LINK_FLAGS = ["-fvisibility=hidden", "-Wl,--version-script=" + os.path.join(CSRC, "libhb.map")]
 
 
 def build(verbose: bool = False) -> str:
@@ -44,7 +47,7 @@ def build(verbose: bool = False) -> str:
     if failed:
         raise RuntimeError("hipcc failed building libhb.so")
     tmp = LIB + ".tmp"
-    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *LINK_FLAGS, "-o", tmp, *objs]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)

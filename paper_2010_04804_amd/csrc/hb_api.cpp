@@ -785,8 +785,13 @@ int hb_predict(hb_handle *h, const float *X, int64_t n_rows, float *scores, int3
   return hb_predict_ws(h, X, n_rows, scores, leaf_ids, strategy, stream, nullptr, 0);
 }
 
-int hb_predict_ws(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
-                  int strategy, void *stream, void *workspace, int64_t workspace_bytes) {
+}  // extern "C"
+
+namespace {
+
+// hb_predict_ws, or with `plan` a dry run that describes the launches instead.
+int predict_impl(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids, int strategy,
+                 void *stream, void *workspace, int64_t workspace_bytes, std::string *plan) {
   if (!h) return fail(HB_ERR_INVALID_ARG, "handle is NULL");
   if (workspace_bytes < 0 || (workspace_bytes > 0 && !workspace))
     return fail(HB_ERR_INVALID_ARG, "workspace_bytes > 0 needs a workspace");
@@ -798,7 +803,7 @@ int hb_predict_ws(hb_handle *h, const float *X, int64_t n_rows, float *scores, i
   if (strategy == HB_STRATEGY_AUTO) strategy = hb_select_strategy(h, n_rows);
   if (!h->info.feasible[strategy]) return fail(HB_ERR_UNSUPPORTED, "strategy infeasible for this ensemble");
   if (n_rows == 0) return HB_OK;
-  if (!X || !scores) return fail(HB_ERR_INVALID_ARG, "X or scores is NULL");
+  if (!plan && (!X || !scores)) return fail(HB_ERR_INVALID_ARG, "X or scores is NULL");
   if (n_rows > (int64_t)std::numeric_limits<int32_t>::max())
     return fail(HB_ERR_INVALID_ARG, "n_rows above 2^31 - 1");
   int prev = -1;
@@ -807,24 +812,49 @@ int hb_predict_ws(hb_handle *h, const float *X, int64_t n_rows, float *scores, i
   std::string err;
   int rc = HB_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hb::Workspace ws;
+  hb::Launch ws;
   if (workspace && workspace_bytes > 0) {
     ws.ptr = workspace;
     ws.bytes = workspace_bytes;
   }
+  ws.plan = plan;
   try {
     if (strategy == HB_STRATEGY_PTT)
       rc = hb::launch_ptt(h->ens, h->ptt, X, n_rows, scores, leaf_ids, ws, s, &err);
     else if (strategy == HB_STRATEGY_TT)
       rc = hb::launch_tt(h->ens, h->tt, X, n_rows, scores, leaf_ids, ws, s, &err);
     else
-      rc = hb::launch_gemm(h->ens, h->gemm, X, n_rows, scores, leaf_ids, s, &err);
+      rc = hb::launch_gemm(h->ens, h->gemm, X, n_rows, scores, leaf_ids, ws, s, &err);
   } catch (...) {
     rc = HB_ERR_HIP;
     err = "unexpected exception in hb_predict";
   }
   if (prev >= 0 && prev != h->device) (void)hipSetDevice(prev);
   if (rc) return fail(rc, err);
+  return HB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int hb_predict_ws(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
+                  int strategy, void *stream, void *workspace, int64_t workspace_bytes) {
+  return predict_impl(h, X, n_rows, scores, leaf_ids, strategy, stream, workspace, workspace_bytes, nullptr);
+}
+
+int hb_plan(const hb_handle *h, int64_t n_rows, int strategy, int64_t workspace_bytes, char *buf, int64_t buf_bytes) {
+  if (!buf || buf_bytes < 1) return fail(HB_ERR_INVALID_ARG, "buf is NULL or empty");
+  buf[0] = '\0';
+  if (workspace_bytes < 0) return fail(HB_ERR_INVALID_ARG, "workspace_bytes < 0");
+  std::string plan;
+  // the dry run reads the workspace pointer only to test it for NULL and alignment
+  void *ws = workspace_bytes > 0 ? reinterpret_cast<void *>(uintptr_t(256)) : nullptr;
+  const int rc = predict_impl(const_cast<hb_handle *>(h), nullptr, n_rows, nullptr, nullptr, strategy, nullptr, ws,
+                              workspace_bytes, &plan);
+  if (rc) return rc;
+  if ((int64_t)plan.size() >= buf_bytes) return fail(HB_ERR_INVALID_ARG, "buf too small for the plan");
+  std::memcpy(buf, plan.c_str(), plan.size() + 1);
   return HB_OK;
 }
 

@@ -732,7 +732,7 @@ GemmFn pick_gemm(bool ct, bool xl, int kmode, int rows, bool cols) {
 }  // namespace
 
 int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t n_rows, float *scores,
-                int32_t *leaf_ids, hipStream_t stream, std::string *err) {
+                int32_t *leaf_ids, const Launch &L, hipStream_t stream, std::string *err) {
   if (!t.node || !t.shape || !t.ct || !t.bias || !t.leaf_value || !t.leaf_id) {
     *err = "GEMM tables missing";
     return HB_ERR_INVALID_ARG;
@@ -769,17 +769,23 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
               : kb == 3 ? pick_gemm<3>(ct, xl, kmode, rows, cols)
                         : pick_gemm<4>(ct, xl, kmode, rows, cols);
   int threads = rows;
+  std::string name = "gemm_kernel<" + std::to_string(kb) + ", " + (ct ? "true" : "false") + ", " +
+                     (xl ? "true" : "false") + ", " + std::to_string(kmode) + ", " + std::to_string(rows) + ", " +
+                     (cols && !xl ? "true" : "false") + ">";
   bool piped = false;
-  if (ct && xl && kb == 4 && t.l_pad == 256) {  // the software-pipelined kernel needs no node chunks
+  if (rows == 512 && ct && xl && kb == 4 && t.l_pad == 256) {
+    // the software-pipelined kernel needs no node chunks; it runs only with
+    // 512-row workgroups (two waves per SIMD), since wherever a 256-row
+    // pipelined workgroup would fit, the 16-row tiles below fit too
     const size_t need = x_bytes(rows) + ct_bytes;
     if (need + stage_bytes(rows) <= (size_t)lds_max) {
-      fn = rows == 512 ? (kmode == 0 ? gemm_pipe_kernel<0, 512> : kmode == 1 ? gemm_pipe_kernel<1, 512> : gemm_pipe_kernel<2, 512>)
-                       : (kmode == 0 ? gemm_pipe_kernel<0, 256> : kmode == 1 ? gemm_pipe_kernel<1, 256> : gemm_pipe_kernel<2, 256>);
+      fn = kmode == 0 ? gemm_pipe_kernel<0, 512> : kmode == 1 ? gemm_pipe_kernel<1, 512> : gemm_pipe_kernel<2, 512>;
+      name = "gemm_pipe_kernel<" + std::to_string(kmode) + ", 512>";
       dyn = need;
       piped = true;
     }
   }
-  if (!(piped && rows == 512) && t.n_shapes == 1 && kb == 4 && t.l_pad == 256) {
+  if (!piped && t.n_shapes == 1 && kb == 4 && t.l_pad == 256) {
     // 16-row tiles with C^T in registers, unless the pipelined kernel gets
     // 512-row workgroups (two waves per SIMD): wide rows, where its feature
     // tile does not fit, and 256-row workgroups, one wave per SIMD (measured:
@@ -795,6 +801,7 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
       dyn = tile_dyn;
       rows = kTileRows;
       threads = 256;
+      name = "gemm_tile_kernel<" + std::to_string(kmode) + ", " + (wide ? "true" : "false") + ">";
     }
   }
   if (!fn) {
@@ -820,13 +827,17 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
   a.k_pad = t.k_pad;
   a.l_pad = t.l_pad;
   a.ids_vec = (e.n_trees % 4 == 0) && ((reinterpret_cast<uintptr_t>(leaf_ids) & 15) == 0);
+  const int64_t blocks = (n_rows + rows - 1) / rows;
+  if (L.plan) {
+    plan_line(L.plan, name, blocks, 1, threads, dyn);
+    return HB_OK;
+  }
   hipError_t rc = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
   if (rc != hipSuccess) {
     *err = std::string("hipFuncSetAttribute: ") + hipGetErrorString(rc);
     return HB_ERR_HIP;
   }
-  const int64_t blocks = (n_rows + rows - 1) / rows;
   hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(threads), dyn, stream, a);
   rc = hipGetLastError();
   if (rc != hipSuccess) {

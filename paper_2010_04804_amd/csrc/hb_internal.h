@@ -161,10 +161,14 @@ struct GemmDev {
   int32_t k_pad, l_pad, n_shapes;
 };
 
-// Caller-provided device scratch for the tree split of small batches.
-struct Workspace {
+// How a launcher is called: the caller-provided device scratch for the tree
+// split of small batches, and, for a dry run, a string that receives a
+// description of the kernels the call would launch (name as the compiler
+// prints the instantiation, grid, block, dynamic LDS) instead of launching.
+struct Launch {
   void *ptr = nullptr;
   int64_t bytes = 0;
+  std::string *plan = nullptr;
 };
 
 // Tree split: batches up to kSplitMaxRows rows may have their trees divided
@@ -183,10 +187,17 @@ inline int64_t split_workspace_bytes(int64_t n_rows, int32_t n_trees, int32_t n_
 // assume, enqueues on `stream`, and returns HB_OK or an error code with a
 // message in *err.
 int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_rows,
-               float *scores, int32_t *leaf_ids, const Workspace &ws, hipStream_t stream, std::string *err);
+               float *scores, int32_t *leaf_ids, const Launch &ws, hipStream_t stream, std::string *err);
 int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_rows,
-              float *scores, int32_t *leaf_ids, const Workspace &ws, hipStream_t stream, std::string *err);
+              float *scores, int32_t *leaf_ids, const Launch &ws, hipStream_t stream, std::string *err);
 int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t n_rows,
-                float *scores, int32_t *leaf_ids, hipStream_t stream, std::string *err);
+                float *scores, int32_t *leaf_ids, const Launch &ws, hipStream_t stream, std::string *err);
+
+// One line of a dry run's plan: "name grid=(x,y) block=b lds=bytes".
+inline void plan_line(std::string *plan, const std::string &name, int64_t gx, int64_t gy, int block, size_t lds) {
+  if (!plan->empty()) *plan += "; ";
+  *plan += name + " grid=(" + std::to_string(gx) + "," + std::to_string(gy) + ") block=" + std::to_string(block) +
+           " lds=" + std::to_string(lds);
+}
 
 }  // namespace hb

@@ -237,7 +237,9 @@ int traverse_plan(const TravArgs &a, int lds_max, bool *x_lds) {
   return 0;
 }
 
-int launch_traverse(bool perfect, TravArgs a, hipStream_t stream, std::string *err) {
+const char *tf(bool b) { return b ? "true" : "false"; }
+
+int launch_traverse(bool perfect, TravArgs a, const Launch &L, hipStream_t stream, std::string *err) {
   if (a.n_rows <= 0) return HB_OK;
   const int lds_max = max_dynamic_lds(err);
   if (lds_max <= 0) return HB_ERR_HIP;
@@ -258,13 +260,21 @@ int launch_traverse(bool perfect, TravArgs a, hipStream_t stream, std::string *e
                                  : cols ? pick_k<true, false, true>(kmax, vec) : pick_k<true, false>(kmax, vec))
                         : (x_lds ? pick_k<false, true>(kmax, vec)
                                  : cols ? pick_k<false, false, true>(kmax, vec) : pick_k<false, false>(kmax, vec));
+  const int64_t blocks = (a.n_rows + kRows - 1) / kRows;
+  if (L.plan) {
+    const int km = vec ? (kmax <= 2 ? 2 : kmax <= 8 ? 8 : 16) : kmax;
+    plan_line(L.plan,
+              std::string("traverse_kernel<") + tf(perfect) + ", " + tf(x_lds) + ", " + std::to_string(km) + ", " +
+                  tf(vec) + ", " + tf(!x_lds && cols) + ">",
+              blocks, 1, kRows, lds);
+    return HB_OK;
+  }
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) {
     *err = std::string("hipFuncSetAttribute: ") + hipGetErrorString(e);
     return HB_ERR_HIP;
   }
-  const int64_t blocks = (a.n_rows + kRows - 1) / kRows;
   hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kRows), lds, stream, a);
   e = hipGetLastError();
   if (e != hipSuccess) {
@@ -486,7 +496,7 @@ __global__ __launch_bounds__(64 * J) void split_finish_kernel(const double *part
 // strategy's leaf-value table), or nullptr for scalar leaves.
 int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int chunks, const int32_t *depth,
                 const float *vec, int vec_stride, const EnsembleDev &e, const float *X, int64_t n_rows,
-                float *scores, int32_t *leaf_ids, const Workspace &ws, hipStream_t stream, std::string *err) {
+                float *scores, int32_t *leaf_ids, const Launch &ws, hipStream_t stream, std::string *err) {
   if (!blocks || (mode == 2 && !leaf) || lg < 1 || lg > kFastMaxLg) return kNotApplicable;
   if (e.leaf_dim != 1 && (!vec || e.leaf_dim != e.n_outputs || e.leaf_dim > HB_MAX_OUTPUTS)) return kNotApplicable;
   const int lds_max = max_dynamic_lds(err);
@@ -580,12 +590,6 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int ch
       a.id_phase |= (uint64_t)1 << (8 * (phi / 4) + rho);
     }
   }
-  hipError_t rc = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
-                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)xbytes);
-  if (rc != hipSuccess) {
-    *err = std::string("hipFuncSetAttribute: ") + hipGetErrorString(rc);
-    return HB_ERR_HIP;
-  }
   const int64_t blocks_n = (n_rows + rows - 1) / rows;
   // Small batch with a workspace: divide the 32-tree groups among `parts`
   // workgroups per row tile. With `resident` workgroups of this shape running
@@ -625,12 +629,31 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int ch
       a.partial = static_cast<double *>(ws.ptr);
     }
   }
+  const unsigned fin_rows = (unsigned)((n_rows + 63) / 64);
+  if (ws.plan) {
+    plan_line(ws.plan,
+              "fast_kernel<" + std::to_string(mode) + ", " + std::to_string(lg) + ", " + std::to_string(km) + ", " +
+                  std::to_string(rows) + ", " + std::to_string(shapes[best].budget) + ">",
+              blocks_n, split, rows, xbytes);
+    if (split > 1) {
+      if (km > 1)
+        plan_line(ws.plan, "split_finish_kernel<16, 8>", fin_rows, 1, 64 * 8, (size_t)8 * e.n_outputs * 64 * 8);
+      else
+        plan_line(ws.plan, "split_finish_kernel<1, 16>", fin_rows, 1, 64 * 16, (size_t)16 * 64 * 8);
+    }
+    return HB_OK;
+  }
+  hipError_t rc = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)xbytes);
+  if (rc != hipSuccess) {
+    *err = std::string("hipFuncSetAttribute: ") + hipGetErrorString(rc);
+    return HB_ERR_HIP;
+  }
   hipLaunchKernelGGL(fn, dim3((unsigned)blocks_n, (unsigned)split), dim3(rows), xbytes, stream, a);
   rc = hipGetLastError();
   if (rc == hipSuccess && split > 1) {
     // 16 waves per 64 rows for scalar outputs, 8 for several (their sums
     // take K times the LDS: at most 64 KiB)
-    const unsigned fin_rows = (unsigned)((n_rows + 63) / 64);
     if (km > 1)
       hipLaunchKernelGGL((split_finish_kernel<HB_MAX_OUTPUTS, 8>), dim3(fin_rows), dim3(64 * 8),
                          (size_t)8 * e.n_outputs * 64 * sizeof(double), stream, a.partial, split, n_rows, a.out);
@@ -658,7 +681,7 @@ bool rows_too_wide(const TravArgs &a, std::string *err) {
 
 // Launches lanes_kernel; returns kNotApplicable if R rows of the input do not
 // fit in LDS.
-int launch_lanes(bool perfect, const TravArgs &a, hipStream_t stream, std::string *err) {
+int launch_lanes(bool perfect, const TravArgs &a, const Launch &L, hipStream_t stream, std::string *err) {
   const int lds_max = max_dynamic_lds(err);
   if (lds_max <= 0) return HB_ERR_HIP;
   const bool vec = a.LD > 1;
@@ -672,13 +695,21 @@ int launch_lanes(bool perfect, const TravArgs &a, hipStream_t stream, std::strin
   LanesFn fn = perfect ? (R == 4 ? pick_lanes_r<true, 4>(kmax, vec) : pick_lanes_r<true, 1>(kmax, vec))
                        : (R == 4 ? pick_lanes_r<false, 4>(kmax, vec) : pick_lanes_r<false, 1>(kmax, vec));
   const size_t lds = need(R);
+  const int64_t blocks = (a.n_rows + R - 1) / R;
+  if (L.plan) {
+    const int km = vec ? (kmax <= 2 ? 2 : kmax <= 8 ? 8 : 16) : kmax;
+    plan_line(L.plan,
+              std::string("lanes_kernel<") + tf(perfect) + ", " + std::to_string(km) + ", " + tf(vec) + ", " +
+                  std::to_string(R) + ">",
+              blocks, 1, kLaneThreads, lds);
+    return HB_OK;
+  }
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) {
     *err = std::string("hipFuncSetAttribute: ") + hipGetErrorString(e);
     return HB_ERR_HIP;
   }
-  const int64_t blocks = (a.n_rows + R - 1) / R;
   hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kLaneThreads), lds, stream, a);
   e = hipGetLastError();
   if (e != hipSuccess) {
@@ -710,7 +741,7 @@ TravArgs common_args(const EnsembleDev &e, const float *X, int64_t n, float *sco
 }  // namespace
 
 int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_rows, float *scores,
-               int32_t *leaf_ids, const Workspace &ws, hipStream_t stream, std::string *err) {
+               int32_t *leaf_ids, const Launch &ws, hipStream_t stream, std::string *err) {
   if (!t.node || !t.node_il || !t.leaf_pk || !t.leaf_value || !t.leaf_id || t.depth < 0 || t.depth > HB_PTT_MAX_DEPTH) {
     *err = "PTT tables missing";
     return HB_ERR_INVALID_ARG;
@@ -728,17 +759,17 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
   a.leaf_slots = 1 << t.depth;
   if (a.slots < 2) a.slots = 2;  // depth 0 still stores two (unused) records per tree
   int rc = kNotApplicable;
-  if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsPtt)) rc = launch_lanes(true, a, stream, err);
+  if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsPtt)) rc = launch_lanes(true, a, ws, stream, err);
   if (rc == kNotApplicable)
     rc = launch_fast(0, t.depth, t.fast, nullptr, t.fast_chunks, nullptr, t.leaf_value, 1 << t.depth, e, X, n_rows,
                      scores, leaf_ids, ws, stream, err);
-  if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(true, a, stream, err);
+  if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(true, a, ws, stream, err);
   if (rc != kNotApplicable) return rc;
-  return launch_traverse(true, a, stream, err);
+  return launch_traverse(true, a, ws, stream, err);
 }
 
 int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_rows, float *scores,
-              int32_t *leaf_ids, const Workspace &ws, hipStream_t stream, std::string *err) {
+              int32_t *leaf_ids, const Launch &ws, hipStream_t stream, std::string *err) {
   if (!t.node || !t.node_il || !t.leaf_pk || !t.leaf_value || !t.leaf_id || !t.depth || t.n_pad < 1) {
     *err = "TT tables missing";
     return HB_ERR_INVALID_ARG;
@@ -758,13 +789,13 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
   a.slots = t.n_pad;
   a.leaf_slots = t.n_pad;
   int rc = kNotApplicable;
-  if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsTt)) rc = launch_lanes(false, a, stream, err);
+  if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsTt)) rc = launch_lanes(false, a, ws, stream, err);
   if (rc == kNotApplicable)
     rc = launch_fast(t.fast_mode, t.fast_lg, t.fast, t.fast_leaf, t.fast_chunks, t.depth, t.leaf_value, t.n_pad, e, X,
                      n_rows, scores, leaf_ids, ws, stream, err);
-  if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(false, a, stream, err);
+  if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(false, a, ws, stream, err);
   if (rc != kNotApplicable) return rc;
-  return launch_traverse(false, a, stream, err);
+  return launch_traverse(false, a, ws, stream, err);
 }
 
 

@@ -33,6 +33,23 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, name), name
 
 
+def test_library_exports_only_the_c_abi():
+    """Built with hidden visibility and a version script: the dynamic symbol
+    table holds the declared hb_* functions and nothing else."""
+    import subprocess
+
+    out = subprocess.run(["nm", "-D", "--defined-only", hb.LIB_PATH], capture_output=True, text=True, check=True)
+    syms = sorted(line.split()[-1] for line in out.stdout.splitlines() if line.strip())
+    assert syms == declared_functions(), syms
+
+
+def test_plan_needs_a_device_handle():
+    h = hb.compile(synth.make_model(1), device=-1)
+    with pytest.raises(hb.HBError) as e:
+        h.plan(1000, "ptt")
+    assert e.value.code == -1 and "host-only" in str(e.value)
+
+
 def test_host_only_handle_cannot_predict():
     h = hb.compile(synth.make_model(1), device=-1)
     with pytest.raises(hb.HBError) as e:

@@ -205,6 +205,56 @@ def test_gemm_wide_rows(kind, n_trees, n):
     check(model, X, scores, ids, f"gemm wide {kind}/{n_trees}/{n}")
 
 
+def _gemm_512_model(kind):
+    """Shared-shape forests that reach the GEMM kernels with 512-row
+    workgroups (batches of 32,768 rows and more whose feature tile fits
+    beside C^T in LDS): the headline model; a two-output model with scalar
+    leaves and a class per tree; perfect trees of depth 7 and 6 (128 and 64
+    leaves, the 64-node slice kernels); depth 7 with 2-vector leaves."""
+    if kind == "cfg2":
+        return synth.make_model(2)
+    rng = np.random.Generator(np.random.PCG64({"two_class": 9400, "depth7": 9401, "depth6": 9402,
+                                                "depth7_vec": 9403}[kind]))
+    depth = 6 if kind == "depth6" else 7 if kind.startswith("depth7") else 8
+    ld = 2 if kind == "depth7_vec" else 1
+    m = synth.perfect_forest(rng, 300 if kind != "two_class" else 200, depth, 28,
+                             lambda r, f: r.standard_normal(f.size), lambda r, k: r.normal(0.0, 0.05, k * ld),
+                             leaf_dim=ld)
+    T = m["n_trees"]
+    if kind == "two_class":
+        m.update(n_outputs=2, tree_class=(np.arange(T) % 2).astype(np.int32), aggregation="sum",
+                 transform="softmax", base_score=np.asarray([0.1, -0.2], np.float32))
+    elif kind == "depth7_vec":
+        m.update(n_outputs=2, tree_class=None, aggregation="mean", transform="none", base_score=None)
+    else:
+        m.update(n_outputs=1, tree_class=None, aggregation="sum", transform="sigmoid", base_score=None)
+    return synth.permute_nodes(m, 31 + depth)
+
+
+@pytest.mark.parametrize("kind,n,kernel", [
+    ("cfg2", 65_536, "gemm_pipe_kernel<0, 512>"),
+    ("two_class", 40_000, "gemm_pipe_kernel<1, 512>"),
+    ("depth7", 40_001, "gemm_kernel<2, true, true, 0, 512, false>"),
+    ("depth6", 33_000, "gemm_kernel<1, true, true, 0, 512, false>"),
+    ("depth7_vec", 32_768, "gemm_kernel<2, true, true, 2, 512, false>"),
+])
+def test_gemm_512_row_workgroups(kind, n, kernel):
+    """GEMM with 512-row workgroups (Algorithm 1, Table 3): every row's
+    scores and leaf ids against the oracle. The launch plan the library
+    reports names the kernel each case is meant to reach, the headline
+    workload's included (the one its GEMM throughput is measured on)."""
+    m = _gemm_512_model(kind)
+    h = handle(2)[1] if kind == "cfg2" else hb.compile(m, device=0)
+    plan = h.plan(n, "gemm")
+    assert [p["kernel"] for p in plan] == [kernel], plan
+    X = synth.make_rows(2, n)
+    if kind != "cfg2":
+        X = np.ascontiguousarray(pins.tricky_rows(np.random.Generator(np.random.PCG64(n)), m, n))
+    say("gemm 512-row", kind, n, kernel)
+    scores, ids = run(h, X, "gemm", workspace=False)
+    check(m, X, scores, ids, f"gemm512 {kind}/{n}")
+
+
 def _vector_forest(n_features, n_trees, depth, seed):
     rng = np.random.Generator(np.random.PCG64(seed))
 
