@@ -84,12 +84,24 @@ struct FastCfg {
   // leaf ids and sums are taken one chunk late
   static constexpr bool LAG = MODE == 2 && KM == 1 && TC <= 8;
   static constexpr int LH = LAG ? TC : 1;
+  // chunks of 8 trees: the leaf-id lines that end inside the chunk (at its
+  // fourth tree) leave at the start of the next chunk, with those that end
+  // at its last tree, and the ids of its last four trees wait in two
+  // registers until then (their slots still hold ids those lines need)
+  static constexpr bool DEFER = TC == 8;
 };
 
 // Leaf ids of a 32-tree group, one row per lane, as 16-bit halves: tree q of
 // the group sits in bits 16 (q & 1) of dword (q >> 1) & 3 of quad q >> 3.
+// pend holds the ids of trees 4..7 of a chunk of 8 until they may take their
+// slots (same halves: trees 4 and 5 in pend[0], 6 and 7 in pend[1]).
 constexpr int kIdQuads = kFastIdGroup / 8;
-using IdPack = u32x4[kIdQuads];
+struct IdPack {
+  u32x4 q[kIdQuads];
+  uint32_t pend[2];
+  __device__ __forceinline__ u32x4 &operator[](int j) { return q[j]; }
+  __device__ __forceinline__ const u32x4 &operator[](int j) const { return q[j]; }
+};
 
 // q is a constant once the chunk loop is unrolled
 __device__ __forceinline__ void put_id(IdPack &ids, int q, uint32_t id) {
@@ -117,7 +129,7 @@ __device__ __forceinline__ void put_id(IdPack &ids, int q, uint32_t id) {
 // memory whole.
 struct IdOut {
   bool on;            // leaf ids requested and the row layout allows vector stores (uniform)
-  u32x4 *stage;       // this wave's staging area: 8 rows x 64 bytes
+  u32x4 *stage;       // this wave's staging area: two lines of 8 rows x 64 bytes
   int64_t r0w;        // first row of the wave
   int t_begin;        // first tree of this workgroup's part
 };
@@ -160,6 +172,66 @@ __device__ __forceinline__ void id_pass(int32_t *leaf_ids, int64_t n_rows, int T
     // streaming: whole lines need no merging in L2, and allocating them
     // there would evict the blocks other workgroups are about to stage
     __builtin_nontemporal_store(o, reinterpret_cast<i32x4 *>(dst));
+  }
+  __builtin_amdgcn_wave_barrier();
+}
+
+// Two lines per row group at once (chunks of 8 trees, one residue ending a
+// line at each of the chunk's two line trees): the rows of residue rho0,
+// whose line ended at tree te0 (the chunk's fourth tree), stage the pack as
+// it stood then (quad QX's upper half still holding the ids of 32 trees
+// earlier), the rows of rho1 (line ended at te1, the chunk's last tree) stage
+// it with that half from pend; the 16 writers of one instruction touch
+// distinct banks (row i of line r is rotated by ((i / 4) + 2 r) mod 4
+// quads). Then every lane stores four ids of one row of each line. The two
+// staged lines take the wave's two 512-byte staging halves; a write of 8 or
+// 16 lanes costs the LDS as much as one of 64, so this halves the staging
+// writes of two separate passes.
+// The lane's index in its wave, read afresh at each use: the compiler cannot
+// hoist it, or the per-lane offsets derived from it, out of the tree loop
+// (held across the walk they would take the registers the walk needs).
+__device__ __forceinline__ int lane_fresh() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
+template <int QX>
+__device__ __forceinline__ void id_pass2(int32_t *leaf_ids, int64_t n_rows, int T, const IdOut &io, const IdPack &ids,
+                                         int rho0, int te0, int c0, int rho1, int te1, int c1, int lo) {
+  const int lane = lane_fresh();
+  const int k = lane & 7, i = lane >> 3;
+  if (k == rho0 || k == rho1) {
+    const int r = k == rho1 ? 1 : 0;
+    const int rot = ((i >> 2) + 2 * r) & 3;
+    u32x4 *dst = io.stage + r * (8 * kIdQuads) + i * kIdQuads;
+#pragma unroll
+    for (int j = 0; j < kIdQuads; ++j) {
+      u32x4 q = ids[j];
+      if (j == QX) {
+        q[2] = r ? ids.pend[0] : q[2];
+        q[3] = r ? ids.pend[1] : q[3];
+      }
+      dst[(j + rot) & 3] = q;
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int c = r ? c1 : c0;
+    const int rot = ((i >> 2) + 2 * r) & 3;
+    // ids 2 slot .. of row i of line r sit at byte 2 slot of its staged row, rotated by 16 rot
+    const uint2 v = *reinterpret_cast<const uint2 *>(reinterpret_cast<const unsigned char *>(io.stage) + 512 * r +
+                                                     64 * i + ((2 * c + 8 * k + 16 * rot) & 63));
+    const int64_t row0 = io.r0w + (r ? rho1 : rho0);
+    const int rem = (int)min(n_rows - row0, (int64_t)64);
+    const int tb = (r ? te1 : te0) - 31;
+    const int k4 = 4 * k;
+    if (8 * i < rem && k4 >= lo - tb && k4 < T - tb) {
+      int32_t *dst = leaf_ids + (row0 * T + tb) + ((uint32_t)(8 * i) * (uint32_t)T + (uint32_t)k4);
+      const i32x4 o{(int)(v.x & 0xffffu), (int)(v.x >> 16), (int)(v.y & 0xffffu), (int)(v.y >> 16)};
+      __builtin_nontemporal_store(o, reinterpret_cast<i32x4 *>(dst));
+    }
   }
   __builtin_amdgcn_wave_barrier();
 }
@@ -212,8 +284,15 @@ __device__ __forceinline__ void fast_leaves(const FastArgs &a, const uint2 (&lrs
   for (int g = 0; g < TC; ++g) {
     const int t = tb + g;
     const uint2 lr = lrs[g];
-    put_id(ids, QP * TC + g, lr.y);
-    if (((QP * TC + g) & 3) == 3 && g < TC - 1 && io.on) {  // lines that end at tree t, within the chunk
+    if (C::DEFER && g >= 4 && io.on) {  // held until the lines that end at tree tb + 3 have left
+      if (g & 1)
+        ids.pend[(g - 4) >> 1] |= lr.y << 16;
+      else
+        ids.pend[(g - 4) >> 1] = lr.y;
+    } else {
+      put_id(ids, QP * TC + g, lr.y);
+    }
+    if (!C::DEFER && ((QP * TC + g) & 3) == 3 && g < TC - 1 && io.on) {  // lines that end at tree t, within the chunk
       const int c = (QP * TC + g + 1) & 31;
       uint32_t m = (uint32_t)(a.id_phase >> (8 * (c >> 2))) & 0xffu;
       while (m) {
@@ -239,6 +318,22 @@ __device__ __forceinline__ void fast_leaves(const FastArgs &a, const uint2 (&lrs
   // stores (here with LAG, whose groups end one chunk late; else after the group)
   if (C::LAG && QP == C::CPF - 1 && a.leaf_ids && !a.ids_vec)
     flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, io.r0w, tb - (C::CPF - 1) * TC);
+}
+
+// Chunks of 8 trees (DEFER): the lines that ended at tree tb + 3 of the
+// chunk with index QX in its group (first tree tb) leave, then the ids of
+// the chunk's last four trees take their slots.
+template <int QX>
+__device__ __forceinline__ void fast_deferred(const FastArgs &a, IdPack &ids, int tb, const IdOut &io) {
+  constexpr int kC = (QX * 8 + 4) & 31;  // slot of tree tb + 3 - 31
+  uint32_t m = (uint32_t)(a.id_phase >> (8 * (kC >> 2))) & 0xffu;
+  while (m) {
+    const int rho = __builtin_ctz(m);
+    m &= m - 1;
+    id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, rho, tb + 3, kC, io.t_begin);
+  }
+  ids[QX][2] = ids.pend[0];
+  ids[QX][3] = ids.pend[1];
 }
 
 template <int MODE, int LG, int KM, int ROWS, int BUDGET, int B, int Q>
@@ -273,13 +368,31 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   // stores
   constexpr int kLag = C::LAG ? 1 : 0;
   constexpr int kQE = (Q + C::CPF - kLag) % C::CPF;  // the chunk that ended, within its group
-  if (((kQE * TC) & 3) == 0 && io.on && t0 - kLag * TC > io.t_begin) {
+  const bool ended = io.on && t0 - kLag * TC > io.t_begin;
+  if (ended) {
     constexpr int kC = (kQE * TC) & 31;
-    uint32_t m = (uint32_t)(a.id_phase >> (8 * (kC >> 2))) & 0xffu;
-    while (m) {
-      const int rho = __builtin_ctz(m);
-      m &= m - 1;
-      id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, rho, t0 - kLag * TC - 1, kC, io.t_begin);
+    const uint32_t m_end = ((kQE * TC) & 3) == 0 ? (uint32_t)(a.id_phase >> (8 * (kC >> 2))) & 0xffu : 0u;
+    if constexpr (C::DEFER) {
+      // the lines that ended inside that chunk, then its last ids, then the
+      // lines that ended with it: one staging for both when each of the two
+      // trees ends the lines of a single residue (tree counts of 4 mod 8)
+      constexpr int kQX = (Q + 2 * C::CPF - 1 - kLag) % C::CPF;
+      constexpr int kCI = (kQX * 8 + 4) & 31;
+      const uint32_t m_in = (uint32_t)(a.id_phase >> (8 * (kCI >> 2))) & 0xffu;
+      const int tb = t0 - (1 + kLag) * TC;  // first tree of the chunk that ended
+      if (__builtin_popcount(m_in) == 1 && __builtin_popcount(m_end) == 1) {
+        id_pass2<kQX>(a.leaf_ids, a.n_rows, a.out.T, io, ids, __builtin_ctz(m_in), tb + 3, kCI, __builtin_ctz(m_end),
+                      tb + TC - 1, kC, io.t_begin);
+        ids[kQX][2] = ids.pend[0];
+        ids[kQX][3] = ids.pend[1];
+      } else {
+        fast_deferred<kQX>(a, ids, tb, io);
+        for (uint32_t m = m_end; m; m &= m - 1)
+          id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, __builtin_ctz(m), t0 - kLag * TC - 1, kC, io.t_begin);
+      }
+    } else {
+      for (uint32_t m = m_end; m; m &= m - 1)
+        id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, __builtin_ctz(m), t0 - kLag * TC - 1, kC, io.t_begin);
     }
   }
   __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the walk
@@ -429,7 +542,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   const int c_begin = a.split ? (int)blockIdx.y * a.split : 0;
   if (a.split) a.n_chunks = min(c_begin + a.split, a.n_chunks);
   __shared__ __align__(16) uint4 tbuf[C::BUFS][C::CHUNK16];
-  __shared__ __align__(16) u32x4 idstage[ROWS / 64][8 * kIdQuads];
+  __shared__ __align__(16) u32x4 idstage[ROWS / 64][2 * 8 * kIdQuads];
   extern __shared__ __align__(16) float fxs[];  // [F][ROWS]
   const int tid = threadIdx.x;
   const int64_t r0 = (int64_t)blockIdx.x * ROWS;
@@ -474,10 +587,14 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
     fast_group<MODE, LG, KM, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, vh, lh, io);
     if (!C::LAG && a.leaf_ids && !a.ids_vec) flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, io.r0w, c * C::TC);
   }
+  if constexpr (C::DEFER && !C::LAG)  // the last chunk's inside lines and ids
+    if (io.on) fast_deferred<C::CPF - 1>(a, ids, a.n_chunks * C::TC - C::TC, io);
   if (C::LAG) {
     // the lines that ended with the next-to-last chunk, then the last
     // chunk's leaf ids and sums
     const int t_last = a.n_chunks * C::TC - C::TC;  // first tree of the last chunk
+    if constexpr (C::DEFER)
+      if (io.on && t_last - C::TC >= io.t_begin) fast_deferred<(2 * C::CPF - 2) % C::CPF>(a, ids, t_last - C::TC, io);
     constexpr int kC = ((C::CPF - 1) * C::TC) & 31;
     if ((kC & 3) == 0 && io.on && t_last > io.t_begin) {
       uint32_t m = (uint32_t)(a.id_phase >> (8 * (kC >> 2))) & 0xffu;
@@ -491,6 +608,8 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
 #pragma unroll
     for (int g = 0; g < C::TC; ++g) last[g] = lh[g < C::LH ? g : 0];
     fast_leaves<MODE, LG, KM, ROWS, BUDGET, C::CPF - 1>(a, last, t_last, acc, ids, cls, io);
+    if constexpr (C::DEFER)
+      if (io.on) fast_deferred<C::CPF - 1>(a, ids, t_last, io);
   }
   if (C::VHOLD && a.vec) {  // the last chunk's 2-vector leaves
 #pragma unroll

@@ -41,10 +41,10 @@ constexpr int kFastTableLds = 64 * 1024;
 constexpr int kFastIdGroup = 32;
 // The fast kernels hold and stage leaf ids as 16-bit halves: every caller id
 // they report is a local node id of a tree with at most 2^(kFastMaxLg + 1)
-// nodes. Each wave stages 8 of its 64 rows at a time (the 32 ids of one
-// 128-byte output line per row), so the staging costs 8 bytes per row of a
-// workgroup.
-constexpr int kFastIdStageBytes = 8 * kFastIdGroup * 2 / 64;
+// nodes. Each wave stages up to 16 of its 64 rows at a time (the 32 ids of
+// one 128-byte output line per row, for two lines), so the staging costs 16
+// bytes per row of a workgroup.
+constexpr int kFastIdStageBytes = 2 * 8 * kFastIdGroup * 2 / 64;
 constexpr int fast_node_bytes(int mode) { return (void)mode, 8; }
 constexpr int fast_tree_bytes(int mode, int lg) { return (1 << lg) * (fast_node_bytes(mode) + (mode == 2 ? 0 : 8)); }
 // TT leaf records up to this size stay in global memory (mode 2); measured
