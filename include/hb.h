@@ -179,6 +179,26 @@ HB_API int hb_predict(hb_handle *h, const float *X, int64_t n_rows, float *score
 HB_API int hb_predict_ws(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
                   int strategy, void *stream, void *workspace, int64_t workspace_bytes);
 
+/*
+ * hb_predict_ws for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the workspace is the library's own static device scratch of
+ * HB_SCRATCH_BYTES bytes, one copy per GPU, held from the first such call on
+ * a device until the process ends. scratch_bytes (0 .. HB_SCRATCH_BYTES) is
+ * how much of it the call may use, as workspace_bytes in hb_predict_ws (e.g.
+ * hb_workspace_bytes(), capped at HB_SCRATCH_BYTES; the split then uses the
+ * most parts whose partial sums fit). Allocates nothing: no hipMalloc, no
+ * hipFree. Every call on a GPU shares that GPU's scratch, so calls that may
+ * overlap on one device (other streams, other threads) race and must be
+ * serialised by the caller; the scratch keeps the last call's partial sums,
+ * which a call overwrites before reading. Errors as hb_predict_ws, plus
+ * HB_ERR_INVALID_ARG for scratch_bytes outside [0, HB_SCRATCH_BYTES], and
+ * HB_ERR_HIP if the scratch's device address cannot be obtained.
+ */
+#define HB_SCRATCH_BYTES ((int64_t)32 << 20)
+HB_API int hb_predict_scratch(hb_handle *h, const float *X, int64_t n_rows, float *scores, int32_t *leaf_ids,
+                              int strategy, void *stream, int64_t scratch_bytes);
+
 /* Workspace bytes that let hb_predict_ws split the trees of a batch of
  * n_rows rows under `strategy` (AUTO: the selector's choice); 0 when that
  * batch never splits. A negative value is an error code. The split serves

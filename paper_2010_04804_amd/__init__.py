@@ -2,7 +2,7 @@
 
 This module only marshals arguments into the C-ABI declared in
 ``include/hb.h`` (``hb_compile``, ``hb_predict``, ``hb_predict_ws``,
-``hb_workspace_bytes``, ``hb_query``, ``hb_table``, ``hb_select_strategy``,
+``hb_predict_scratch``, ``hb_workspace_bytes``, ``hb_query``, ``hb_table``, ``hb_select_strategy``,
 ``hb_plan``, ``hb_destroy``, ``hb_last_error``). Every step of
 scoring runs in the library's HIP kernels; PyTorch only supplies device
 memory and the current stream. If ``libhb.so`` has not been built, importing
@@ -17,7 +17,7 @@ import os
 
 import numpy as np
 
-__all__ = ["compile", "predict", "predict_ptr", "workspace_bytes", "Handle", "HBError", "STRATEGY", "load_library",
+__all__ = ["compile", "predict", "predict_ptr", "predict_scratch_ptr", "workspace_bytes", "SCRATCH_BYTES", "Handle", "HBError", "STRATEGY", "load_library",
            "LIB_PATH"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhb.so")
@@ -80,6 +80,8 @@ def load_library(path: str = LIB_PATH):
     lib.hb_predict.argtypes = [_P, _P, ctypes.c_int64, _P, _P, ctypes.c_int, _P]
     lib.hb_predict_ws.restype = ctypes.c_int
     lib.hb_predict_ws.argtypes = [_P, _P, ctypes.c_int64, _P, _P, ctypes.c_int, _P, _P, ctypes.c_int64]
+    lib.hb_predict_scratch.restype = ctypes.c_int
+    lib.hb_predict_scratch.argtypes = [_P, _P, ctypes.c_int64, _P, _P, ctypes.c_int, _P, ctypes.c_int64]
     lib.hb_workspace_bytes.restype = ctypes.c_int64
     lib.hb_workspace_bytes.argtypes = [_P, ctypes.c_int64, ctypes.c_int]
     lib.hb_select_strategy.restype = ctypes.c_int
@@ -220,6 +222,18 @@ def predict_ptr(h: Handle, x_ptr: int, n_rows: int, scores_ptr: int, ids_ptr: in
     else:
         _check(load_library().hb_predict(h.ptr, x_ptr, int(n_rows), scores_ptr, ids_ptr or None,
                                          _strategy(strategy), stream or None))
+
+
+SCRATCH_BYTES = 32 << 20  # HB_SCRATCH_BYTES of include/hb.h
+
+
+def predict_scratch_ptr(h: Handle, x_ptr: int, n_rows: int, scores_ptr: int, ids_ptr: int | None,
+                        strategy="auto", stream: int | None = None, scratch_bytes: int = 0):
+    """hb_predict_scratch on raw device pointers: hb_predict_ws with the
+    library's static device scratch (up to ``scratch_bytes`` of it) as the
+    workspace; allocates nothing."""
+    _check(load_library().hb_predict_scratch(h.ptr, x_ptr, int(n_rows), scores_ptr, ids_ptr or None,
+                                             _strategy(strategy), stream or None, int(scratch_bytes)))
 
 
 def predict(h: Handle, X, strategy="auto", leaves: bool = True, out=None, stream=None,

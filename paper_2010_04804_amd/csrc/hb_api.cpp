@@ -749,6 +749,11 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
 
 }  // namespace
 
+namespace hb {
+int set_error(int code, const std::string &msg) { return fail(code, msg); }
+int handle_device(const hb_handle *h) { return h ? h->device : -1; }
+}  // namespace hb
+
 extern "C" {
 
 int hb_compile(const hb_ensemble_desc *desc, int strategy_hint, int device, hb_handle **out) {

@@ -171,6 +171,11 @@ struct Launch {
   std::string *plan = nullptr;
 };
 
+// The error message hb_last_error() returns on this thread; returns code.
+int set_error(int code, const std::string &msg);
+// The HIP device of a compiled handle (-1: host-only handle or NULL).
+int handle_device(const hb_handle *h);
+
 // Tree split: batches up to kSplitMaxRows rows may have their trees divided
 // among up to one workgroup per 32-tree group of each row tile, so that a
 // small batch still fills the chip; the workgroups leave double partial sums

@@ -153,3 +153,19 @@ def test_workspace_bytes_and_errors():
     # a valid workspace on a host-only handle reaches the device check
     assert lib.hb_predict_ws(h.ptr, 1, 10, 1, None, 0, None, 64, 64) == -1
     assert "host-only" in lib.hb_last_error().decode()
+
+
+def test_scratch_entry_point_rejects_sizes_beyond_the_maximum():
+    """hb_predict_scratch checks scratch_bytes before anything else (no GPU
+    is touched): outside [0, HB_SCRATCH_BYTES] is an argument error; a
+    host-only handle is rejected as by hb_predict."""
+    h = hb.compile(synth.make_model(1), device=-1)
+    for bad in (-1, hb.SCRATCH_BYTES + 1):
+        with pytest.raises(hb.HBError) as e:
+            hb.predict_scratch_ptr(h, 1, 10, 1, None, "ptt", None, bad)
+        assert e.value.code == -1 and "HB_SCRATCH_BYTES" in str(e.value)
+    with pytest.raises(hb.HBError) as e:
+        hb.predict_scratch_ptr(h, 1, 10, 1, None, "ptt", None, 1024)
+    assert e.value.code == -1 and "host-only" in str(e.value)
+    src = open(os.path.join(ROOT, "include", "hb.h")).read()
+    assert f"#define HB_SCRATCH_BYTES ((int64_t)32 << 20)" in src and hb.SCRATCH_BYTES == 32 << 20
