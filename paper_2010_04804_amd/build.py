@@ -12,6 +12,7 @@ LIB = os.path.join(PKG, "libhb.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["hb_api.cpp", "hb_scratch.hip", "hb_kernels.hip", "hb_gemm.hip", "hb_fast_ptt_128.hip", "hb_fast_ptt_256.hip", "hb_fast_ptt_256s.hip", "hb_fast_ptt_512.hip",
            "hb_fast_ptt_512s.hip", "hb_fast_ptt_768.hip", "hb_fast_ptt_1024.hip",
+           "hb_fast_pttg_128.hip", "hb_fast_pttg_256.hip", "hb_fast_pttg_512.hip", "hb_fast_pttg_1024.hip",
            "hb_fast_tt_128.hip", "hb_fast_tt_256.hip", "hb_fast_tt_1024.hip", "hb_fast_ttg_1024.hip", "hb_fast_tt_256s.hip",
            "hb_fast_tt_512.hip", "hb_fast_tt_512s.hip", "hb_fast_ttg_128.hip", "hb_fast_ttg_256.hip",
            "hb_fast_ttg_256s.hip", "hb_fast_ttg_512.hip", "hb_fast_ttg_512s.hip"]

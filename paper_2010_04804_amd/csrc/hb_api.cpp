@@ -150,7 +150,9 @@ struct hb_handle {
   int32_t gemm_k_pad = 0, gemm_l_pad = 0, gemm_n_shapes = 0;
   // packed blocks of the fast traversal kernels (device layout only)
   std::vector<uint32_t> ptt_fast, tt_fast, tt_fast_leaf;
+  std::vector<float> ptt_fast_leafv;  // mode 3: [padded T][2^D] leaf values
   int32_t ptt_fast_chunks = 0, tt_fast_lg = 0, tt_fast_chunks = 0, tt_fast_mode = 1;
+  int32_t ptt_fast_mode = 0, ptt_id_base = 0;
   // device
   std::vector<void *> allocations;
   hb::EnsembleDev ens{};
@@ -272,11 +274,39 @@ void build_fast(hb_handle *h, const hb_ensemble_desc *d, const std::vector<Canon
   const int32_t T = d->n_trees;
   const int32_t D = h->info.max_depth;
   if (h->info.feasible[HB_STRATEGY_PTT] && D >= 1 && D <= hb::kFastMaxLg) {
+    const size_t S = (size_t)1 << D;
+    const size_t padded = (size_t)(T + hb::kFastIdGroup - 1) / hb::kFastIdGroup * hb::kFastIdGroup;
+    // Mode 3 (leaf values apart, in global memory, ids formed from the leaf
+    // slot): one scalar output, depth <= 8 (slots fit a byte), every leaf's
+    // caller id its slot plus one base (heap-ordered perfect trees), and the
+    // values small enough to stay in an XCD's L2.
+    bool affine = d->n_outputs == 1 && ld == 1 && D <= 8 && (int64_t)(padded * S * 4) <= hb::kTtLeafGlobalMax;
+    const int32_t base = h->ptt_leaf_id.empty() ? 0 : h->ptt_leaf_id[0];
+    for (size_t i = 0; affine && i < (size_t)T * S; ++i) affine = h->ptt_leaf_id[i] == base + (int32_t)(i % S);
+    if (affine) {
+      const int tb = hb::fast_tree_bytes(3, D);
+      const int tc = hb::fast_tc_m(3, tb);
+      h->ptt_fast.assign(padded * S * 2, 0u);
+      h->ptt_fast_leafv.assign(padded * S, 0.0f);  // padding trees add zero
+      for (int32_t t = 0; t < T; ++t) {
+        uint32_t *blk = &h->ptt_fast[(size_t)t * S * 2];
+        for (size_t p = 1; p < S; ++p) {
+          blk[2 * p] = h->ptt_node[((size_t)t * S + p) * 2];
+          blk[2 * p + 1] = h->ptt_node[((size_t)t * S + p) * 2 + 1];
+        }
+        for (size_t q = 0; q < S; ++q) h->ptt_fast_leafv[(size_t)t * S + q] = h->ptt_leaf_value[(size_t)t * S + q];
+      }
+      h->ptt_fast_chunks = (int)(padded / tc);
+      h->ptt_fast_mode = 3;
+      h->ptt_id_base = base;
+    }
+  }
+  if (h->info.feasible[HB_STRATEGY_PTT] && D >= 1 && D <= hb::kFastMaxLg && h->ptt_fast_mode != 3) {
+    const size_t S = (size_t)1 << D;
     const int tb = hb::fast_tree_bytes(0, D);
     const int tc = hb::fast_tc(tb);
     const int chunks = (T + hb::kFastIdGroup - 1) / hb::kFastIdGroup * (hb::kFastIdGroup / tc);
     const size_t words = (size_t)tb / 4;
-    const size_t S = (size_t)1 << D;
     h->ptt_fast.assign((size_t)chunks * tc * words, 0u);
     for (int32_t t = 0; t < T; ++t) {
       uint32_t *blk = &h->ptt_fast[(size_t)t * words];
@@ -687,6 +717,9 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
         rc = upload(h, h->ptt_fast, &pn);
         h->ptt.fast = reinterpret_cast<const uint4 *>(pn);
         h->ptt.fast_chunks = h->ptt_fast_chunks;
+        h->ptt.fast_mode = h->ptt_fast_mode;
+        h->ptt.id_base = h->ptt_id_base;
+        if (!rc && h->ptt_fast_mode == 3) rc = upload(h, h->ptt_fast_leafv, &h->ptt.fast_leafv);
       }
     }
     if (!rc && I.feasible[HB_STRATEGY_TT]) {

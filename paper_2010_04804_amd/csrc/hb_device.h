@@ -182,6 +182,8 @@ struct FastArgs {
   const int32_t *tree_class;
   const uint4 *blocks;        // [chunks * TC][tree bytes / 16]
   const uint2 *leaf;          // TT mode 2: [chunks * TC][2^lg] leaf records (global memory)
+  const float *leafv;         // PTT mode 3: [chunks * TC][2^lg] leaf values (global memory)
+  int32_t id_base;            // PTT mode 3: caller id of leaf slot 0
   const int32_t *tree_depth;  // TT: [T]
   int32_t n_chunks;
   // Tree split (small batches): workgroup (x, y) walks chunks [y * split,
@@ -213,6 +215,12 @@ FastFn fast_ptt_kernel_512(int lg, int km);
 FastFn fast_ptt_kernel_512s(int lg, int km);
 FastFn fast_ptt_kernel_768(int lg, int km);
 FastFn fast_ptt_kernel_1024(int lg, int km);
+// PTT with the leaf values in global memory and 8-bit slot ids (mode 3):
+// one output only (km == 1), lg <= 8, 32 KiB of double-buffered chunks.
+FastFn fast_pttg_kernel_1024(int lg, int km);
+FastFn fast_pttg_kernel_512(int lg, int km);
+FastFn fast_pttg_kernel_256(int lg, int km);
+FastFn fast_pttg_kernel_128(int lg, int km);
 FastFn fast_tt_kernel_1024(int lg, int km);
 FastFn fast_tt_kernel_256(int lg, int km);
 FastFn fast_tt_kernel_512(int lg, int km);

@@ -2,6 +2,8 @@
 // included by the hb_fast_{ptt,tt}_<rows>.hip units, which instantiate it.
 #pragma once
 
+#include <type_traits>
+
 #include "hb_device.h"
 
 namespace hb {
@@ -64,13 +66,16 @@ struct ChunkPrefetch {
 };
 
 template <int MODE>
-constexpr int kFastMaxLgFor = MODE == 0 ? 10 : 11;
+constexpr int kFastMaxLgFor = MODE == 0 ? 10 : MODE == 3 ? 8 : 11;
+
+struct IdPack;
+struct IdPack8;
 
 template <int MODE, int LG, int KM, int ROWS, int BUDGET>
 struct FastCfg {
   static constexpr int TB = fast_tree_bytes(MODE, LG);
-  static constexpr int TC = fast_tc(TB, BUDGET);
-  static constexpr int BUFS = fast_bufs(TB, BUDGET);
+  static constexpr int TC = fast_tc_m(MODE, TB, BUDGET);
+  static constexpr int BUFS = fast_bufs_m(MODE, TB, BUDGET);
   static constexpr int CPF = kFastIdGroup / TC;  // chunks per leaf-id flush
   static constexpr int CHUNK16 = TC * TB / 16;
   static constexpr int KMAX = KM;  // accumulators: 1, 2 or HB_MAX_OUTPUTS
@@ -89,6 +94,12 @@ struct FastCfg {
   // at its last tree, and the ids of its last four trees wait in two
   // registers until then (their slots still hold ids those lines need)
   static constexpr bool DEFER = TC == 8;
+  // PTT with the leaf values in global memory (mode 3): the values are read
+  // right after the walk and added after the next one, so their latency
+  // hides behind a walk; the ids are the leaves' slots, held as bytes
+  static constexpr bool GV = MODE == 3;
+  static constexpr int GVH = GV ? TC : 1;
+  using Pack = typename std::conditional<GV, IdPack8, IdPack>::type;
 };
 
 // Leaf ids of a 32-tree group, one row per lane, as 16-bit halves: tree q of
@@ -109,6 +120,47 @@ __device__ __forceinline__ void put_id(IdPack &ids, int q, uint32_t id) {
     ids[q >> 3][(q >> 1) & 3] |= id << 16;
   else
     ids[q >> 3][(q >> 1) & 3] = id;
+}
+// tree g in 4..7 of a chunk of 8, held until its slot is free
+__device__ __forceinline__ void hold_id(IdPack &ids, int g, uint32_t id) {
+  if (g & 1)
+    ids.pend[(g - 4) >> 1] |= id << 16;
+  else
+    ids.pend[(g - 4) >> 1] = id;
+}
+template <int QX>
+__device__ __forceinline__ void put_pending(IdPack &ids) {
+  ids[QX][2] = ids.pend[0];
+  ids[QX][3] = ids.pend[1];
+}
+
+// Leaf slots of a 32-tree group as bytes, for PTT trees of depth <= 8 whose
+// caller ids are the slot plus one base (heap-ordered perfect trees: the
+// leaves follow the 2^D - 1 decision nodes); the ids are formed as they
+// leave. Tree q of the group sits in byte q & 3 of dword q >> 2 (component
+// (q >> 2) & 3 of quad q >> 4); pend holds trees 4..7 of a chunk of 8, the
+// whole dword their slots take. Half the registers and half the staging of
+// 16-bit ids.
+struct IdPack8 {
+  u32x4 q[2];
+  uint32_t pend;
+};
+__device__ __forceinline__ void put_id(IdPack8 &ids, int q, uint32_t slot) {
+  const int d = q >> 2;
+  if ((q & 3) == 0)
+    ids.q[d >> 2][d & 3] = slot;
+  else
+    ids.q[d >> 2][d & 3] |= slot << (8 * (q & 3));
+}
+__device__ __forceinline__ void hold_id(IdPack8 &ids, int g, uint32_t slot) {
+  if (g == 4)
+    ids.pend = slot;
+  else
+    ids.pend |= slot << (8 * (g - 4));
+}
+template <int QX>
+__device__ __forceinline__ void put_pending(IdPack8 &ids) {
+  ids.q[(2 * QX + 1) >> 2][(2 * QX + 1) & 3] = ids.pend;
 }
 
 // Leaf ids leave in whole 128-byte lines of the output, each as soon as its
@@ -132,14 +184,15 @@ struct IdOut {
   u32x4 *stage;       // this wave's staging area: two lines of 8 rows x 64 bytes
   int64_t r0w;        // first row of the wave
   int t_begin;        // first tree of this workgroup's part
+  uint32_t id_base;   // IdPack8: caller id of leaf slot 0
 };
 
 template <int ROWS>
-__device__ __forceinline__ IdOut make_id_out(bool on, u32x4 *stage, int t_begin) {
+__device__ __forceinline__ IdOut make_id_out(bool on, u32x4 *stage, int t_begin, uint32_t id_base) {
   // the wave's first row is uniform: keep it (and the per-pass row and tree
   // offsets computed from it) in scalar registers
   const int64_t r0w = (int64_t)blockIdx.x * ROWS + 64 * __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  return IdOut{on, stage, r0w, t_begin};
+  return IdOut{on, stage, r0w, t_begin, id_base};
 }
 
 // Writes, for the rows of residue rho in this wave, the ids of trees
@@ -176,6 +229,42 @@ __device__ __forceinline__ void id_pass(int32_t *leaf_ids, int64_t n_rows, int T
   __builtin_amdgcn_wave_barrier();
 }
 
+// id_pass for 8-bit slots: a staged row is 32 bytes (two quads, the eight
+// writers of one instruction 32 bytes apart: distinct banks); a reader takes
+// the four slots of its ids in one dword and adds the base.
+__device__ __forceinline__ void id_pass(int32_t *leaf_ids, int64_t n_rows, int T, const IdOut &io,
+                                        const IdPack8 &ids, int rho, int t_end, int c, int lo) {
+  const int lane = threadIdx.x & 63;
+  const int k4 = 4 * (lane & 7), i = lane >> 3;
+  if (k4 == 4 * rho) {
+    io.stage[2 * i] = ids.q[0];
+    io.stage[2 * i + 1] = ids.q[1];
+  }
+  __builtin_amdgcn_wave_barrier();
+  const uint32_t v =
+      *reinterpret_cast<const uint32_t *>(reinterpret_cast<const unsigned char *>(io.stage) + 32 * i + ((c + k4) & 31));
+  const int64_t row0 = io.r0w + rho;
+  const int rem = (int)min(n_rows - row0, (int64_t)64);
+  const int tb = t_end - 31;
+  if (8 * i < rem && k4 >= lo - tb && k4 < T - tb) {
+    int32_t *dst = leaf_ids + (row0 * T + tb) + ((uint32_t)(8 * i) * (uint32_t)T + (uint32_t)k4);
+    const uint32_t b = io.id_base;
+    const i32x4 o{(int)(b + (v & 0xffu)), (int)(b + ((v >> 8) & 0xffu)), (int)(b + ((v >> 16) & 0xffu)),
+                  (int)(b + (v >> 24))};
+    __builtin_nontemporal_store(o, reinterpret_cast<i32x4 *>(dst));
+  }
+  __builtin_amdgcn_wave_barrier();
+}
+
+// The lane's index in its wave, read afresh at each use: the compiler cannot
+// hoist it, or the per-lane offsets derived from it, out of the tree loop
+// (held across the walk they would take the registers the walk needs).
+__device__ __forceinline__ int lane_fresh() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
 // Two lines per row group at once (chunks of 8 trees, one residue ending a
 // line at each of the chunk's two line trees): the rows of residue rho0,
 // whose line ended at tree te0 (the chunk's fourth tree), stage the pack as
@@ -187,15 +276,6 @@ __device__ __forceinline__ void id_pass(int32_t *leaf_ids, int64_t n_rows, int T
 // staged lines take the wave's two 512-byte staging halves; a write of 8 or
 // 16 lanes costs the LDS as much as one of 64, so this halves the staging
 // writes of two separate passes.
-// The lane's index in its wave, read afresh at each use: the compiler cannot
-// hoist it, or the per-lane offsets derived from it, out of the tree loop
-// (held across the walk they would take the registers the walk needs).
-__device__ __forceinline__ int lane_fresh() {
-  int l;
-  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
-  return l;
-}
-
 template <int QX>
 __device__ __forceinline__ void id_pass2(int32_t *leaf_ids, int64_t n_rows, int T, const IdOut &io, const IdPack &ids,
                                          int rho0, int te0, int c0, int rho1, int te1, int c1, int lo) {
@@ -236,9 +316,61 @@ __device__ __forceinline__ void id_pass2(int32_t *leaf_ids, int64_t n_rows, int 
   __builtin_amdgcn_wave_barrier();
 }
 
+// id_pass2 for 8-bit slots: line r's staged rows take 256 bytes from byte
+// 256 r, row i of line r rotated by r quads (the 16 writers of one
+// instruction touch distinct banks).
+template <int QX>
+__device__ __forceinline__ void id_pass2(int32_t *leaf_ids, int64_t n_rows, int T, const IdOut &io, const IdPack8 &ids,
+                                         int rho0, int te0, int c0, int rho1, int te1, int c1, int lo) {
+  const int lane = lane_fresh();
+  const int k = lane & 7, i = lane >> 3;
+  constexpr int kD = 2 * QX + 1;  // the dword trees 4..7 of chunk QX take
+  if (k == rho0 || k == rho1) {
+    const int r = k == rho1 ? 1 : 0;
+    u32x4 *dst = io.stage + 16 * r + 2 * i;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      u32x4 q = ids.q[j];
+      if (j == (kD >> 2)) q[kD & 3] = r ? ids.pend : q[kD & 3];
+      dst[(j + r) & 1] = q;
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int c = r ? c1 : c0;
+    const uint32_t v = *reinterpret_cast<const uint32_t *>(reinterpret_cast<const unsigned char *>(io.stage) +
+                                                           256 * r + 32 * i + ((c + 4 * k + 16 * r) & 31));
+    const int64_t row0 = io.r0w + (r ? rho1 : rho0);
+    const int rem = (int)min(n_rows - row0, (int64_t)64);
+    const int tb = (r ? te1 : te0) - 31;
+    const int k4 = 4 * k;
+    if (8 * i < rem && k4 >= lo - tb && k4 < T - tb) {
+      int32_t *dst = leaf_ids + (row0 * T + tb) + ((uint32_t)(8 * i) * (uint32_t)T + (uint32_t)k4);
+      const uint32_t b = io.id_base;
+      const i32x4 o{(int)(b + (v & 0xffu)), (int)(b + ((v >> 8) & 0xffu)), (int)(b + ((v >> 16) & 0xffu)),
+                    (int)(b + (v >> 24))};
+      __builtin_nontemporal_store(o, reinterpret_cast<i32x4 *>(dst));
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+}
+
 // Rows not 16-byte aligned: one int32 per store, a 32-tree group at a time.
-__device__ __forceinline__ void flush_scalar(int32_t *leaf_ids, int64_t n_rows, int T, const IdPack &ids, int64_t r0w,
-                                             int t0) {
+__device__ __forceinline__ void flush_scalar(int32_t *leaf_ids, int64_t n_rows, int T, const IdPack8 &ids,
+                                             const IdOut &io, int t0) {
+  const int ntrees = min(kFastIdGroup, T - t0);
+  const int64_t row = io.r0w + (threadIdx.x & 63);
+  if (row < n_rows) {
+#pragma unroll
+    for (int g = 0; g < kFastIdGroup; ++g)
+      if (g < ntrees)
+        leaf_ids[row * T + t0 + g] = (int)(io.id_base + ((ids.q[g >> 4][(g >> 2) & 3] >> (8 * (g & 3))) & 0xffu));
+  }
+}
+__device__ __forceinline__ void flush_scalar(int32_t *leaf_ids, int64_t n_rows, int T, const IdPack &ids,
+                                             const IdOut &io, int t0) {
+  const int64_t r0w = io.r0w;
   const int ntrees = min(kFastIdGroup, T - t0);
   const int64_t row = r0w + (threadIdx.x & 63);
   if (row < n_rows) {
@@ -277,7 +409,8 @@ __device__ __forceinline__ const float *fast_vec_leaf(const FastArgs &a, int t, 
 template <int MODE, int LG, int KM, int ROWS, int BUDGET, int QP>
 __device__ __forceinline__ void fast_leaves(const FastArgs &a, const uint2 (&lrs)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::TC],
                                             int tb, double (&acc)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::KMAX],
-                                            IdPack &ids, int cls, const IdOut &io) {
+                                            typename FastCfg<MODE, LG, KM, ROWS, BUDGET>::Pack &ids, int cls,
+                                            const IdOut &io) {
   using C = FastCfg<MODE, LG, KM, ROWS, BUDGET>;
   constexpr int TC = C::TC;
 #pragma unroll
@@ -285,10 +418,7 @@ __device__ __forceinline__ void fast_leaves(const FastArgs &a, const uint2 (&lrs
     const int t = tb + g;
     const uint2 lr = lrs[g];
     if (C::DEFER && g >= 4 && io.on) {  // held until the lines that end at tree tb + 3 have left
-      if (g & 1)
-        ids.pend[(g - 4) >> 1] |= lr.y << 16;
-      else
-        ids.pend[(g - 4) >> 1] = lr.y;
+      hold_id(ids, g, lr.y);
     } else {
       put_id(ids, QP * TC + g, lr.y);
     }
@@ -301,7 +431,7 @@ __device__ __forceinline__ void fast_leaves(const FastArgs &a, const uint2 (&lrs
         id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, rho, t, c, io.t_begin);
       }
     }
-    if (t < a.out.T) {
+    if (t < a.out.T && !C::GV) {  // (GV: the values are added by the caller)
       const double v = (double)as_float(lr.x);
       if (C::MULTI && a.vec) {
         // vector leaves are added by the caller
@@ -317,14 +447,14 @@ __device__ __forceinline__ void fast_leaves(const FastArgs &a, const uint2 (&lrs
   // rows not 16-byte aligned: a 32-tree group's ids leave at once, by scalar
   // stores (here with LAG, whose groups end one chunk late; else after the group)
   if (C::LAG && QP == C::CPF - 1 && a.leaf_ids && !a.ids_vec)
-    flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, io.r0w, tb - (C::CPF - 1) * TC);
+    flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, io, tb - (C::CPF - 1) * TC);
 }
 
 // Chunks of 8 trees (DEFER): the lines that ended at tree tb + 3 of the
 // chunk with index QX in its group (first tree tb) leave, then the ids of
 // the chunk's last four trees take their slots.
-template <int QX>
-__device__ __forceinline__ void fast_deferred(const FastArgs &a, IdPack &ids, int tb, const IdOut &io) {
+template <int QX, class P>
+__device__ __forceinline__ void fast_deferred(const FastArgs &a, P &ids, int tb, const IdOut &io) {
   constexpr int kC = (QX * 8 + 4) & 31;  // slot of tree tb + 3 - 31
   uint32_t m = (uint32_t)(a.id_phase >> (8 * (kC >> 2))) & 0xffu;
   while (m) {
@@ -332,16 +462,17 @@ __device__ __forceinline__ void fast_deferred(const FastArgs &a, IdPack &ids, in
     m &= m - 1;
     id_pass(a.leaf_ids, a.n_rows, a.out.T, io, ids, rho, tb + 3, kC, io.t_begin);
   }
-  ids[QX][2] = ids.pend[0];
-  ids[QX][3] = ids.pend[1];
+  put_pending<QX>(ids);
 }
 
 template <int MODE, int LG, int KM, int ROWS, int BUDGET, int B, int Q>
 __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbuf)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
                                            double (&acc)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::KMAX],
-                                           IdPack &ids, int &cls, int &dep, float2 (&vh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::VH],
-                                           uint2 (&lh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::LH], const IdOut &io) {
+                                           typename FastCfg<MODE, LG, KM, ROWS, BUDGET>::Pack &ids, int &cls, int &dep,
+                                           float2 (&vh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::VH],
+                                           uint2 (&lh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::LH],
+                                           float (&gv)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::GVH], const IdOut &io) {
   using C = FastCfg<MODE, LG, KM, ROWS, BUDGET>;
   constexpr int TC = C::TC;
   constexpr int TB = C::TB;
@@ -383,8 +514,7 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
       if (__builtin_popcount(m_in) == 1 && __builtin_popcount(m_end) == 1) {
         id_pass2<kQX>(a.leaf_ids, a.n_rows, a.out.T, io, ids, __builtin_ctz(m_in), tb + 3, kCI, __builtin_ctz(m_end),
                       tb + TC - 1, kC, io.t_begin);
-        ids[kQX][2] = ids.pend[0];
-        ids[kQX][3] = ids.pend[1];
+        put_pending<kQX>(ids);
       } else {
         fast_deferred<kQX>(a, ids, tb, io);
         for (uint32_t m = m_end; m; m &= m - 1)
@@ -399,7 +529,7 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   const unsigned char *base = reinterpret_cast<const unsigned char *>(tbuf[B]);
   const unsigned char *xb = reinterpret_cast<const unsigned char *>(xs);
   uint32_t s[TC];
-  if (MODE == 0) {
+  if (MODE == 0 || MODE == 3) {
     // Software-pipelined in issue order: LDS reads complete in order, so the
     // node reads of all TC trees go first, then their feature reads, then
     // each tree's step immediately issues its next node read; every wait is
@@ -462,8 +592,19 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   // read before the first leaf-id store: a load issued behind a store would
   // also wait for the store to complete.
   uint2 lrs[TC];
+  if (C::GV) {
+    // the leaf slots are the ids; the previous chunk's values (read a walk
+    // ago) are added in tree order, then this chunk's are read
 #pragma unroll
-  for (int g = 0; g < TC; ++g) {
+    for (int g = 0; g < TC; ++g) {
+      const uint32_t slot = (s[g] >> 3) & ((1u << LG) - 1u);
+      lrs[g] = make_uint2(0u, slot);
+      acc[0] += (double)gv[g < C::GVH ? g : 0];
+      gv[g < C::GVH ? g : 0] = a.leafv[((size_t)(t0 + g) << LG) | slot];
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < TC && !C::GV; ++g) {
     if (MODE == 2)
       lrs[g] = a.leaf[(size_t)(t0 + g) * (1u << LG) + ((s[g] >> 3) & ((1u << LG) - 1u))];
     else
@@ -524,13 +665,15 @@ template <int MODE, int LG, int KM, int ROWS, int BUDGET, int Q>
 __device__ __forceinline__ void fast_group(const FastArgs &a, int c0, uint4 (*tbuf)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::CHUNK16],
                                            const float *xs, uint32_t lane4,
                                            double (&acc)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::KMAX],
-                                           IdPack &ids, int &cls, int &dep, float2 (&vh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::VH],
-                                           uint2 (&lh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::LH], const IdOut &io) {
+                                           typename FastCfg<MODE, LG, KM, ROWS, BUDGET>::Pack &ids, int &cls, int &dep,
+                                           float2 (&vh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::VH],
+                                           uint2 (&lh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::LH],
+                                           float (&gv)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::GVH], const IdOut &io) {
   using C = FastCfg<MODE, LG, KM, ROWS, BUDGET>;
   if constexpr (Q < C::CPF) {
     fast_chunk<MODE, LG, KM, ROWS, BUDGET, C::BUFS == 2 ? (Q & 1) : 0, Q>(a, c0 + Q, tbuf, xs, lane4, acc, ids,
-                                                                           cls, dep, vh, lh, io);
-    fast_group<MODE, LG, KM, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls, dep, vh, lh, io);
+                                                                           cls, dep, vh, lh, gv, io);
+    fast_group<MODE, LG, KM, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls, dep, vh, lh, gv, io);
   }
 }
 
@@ -573,7 +716,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   double acc[C::KMAX];
 #pragma unroll
   for (int k = 0; k < C::KMAX; ++k) acc[k] = 0.0;
-  IdPack ids;
+  typename C::Pack ids;
   int cls = C::MULTI && !a.vec ? a.tree_class[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
   int dep = MODE != 0 ? a.tree_depth[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
   float2 vh[C::VH];
@@ -582,10 +725,14 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   uint2 lh[C::LH];
 #pragma unroll
   for (int g = 0; g < C::LH; ++g) lh[g] = make_uint2(0u, 0u);
-  const IdOut io = make_id_out<ROWS>(a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], c_begin * C::TC);
+  float gv[C::GVH];
+#pragma unroll
+  for (int g = 0; g < C::GVH; ++g) gv[g] = 0.0f;
+  const IdOut io = make_id_out<ROWS>(a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], c_begin * C::TC,
+                                     (uint32_t)a.id_base);
   for (int c = c_begin; c < a.n_chunks; c += C::CPF) {  // chunk counts are multiples of CPF
-    fast_group<MODE, LG, KM, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, vh, lh, io);
-    if (!C::LAG && a.leaf_ids && !a.ids_vec) flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, io.r0w, c * C::TC);
+    fast_group<MODE, LG, KM, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, vh, lh, gv, io);
+    if (!C::LAG && a.leaf_ids && !a.ids_vec) flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, io, c * C::TC);
   }
   if constexpr (C::DEFER && !C::LAG)  // the last chunk's inside lines and ids
     if (io.on) fast_deferred<C::CPF - 1>(a, ids, a.n_chunks * C::TC - C::TC, io);
@@ -610,6 +757,10 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
     fast_leaves<MODE, LG, KM, ROWS, BUDGET, C::CPF - 1>(a, last, t_last, acc, ids, cls, io);
     if constexpr (C::DEFER)
       if (io.on) fast_deferred<C::CPF - 1>(a, ids, t_last, io);
+  }
+  if (C::GV) {  // the last chunk's values
+#pragma unroll
+    for (int g = 0; g < C::GVH; ++g) acc[0] += (double)gv[g];
   }
   if (C::VHOLD && a.vec) {  // the last chunk's 2-vector leaves
 #pragma unroll

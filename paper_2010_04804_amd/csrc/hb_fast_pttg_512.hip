@@ -1,0 +1,10 @@
+// hb_fast_pttg_512.hip -- instantiations of the fast PerfectTreeTraversal
+// kernel with the leaf values in global memory (mode 3) for 512-row
+// workgroups: one output, depth <= 8, 8-bit leaf-slot ids.
+#include "hb_fast.h"
+
+namespace hb {
+
+FastFn fast_pttg_kernel_512(int lg, int km) { return km == 1 ? pick_fast<3, 1, 512, kFastTableSmall>(lg) : nullptr; }
+
+}  // namespace hb

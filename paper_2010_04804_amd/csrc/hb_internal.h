@@ -46,7 +46,8 @@ constexpr int kFastIdGroup = 32;
 // bytes per row of a workgroup.
 constexpr int kFastIdStageBytes = 2 * 8 * kFastIdGroup * 2 / 64;
 constexpr int fast_node_bytes(int mode) { return (void)mode, 8; }
-constexpr int fast_tree_bytes(int mode, int lg) { return (1 << lg) * (fast_node_bytes(mode) + (mode == 2 ? 0 : 8)); }
+// modes 2 (TT) and 3 (PTT) keep the leaves apart, in global memory
+constexpr int fast_tree_bytes(int mode, int lg) { return (1 << lg) * (fast_node_bytes(mode) + (mode >= 2 ? 0 : 8)); }
 // TT leaf records up to this size stay in global memory (mode 2); measured
 // on 1M rows: leaf-wise 500 trees (2 MB) 5.1 -> 3.9 ms, 3500 depth-8 trees
 // (14 MB, L2 misses on every leaf read) 16.6 -> 21.6 ms.
@@ -62,6 +63,15 @@ constexpr bool fast_single(int tree_bytes, int budget = kFastTableLds) {
 constexpr int fast_bufs(int tree_bytes, int budget = kFastTableLds) { return fast_single(tree_bytes, budget) ? 1 : 2; }
 constexpr int fast_tc(int tree_bytes, int budget = kFastTableLds) {
   return fast_pow2_fit(budget / fast_bufs(tree_bytes, budget), tree_bytes);
+}
+// PTT with the leaves in global memory (mode 3) always double-buffers: its
+// blocks are half the size, so the same budget holds two chunks of the
+// trees a mode-0 chunk holds, and a chunk needs one barrier instead of two.
+constexpr int fast_bufs_m(int mode, int tree_bytes, int budget = kFastTableLds) {
+  return mode == 3 ? 2 : fast_bufs(tree_bytes, budget);
+}
+constexpr int fast_tc_m(int mode, int tree_bytes, int budget = kFastTableLds) {
+  return mode == 3 ? fast_pow2_fit(budget / 2, tree_bytes) : fast_tc(tree_bytes, budget);
 }
 // Kernels with the half budget trade chunk size for occupancy: wider
 // workgroups, or wider feature tiles, leave room for half the chunk. Blocks
@@ -123,8 +133,11 @@ struct PttDev {
                             // consecutive trees interleaved slot by slot
   const uint32_t *leaf_pk;  // [T][2^D][leaf_pk_words]: values, then caller id
   const uint4 *last_il;     // D >= 1 and leaf_dim <= 2: the last level with its leaves, else nullptr
-  const uint4 *fast;        // packed blocks (mode 0, lg = D), or nullptr
-  int32_t fast_chunks;
+  const uint4 *fast;        // packed blocks (mode 0 or 3, lg = D), or nullptr
+  const float *fast_leafv;  // mode 3: [padded T][2^D] leaf values; else nullptr
+  int32_t fast_mode;        // 0: each block holds its leaf records; 3: leaf values apart, ids = slot + id_base
+  int32_t fast_chunks;      // padded trees / fast_tc_m(fast_mode, block bytes)
+  int32_t id_base;          // mode 3: caller id of leaf slot 0 in every tree
 };
 
 // TreeTraversal tensors (Table 5, Algorithm 2), breadth-first per tree with

@@ -494,10 +494,11 @@ __global__ __launch_bounds__(64 * J) void split_finish_kernel(const double *part
 // kNotApplicable to fall back to traverse_kernel.
 // vec, vec_stride: vector leaves' values [T][vec_stride][leaf_dim] (the
 // strategy's leaf-value table), or nullptr for scalar leaves.
-int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int chunks, const int32_t *depth,
-                const float *vec, int vec_stride, const EnsembleDev &e, const float *X, int64_t n_rows,
+int launch_fast(int mode, int lg, const uint4 *blocks, const void *leaf, int chunks, const int32_t *depth,
+                const float *vec, int vec_stride, int id_base, const EnsembleDev &e, const float *X, int64_t n_rows,
                 float *scores, int32_t *leaf_ids, const Launch &ws, hipStream_t stream, std::string *err) {
-  if (!blocks || (mode == 2 && !leaf) || lg < 1 || lg > kFastMaxLg) return kNotApplicable;
+  if (!blocks || (mode >= 2 && !leaf) || lg < 1 || lg > kFastMaxLg) return kNotApplicable;
+  if (mode == 3 && (e.n_outputs != 1 || e.leaf_dim != 1 || lg > 8)) return kNotApplicable;
   if (e.leaf_dim != 1 && (!vec || e.leaf_dim != e.n_outputs || e.leaf_dim > HB_MAX_OUTPUTS)) return kNotApplicable;
   const int lds_max = max_dynamic_lds(err);
   if (lds_max <= 0) return HB_ERR_HIP;
@@ -530,12 +531,16 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int ch
                                {256, kFastTableLds, fast_ttg_kernel_256},
                                {256, kFastTableSmall, fast_ttg_kernel_256s},
                                {128, kFastTableSmall, fast_ttg_kernel_128}};
-  const Shape *shapes = mode == 0 ? kPtt : mode == 1 ? kTt : kTtg;
-  const int n_shapes = mode == 0 ? 7 : 6;
+  static const Shape kPttg[] = {{1024, kFastTableSmall, fast_pttg_kernel_1024},
+                                {512, kFastTableSmall, fast_pttg_kernel_512},
+                                {256, kFastTableSmall, fast_pttg_kernel_256},
+                                {128, kFastTableSmall, fast_pttg_kernel_128}};
+  const Shape *shapes = mode == 0 ? kPtt : mode == 1 ? kTt : mode == 2 ? kTtg : kPttg;
+  const int n_shapes = mode == 0 ? 7 : mode == 3 ? 4 : 6;
   // static LDS: the chunk buffer(s) and the leaf-id staging (16-bit ids of a
   // 32-tree group per row); dynamic LDS: the feature tile (F x rows floats)
   auto lds_of = [&](const Shape &sh) {
-    const size_t table = (size_t)fast_bufs(tb, sh.budget) * fast_tc(tb, sh.budget) * tb;
+    const size_t table = (size_t)fast_bufs_m(mode, tb, sh.budget) * fast_tc_m(mode, tb, sh.budget) * tb;
     return table + (size_t)sh.rows * kFastIdStageBytes + (size_t)e.n_cols * sh.rows * 4;
   };
   int best = -1;
@@ -555,7 +560,8 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int ch
   // Below four waves per CU the row-parallel walk is latency-bound; the
   // trees-across-lanes kernel then wins when the node tables are small
   // enough to stay in L1 (depth-3 forests: 0.9 vs 1.5 ms at 1M rows).
-  const int64_t table_bytes = (int64_t)chunks * fast_tc(tb) * (tb + (mode == 2 ? (8 << lg) : 0));
+  const int64_t table_bytes =
+      (int64_t)chunks * fast_tc_m(mode, tb) * (tb + (mode == 2 ? (8 << lg) : mode == 3 ? (4 << lg) : 0));
   if (best_waves < 4 && table_bytes <= (int64_t)64 << 10) return kPreferLanes;
   const int rows = shapes[best].rows;
   const size_t xbytes = (size_t)e.n_cols * rows * 4;
@@ -576,9 +582,11 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int ch
     a.LD = e.leaf_dim;
   }
   a.blocks = blocks;
-  a.leaf = leaf;
+  a.leaf = mode == 2 ? static_cast<const uint2 *>(leaf) : nullptr;
+  a.leafv = mode == 3 ? static_cast<const float *>(leaf) : nullptr;
+  a.id_base = id_base;
   a.tree_depth = depth;
-  a.n_chunks = (int)((int64_t)chunks * fast_tc(tb) / fast_tc(tb, shapes[best].budget));
+  a.n_chunks = (int)((int64_t)chunks * fast_tc_m(mode, tb) / fast_tc_m(mode, tb, shapes[best].budget));
   a.ids_vec = (e.n_trees % 4 == 0) && ((reinterpret_cast<uintptr_t>(leaf_ids) & 15) == 0);
   if (a.ids_vec) {
     // row r's ids begin at int b + r T of a line (b the output's offset in
@@ -601,7 +609,7 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const uint2 *leaf, int ch
   // depth-12 and 7-class models from 10K to 64K rows, this picks the fastest
   // count or one within 3% of it.
   int split = 1;
-  const int cpf = kFastIdGroup / fast_tc(tb, shapes[best].budget);  // chunks per 32 trees
+  const int cpf = kFastIdGroup / fast_tc_m(mode, tb, shapes[best].budget);  // chunks per 32 trees
   const int64_t groups = a.n_chunks / cpf;
   if (ws.ptr && n_rows <= kSplitMaxRows && groups >= 2) {
     int cus = 0, dev = 0;
@@ -761,8 +769,8 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
   int rc = kNotApplicable;
   if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsPtt)) rc = launch_lanes(true, a, ws, stream, err);
   if (rc == kNotApplicable)
-    rc = launch_fast(0, t.depth, t.fast, nullptr, t.fast_chunks, nullptr, t.leaf_value, 1 << t.depth, e, X, n_rows,
-                     scores, leaf_ids, ws, stream, err);
+    rc = launch_fast(t.fast_mode, t.depth, t.fast, t.fast_leafv, t.fast_chunks, nullptr, t.leaf_value, 1 << t.depth,
+                     t.id_base, e, X, n_rows, scores, leaf_ids, ws, stream, err);
   if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(true, a, ws, stream, err);
   if (rc != kNotApplicable) return rc;
   return launch_traverse(true, a, ws, stream, err);
@@ -791,7 +799,7 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
   int rc = kNotApplicable;
   if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsTt)) rc = launch_lanes(false, a, ws, stream, err);
   if (rc == kNotApplicable)
-    rc = launch_fast(t.fast_mode, t.fast_lg, t.fast, t.fast_leaf, t.fast_chunks, t.depth, t.leaf_value, t.n_pad, e, X,
+    rc = launch_fast(t.fast_mode, t.fast_lg, t.fast, t.fast_leaf, t.fast_chunks, t.depth, t.leaf_value, t.n_pad, 0, e, X,
                      n_rows, scores, leaf_ids, ws, stream, err);
   if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(false, a, ws, stream, err);
   if (rc != kNotApplicable) return rc;

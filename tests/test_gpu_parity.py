@@ -142,23 +142,32 @@ def test_tree_split_uses_and_reuses_the_workspace(strategy):
         check(model, X, scores.cpu().numpy(), ids.cpu().numpy(), f"ws {strategy}/{n}/{avail}")
 
 
-@pytest.mark.parametrize("n_trees", [500, 64, 48, 40, 36, 3500])
-def test_leaf_id_lines_at_any_offset(n_trees):
+@pytest.mark.parametrize("n_trees,depth,heap", [(500, 8, True), (64, 6, False), (48, 6, False), (40, 6, False),
+                                                 (36, 6, False), (3500, 8, False), (64, 8, True), (40, 8, True),
+                                                 (48, 6, True), (36, 5, True)])
+def test_leaf_id_lines_at_any_offset(n_trees, depth, heap):
     """Leaf ids leave as whole 128-byte lines whose first tree depends on the
     output's offset within a line and on the row (tree counts with 1, 2, 4 or
     8 line phases); every offset gives the oracle's ids, and nothing outside
-    the output changes. Offsets of 1 and 2 ints take the unaligned path."""
+    the output changes. Offsets of 1 and 2 ints take the unaligned path.
+    Heap-ordered perfect trees of depth <= 8 (heap=True) keep their leaf
+    values apart and form ids from 8-bit leaf slots; permuted numberings keep
+    16-bit ids: both with 8-tree chunks (one or several line phases per line
+    tree) and with 16-tree chunks (depth 5 and 6)."""
     if n_trees == 500:
         model, h = handle(2)
     else:
-        rng = np.random.Generator(np.random.PCG64(700 + n_trees))
-        depth = 8 if n_trees == 3500 else 6
+        rng = np.random.Generator(np.random.PCG64(700 + n_trees + 1000 * heap))
         model = synth.perfect_forest(rng, n_trees, depth, 28, lambda r, f: r.standard_normal(f.size),
                                      lambda r, n: r.normal(0.0, 0.05, n))
         model.update(n_outputs=1, tree_class=None, aggregation="sum", transform="none", base_score=None)
-        model = synth.permute_nodes(model, n_trees)
+        if not heap:
+            model = synth.permute_nodes(model, n_trees)
         h = hb.compile(model, device=0)
     sizes = [3001] if n_trees == 3500 else [3001, 20_000]
+    if n_trees != 3500:
+        ptt_kernels = [p["kernel"] for p in h.plan(20_000, "ptt")]
+        assert any(k.startswith("fast_kernel<3,") for k in ptt_kernels) == heap, ptt_kernels
     for n in sizes:
         X = synth.make_rows(2, n)
         Xd = torch.from_numpy(X).cuda()
