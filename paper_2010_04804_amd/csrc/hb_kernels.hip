@@ -441,6 +441,191 @@ LanesFn pick_lanes_r(int kmax, bool vec) {
 // 500 perfect depth-8 trees cross at about 16K rows, 7 x 500 such trees with
 // seven outputs at 12K-14K, and the leaf-wise depth-12 trees (TT, whose
 // row-parallel walk is slower) at about 20K.
+// Rows across lanes, for inputs too wide for the row-parallel tile: a
+// workgroup stages RW whole rows in LDS and each wave walks TPW = 64 / RW
+// trees for all RW rows at once (lane = tree slot q, row r), so the RW
+// lanes of one tree read its nodes and leaves together and share the
+// cache lines: a level-L read of a wave touches at most min(RW, 2^L) lines
+// of each of its trees, against up to one line per lane when every lane
+// walks its own tree. Trees come from the per-tree tables (node [T][slots]
+// and leaf_pk), which stay in L2. Each lane walks ILP consecutive trees
+// together (ILP node reads in flight: the walk waits on L2 latency), adds
+// their values for its row in tree order and stores their ids as 16-byte
+// pieces; the per-lane sums
+// of a row are added in a fixed order (the wave's tree slots, then the
+// waves) before finish_row, so results are reproducible run to run.
+constexpr int kRowsThreads = 1024;
+constexpr int kRowsIlp = 4;
+// The rows of one tile in registers, between their global load (issued
+// before the previous tile is walked) and their LDS store (after it): lane i
+// holds 16-byte pieces i, i + 1024, ... of the tile's RW x F floats, which
+// are contiguous in X when the tile is the whole rows (no column map).
+template <int RW>
+struct RowsPrefetch {
+  static constexpr int PER = (RW * 2000 / 4 + kRowsThreads - 1) / kRowsThreads;  // up to 2000 features at RW rows
+  float4 v[PER];
+  __device__ __forceinline__ void load(const float *X, int64_t r0, int nr, int F) {
+    const int n4 = nr * F / 4;
+    const float4 *src = reinterpret_cast<const float4 *>(X + r0 * F);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = i * kRowsThreads + (int)threadIdx.x;
+      v[i] = e < n4 ? src[e] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    }
+  }
+  __device__ __forceinline__ void store(float *xs, int nr, int F) const {
+    const int n4 = RW * F / 4;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = i * kRowsThreads + (int)threadIdx.x;
+      if (e < n4) reinterpret_cast<float4 *>(xs)[e] = v[i];  // rows past nr hold zeros
+    }
+  }
+};
+
+template <bool PERFECT, int KMAX, bool LEAF_VEC, int RW>
+__global__ __launch_bounds__(kRowsThreads) void rows_kernel(TravArgs a) {
+  constexpr int TPW = 64 / RW;                    // trees of one wave-level read
+  constexpr int WAVES = kRowsThreads / 64;
+  constexpr int PASS = WAVES * TPW * kRowsIlp;  // trees per pass of the workgroup
+  extern __shared__ __align__(16) unsigned char smem[];
+  float *xs = reinterpret_cast<float *>(smem);  // [RW][F]
+  // per-lane sums after the walk, apart from the rows (the next tile's rows
+  // are stored while the sums are read): [WAVES][TPW][RW][KMAX]
+  double *red = reinterpret_cast<double *>(smem + ((size_t)RW * a.F * 4 + 15) / 16 * 16);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int r = lane & (RW - 1), q = lane / RW;
+  const int64_t n_tiles = (a.n_rows + RW - 1) / RW;
+  // a workgroup walks tiles blockIdx.x, + gridDim.x, ...; the next tile's
+  // rows arrive in registers during the walk when the rows are contiguous
+  const bool pf = a.cols == nullptr && a.Fs == a.F && (a.F & 3) == 0 && a.F <= 2000 &&
+                  (reinterpret_cast<uintptr_t>(a.X) & 15) == 0;
+  RowsPrefetch<RW> next;
+  auto stage_rows = [&](int64_t tile) {  // load and store at once (no prefetch)
+    const int64_t r0 = tile * RW;
+    const int nr = (int)min((int64_t)RW, a.n_rows - r0);
+    for (int i = tid; i < RW * a.F; i += kRowsThreads) {
+      const int rr = i / a.F, c = i - rr * a.F;
+      xs[rr * a.F + c] = rr < nr ? xval(a.X + (r0 + rr) * a.Fs, a.cols, c) : 0.0f;
+    }
+  };
+  int64_t tile = blockIdx.x;
+  if (pf) {
+    next.load(a.X, tile * RW, (int)min((int64_t)RW, a.n_rows - tile * RW), a.F);
+    next.store(xs, RW, a.F);
+  } else {
+    stage_rows(tile);
+  }
+  __syncthreads();
+  const int LD = LEAF_VEC ? a.LD : 1;
+  const int pkw = leaf_pk_words(LD);
+  const bool ids_vec = a.leaf_ids != nullptr && (a.T & 3) == 0 && (reinterpret_cast<uintptr_t>(a.leaf_ids) & 15) == 0;
+  for (; tile < n_tiles; tile += gridDim.x) {
+    const int64_t r0 = tile * RW;
+    const int nr = (int)min((int64_t)RW, a.n_rows - r0);
+    const int64_t nt = tile + gridDim.x;
+    if (pf && nt < n_tiles) next.load(a.X, nt * RW, (int)min((int64_t)RW, a.n_rows - nt * RW), a.F);
+    const float *xrow = xs + r * a.F;
+    double acc[KMAX];
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) acc[k] = 0.0;
+    for (int P = 0; P < a.T; P += PASS) {
+      const int t0 = P + wave * (TPW * kRowsIlp) + q * kRowsIlp;  // this lane's first tree
+      if (t0 >= a.T) continue;
+      const uint2 *nb[kRowsIlp];
+      uint32_t idx[kRowsIlp];
+      int levels = PERFECT ? a.depth : 0;
+#pragma unroll
+      for (int j = 0; j < kRowsIlp; ++j) {
+        const int t = min(t0 + j, a.T - 1);  // past the last tree: walk it again, discard
+        nb[j] = a.node + (size_t)t * a.slots;
+        idx[j] = PERFECT ? 1u : 0u;
+        if (!PERFECT) levels = max(levels, a.tree_depth[t]);
+      }
+      for (int lvl = 0; lvl < levels; ++lvl) {
+        uint2 rec[kRowsIlp];
+#pragma unroll
+        for (int j = 0; j < kRowsIlp; ++j) rec[j] = nb[j][idx[j]];
+#pragma unroll
+        for (int j = 0; j < kRowsIlp; ++j) {
+          const uint32_t f = PERFECT ? rec[j].y : (rec[j].y & 0xffffu);
+          const bool go_left = xrow[f] < as_float(rec[j].x);
+          idx[j] = PERFECT ? 2u * idx[j] + (go_left ? 0u : 1u) : (rec[j].y >> 16) - (go_left ? 1u : 0u);
+        }
+      }
+      uint32_t id[kRowsIlp];
+#pragma unroll
+      for (int j = 0; j < kRowsIlp; ++j) {
+        const int t = min(t0 + j, a.T - 1);
+        const uint32_t slot = PERFECT ? idx[j] - (uint32_t)a.leaf_slots : idx[j];
+        const uint32_t *lrec = a.leaf_pk + ((size_t)t * a.leaf_slots + slot) * pkw;
+        const bool live = t0 + j < a.T;
+        if (!LEAF_VEC) {
+          const uint2 v = *reinterpret_cast<const uint2 *>(lrec);
+          if (live) {
+            if (KMAX == 1) {
+              acc[0] += (double)as_float(v.x);
+            } else {
+              const int cls = a.tree_class ? a.tree_class[t] : 0;
+#pragma unroll
+              for (int k = 0; k < KMAX; ++k) acc[k] += k == cls ? (double)as_float(v.x) : 0.0;
+            }
+          }
+          id[j] = v.y;
+        } else {  // KMAX == 2: {v0, v1, id, 0}
+          const uint4 v = *reinterpret_cast<const uint4 *>(lrec);
+          if (live) {
+            acc[0] += (double)as_float(v.x);
+            acc[1] += (double)as_float(v.y);
+          }
+          id[j] = v.z;
+        }
+      }
+      if (a.leaf_ids && r < nr) {
+        int32_t *dst = a.leaf_ids + (r0 + r) * a.T + t0;
+        if (ids_vec && t0 + kRowsIlp <= a.T) {
+#pragma unroll
+          for (int j = 0; j < kRowsIlp; j += 4)
+            __builtin_nontemporal_store(i32x4{(int)id[j], (int)id[j + 1], (int)id[j + 2], (int)id[j + 3]},
+                                        reinterpret_cast<i32x4 *>(dst + j));
+        } else {
+#pragma unroll
+          for (int j = 0; j < kRowsIlp; ++j)
+            if (t0 + j < a.T) dst[j] = (int32_t)id[j];
+        }
+      }
+    }
+    // per-row totals in a fixed order: over the wave's tree slots, then the waves
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) red[((wave * TPW + q) * RW + r) * KMAX + k] = acc[k];
+    __syncthreads();  // every wave is done with this tile's rows and sums
+    if (nt < n_tiles) {
+      if (pf)
+        next.store(xs, RW, a.F);
+      else
+        stage_rows(nt);
+    }
+    if (tid < nr) {
+      double tot[KMAX];
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k) {
+        double v = 0.0;
+#pragma unroll 1
+        for (int w = 0; w < WAVES * TPW; ++w) v += red[(w * RW + tid) * KMAX + k];
+        tot[k] = v;
+      }
+      finish_row<KMAX>(OutArgs{a.scores, a.T, a.K, a.aggregation, a.transform, a.base_score}, tot, r0 + tid);
+    }
+    __syncthreads();  // the next tile's rows are in place; its sums may overwrite these
+  }
+}
+
+// Bytes of LDS rows_kernel needs: the RW rows and the per-lane sums.
+inline size_t rows_lds(int F, int RW, int kmax) {
+  return ((size_t)RW * (size_t)F * 4 + 15) / 16 * 16 + (size_t)kRowsThreads * kmax * 8;
+}
+
 constexpr int64_t kLanesMaxRowsPtt = 12288;
 constexpr int64_t kLanesMaxRowsTt = 16384;
 // With a workspace the tree-split row-parallel kernel takes over from here
@@ -677,6 +862,64 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const void *leaf, int chu
   return HB_OK;
 }
 
+using RowsFn = void (*)(TravArgs);
+template <bool PERFECT, int RW>
+RowsFn pick_rows(int kmax, bool vec) {
+  if (vec) return kmax == 2 ? rows_kernel<PERFECT, 2, true, RW> : nullptr;
+  return kmax == 1 ? rows_kernel<PERFECT, 1, false, RW> : kmax == 2 ? rows_kernel<PERFECT, 2, false, RW> : nullptr;
+}
+
+// Launches rows_kernel for batches whose rows are too wide for the
+// row-parallel tile: 16 rows per workgroup (8 when 16 do not fit in LDS),
+// one or two outputs, and enough rows for a workgroup per CU; returns
+// kNotApplicable otherwise (the trees-across-lanes kernel then runs).
+constexpr int64_t kRowsMinRows = 4096;
+int launch_rows(bool perfect, const TravArgs &a, const Launch &L, hipStream_t stream, std::string *err) {
+  if (a.n_rows < kRowsMinRows) return kNotApplicable;
+  const bool vec = a.LD > 1;
+  const int kmax = kmax_for(vec ? a.LD : a.K);
+  if (kmax > 2 || (vec && a.LD != 2)) return kNotApplicable;
+  const int lds_max = max_dynamic_lds(err);
+  if (lds_max <= 0) return HB_ERR_HIP;
+  int RW = 16;
+  if (rows_lds(a.F, RW, kmax) > (size_t)lds_max) RW = 8;
+  if (rows_lds(a.F, RW, kmax) > (size_t)lds_max) return kNotApplicable;
+  RowsFn fn = perfect ? (RW == 16 ? pick_rows<true, 16>(kmax, vec) : pick_rows<true, 8>(kmax, vec))
+                      : (RW == 16 ? pick_rows<false, 16>(kmax, vec) : pick_rows<false, 8>(kmax, vec));
+  if (!fn) return kNotApplicable;
+  const size_t lds = rows_lds(a.F, RW, kmax);
+  // persistent: as many workgroups as run at once (the row tiles are dealt
+  // out round-robin), so each loads the next tile's rows during its walk
+  int cus = 0, dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) {
+    *err = "hipDeviceGetAttribute(MultiprocessorCount) failed";
+    return HB_ERR_HIP;
+  }
+  const int64_t tiles = (a.n_rows + RW - 1) / RW;
+  const int64_t blocks = std::min(tiles, (int64_t)cus * (int64_t)std::max<size_t>(1, (size_t)lds_max / lds));
+  if (L.plan) {
+    plan_line(L.plan,
+              std::string("rows_kernel<") + tf(perfect) + ", " + std::to_string(kmax) + ", " + tf(vec) + ", " +
+                  std::to_string(RW) + ">",
+              blocks, 1, kRowsThreads, lds);
+    return HB_OK;
+  }
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)lds);
+  if (e != hipSuccess) {
+    *err = std::string("hipFuncSetAttribute: ") + hipGetErrorString(e);
+    return HB_ERR_HIP;
+  }
+  hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kRowsThreads), lds, stream, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) {
+    *err = std::string("kernel launch: ") + hipGetErrorString(e);
+    return HB_ERR_HIP;
+  }
+  return HB_OK;
+}
+
 // True when traverse_kernel would have to read the features from global
 // memory (rows too wide for its LDS tile) or cannot stage a single tree:
 // lanes_kernel is then the better choice at any batch size, since it stages a
@@ -767,11 +1010,15 @@ int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_
   a.leaf_slots = 1 << t.depth;
   if (a.slots < 2) a.slots = 2;  // depth 0 still stores two (unused) records per tree
   int rc = kNotApplicable;
-  if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsPtt)) rc = launch_lanes(true, a, ws, stream, err);
+  // rows too wide for the row-parallel tile: rows across lanes from a
+  // workgroup per CU up, else (and for smaller batches) trees across lanes
+  const bool wide = rows_too_wide(a, err);
+  if (wide) rc = launch_rows(true, a, ws, stream, err);
+  if (rc == kNotApplicable && n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsPtt)) rc = launch_lanes(true, a, ws, stream, err);
   if (rc == kNotApplicable)
     rc = launch_fast(t.fast_mode, t.depth, t.fast, t.fast_leafv, t.fast_chunks, nullptr, t.leaf_value, 1 << t.depth,
                      t.id_base, e, X, n_rows, scores, leaf_ids, ws, stream, err);
-  if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(true, a, ws, stream, err);
+  if (rc == kPreferLanes || (rc == kNotApplicable && wide)) rc = launch_lanes(true, a, ws, stream, err);
   if (rc != kNotApplicable) return rc;
   return launch_traverse(true, a, ws, stream, err);
 }
@@ -797,11 +1044,15 @@ int launch_tt(const EnsembleDev &e, const TtDev &t, const float *X, int64_t n_ro
   a.slots = t.n_pad;
   a.leaf_slots = t.n_pad;
   int rc = kNotApplicable;
-  if (n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsTt)) rc = launch_lanes(false, a, ws, stream, err);
+  // rows too wide for the row-parallel tile: rows across lanes from a
+  // workgroup per CU up, else (and for smaller batches) trees across lanes
+  const bool wide = rows_too_wide(a, err);
+  if (wide) rc = launch_rows(false, a, ws, stream, err);
+  if (rc == kNotApplicable && n_rows <= (ws.ptr ? kLanesMaxRowsSplit : kLanesMaxRowsTt)) rc = launch_lanes(false, a, ws, stream, err);
   if (rc == kNotApplicable)
     rc = launch_fast(t.fast_mode, t.fast_lg, t.fast, t.fast_leaf, t.fast_chunks, t.depth, t.leaf_value, t.n_pad, 0, e, X,
                      n_rows, scores, leaf_ids, ws, stream, err);
-  if (rc == kPreferLanes || (rc == kNotApplicable && rows_too_wide(a, err))) rc = launch_lanes(false, a, ws, stream, err);
+  if (rc == kPreferLanes || (rc == kNotApplicable && wide)) rc = launch_lanes(false, a, ws, stream, err);
   if (rc != kNotApplicable) return rc;
   return launch_traverse(false, a, ws, stream, err);
 }

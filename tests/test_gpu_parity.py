@@ -627,6 +627,80 @@ def test_full_size_every_row(cfg):
         assert np.all((sc >= 0) & (sc <= 1))
 
 
+def test_full_size_wide_forest_every_row():
+    """The 2000-feature random forest (workload 3) at its benchmark size,
+    100,000 rows, in the benchmark's launch configuration (AUTO, leaf ids, no
+    workspace: rows across lanes, 16 rows per workgroup): every row's class
+    probabilities and leaf ids against the oracle."""
+    model, h = handle(3)
+    n = 100_000
+    X = synth.make_rows(3, n)
+    assert [p["kernel"] for p in h.plan(n, "auto")] == ["rows_kernel<true, 2, true, 16>"], h.plan(n, "auto")
+    say("full size every row", 3, n)
+    Xd = torch.from_numpy(X).cuda()
+    s, ids = hb.predict(h, Xd, strategy="auto", workspace=False)
+    torch.cuda.synchronize()
+    for lo in range(0, n, 25_000):
+        check(model, X[lo:lo + 25_000], s[lo:lo + 25_000].cpu().numpy(), ids[lo:lo + 25_000].cpu().numpy(),
+              f"cfg3-100K rows {lo}..")
+
+
+def _wide_model(kind, n_trees, depth, leafwise, seed):
+    """Trees over 2000 features, too wide for the row-parallel tile: scalar
+    leaves with one output, scalar leaves with two classes (tree t to class
+    t mod 2), or 2-vector leaves averaged."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    F = 2000
+    ld = 2 if kind == "vector" else 1
+    thr = lambda r, f: r.uniform(-1.0, 1.0, f.size)
+    leaves = (lambda r, n: np.stack([1 - r.random(n), r.random(n)], 1)) if ld == 2 else (lambda r, n: r.normal(0, .1, n))
+    if leafwise:
+        model = synth.leafwise_forest(rng, n_trees, 64, depth, 0.7, F, thr, lambda r, n: r.normal(0, .1, n))
+        if ld == 2:  # probability pairs at the leaves
+            p = np.random.Generator(np.random.PCG64(seed + 1)).random(model["feature"].size).astype(np.float32)
+            model["leaf_value"] = np.stack([1 - p, p], 1).reshape(-1)
+    else:
+        model = synth.perfect_forest(rng, n_trees, depth, F, thr, leaves, leaf_dim=ld)
+    model.update(n_outputs=2 if kind != "scalar" else 1, leaf_dim=ld,
+                 tree_class=(np.arange(n_trees) % 2).astype(np.int32) if kind == "classes" else None,
+                 aggregation="mean" if kind == "vector" else "sum",
+                 transform="softmax" if kind == "classes" else "none", base_score=None)
+    return model
+
+
+@pytest.mark.parametrize("strategy", ["ptt", "tt"])
+@pytest.mark.parametrize("kind,n_trees,depth,leafwise,n", [
+    ("vector", 500, 8, False, 4096), ("vector", 37, 6, False, 4111), ("scalar", 61, 7, False, 4100),
+    ("classes", 130, 5, False, 5003), ("scalar", 90, 10, True, 4099), ("vector", 41, 9, True, 4500)])
+def test_rows_across_lanes(kind, n_trees, depth, leafwise, n, strategy):
+    """Rows too wide for the row-parallel tile, at batches of a workgroup per
+    CU or more, take rows_kernel (16 rows per workgroup, each wave walking
+    four trees for all 16 rows): tree counts that do not fill a pass,
+    ragged row tiles, scalar, two-class and vector leaves, perfect and
+    leaf-wise trees, on PTT and TT, and leaf ids at an unaligned offset."""
+    model = _wide_model(kind, n_trees, depth, leafwise, 900 + n_trees)
+    h = hb.compile(model, device=0)
+    if not h.info()["feasible"][strategy]:
+        pytest.skip("strategy infeasible")
+    kernels = [p["kernel"] for p in h.plan(n, strategy)]
+    assert kernels[0].startswith("rows_kernel<"), kernels
+    X = np.random.Generator(np.random.PCG64(n)).uniform(-1, 1, (n, 2000)).astype(np.float32)
+    say("rows across lanes", kind, n_trees, depth, leafwise, n, strategy)
+    scores, ids = run(h, X, strategy, workspace=False)
+    check(model, X, scores, ids, f"rows {kind}/{n_trees}/{strategy}/{n}")
+    # leaf ids one int past a 16-byte boundary: one int32 store per id
+    Xd = torch.from_numpy(X).cuda()
+    buf = torch.full((n * n_trees + 8,), -7, dtype=torch.int32, device="cuda")
+    sc = torch.empty((n, model["n_outputs"]), dtype=torch.float32, device="cuda")
+    hb.predict_ptr(h, Xd.data_ptr(), n, sc.data_ptr(), buf.data_ptr() + 4, strategy,
+                   torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    b = buf.cpu().numpy()
+    assert b[0] == -7 and np.all(b[1 + n * n_trees:] == -7)
+    assert np.array_equal(b[1:1 + n * n_trees].reshape(n, n_trees), ids)
+    h.close()
+
+
 def test_full_size_multiclass_sampled():
     """The 7-class model at 1,000,000 rows (14 GB of leaf ids on the device):
     every output of a seeded sample of 40,000 rows, the first and last
