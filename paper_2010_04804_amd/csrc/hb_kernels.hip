@@ -533,32 +533,33 @@ __global__ __launch_bounds__(kRowsThreads) void rows_kernel(TravArgs a) {
     for (int P = 0; P < a.T; P += PASS) {
       const int t0 = P + wave * (TPW * kRowsIlp) + q * kRowsIlp;  // this lane's first tree
       if (t0 >= a.T) continue;
-      const uint2 *nb[kRowsIlp];
-      uint32_t idx[kRowsIlp];
+      uint32_t idx[kRowsIlp];  // record index within the node table (32 bits: tables below 32 GB)
       int levels = PERFECT ? a.depth : 0;
 #pragma unroll
       for (int j = 0; j < kRowsIlp; ++j) {
         const int t = min(t0 + j, a.T - 1);  // past the last tree: walk it again, discard
-        nb[j] = a.node + (size_t)t * a.slots;
-        idx[j] = PERFECT ? 1u : 0u;
+        idx[j] = (uint32_t)t * (uint32_t)a.slots + (PERFECT ? 1u : 0u);
         if (!PERFECT) levels = max(levels, a.tree_depth[t]);
       }
       for (int lvl = 0; lvl < levels; ++lvl) {
         uint2 rec[kRowsIlp];
 #pragma unroll
-        for (int j = 0; j < kRowsIlp; ++j) rec[j] = nb[j][idx[j]];
+        for (int j = 0; j < kRowsIlp; ++j) rec[j] = a.node[idx[j]];
 #pragma unroll
         for (int j = 0; j < kRowsIlp; ++j) {
           const uint32_t f = PERFECT ? rec[j].y : (rec[j].y & 0xffffu);
           const bool go_left = xrow[f] < as_float(rec[j].x);
-          idx[j] = PERFECT ? 2u * idx[j] + (go_left ? 0u : 1u) : (rec[j].y >> 16) - (go_left ? 1u : 0u);
+          // PTT: heap index h of tree t at record t S + h, so 2 h + b is at 2 (t S + h) - t S + b
+          const uint32_t tb = (uint32_t)min(t0 + j, a.T - 1) * (uint32_t)a.slots;
+          idx[j] = PERFECT ? 2u * idx[j] - tb + (go_left ? 0u : 1u) : tb + (rec[j].y >> 16) - (go_left ? 1u : 0u);
         }
       }
       uint32_t id[kRowsIlp];
 #pragma unroll
       for (int j = 0; j < kRowsIlp; ++j) {
         const int t = min(t0 + j, a.T - 1);
-        const uint32_t slot = PERFECT ? idx[j] - (uint32_t)a.leaf_slots : idx[j];
+        const uint32_t h = idx[j] - (uint32_t)t * (uint32_t)a.slots;  // heap index (PTT) or node (TT)
+        const uint32_t slot = PERFECT ? h - (uint32_t)a.leaf_slots : h;
         const uint32_t *lrec = a.leaf_pk + ((size_t)t * a.leaf_slots + slot) * pkw;
         const bool live = t0 + j < a.T;
         if (!LEAF_VEC) {
