@@ -135,9 +135,10 @@ def _event_ms(stream, fn, reps):
 
 def run_sweep():
     """Strategy crossover: every feasible strategy on 100-tree forests of depth
-    3, 7 and 12 over 200 features, at batch sizes 1 to 1M (scores only, as a
-    scoring service would call it). One JSON line per point, then a summary
-    of the fastest strategy per (model, batch) beside the selector's choice."""
+    3, 7, 11 and 12 over 200 or 28 features, at batch sizes 1 to 1M (scores
+    only, as a scoring service would call it), each with and without a
+    tree-split workspace. One JSON line per point, then a summary of the
+    fastest strategy per (model, batch) beside the selector's choice."""
     import torch
 
     import paper_2010_04804_amd as hb
@@ -146,10 +147,16 @@ def run_sweep():
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
     nmax = max(synth.SWEEP["batches"])
-    X = torch.from_numpy(synth.sweep_rows(nmax)).to(dev)
     scores = torch.empty((nmax, 1), dtype=torch.float32, device=dev)
     table = {}
+    xs = {}
     for kind in synth.SWEEP["models"]:
+        F = synth.sweep_features(kind)
+        if F not in xs:
+            xs.clear()
+            torch.cuda.empty_cache()
+            xs[F] = torch.from_numpy(synth.sweep_rows(nmax, F)).to(dev)
+        X = xs[F]
         h = hb.compile(synth.sweep_model(kind), device=0)
         info = h.info()
         for n in synth.SWEEP["batches"]:
@@ -157,16 +164,25 @@ def run_sweep():
             for s in ("gemm", "ptt", "tt"):
                 if not info["feasible"][s]:
                     continue
-                fn = lambda: hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), None, s,
-                                            stream.cuda_stream)
-                fn()
-                torch.cuda.synchronize()
-                probe = _event_ms(stream, fn, 1)
-                reps = int(min(200, max(3, 100.0 / max(probe, 1e-3))))
-                ms = _event_ms(stream, fn, reps)
-                row[s] = ms
-                print(json.dumps({"sweep": kind, "batch": n, "strategy": s, "us": round(ms * 1e3, 2),
-                                  "rows_per_s": n / (ms * 1e-3), "reps": reps}), flush=True)
+                # each strategy as hb_predict, and as hb_predict_ws with the
+                # workspace it can use (the better of the two counts)
+                nws = hb.workspace_bytes(h, n, s)
+                ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+                best_ms = None
+                for use_ws in ((False, True) if nws else (False,)):
+                    fn = lambda: hb.predict_ptr(h, X.data_ptr(), n, scores.data_ptr(), None, s,
+                                                stream.cuda_stream, ws.data_ptr() if use_ws else None,
+                                                nws if use_ws else 0)
+                    fn()
+                    torch.cuda.synchronize()
+                    probe = _event_ms(stream, fn, 1)
+                    reps = int(min(200, max(3, 100.0 / max(probe, 1e-3))))
+                    ms = _event_ms(stream, fn, reps)
+                    print(json.dumps({"sweep": kind, "batch": n, "strategy": s, "workspace": use_ws,
+                                      "us": round(ms * 1e3, 2), "rows_per_s": n / (ms * 1e-3), "reps": reps}),
+                          flush=True)
+                    best_ms = ms if best_ms is None else min(best_ms, ms)
+                row[s] = best_ms
             best = min(row, key=row.get)
             table[f"{kind}/{n}"] = {"best": best, "auto": h.select(n),
                                     "us": {k: round(v * 1e3, 2) for k, v in row.items()}}
@@ -180,7 +196,7 @@ def run_latency(config, batches=(1, 10, 100, 1_000, 10_000, 30_000)):
     plus a stream synchronisation timed on the host, both for the eager call
     and for a replay of it captured in a HIP graph. The selector's strategy
     runs with and without a tree-split workspace (hb_predict_ws), and GEMM
-    beside it."""
+    beside it, also both ways."""
     import statistics
 
     import torch
@@ -197,7 +213,7 @@ def run_latency(config, batches=(1, 10, 100, 1_000, 10_000, 30_000)):
     side = torch.cuda.Stream(dev)
     out = {}
     for n in batches:
-        for strat, use_ws in (("auto", False), ("auto", True), ("gemm", False)):
+        for strat, use_ws in (("auto", False), ("auto", True), ("gemm", False), ("gemm", True)):
             s_name = h.select(n) if strat == "auto" else strat
             if not info["feasible"][s_name]:
                 continue

@@ -210,8 +210,11 @@ HB_API int64_t hb_workspace_bytes(const hb_handle *h, int64_t n_rows, int strate
 /* The strategy hb_predict would run for this batch size under AUTO: the
  * selector of Sec. 5.1 ("Execution Strategy Selection"), which picks among
  * GEMM, TreeTraversal and PerfectTreeTraversal by tree depth and batch
- * size, with thresholds re-measured on this device. Returns the enum value,
- * or a negative error code for a NULL handle. */
+ * size, re-measured on this device: PTT while it holds the trees (depth up
+ * to HB_PTT_MAX_DEPTH) and they are near-perfect (balance <= 4) or the
+ * batch is small (<= 256 rows), TT otherwise; GEMM only when forced or when
+ * nothing else holds the model. Returns the enum value, or a negative error
+ * code for a NULL handle. */
 HB_API int hb_select_strategy(const hb_handle *h, int64_t n_rows);
 
 /* Shape statistics, feasibility and table sizes of a compiled handle: the

@@ -164,22 +164,25 @@ struct hb_handle {
 namespace {
 
 // Sec. 5.1 picks GEMM for shallow trees or small batches, PTT up to depth 10
-// and TT beyond. Re-measured on MI355X over 100-tree forests of depth 3, 7
-// and 12 at batch sizes 1 to 1M: PTT is fastest or tied everywhere except on
-// unbalanced trees, where TT wins from about a thousand rows on, and GEMM is
-// slower than PTT at every depth and batch size (here small batches go to the
-// trees-across-lanes walk, which is a few microseconds at batch 1). So AUTO
-// takes PTT while the padded perfect tree stays within a small multiple of
-// the real node count and TT otherwise; GEMM only when asked for, or when
-// nothing else can hold the model.
-constexpr int32_t kAutoPttMaxDepth = 10;
+// and TT beyond. Re-measured on MI355X (the crossover sweep: 100-tree
+// forests of depth 3, 7, 11 and 12, perfect and leaf-wise, over 200 and 28
+// features, batch 1 to 1M, each strategy with and without a tree-split
+// workspace): PTT is fastest, or within a few percent, on every near-perfect
+// forest at every batch size and depth up to 12 (with narrow rows a depth-11
+// or -12 PTT walk is 2x to 3x faster than TT's from 10K rows on); on
+// unbalanced trees PTT's trees-across-lanes walk still wins up to a few
+// hundred rows, TT from about a thousand on; GEMM is slower than PTT at every
+// point (its tree split brings batch 1 of a 500-tree depth-8 forest from 305
+// to 12 us, against 6 us for PTT). So AUTO takes PTT while the padded
+// perfect tree stays within a small multiple of the real node count, or for
+// small batches; TT otherwise; GEMM only when asked for, or when nothing else
+// can hold the model.
 constexpr double kAutoPttMaxBalance = 4.0;
+constexpr int64_t kAutoPttSmallBatch = 256;
 
 int select_strategy(const hb_handle *h, int64_t n_rows) {
-  (void)n_rows;
   const hb_info &I = h->info;
-  if (I.feasible[HB_STRATEGY_PTT] && I.max_depth <= kAutoPttMaxDepth &&
-      I.balance <= kAutoPttMaxBalance)
+  if (I.feasible[HB_STRATEGY_PTT] && (I.balance <= kAutoPttMaxBalance || n_rows <= kAutoPttSmallBatch))
     return HB_STRATEGY_PTT;
   if (I.feasible[HB_STRATEGY_TT]) return HB_STRATEGY_TT;
   if (I.feasible[HB_STRATEGY_PTT]) return HB_STRATEGY_PTT;
@@ -815,6 +818,10 @@ int64_t hb_workspace_bytes(const hb_handle *h, int64_t n_rows, int strategy) {
   if (strategy == HB_STRATEGY_AUTO) strategy = hb_select_strategy(h, n_rows);
   const bool fast = (strategy == HB_STRATEGY_PTT && !h->ptt_fast.empty()) ||
                     (strategy == HB_STRATEGY_TT && !h->tt_fast.empty());
+  // GEMM splits on its 16-row tiles: every tree one shape of 256 leaves
+  const bool tiles = strategy == HB_STRATEGY_GEMM && h->gemm_n_shapes == 1 && h->gemm_k_pad == 256 &&
+                     h->gemm_l_pad == 256;
+  if (tiles) return hb::gemm_split_workspace_bytes(n_rows, h->info.n_trees, h->info.n_outputs);
   return fast ? hb::split_workspace_bytes(n_rows, h->info.n_trees, h->info.n_outputs) : 0;
 }
 

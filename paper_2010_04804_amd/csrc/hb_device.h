@@ -204,6 +204,11 @@ struct FastArgs {
 
 using FastFn = void (*)(FastArgs);
 
+// Adds the partial sums of a tree split ([split][n_rows][K] doubles) in a
+// fixed order and finishes the rows; with plan, describes the launch instead.
+int split_finish(const double *partial, int split, int64_t n_rows, const OutArgs &out, std::string *plan,
+                 hipStream_t stream, std::string *err);
+
 // Accumulators per row of a fast kernel: 1 (one output), 2 (two outputs,
 // e.g. binary classifiers with probability-vector leaves) or HB_MAX_OUTPUTS.
 

@@ -60,6 +60,11 @@ struct GemmArgs {
   const int32_t *leaf_id;   // [T][l_pad]
   int32_t k_pad, l_pad;
   int32_t ids_vec;
+  // tree split (small batches, gemm_tile_kernel): workgroup (x, y) takes
+  // trees [y * split, min((y + 1) * split, T)) of row tile x and stores its
+  // raw sums in partial[y][row][K]; 0 = every tree, rows finished in place
+  int32_t split;
+  double *partial;
 };
 
 // LDS bytes of one tree's node records: groups of 16 records (128 B) are
@@ -598,8 +603,8 @@ __device__ __forceinline__ void tile_pair(const GemmArgs &a, int t, const float 
                                           unsigned char (*bt)[2][kTileRows * kTileBStride], uint2 (*rtab)[2][256],
                                           int (*red)[2][16][kTileRows], uint2 (&rset)[2][2], const v4i (&ctr)[4][4],
                                           const v4i (&b4)[4], TileLeaf<KMODE> &pend,
-                                          double (&acc)[TileLeaf<KMODE>::KMAX], int64_t r0) {
-  const int T = a.out.T;
+                                          double (&acc)[TileLeaf<KMODE>::KMAX], int64_t r0, int T) {
+  // T: one past this workgroup's last tree
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, r16 = lane & 15;
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
@@ -620,7 +625,7 @@ __device__ __forceinline__ void tile_pair(const GemmArgs &a, int t, const float 
   lds_sync();
   // the leaves of trees t and t+1, by waves t mod 4 and t+1 mod 4 (a wave's
   // previous lookup is consumed first)
-  const int u = wave - (t & 3);
+  const int u = wave - (t & 3);  // (split parts start at multiples of 4 trees)
   if ((u == 0 || (u == 1 && t + 1 < T)) && lane < kTileRows) {
     tile_leaf_consume<KMODE>(a, pend, acc, r0 + lane);
     int col = red[P][u][0][lane];
@@ -642,7 +647,9 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
   __shared__ __align__(16) uint2 rtab[2][2][256];
   __shared__ int red[2][2][16][kTileRows];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, r16 = lane & 15;
-  const int T = a.out.T;
+  // this workgroup's trees [tb, T): all of them unless the trees are split
+  const int tb = a.split ? (int)blockIdx.y * a.split : 0;
+  const int T = a.split ? min(tb + a.split, a.out.T) : a.out.T;
   const int XS = gemm_tile_xs(a.F);
   float *xs = reinterpret_cast<float *>(smem);
   const int64_t r0 = (int64_t)blockIdx.x * kTileRows;
@@ -673,12 +680,12 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
     for (int kb = 0; kb < 4; ++kb)
       ctr[j][kb] = *reinterpret_cast<const v4i *>(a.ct + (size_t)(lt * 16 + r16) * 256 + kb * 64 + 16 * g4);
   }
-  // records of trees 0-3 in LDS, 4-7 in registers
+  // records of trees tb .. tb+3 in LDS, tb+4 .. tb+7 in registers
   uint2 rset[2][2];
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    rtab[u >> 1][u & 1][tid] = a.node[(size_t)min(u, T - 1) * 256 + tid];
-    rset[u >> 1][u & 1] = a.node[(size_t)min(u + 4, T - 1) * 256 + tid];
+    rtab[u >> 1][u & 1][tid] = a.node[(size_t)min(tb + u, T - 1) * 256 + tid];
+    rset[u >> 1][u & 1] = a.node[(size_t)min(tb + u + 4, T - 1) * 256 + tid];
   }
   lds_sync();
   tile_build2(xs, XS, rtab[0], bt[0]);
@@ -687,9 +694,9 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
 #pragma unroll
   for (int k = 0; k < KMAX; ++k) acc[k] = 0.0;
   TileLeaf<KMODE> pend;
-  for (int t = 0; t < T; t += 4) {
-    tile_pair<KMODE, WIDE, 0>(a, t, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0);
-    if (t + 2 < T) tile_pair<KMODE, WIDE, 1>(a, t + 2, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0);
+  for (int t = tb; t < T; t += 4) {
+    tile_pair<KMODE, WIDE, 0>(a, t, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0, T);
+    if (t + 2 < T) tile_pair<KMODE, WIDE, 1>(a, t + 2, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0, T);
   }
   if (lane < kTileRows) tile_leaf_consume<KMODE>(a, pend, acc, r0 + lane);
   // partial sums in wave order (the feature tile is no longer read)
@@ -707,7 +714,14 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
 #pragma unroll
       for (int k = 0; k < KMAX; ++k) s[k] += part[(w * kTileRows + lane) * KMAX + k];
     }
-    finish_row<KMAX>(a.out, s, r0 + lane);
+    if (a.split) {
+      double *dst = a.partial + ((size_t)blockIdx.y * a.n_rows + r0 + lane) * a.out.K;
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k)
+        if (k < a.out.K) dst[k] = s[k];
+    } else {
+      finish_row<KMAX>(a.out, s, r0 + lane);
+    }
   }
 }
 
@@ -772,7 +786,7 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
   std::string name = "gemm_kernel<" + std::to_string(kb) + ", " + (ct ? "true" : "false") + ", " +
                      (xl ? "true" : "false") + ", " + std::to_string(kmode) + ", " + std::to_string(rows) + ", " +
                      (cols && !xl ? "true" : "false") + ">";
-  bool piped = false;
+  bool piped = false, tile_wide = false;
   if (rows == 512 && ct && xl && kb == 4 && t.l_pad == 256) {
     // the software-pipelined kernel needs no node chunks; it runs only with
     // 512-row workgroups (two waves per SIMD), since wherever a 256-row
@@ -796,6 +810,7 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
     const size_t tile_static = (size_t)4 * kTileRows * kTileBStride + 4 * 256 * 8 + 4 * 16 * kTileRows * 4;
     if (tile_dyn + tile_static <= (size_t)lds_max) {
       const bool wide = 2 * (tile_dyn + tile_static) > (size_t)lds_max;  // one workgroup per CU
+      tile_wide = wide;
       fn = wide ? (kmode == 0 ? gemm_tile_kernel<0, true> : kmode == 1 ? gemm_tile_kernel<1, true> : gemm_tile_kernel<2, true>)
                 : (kmode == 0 ? gemm_tile_kernel<0, false> : kmode == 1 ? gemm_tile_kernel<1, false> : gemm_tile_kernel<2, false>);
       dyn = tile_dyn;
@@ -828,8 +843,43 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
   a.l_pad = t.l_pad;
   a.ids_vec = (e.n_trees % 4 == 0) && ((reinterpret_cast<uintptr_t>(leaf_ids) & 15) == 0);
   const int64_t blocks = (n_rows + rows - 1) / rows;
+  // Small batch with a workspace on the 16-row tiles: divide the trees, in
+  // groups of 4, among `parts` workgroups per tile (a batch of a few tiles
+  // otherwise walks every tree on a few CUs), then add the partial sums in
+  // a fixed order. With `resident` tile workgroups at once the call takes
+  // about ceil(parts x tiles / resident) rounds of `per` groups each plus a
+  // fixed cost per workgroup (C^T, feature tile) worth about
+  // kTileOverheadGroups groups; take the fewest parts reaching the least.
+  int split = 1;
+  if (rows == kTileRows && L.ptr && n_rows <= kGemmSplitMaxRows) {
+    const int64_t groups = (e.n_trees + kGemmSplitGroup - 1) / kGemmSplitGroup;
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) {
+      *err = "hipDeviceGetAttribute(MultiprocessorCount) failed";
+      return HB_ERR_HIP;
+    }
+    const int64_t resident = (int64_t)cus * (tile_wide ? 1 : 2);
+    const int64_t row_bytes = n_rows * e.n_outputs * 8;
+    constexpr int64_t kTileOverheadGroups = 8;
+    int64_t best_cost = (blocks + resident - 1) / resident * (groups + kTileOverheadGroups), best_per = groups;
+    for (int64_t p = 2; p <= groups; ++p) {
+      const int64_t per = (groups + p - 1) / p, parts = (groups + per - 1) / per;
+      if (parts * row_bytes > L.bytes) break;
+      const int64_t cost = (parts * blocks + resident - 1) / resident * (per + kTileOverheadGroups);
+      if (cost < best_cost) {
+        best_cost = cost;
+        best_per = per;
+      }
+    }
+    if (best_per < groups) {
+      split = (int)((groups + best_per - 1) / best_per);
+      a.split = (int)best_per * kGemmSplitGroup;
+      a.partial = static_cast<double *>(L.ptr);
+    }
+  }
   if (L.plan) {
-    plan_line(L.plan, name, blocks, 1, threads, dyn);
+    plan_line(L.plan, name, blocks, split, threads, dyn);
+    if (split > 1) return split_finish(nullptr, split, n_rows, a.out, L.plan, stream, err);
     return HB_OK;
   }
   hipError_t rc = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
@@ -838,12 +888,13 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
     *err = std::string("hipFuncSetAttribute: ") + hipGetErrorString(rc);
     return HB_ERR_HIP;
   }
-  hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(threads), dyn, stream, a);
+  hipLaunchKernelGGL(fn, dim3((unsigned)blocks, (unsigned)split), dim3(threads), dyn, stream, a);
   rc = hipGetLastError();
   if (rc != hipSuccess) {
     *err = std::string("kernel launch: ") + hipGetErrorString(rc);
     return HB_ERR_HIP;
   }
+  if (split > 1) return split_finish(a.partial, split, n_rows, a.out, nullptr, stream, err);
   return HB_OK;
 }
 

@@ -184,6 +184,16 @@ struct Launch {
   std::string *plan = nullptr;
 };
 
+// GEMM tree split: batches up to kGemmSplitMaxRows rows may divide their
+// trees, in groups of kGemmSplitGroup, among the 16-row tile workgroups.
+constexpr int64_t kGemmSplitMaxRows = 4096;
+constexpr int kGemmSplitGroup = 4;
+inline int64_t gemm_split_workspace_bytes(int64_t n_rows, int32_t n_trees, int32_t n_outputs) {
+  if (n_rows < 1 || n_rows > kGemmSplitMaxRows) return 0;
+  const int64_t groups = (n_trees + kGemmSplitGroup - 1) / kGemmSplitGroup;
+  return groups < 2 ? 0 : groups * n_rows * n_outputs * 8;
+}
+
 // The error message hb_last_error() returns on this thread; returns code.
 int set_error(int code, const std::string &msg);
 // The HIP device of a compiled handle (-1: host-only handle or NULL).

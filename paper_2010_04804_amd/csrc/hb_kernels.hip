@@ -676,6 +676,35 @@ __global__ __launch_bounds__(64 * J) void split_finish_kernel(const double *part
   finish_row<KMAX>(out, tot, row);
 }
 
+// Adds the partial sums of a tree split ([split][n_rows][K] doubles) in a
+// fixed order and finishes the rows (or, with plan, describes that launch).
+int launch_split_finish(const double *partial, int split, int64_t n_rows, const OutArgs &out, std::string *plan,
+                        hipStream_t stream, std::string *err) {
+  const unsigned fin_rows = (unsigned)((n_rows + 63) / 64);
+  const bool multi = out.K > 1;
+  // 16 waves per 64 rows for scalar outputs, 8 for several (their sums take
+  // K times the LDS: at most 64 KiB)
+  if (plan) {
+    if (multi)
+      plan_line(plan, "split_finish_kernel<16, 8>", fin_rows, 1, 64 * 8, (size_t)8 * out.K * 64 * 8);
+    else
+      plan_line(plan, "split_finish_kernel<1, 16>", fin_rows, 1, 64 * 16, (size_t)16 * 64 * 8);
+    return HB_OK;
+  }
+  if (multi)
+    hipLaunchKernelGGL((split_finish_kernel<HB_MAX_OUTPUTS, 8>), dim3(fin_rows), dim3(64 * 8),
+                       (size_t)8 * out.K * 64 * sizeof(double), stream, partial, split, n_rows, out);
+  else
+    hipLaunchKernelGGL((split_finish_kernel<1, 16>), dim3(fin_rows), dim3(64 * 16), (size_t)16 * 64 * sizeof(double),
+                       stream, partial, split, n_rows, out);
+  const hipError_t rc = hipGetLastError();
+  if (rc != hipSuccess) {
+    *err = std::string("kernel launch: ") + hipGetErrorString(rc);
+    return HB_ERR_HIP;
+  }
+  return HB_OK;
+}
+
 // Launches the fast kernel when its layout exists and its LDS fits; returns
 // kNotApplicable to fall back to traverse_kernel.
 // vec, vec_stride: vector leaves' values [T][vec_stride][leaf_dim] (the
@@ -991,6 +1020,11 @@ TravArgs common_args(const EnsembleDev &e, const float *X, int64_t n, float *sco
 }
 
 }  // namespace
+
+int split_finish(const double *partial, int split, int64_t n_rows, const OutArgs &out, std::string *plan,
+                 hipStream_t stream, std::string *err) {
+  return launch_split_finish(partial, split, n_rows, out, plan, stream, err);
+}
 
 int launch_ptt(const EnsembleDev &e, const PttDev &t, const float *X, int64_t n_rows, float *scores,
                int32_t *leaf_ids, const Launch &ws, hipStream_t stream, std::string *err) {

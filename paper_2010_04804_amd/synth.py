@@ -226,22 +226,31 @@ def make_model(cfg: int) -> dict:
 # from 1 to 1M. Depth 12 comes both perfect (4096 leaves, no GEMM) and
 # leaf-wise with 256 leaves (the unbalanced shape GEMM can still hold).
 SWEEP = dict(
-    models=("perfect-d3", "perfect-d7", "perfect-d12", "leafwise-d12"),
+    models=("perfect-d3", "perfect-d7", "perfect-d12", "leafwise-d12",
+            "perfect-d3-n28", "perfect-d11-n28", "perfect-d12-n28", "leafwise-d12-n28"),
     batches=(1, 10, 100, 1_000, 10_000, 100_000, 1_000_000),
     n_trees=100, n_features=200, seed=6,
 )
 
 
+def sweep_features(kind: str) -> int:
+    """Input columns of a sweep model: 200, or 28 for the ``-n28`` models."""
+    return 28 if kind.endswith("-n28") else SWEEP["n_features"]
+
+
 def sweep_model(kind: str) -> dict:
-    """One model of the crossover sweep: ``perfect-d{3,7,12}`` or
-    ``leafwise-d12``; thresholds N(0,1), leaves N(0, 0.05), SUM -> sigmoid."""
+    """One model of the crossover sweep: ``perfect-d{3,7,11,12}`` or
+    ``leafwise-d12`` over 200 features, or with ``-n28`` over 28 (narrow
+    rows: the row-parallel kernels' tile holds them); thresholds N(0,1),
+    leaves N(0, 0.05), SUM -> sigmoid."""
     rng, _ = _streams(SWEEP["seed"] + SWEEP["models"].index(kind))
-    T, F = SWEEP["n_trees"], SWEEP["n_features"]
+    T, F = SWEEP["n_trees"], sweep_features(kind)
+    base = kind[:-len("-n28")] if kind.endswith("-n28") else kind
     thr = lambda r, f: r.standard_normal(f.size)
     leaves = lambda r, n: r.normal(0.0, 0.05, n)
-    if kind.startswith("perfect-d"):
-        m = perfect_forest(rng, T, int(kind[len("perfect-d"):]), F, thr, leaves)
-    elif kind == "leafwise-d12":
+    if base.startswith("perfect-d"):
+        m = perfect_forest(rng, T, int(base[len("perfect-d"):]), F, thr, leaves)
+    elif base == "leafwise-d12":
         m = leafwise_forest(rng, T, 256, 12, 0.7, F, thr, leaves)
     else:
         raise ValueError(f"unknown sweep model {kind}")
@@ -249,10 +258,10 @@ def sweep_model(kind: str) -> dict:
     return m
 
 
-def sweep_rows(n_rows: int) -> np.ndarray:
-    """Input rows of the crossover sweep: N(0,1) over 200 features."""
+def sweep_rows(n_rows: int, n_features: int = SWEEP["n_features"]) -> np.ndarray:
+    """Input rows of the crossover sweep: N(0,1) over 200 (or 28) features."""
     _, rng = _streams(SWEEP["seed"])
-    return np.ascontiguousarray(_f32(rng.standard_normal((n_rows, SWEEP["n_features"]))))
+    return np.ascontiguousarray(_f32(rng.standard_normal((n_rows, n_features))))
 
 
 # A binary random-forest classifier over narrow rows (the shape of the

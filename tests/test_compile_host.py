@@ -142,6 +142,14 @@ def test_selector_choices():
     assert host(shallow).select(1000) == "ptt"
     assert host(synth.sweep_model("leafwise-d12")).select(1000) == "tt"
     assert host(synth.sweep_model("perfect-d7")).select(1) == "ptt"
+    # batch-aware since the sweep with depth-11/12 models and narrow rows:
+    # near-perfect trees take PTT up to its depth limit (12), unbalanced
+    # trees PTT up to 256 rows (the trees-across-lanes walk) and TT above
+    assert host(synth.sweep_model("perfect-d12")).select(1_000_000) == "ptt"
+    assert host(synth.sweep_model("perfect-d11-n28")).select(100_000) == "ptt"
+    assert host(synth.sweep_model("leafwise-d12-n28")).select(256) == "ptt"
+    assert host(synth.sweep_model("leafwise-d12-n28")).select(257) == "tt"
+    assert host(synth.make_model(5)).select(100) == "ptt"
     assert hb.compile(synth.make_model(2), strategy="tt", device=-1).select(10) == "tt"
 
 

@@ -118,6 +118,27 @@ def test_tree_split_parity(cfg, n, strategy):
     assert np.array_equal(i_ws, i_no)
 
 
+@pytest.mark.parametrize("cfg,n", [(2, 1), (2, 2), (2, 17), (2, 100), (2, 1000), (2, 4096), (4, 1), (4, 300),
+                                   (1, 33)])
+def test_gemm_tree_split(cfg, n):
+    """GEMM with a workspace (hb_predict_ws) on batches of up to 4,096 rows
+    divides the trees, in groups of four, among 16-row tile workgroups and
+    adds the partial sums in a second kernel: the oracle bar, and leaf ids
+    equal to the unsplit call's (Algorithm 1, Table 3)."""
+    model, h = handle(cfg)
+    say("gemm tree split", cfg, n)
+    nbytes = hb.workspace_bytes(h, n, "gemm")
+    kernels = [p["kernel"] for p in h.plan(n, "gemm", nbytes)]
+    if cfg != 1:  # config 1's depth-3 trees have no 256-leaf tiles
+        assert nbytes > 0 and kernels[0].startswith("gemm_tile_kernel<") and kernels[-1].startswith("split_finish"), kernels
+    X = synth.make_rows(cfg, n)
+    s_ws, i_ws = run(h, X, "gemm")
+    s_no, i_no = run(h, X, "gemm", workspace=False)
+    check(model, X, s_ws, i_ws, f"gemm split cfg{cfg}/{n}")
+    check(model, X, s_no, i_no, f"gemm unsplit cfg{cfg}/{n}")
+    assert np.array_equal(i_ws, i_no)
+
+
 @pytest.mark.parametrize("strategy", ["ptt", "tt"])
 def test_tree_split_uses_and_reuses_the_workspace(strategy):
     """The split writes its partial sums into the caller's workspace; one
