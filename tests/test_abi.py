@@ -137,7 +137,9 @@ def test_workspace_bytes_and_errors():
     assert hb.workspace_bytes(h, 65536, "tt") == 16 * 65536 * 8
     assert hb.workspace_bytes(h, 65537, "ptt") == 0  # large batches never split
     assert hb.workspace_bytes(h, 0, "ptt") == 0
-    assert hb.workspace_bytes(h, 1000, "gemm") == 0
+    # GEMM splits its 16-row tiles in groups of 4 trees, up to 4,096 rows
+    assert hb.workspace_bytes(h, 1000, "gemm") == 125 * 1000 * 8
+    assert hb.workspace_bytes(h, 4097, "gemm") == 0
     assert lib.hb_workspace_bytes(h.ptr, -1, 0) == -1
     assert lib.hb_workspace_bytes(None, 10, 0) == -1
     assert lib.hb_workspace_bytes(h.ptr, 10, 9) == -1
