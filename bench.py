@@ -120,6 +120,61 @@ def cpu_baseline(model, cfg, seconds_target=15.0):
             "host_cpus": os.cpu_count()}
 
 
+def mfma_peak_measured():
+    """Sustained dense int8 matrix-core rate of this GPU in ops/s, from the
+    probe library built beside libhb.so (None if it is not built)."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2010_04804_amd", "libhb_probe.so")
+    if not os.path.exists(path):
+        return None
+    lib = ctypes.CDLL(path)
+    lib.hb_probe_mfma_i8.restype = ctypes.c_int
+    lib.hb_probe_mfma_i8.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    v = ctypes.c_double(0.0)
+    rc = lib.hb_probe_mfma_i8(0, ctypes.byref(v))
+    return v.value if rc == 0 else None
+
+
+def end_to_end(hb, h, X, n, info, leaves, strategy, dev, reps=3):
+    """The whole request from host memory: X copied in from pinned host
+    memory, the scoring call, scores (and leaf ids) copied back to pinned host
+    memory, one stream, timed from the first copy's start to the last copy's
+    end (HIP events), median of a few repetitions; the three parts are timed
+    by events between them. The paper times whole runs of its frameworks the
+    same way (processor time), Sec. 6."""
+    import torch
+    stream = torch.cuda.current_stream(dev)
+    Xh = torch.from_numpy(X).pin_memory()
+    K, T = info["n_outputs"], info["n_trees"]
+    sh = torch.empty((n, K), dtype=torch.float32).pin_memory()
+    ih = torch.empty((n, T), dtype=torch.int32).pin_memory() if leaves else None
+    Xd = torch.empty_like(Xh, device=dev)
+    sd = torch.empty((n, K), dtype=torch.float32, device=dev)
+    idd = torch.empty((n, T), dtype=torch.int32, device=dev) if leaves else None
+    runs = []
+    for _ in range(reps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record(stream)
+        Xd.copy_(Xh, non_blocking=True)
+        ev[1].record(stream)
+        hb.predict_ptr(h, Xd.data_ptr(), n, sd.data_ptr(), idd.data_ptr() if leaves else None, strategy,
+                       stream.cuda_stream)
+        ev[2].record(stream)
+        sh.copy_(sd, non_blocking=True)
+        if leaves:
+            ih.copy_(idd, non_blocking=True)
+        ev[3].record(stream)
+        torch.cuda.synchronize()
+        runs.append([ev[0].elapsed_time(ev[3]), ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]),
+                     ev[2].elapsed_time(ev[3])])
+    runs.sort()
+    tot, h2d, kern, d2h = runs[len(runs) // 2]
+    del Xh, sh, ih, Xd, sd, idd
+    torch.cuda.empty_cache()
+    return {"ms": tot, "rows_per_s": n / (tot * 1e-3), "h2d_ms": h2d, "kernel_ms": kern, "d2h_ms": d2h,
+            "note": "inputs from and outputs to pinned host memory over PCIe; not the bench value"}
+
+
 def _event_ms(stream, fn, reps):
     """Average time of ``reps`` back-to-back calls of fn, HIP events on ``stream``."""
     import torch
@@ -356,6 +411,7 @@ def main():
     ap.add_argument("--no-leaves", action="store_true", help="scores only")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--only-main", action="store_true", help="skip the other strategies")
+    ap.add_argument("--no-e2e", action="store_true", help="skip the end-to-end timing with host copies")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (to scale HBM byte counters)")
     ap.add_argument("--sweep", action="store_true",
@@ -409,27 +465,39 @@ def main():
         hb.predict_ptr(h, Xd.data_ptr(), n, scores.data_ptr(),
                        ids.data_ptr() if ids is not None else None, strat, stream.cuda_stream)
 
+    per_call = {}
+
     def timed(strat, steps, warmup):
-        """Average launch time in ms, HIP events recorded on the launch stream."""
+        """Average launch time in ms, HIP events recorded on the launch stream
+        around the K back-to-back calls; an event between every two calls
+        also gives the per-call median and minimum (per_call[strat])."""
         for _ in range(warmup):
             step(strat)
         torch.cuda.synchronize()
-        ev0 = torch.cuda.Event(enable_timing=True)
-        ev1 = torch.cuda.Event(enable_timing=True)
-        ev0.record(stream)
-        for _ in range(steps):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        evs[0].record(stream)
+        for i in range(steps):
             step(strat)
-        ev1.record(stream)
+            evs[i + 1].record(stream)
         torch.cuda.synchronize()
-        return ev0.elapsed_time(ev1) / steps
+        calls = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(steps))
+        per_call[strat] = {"median_ms": calls[len(calls) // 2] if steps % 2 else 0.5 * (calls[steps // 2 - 1] + calls[steps // 2]),
+                           "min_ms": calls[0]}
+        return evs[0].elapsed_time(evs[-1]) / steps
+
+    mfma_measured = mfma_peak_measured()
 
     def roofline(strat, ms):
         if strat == "gemm":
             ops = gemm_ops(model, n)
             achieved = ops / (ms * 1e-3)
-            return {"bound": "mfma", "achieved": achieved / 1e12, "peak": INT8_PEAK / 1e12,
-                    "unit": "TOP/s", "frac": achieved / INT8_PEAK, "traffic": None,
-                    "kernel": kernel_label(h, strat, n), "avg_launch_ms": ms, "ops_per_launch": ops}
+            r = {"bound": "mfma", "achieved": achieved / 1e12, "peak": INT8_PEAK / 1e12,
+                 "unit": "TOP/s", "frac": achieved / INT8_PEAK, "traffic": None,
+                 "kernel": kernel_label(h, strat, n), "avg_launch_ms": ms, "ops_per_launch": ops}
+            if mfma_measured:
+                r["peak_measured"] = mfma_measured / 1e12
+                r["frac_of_measured"] = achieved / mfma_measured
+            return r
         b = algorithmic_bytes(info, n, leaves, strat)
         achieved = b / (ms * 1e-3)
         return {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
@@ -451,6 +519,7 @@ def main():
                    "max_depth": stats["max_depth"], "features": info["n_features"],
                    "outputs": info["n_outputs"], "strategy": strategy, "leaf_ids": leaves},
         "roofline": roofline(strategy, ms),
+        "per_call_ms": per_call[strategy],
         "timed_wall_s": t_wall,
     }
     if not args.only_main:
@@ -462,8 +531,11 @@ def main():
             mss = timed(s, k, 1)
             print(f"[bench] {s}: {mss:.4f} ms per step", flush=True)
             r = roofline(s, mss)
-            others[s] = {"rows_per_s": n / (mss * 1e-3), "ms": mss, "bound": r["bound"],
+            others[s] = {"rows_per_s": n / (mss * 1e-3), "ms": mss, "per_call_ms": per_call[s], "bound": r["bound"],
                          "achieved": r["achieved"], "unit": r["unit"], "frac": r["frac"]}
+            if "frac_of_measured" in r:
+                others[s]["peak_measured"] = r["peak_measured"]
+                others[s]["frac_of_measured"] = r["frac_of_measured"]
         out["other_strategies"] = others
     if strategy != "gemm" and not args.copy_calibration:
         # HBM fraction also against what a plain 1 GiB device copy reaches here
@@ -483,6 +555,8 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         out["copy_calibration_bytes"] = 1 << 30
+    if not args.no_e2e:
+        out["end_to_end"] = end_to_end(hb, h, X, n, info, leaves, strategy, dev)
     if not args.no_cpu:
         print("[bench] timing the CPU oracle", flush=True)
         out["cpu_baseline"] = cpu_baseline(model, cfg)

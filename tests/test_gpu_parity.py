@@ -118,6 +118,27 @@ def test_tree_split_parity(cfg, n, strategy):
     assert np.array_equal(i_ws, i_no)
 
 
+@pytest.mark.parametrize("strategy", STRATEGIES)
+@pytest.mark.parametrize("cfg,n", [(2, 20_000), (2, 300), (4, 20_000), (4, 300)])
+def test_raw_margins(cfg, n, strategy):
+    """The sigmoid and softmax workloads with the transform removed: the
+    aggregated margins themselves meet the bar against the oracle's raw
+    margins (a saturated sigmoid or a dominant softmax class can hide margin
+    error in the transformed scores). The worst error as a fraction of the
+    tolerance is printed."""
+    model = dict(synth.make_model(cfg))
+    model["transform"] = "none"
+    h = hb.compile(model, device=0)
+    X = synth.make_rows(cfg, n)
+    say("raw margins", cfg, n, strategy)
+    scores, ids = run(h, X, strategy)
+    o_raw, o_out, o_ids = oracle.predict(model, X, n_threads=ORACLE_THREADS)
+    assert np.array_equal(o_raw, o_out)  # no transform: the oracle's output is its margin
+    worst = check(model, X, scores, ids, f"raw cfg{cfg}/{n}/{strategy}")
+    say("worst raw-margin error / tolerance", cfg, strategy, n, f"{worst:.3g}")
+    h.close()
+
+
 @pytest.mark.parametrize("cfg,n", [(2, 1), (2, 2), (2, 17), (2, 100), (2, 1000), (2, 4096), (4, 1), (4, 300),
                                    (1, 33)])
 def test_gemm_tree_split(cfg, n):
