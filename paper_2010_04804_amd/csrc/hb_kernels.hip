@@ -463,14 +463,16 @@ constexpr int kRowsIlp = 4;
 template <int RW>
 struct RowsPrefetch {
   static constexpr int PER = (RW * 2000 / 4 + kRowsThreads - 1) / kRowsThreads;  // up to 2000 features at RW rows
-  float4 v[PER];
+  i32x4 v[PER];
   __device__ __forceinline__ void load(const float *X, int64_t r0, int nr, int F) {
     const int n4 = nr * F / 4;
-    const float4 *src = reinterpret_cast<const float4 *>(X + r0 * F);
+    const i32x4 *src = reinterpret_cast<const i32x4 *>(X + r0 * F);
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int e = i * kRowsThreads + (int)threadIdx.x;
-      v[i] = e < n4 ? src[e] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      // rows are read once: non-temporal, so they pass through L2 without
+      // displacing the tree tables every walk reads
+      v[i] = e < n4 ? __builtin_nontemporal_load(src + e) : i32x4{0, 0, 0, 0};
     }
   }
   __device__ __forceinline__ void store(float *xs, int nr, int F) const {
@@ -478,7 +480,7 @@ struct RowsPrefetch {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int e = i * kRowsThreads + (int)threadIdx.x;
-      if (e < n4) reinterpret_cast<float4 *>(xs)[e] = v[i];  // rows past nr hold zeros
+      if (e < n4) reinterpret_cast<i32x4 *>(xs)[e] = v[i];  // rows past nr hold zeros
     }
   }
 };
