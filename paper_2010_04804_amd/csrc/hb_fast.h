@@ -185,14 +185,19 @@ struct IdOut {
   int64_t r0w;        // first row of the wave
   int t_begin;        // first tree of this workgroup's part
   uint32_t id_base;   // IdPack8: caller id of leaf slot 0
+  // IdPack8 two-line passes, per lane (i = lane / 8, k = lane % 8): 4 k,
+  // 32 i, and the byte offset (8 i T + 4 k) 4 of the four ids it stores
+  uint32_t k4, i32, goff;
 };
 
 template <int ROWS>
-__device__ __forceinline__ IdOut make_id_out(bool on, u32x4 *stage, int t_begin, uint32_t id_base) {
+__device__ __forceinline__ IdOut make_id_out(bool on, u32x4 *stage, int t_begin, uint32_t id_base, int T) {
   // the wave's first row is uniform: keep it (and the per-pass row and tree
   // offsets computed from it) in scalar registers
   const int64_t r0w = (int64_t)blockIdx.x * ROWS + 64 * __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  return IdOut{on, stage, r0w, t_begin, id_base};
+  const uint32_t lane = threadIdx.x & 63u;
+  const uint32_t k4 = 4u * (lane & 7u), i8 = lane & ~7u;
+  return IdOut{on, stage, r0w, t_begin, id_base, k4, 4u * i8, 4u * (i8 * (uint32_t)T + k4)};
 }
 
 // Writes, for the rows of residue rho in this wave, the ids of trees
@@ -322,6 +327,38 @@ __device__ __forceinline__ void id_pass2(int32_t *leaf_ids, int64_t n_rows, int 
 template <int QX>
 __device__ __forceinline__ void id_pass2(int32_t *leaf_ids, int64_t n_rows, int T, const IdOut &io, const IdPack8 &ids,
                                          int rho0, int te0, int c0, int rho1, int te1, int c1, int lo) {
+  // the usual case, uniform over the wave: every row of the wave exists and
+  // both lines lie inside the trees [lo, T), so no lane needs a bound check
+  if (io.r0w + 64 <= n_rows && te0 - 31 >= lo && te1 + 1 <= T) {
+    constexpr int kD = 2 * QX + 1;
+    const uint32_t k4 = io.k4;
+    const bool w0 = k4 == 4u * (uint32_t)rho0, w1 = k4 == 4u * (uint32_t)rho1;
+    if (w0 || w1) {
+      unsigned char *dst = reinterpret_cast<unsigned char *>(io.stage) + (w1 ? 256u : 0u) + io.i32;
+      u32x4 q0 = ids.q[0], q1 = ids.q[1];
+      if (kD >> 2) q1[kD & 3] = w1 ? ids.pend : q1[kD & 3];
+      else q0[kD & 3] = w1 ? ids.pend : q0[kD & 3];
+      // line 1's rows rotated by one quad: the 16 writers touch distinct banks
+      *reinterpret_cast<u32x4 *>(dst + (w1 ? 16u : 0u)) = q0;
+      *reinterpret_cast<u32x4 *>(dst + (w1 ? 0u : 16u)) = q1;
+    }
+    __builtin_amdgcn_wave_barrier();
+    const uint32_t b = io.id_base;
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int c = r ? c1 : c0;
+      const uint32_t v = *reinterpret_cast<const uint32_t *>(reinterpret_cast<const unsigned char *>(io.stage) +
+                                                             256 * r + io.i32 + ((k4 + (uint32_t)(c + 16 * r)) & 31u));
+      const int64_t row0 = io.r0w + (r ? rho1 : rho0);
+      const int tb = (r ? te1 : te0) - 31;
+      unsigned char *line = reinterpret_cast<unsigned char *>(leaf_ids + (row0 * T + tb));
+      const i32x4 o{(int)(b + (v & 0xffu)), (int)(b + ((v >> 8) & 0xffu)), (int)(b + ((v >> 16) & 0xffu)),
+                    (int)(b + (v >> 24))};
+      __builtin_nontemporal_store(o, reinterpret_cast<i32x4 *>(line + io.goff));
+    }
+    __builtin_amdgcn_wave_barrier();
+    return;
+  }
   const int lane = lane_fresh();
   const int k = lane & 7, i = lane >> 3;
   constexpr int kD = 2 * QX + 1;  // the dword trees 4..7 of chunk QX take
@@ -729,7 +766,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
 #pragma unroll
   for (int g = 0; g < C::GVH; ++g) gv[g] = 0.0f;
   const IdOut io = make_id_out<ROWS>(a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], c_begin * C::TC,
-                                     (uint32_t)a.id_base);
+                                     (uint32_t)a.id_base, a.out.T);
   for (int c = c_begin; c < a.n_chunks; c += C::CPF) {  // chunk counts are multiples of CPF
     fast_group<MODE, LG, KM, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, vh, lh, gv, io);
     if (!C::LAG && a.leaf_ids && !a.ids_vec) flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, io, c * C::TC);
