@@ -46,7 +46,7 @@ def load(path: str = _LIB):
     P = ctypes.c_void_p
     i32, i64 = ctypes.c_int32, ctypes.c_int64
     lib.oracle_predict.restype = ctypes.c_int
-    lib.oracle_predict.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P, P, i32, i32, P, P, P,
+    lib.oracle_predict.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P, P, i32, i32, P, P, P, P, P,
                                    i64, P, P, P, i32]
     if path == _LIB:
         _lib = lib
@@ -85,6 +85,12 @@ def predict(model: dict, X: np.ndarray, leaves: bool = True, n_threads: int | No
     bs = None if bs is None else np.ascontiguousarray(bs, np.float32)
     dl = model.get("default_left")
     dl = None if dl is None else np.ascontiguousarray(dl, np.uint8)
+    co = model.get("cat_offset")
+    co = None if co is None else np.ascontiguousarray(co, np.int64)
+    cb = model.get("cat_bits")
+    cb = None if cb is None else np.ascontiguousarray(cb, np.uint32)
+    if co is not None and (cb is None or cb.size == 0):
+        cb = np.zeros(1, np.uint32)
     raw = np.empty((n, K), np.float64)
     out = np.empty((n, K), np.float64)
     ids = np.empty((n, T), np.int32) if leaves else None
@@ -93,7 +99,8 @@ def predict(model: dict, X: np.ndarray, leaves: bool = True, n_threads: int | No
     rc = lib.oracle_predict(T, F, K, int(model["leaf_dim"]), _ptr(arr["off"]), _ptr(arr["feature"]),
                             _ptr(arr["threshold"]), _ptr(arr["left"]), _ptr(arr["right"]),
                             _ptr(arr["value"]), _ptr(tc), AGG[model["aggregation"]],
-                            POST[model["transform"]], _ptr(bs), _ptr(dl), _ptr(X), n, _ptr(raw), _ptr(out),
+                            POST[model["transform"]], _ptr(bs), _ptr(dl), _ptr(co), _ptr(cb), _ptr(X), n,
+                            _ptr(raw), _ptr(out),
                             _ptr(ids), int(n_threads))
     if rc != 0:
         raise ValueError(f"oracle: {ERRORS.get(rc, rc)}")

@@ -22,6 +22,12 @@
  *    missing values to future work (Sec. 4.1 notes they are not supported
  *    yet), and this extension follows the common per-node "missing values go
  *    left" flag of tree learners;
+ *  - categorical splits (also future work in Sec. 4.1): a node may carry a
+ *    category set, a bit set of 32-bit words (bit j of word w is category
+ *    32 w + j); the category of a row is the integer part of a non-negative
+ *    feature value below 32 times the word count, and the row goes left when
+ *    the set holds it; every other value goes right, and NaN is missing as
+ *    above;
  *  - the reported leaf index is the caller's local node id of the leaf;
  *  - ensemble aggregation is SUM or MEAN (the paper's ReduceMean) over
  *    trees, per output column, plus an optional base score; the paper's
@@ -63,6 +69,9 @@ typedef struct {
   int32_t aggregation, transform;
   const float *base_score;         /* [n_outputs] or NULL */
   const uint8_t *default_left;     /* [nodes] or NULL: NaN goes left where 1 */
+  const int64_t *cat_offset;       /* [nodes + 1] or NULL: node i's category set is
+                                      cat_bits[cat_offset[i] .. cat_offset[i + 1]) */
+  const uint32_t *cat_bits;
   const float *X;                  /* [n_rows, n_features] row-major */
   int64_t n_rows;
   double *raw;                     /* [n_rows, n_outputs] before transform */
@@ -82,9 +91,19 @@ static int64_t walk(const oracle_job *J, int32_t t, const float *x) {
     if (++steps > count) return ORACLE_ERR_CYCLE;
     /* Sec. 4.1: every decision node performs a strict < comparison; a
        missing (NaN) value follows the node's default direction if given. */
+    const int64_t node = base + v;
     if (J->default_left && isnan(x[f]))
-      v = J->default_left[base + v] ? J->left[base + v] : J->right[base + v];
-    else if (x[f] < J->threshold[base + v])
+      v = J->default_left[node] ? J->left[node] : J->right[node];
+    else if (J->cat_offset && J->cat_offset[node + 1] > J->cat_offset[node]) {
+      /* categorical node: left when the set holds the row's category */
+      const int64_t words = J->cat_offset[node + 1] - J->cat_offset[node];
+      int in_set = 0;
+      if (x[f] >= 0.0f && (double)x[f] < 32.0 * (double)words) {
+        const int64_t c = (int64_t)x[f]; /* integer part */
+        in_set = (J->cat_bits[J->cat_offset[node] + c / 32] >> (c % 32)) & 1u;
+      }
+      v = in_set ? J->left[node] : J->right[node];
+    } else if (x[f] < J->threshold[base + v])
       v = J->left[base + v];
     else
       v = J->right[base + v];
@@ -169,6 +188,7 @@ int oracle_predict(int32_t n_trees, int32_t n_features, int32_t n_outputs,
                    const float *leaf_value, const int32_t *tree_class,
                    int32_t aggregation, int32_t transform,
                    const float *base_score, const uint8_t *default_left,
+                   const int64_t *cat_offset, const uint32_t *cat_bits,
                    const float *X, int64_t n_rows,
                    double *raw, double *out, int32_t *leaf_ids,
                    int32_t n_threads) {
@@ -181,6 +201,12 @@ int oracle_predict(int32_t n_trees, int32_t n_features, int32_t n_outputs,
   if (transform < ORACLE_POST_NONE || transform > ORACLE_POST_SOFTMAX) return ORACLE_ERR_ARG;
   for (int32_t t = 0; t < n_trees; ++t)
     if (tree_node_offset[t + 1] <= tree_node_offset[t]) return ORACLE_ERR_ARG;
+  if (cat_offset) {
+    const int64_t n_nodes = tree_node_offset[n_trees];
+    if (cat_offset[0] < 0 || (!cat_bits && cat_offset[n_nodes] > 0)) return ORACLE_ERR_ARG;
+    for (int64_t i = 0; i < n_nodes; ++i)
+      if (cat_offset[i + 1] < cat_offset[i]) return ORACLE_ERR_ARG;
+  }
   if (leaf_dim == 1 && tree_class) {
     for (int32_t t = 0; t < n_trees; ++t)
       if (tree_class[t] < 0 || tree_class[t] >= n_outputs) return ORACLE_ERR_ARG;
@@ -189,7 +215,7 @@ int oracle_predict(int32_t n_trees, int32_t n_features, int32_t n_outputs,
 
   oracle_job J = {n_trees, n_features, n_outputs, leaf_dim, tree_node_offset,
                   feature, threshold, left, right, leaf_value, tree_class,
-                  aggregation, transform, base_score, default_left, X, n_rows,
+                  aggregation, transform, base_score, default_left, cat_offset, cat_bits, X, n_rows,
                   raw, out, leaf_ids};
   if (n_threads < 1) n_threads = 1;
   if ((int64_t)n_threads > n_rows) n_threads = (int32_t)n_rows;

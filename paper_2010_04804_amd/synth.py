@@ -336,6 +336,55 @@ def with_missing(model: dict, X: np.ndarray, seed: int, p_left: float = 0.5, p_m
     return m, Xm
 
 
+def with_categories(model: dict, X: np.ndarray, seed: int, cat_cols, n_categories: int,
+                    p_member: float = 0.5):
+    """The same model with every internal node that tests a column of
+    ``cat_cols`` made categorical, and a copy of ``X`` whose ``cat_cols`` hold
+    category values; returns ``(model, X)``.
+
+    Each such node gets a random set over categories ``[0, n_categories)``
+    (each category in it with probability ``p_member``) as
+    ``ceil(n_categories / 32)`` 32-bit words, one node in four with an extra
+    all-zero word. The rows' category columns hold integers drawn from
+    ``[0, n_categories + 4)``, a quarter of them with a fractional part added,
+    and a few negative values, NaN, +inf and -0.0.
+    """
+    rng = np.random.Generator(np.random.PCG64(seed))
+    m = dict(model)
+    cat_cols = np.asarray(cat_cols, np.int64)
+    feat = np.asarray(model["feature"])
+    words = (n_categories + 31) // 32
+    off = [0]
+    bits = []
+    for i in range(feat.size):
+        if feat[i] >= 0 and np.isin(feat[i], cat_cols):
+            w = words + (1 if rng.random() < 0.25 else 0)
+            member = rng.random(32 * w) < p_member
+            member[n_categories:] = False
+            node_bits = np.zeros(w, np.uint64)
+            for c in np.flatnonzero(member):
+                node_bits[c // 32] |= np.uint64(1) << np.uint64(c % 32)
+            bits.extend(int(b) for b in node_bits)
+            off.append(off[-1] + w)
+        else:
+            off.append(off[-1])
+    m["cat_offset"] = np.asarray(off, np.int64)
+    m["cat_bits"] = np.asarray(bits, np.uint32)
+    Xc = np.array(X, np.float32, copy=True)
+    n = Xc.shape[0]
+    for c in cat_cols:
+        v = rng.integers(0, n_categories + 4, size=n).astype(np.float64)
+        frac = rng.random(n) < 0.25
+        v[frac] += rng.random(int(frac.sum()))
+        u = rng.random(n)
+        v[u < 0.03] = -rng.random(int((u < 0.03).sum())) * 3.0
+        v[(u >= 0.03) & (u < 0.05)] = np.nan
+        v[(u >= 0.05) & (u < 0.06)] = np.inf
+        v[(u >= 0.06) & (u < 0.07)] = -0.0
+        Xc[:, c] = _f32(v)
+    return m, Xc
+
+
 def make_rows(cfg: int, n_rows: int) -> np.ndarray:
     """``n_rows`` seeded input rows of workload ``cfg``, float32 [n_rows, F]."""
     _, rng = _streams(CONFIGS[cfg]["seed"])

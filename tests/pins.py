@@ -16,7 +16,12 @@ oracle disagrees with what the paper and the mathematics fix:
   thresholds, copies of one tree, one-hot votes, sigmoid(0), softmax of equal
   or shifted logits);
 * ``pin_sklearn``: scikit-learn's own tree walk (``apply``/``predict``/
-  ``predict_proba``) on fitted trees, a library routine the oracle reduces to.
+  ``predict_proba``) on fitted trees, a library routine the oracle reduces to;
+* ``pin_categorical``: hand-traced categorical splits (tests/golden), and
+  random categorical ensembles against numeric-only trees built here from the
+  definition of a category set (each categorical node replaced by a search
+  tree over the intervals of the real line on which its decision is constant,
+  with copies of the children below), whose walk the other pins fix.
 """
 from __future__ import annotations
 
@@ -40,6 +45,7 @@ def model_from_trees(trees, n_features, n_outputs=1, leaf_dim=1, tree_class=None
     """trees: list of lists of (feature, threshold, left, right, value or [values])."""
     off = [0]
     f, t, l, r, v, dl = [], [], [], [], [], []
+    cat_off, cat_bits = [0], []
     for tr in trees:
         for node in tr:
             ff, tt, ll, rr, vv = node[:5]
@@ -48,10 +54,20 @@ def model_from_trees(trees, n_features, n_outputs=1, leaf_dim=1, tree_class=None
             l.append(ll)
             r.append(rr)
             dl.append(node[5] if len(node) > 5 else 0)
+            cats = node[6] if len(node) > 6 else None  # (words, [categories]) or None
+            if cats is not None:
+                words = [0] * cats[0]
+                for c in cats[1]:
+                    words[c // 32] |= 1 << (c % 32)
+                cat_bits.extend(words)
+            cat_off.append(len(cat_bits))
             v.extend(np.atleast_1d(np.asarray(vv, np.float64)).tolist() if leaf_dim > 1 else [vv])
         off.append(off[-1] + len(tr))
     with_dl = any(len(node) > 5 for tr in trees for node in tr)
+    with_cat = any(len(node) > 6 and node[6] is not None for tr in trees for node in tr)
     return {
+        "cat_offset": np.asarray(cat_off, np.int64) if with_cat else None,
+        "cat_bits": np.asarray(cat_bits, np.uint32) if with_cat else None,
         "n_trees": len(trees), "n_features": n_features, "n_outputs": n_outputs,
         "leaf_dim": leaf_dim,
         "tree_node_offset": np.asarray(off, np.int64),
@@ -77,6 +93,9 @@ def load_golden(name="hand_traced_two_trees.txt"):
                 name_, nid = parts[1], int(parts[2])
                 ff, tt, ll, rr, vv = int(parts[3]), float(parts[4]), int(parts[5]), int(parts[6]), float(parts[7])
                 node = (ff, tt, ll, rr, vv) if len(parts) < 9 else (ff, tt, ll, rr, vv, int(parts[8]))
+                if len(parts) > 9 and parts[9] != "-":  # wN:c1,c2,...
+                    w, _, cs = parts[9][1:].partition(":")
+                    node = node + ((int(w), [int(c) for c in cs.split(",") if c]),)
                 trees.setdefault(name_, {})[nid] = node
             elif parts[0] == "row":
                 arrow = parts.index("->")
@@ -226,8 +245,19 @@ def pin_golden_default_left(lib):
     assert np.array_equal(ids0, ids1)
 
 
+def pin_golden_categorical(lib):
+    """Hand-traced categorical splits."""
+    trees, rows = load_golden("hand_traced_categorical.txt")
+    m = model_from_trees(trees, 3)
+    X = np.asarray([r[0] for r in rows], np.float32)
+    raw, _, ids = oracle.predict(m, X, lib=lib, n_threads=2)
+    assert np.array_equal(ids, np.asarray([r[1] for r in rows], np.int32)), ids
+    assert np.array_equal(raw[:, 0], np.asarray([r[2] for r in rows]))
+
+
 def pin_golden(lib):
     pin_golden_default_left(lib)
+    pin_golden_categorical(lib)
     trees, rows = load_golden()
     m = model_from_trees(trees, 3)
     X = np.asarray([r[0] for r in rows], np.float32)
@@ -302,6 +332,109 @@ def pin_brute_force(lib, seeds=range(6), n_rows=60):
                 assert ids[r, t] == leaf, (seed, r, t, ids[r, t], leaf)
                 acc += float(m["leaf_value"][int(m["tree_node_offset"][t]) + leaf])
             assert math.isclose(raw[r, 0], acc, rel_tol=1e-12, abs_tol=1e-12), (raw[r, 0], acc)
+
+
+def categorical_as_intervals(model):
+    """An equivalent ensemble of numeric nodes only, and per tree the map from
+    its node ids to the original ones.
+
+    A categorical node with a bit set of W words decides by intervals of the
+    real line: (-inf, 0) goes right, [k, k + 1) goes left exactly when the
+    set holds category k (0 <= k < 32 W), [32 W, +inf] goes right, and NaN
+    follows the node's default direction. Merging neighbouring intervals of
+    the same direction gives runs; the node becomes a search tree of x < b
+    nodes over the runs' lower bounds, each run ending in a fresh copy of the
+    child subtree it leads to. NaN goes right at every x < b node and so ends
+    in the last run, which goes right; a node whose missing values go left
+    gets a first node x < -inf (false for every number) whose NaN-left side
+    leads to a copy of the left subtree.
+    """
+    off = model["tree_node_offset"]
+    ld = model["leaf_dim"]
+    co, cb = model["cat_offset"], model["cat_bits"]
+    dl_in = model.get("default_left")
+    val_in = np.asarray(model["leaf_value"]).reshape(-1, ld)
+    F, TH, L, R, V, DL, OFF, MAPS = [], [], [], [], [], [], [0], []
+    for t in range(model["n_trees"]):
+        a = int(off[t])
+        f_, th_, l_, r_, v_, dl_, orig = [], [], [], [], [], [], []
+
+        def new_node(feat, thr, dl, o, value):
+            f_.append(feat); th_.append(thr); l_.append(-1); r_.append(-1)
+            dl_.append(dl); orig.append(o); v_.append(value)
+            return len(f_) - 1
+
+        def expand(v):
+            g = a + v
+            feat = int(model["feature"][g])
+            if feat < 0:
+                return new_node(-1, 0.0, 0, v, val_in[g])
+            zero = np.zeros(ld, np.float32)
+            dl = int(dl_in[g]) if dl_in is not None else 0
+            words = int(co[g + 1] - co[g])
+            if words == 0:
+                i = new_node(feat, float(model["threshold"][g]), dl, v, zero)
+                l_[i] = expand(int(model["left"][g]))
+                r_[i] = expand(int(model["right"][g]))
+                return i
+            bits = [int(b) for b in cb[int(co[g]):int(co[g + 1])]]
+            dirs = [(bits[k // 32] >> (k % 32)) & 1 == 1 for k in range(32 * words)]
+            runs = [(-np.inf, False)]  # (lower bound, goes left)
+            for k, d in enumerate(dirs + [False]):  # the last entry: [32 W, +inf]
+                if d != runs[-1][1]:
+                    runs.append((float(k), d))
+
+            def build(i, j):
+                if i == j:
+                    return expand(int(model["left"][g] if runs[i][1] else model["right"][g]))
+                mid = (i + j + 1) // 2
+                n = new_node(feat, runs[mid][0], 0, -1, zero)
+                l_[n] = build(i, mid - 1)
+                r_[n] = build(mid, j)
+                return n
+
+            if dl:
+                n = new_node(feat, -np.inf, 1, -1, zero)
+                l_[n] = expand(int(model["left"][g]))
+                r_[n] = build(0, len(runs) - 1)
+                return n
+            return build(0, len(runs) - 1)
+
+        expand(0)
+        F += f_; TH += th_; L += l_; R += r_; DL += dl_
+        V += [np.asarray(x, np.float32).reshape(ld) for x in v_]
+        OFF.append(OFF[-1] + len(f_))
+        MAPS.append(np.asarray(orig, np.int64))
+    out = dict(model)
+    out.update(tree_node_offset=np.asarray(OFF, np.int64), feature=np.asarray(F, np.int32),
+               threshold=np.asarray(TH, np.float32), left=np.asarray(L, np.int32),
+               right=np.asarray(R, np.int32), leaf_value=np.concatenate(V).astype(np.float32),
+               default_left=np.asarray(DL, np.uint8), cat_offset=None, cat_bits=None)
+    return out, MAPS
+
+
+def random_categorical_ensemble(seed, n_rows=80):
+    """A small mixed ensemble with columns 1 and 3 categorical (6 categories)
+    and rows for it; odd seeds give every node a random default direction."""
+    m = random_small_ensemble(seed, n_trees=5, n_features=4)
+    rng = np.random.Generator(np.random.PCG64(seed + 5))
+    if seed % 2:
+        m["default_left"] = (rng.random(m["feature"].size) < 0.5).astype(np.uint8)
+    X = tricky_rows(rng, m, n_rows)
+    return synth.with_categories(m, X, seed + 9, [1, 3], 6)
+
+
+def pin_categorical(lib, seeds=range(8)):
+    pin_golden_categorical(lib)
+    for seed in seeds:
+        m, X = random_categorical_ensemble(seed)
+        assert m["cat_offset"][-1] > 0
+        mi, maps = categorical_as_intervals(m)
+        raw, _, ids = oracle.predict(m, X, lib=lib, n_threads=2)
+        raw_i, _, ids_i = oracle.predict(mi, X, lib=lib, n_threads=2)
+        assert np.array_equal(raw, raw_i), seed
+        for t in range(m["n_trees"]):
+            assert np.array_equal(ids[:, t], maps[t][ids_i[:, t]]), (seed, t)
 
 
 def pin_gemm_closed_form(lib, seeds=range(8)):

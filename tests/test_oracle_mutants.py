@@ -28,12 +28,26 @@ MUTANTS = {
                           "for (int32_t t = 0; t < J->n_trees - 1; ++t) {\n      int64_t leaf"),
     "feature_off_by_one": ("if (x[f] < J->threshold", "if (x[f == 0 ? 0 : f - 1] < J->threshold"),
     "default_left_ignored": ("if (J->default_left && isnan(x[f]))", "if (0)"),
-    "default_left_inverted": ("J->default_left[base + v] ? J->left[base + v] : J->right[base + v]",
-                              "J->default_left[base + v] ? J->right[base + v] : J->left[base + v]"),
+    "default_left_inverted": ("J->default_left[node] ? J->left[node] : J->right[node]",
+                              "J->default_left[node] ? J->right[node] : J->left[node]"),
+    "category_set_inverted": ("v = in_set ? J->left[node] : J->right[node];",
+                              "v = in_set ? J->right[node] : J->left[node];"),
+    "category_rounded": ("const int64_t c = (int64_t)x[f]; /* integer part */",
+                         "const int64_t c = (int64_t)(x[f] + 0.5f);"),
+    "category_negative_as_zero": ("if (x[f] >= 0.0f && (double)x[f] < 32.0 * (double)words) {",
+                                  "if (x[f] > -1.0f && (double)x[f] < 32.0 * (double)words) {"),
+    "category_bit_order": ("(J->cat_bits[J->cat_offset[node] + c / 32] >> (c % 32))",
+                           "(J->cat_bits[J->cat_offset[node] + c / 32] >> (31 - c % 32))"),
+    "category_wraps": ("if (x[f] >= 0.0f && (double)x[f] < 32.0 * (double)words) {\n        const int64_t c = (int64_t)x[f]; /* integer part */",
+                       "if (x[f] >= 0.0f && x[f] < 1e9f) {\n        const int64_t c = ((int64_t)x[f]) % (32 * words);"),
+    "category_ignored": ("else if (J->cat_offset && J->cat_offset[node + 1] > J->cat_offset[node]) {",
+                         "else if (0) {"),
+    "category_nan_default_ignored": ("    if (J->default_left && isnan(x[f]))\n      v = J->default_left[node]",
+                                     "    if (J->default_left && isnan(x[f]) && !(J->cat_offset && J->cat_offset[node + 1] > J->cat_offset[node]))\n      v = J->default_left[node]"),
 }
 
 PINS = [pins.pin_golden, pins.pin_brute_force, pins.pin_gemm_closed_form, pins.pin_closed_forms,
-        pins.pin_sklearn]
+        pins.pin_sklearn, pins.pin_categorical]
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))

@@ -24,6 +24,10 @@ def test_gemm_closed_form_and_ptt_heap(lib):
     pins.pin_gemm_closed_form(lib)
 
 
+def test_categorical_splits(lib):
+    pins.pin_categorical(lib)
+
+
 def test_closed_forms(lib):
     pins.pin_closed_forms(lib)
 
