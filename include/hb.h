@@ -70,6 +70,7 @@ enum hb_transform { HB_POST_NONE = 0, HB_POST_SIGMOID = 1, HB_POST_SOFTMAX = 2 }
 #define HB_PTT_MAX_DEPTH 12        /* PTT tables grow as 2^depth per tree   */
 #define HB_TT_MAX_NODES 65535      /* nodes per tree for TT (16-bit ids)    */
 #define HB_MAX_FEATURES 65535      /* features (16-bit ids in TT records)   */
+#define HB_MAX_CATEGORY_WORDS 65536 /* words of one node's category set      */
 #define HB_GEMM_MAX_LEAVES 256     /* leaves per tree for GEMM              */
 #define HB_MAX_TREES (1 << 24)     /* n_trees (kernels index eight rows of
                                       leaf ids with 32-bit offsets)          */
@@ -107,6 +108,27 @@ typedef struct hb_ensemble_desc {
                                       The paper leaves missing values to future
                                       work (Sec. 4.1); this is the per-node
                                       default direction of common tree learners. */
+  const int64_t *cat_offset;       /* [nodes + 1] or NULL. Categorical splits: the
+                                      category set of internal node i is the bit set
+                                      cat_bits[cat_offset[i] .. cat_offset[i + 1])
+                                      (bit j of word w is category 32 w + j); an
+                                      empty range makes the node numeric (x < t).
+                                      A row's category is the integer part of a
+                                      non-negative feature value below 32 times the
+                                      word count; it goes left when the set holds
+                                      that category and right otherwise (negative
+                                      values, +inf and values past the bit set go
+                                      right); NaN follows default_left as for a
+                                      numeric node. The threshold of a categorical
+                                      node is not read. Offsets must start at 0 and
+                                      not decrease, and a node may hold at most
+                                      HB_MAX_CATEGORY_WORDS words
+                                      (HB_ERR_INVALID_MODEL otherwise). The paper
+                                      leaves categorical values to future work
+                                      (Sec. 4.1); this is the category-set split of
+                                      common tree learners. */
+  const uint32_t *cat_bits;        /* [cat_offset[nodes]] words, or NULL when
+                                      cat_offset is NULL                       */
 } hb_ensemble_desc;
 
 typedef struct hb_handle hb_handle;
@@ -125,10 +147,13 @@ typedef struct hb_info {
   int32_t n_used_features;         /* feature columns the kernels stage: the
                                       input columns some decision node tests,
                                       one more for each column that nodes with
-                                      default_left = 1 test; n_features (all
-                                      columns, in order) when no node sends
-                                      missing values left and pruning would
-                                      drop less than a quarter of them */
+                                      default_left = 1 test, one for each
+                                      distinct (column, category set,
+                                      default_left) of categorical nodes;
+                                      n_features (all columns, in order) when
+                                      no node is categorical or sends missing
+                                      values left and pruning would drop less
+                                      than a quarter of them */
 } hb_info;
 
 /*

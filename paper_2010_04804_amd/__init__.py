@@ -38,7 +38,7 @@ class hb_ensemble_desc(ctypes.Structure):
         ("tree_node_offset", _P), ("feature", _P), ("threshold", _P), ("left", _P),
         ("right", _P), ("leaf_value", _P), ("tree_class", _P),
         ("aggregation", ctypes.c_int32), ("transform", ctypes.c_int32), ("base_score", _P),
-        ("default_left", _P),
+        ("default_left", _P), ("cat_offset", _P), ("cat_bits", _P),
     ]
 
 
@@ -190,7 +190,11 @@ def compile(model: dict, strategy="auto", device: int = 0) -> Handle:
         "tree_class": _arr(model.get("tree_class"), np.int32),
         "base": _arr(model.get("base_score"), np.float32),
         "default_left": _arr(model.get("default_left"), np.uint8),
+        "cat_offset": _arr(model.get("cat_offset"), np.int64),
+        "cat_bits": _arr(model.get("cat_bits"), np.uint32),
     }
+    if keep["cat_offset"] is not None and (keep["cat_bits"] is None or keep["cat_bits"].size == 0):
+        keep["cat_bits"] = np.zeros(1, np.uint32)
 
     def p(a):
         return None if a is None else a.ctypes.data
@@ -199,7 +203,8 @@ def compile(model: dict, strategy="auto", device: int = 0) -> Handle:
         int(model["n_trees"]), int(model["n_features"]), int(model["n_outputs"]),
         int(model["leaf_dim"]), p(keep["off"]), p(keep["feature"]), p(keep["threshold"]),
         p(keep["left"]), p(keep["right"]), p(keep["value"]), p(keep["tree_class"]),
-        AGG[model["aggregation"]], POST[model["transform"]], p(keep["base"]), p(keep["default_left"]))
+        AGG[model["aggregation"]], POST[model["transform"]], p(keep["base"]), p(keep["default_left"]),
+        p(keep["cat_offset"]), p(keep["cat_bits"]))
     h = _P()
     _check(lib.hb_compile(ctypes.byref(d), _strategy(strategy), int(device), ctypes.byref(h)))
     return Handle(h.value, device)

@@ -9,6 +9,7 @@
 #include <cstring>
 #include <limits>
 #include <map>
+#include <tuple>
 #include <new>
 #include <string>
 #include <vector>
@@ -37,6 +38,8 @@ struct CanonTree {
   std::vector<int32_t> caller;  // canonical -> caller-local id
   std::vector<int32_t> feat;    // -1 at leaves
   std::vector<uint8_t> dleft;   // 1: a missing (NaN) value goes left at this node
+  std::vector<int32_t> cat;     // category set of a categorical node (index into the
+                                // compile's set table), -1 for a numeric node or a leaf
   std::vector<float> thr;
   std::vector<int32_t> left;    // canonical left child (right = left + 1), -1 at leaves
   std::vector<int32_t> parent;  // -1 at the root
@@ -46,7 +49,28 @@ struct CanonTree {
   int32_t size() const { return (int32_t)caller.size(); }
 };
 
-int canonicalise(const hb_ensemble_desc *d, int32_t t, CanonTree *ct) {
+// Category sets, deduplicated: trailing zero words dropped, so sets that hold
+// the same categories share one entry.
+struct CatSets {
+  std::vector<std::vector<uint32_t>> sets;
+  std::map<std::vector<uint32_t>, int32_t> index;
+  int32_t add(const uint32_t *w, int64_t n) {
+    while (n > 0 && w[n - 1] == 0) --n;
+    std::vector<uint32_t> key(w, w + n);
+    auto it = index.find(key);
+    if (it != index.end()) return it->second;
+    const int32_t id = (int32_t)sets.size();
+    index.emplace(key, id);
+    sets.push_back(std::move(key));
+    return id;
+  }
+};
+
+bool is_categorical(const hb_ensemble_desc *d, int64_t node) {
+  return d->cat_offset && d->cat_offset[node + 1] > d->cat_offset[node];
+}
+
+int canonicalise(const hb_ensemble_desc *d, int32_t t, CanonTree *ct, CatSets *cs) {
   const int64_t base = d->tree_node_offset[t];
   const int64_t n64 = d->tree_node_offset[t + 1] - base;
   if (n64 < 1 || n64 > (int64_t)std::numeric_limits<int32_t>::max() / 2)
@@ -64,13 +88,14 @@ int canonicalise(const hb_ensemble_desc *d, int32_t t, CanonTree *ct) {
     if (f >= d->n_features)
       return fail(HB_ERR_INVALID_MODEL, "tree " + std::to_string(t) + " node " +
                                             std::to_string(v) + ": feature out of range");
-    if (std::isnan(d->threshold[base + v]))
+    const bool cat = is_categorical(d, base + v);  // its threshold is not read
+    if (!cat && std::isnan(d->threshold[base + v]))
       return fail(HB_ERR_INVALID_MODEL, "tree " + std::to_string(t) + " node " +
                                             std::to_string(v) + ": NaN threshold");
     if (d->default_left && d->default_left[base + v] > 1)
       return fail(HB_ERR_INVALID_MODEL, "tree " + std::to_string(t) + " node " +
                                             std::to_string(v) + ": default_left must be 0 or 1");
-    if (d->default_left && d->default_left[base + v] && d->threshold[base + v] == -INFINITY)
+    if (!cat && d->default_left && d->default_left[base + v] && d->threshold[base + v] == -INFINITY)
       return fail(HB_ERR_UNSUPPORTED, "tree " + std::to_string(t) + " node " + std::to_string(v) +
                                           ": a node that sends missing values left cannot have threshold -inf");
     const int32_t kids[2] = {d->left[base + v], d->right[base + v]};
@@ -91,6 +116,7 @@ int canonicalise(const hb_ensemble_desc *d, int32_t t, CanonTree *ct) {
                                           " node(s) unreachable from the root");
   ct->feat.assign(n, -1);
   ct->dleft.assign(n, 0);
+  ct->cat.assign(n, -1);
   ct->thr.assign(n, 0.0f);
   ct->left.assign(n, -1);
   ct->parent.assign(n, -1);
@@ -109,6 +135,11 @@ int canonicalise(const hb_ensemble_desc *d, int32_t t, CanonTree *ct) {
     ct->feat[c] = f;
     ct->dleft[c] = d->default_left ? d->default_left[base + v] : 0;
     ct->thr[c] = d->threshold[base + v];
+    if (is_categorical(d, base + v)) {
+      const int64_t lo = d->cat_offset[base + v];
+      ct->cat[c] = cs->add(d->cat_bits + lo, d->cat_offset[base + v + 1] - lo);
+      ct->thr[c] = 0.5f;  // the node tests its 0/1 indicator column
+    }
     const int32_t l = canon_of[d->left[base + v]];
     const int32_t r = canon_of[d->right[base + v]];
     if (r != l + 1) return fail(HB_ERR_INVALID_MODEL, "internal: breadth-first order broken");
@@ -562,6 +593,18 @@ int validate_desc(const hb_ensemble_desc *d) {
     for (int32_t t = 0; t < d->n_trees; ++t)
       if (d->tree_class[t] < 0 || d->tree_class[t] >= d->n_outputs)
         return fail(HB_ERR_INVALID_MODEL, "tree_class out of range at tree " + std::to_string(t));
+  if (d->cat_offset) {
+    const int64_t n_nodes = d->tree_node_offset[d->n_trees];
+    if (d->cat_offset[0] != 0) return fail(HB_ERR_INVALID_MODEL, "cat_offset[0] must be 0");
+    for (int64_t i = 0; i < n_nodes; ++i) {
+      const int64_t w = d->cat_offset[i + 1] - d->cat_offset[i];
+      if (w < 0) return fail(HB_ERR_INVALID_MODEL, "cat_offset must not decrease (node " + std::to_string(i) + ")");
+      if (w > HB_MAX_CATEGORY_WORDS)
+        return fail(HB_ERR_INVALID_MODEL, "node " + std::to_string(i) + ": more than " +
+                                              std::to_string(HB_MAX_CATEGORY_WORDS) + " category words");
+    }
+    if (d->cat_offset[n_nodes] > 0 && !d->cat_bits) return fail(HB_ERR_INVALID_ARG, "cat_bits is NULL");
+  }
   return HB_OK;
 }
 
@@ -572,10 +615,11 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
   if (device < -1) return fail(HB_ERR_INVALID_ARG, "bad device");
   const int32_t T = d->n_trees;
   std::vector<CanonTree> trees(T);
+  CatSets cat_sets;
   int64_t n_nodes = 0, n_int = 0, n_leaf = 0;
   int32_t D = 0, max_nodes = 0, max_leaves = 0;
   for (int32_t t = 0; t < T; ++t) {
-    rc = canonicalise(d, t, &trees[t]);
+    rc = canonicalise(d, t, &trees[t], &cat_sets);
     if (rc) return rc;
     n_nodes += trees[t].size();
     n_int += trees[t].n_internal;
@@ -594,34 +638,67 @@ int compile_impl(const hb_ensemble_desc *d, int hint, int device, hb_handle **ou
   // default-left flag test gets a second tile column that reads NaN as -inf
   // (then x < t holds for every finite or +inf threshold, so NaN goes left),
   // and those nodes test that column; every other node sees NaN, which no
-  // x < t accepts, so NaN goes right. The walk itself is unchanged.
+  // x < t accepts, so NaN goes right. Categorical nodes: each distinct
+  // (column, category set, default-left) gets a tile column holding the 0/1
+  // indicator of the row going left, which the node tests against 0.5. The
+  // walk itself is unchanged.
+  int32_t n_cols = d->n_features;
   {
     std::vector<int32_t> rank(2 * (size_t)d->n_features, -1);  // [column][default-left]
+    std::map<std::tuple<int32_t, int32_t, int32_t>, int32_t> cat_rank;  // (column, set, dl)
     for (const CanonTree &ct : trees)
       for (int32_t c = 0; c < ct.size(); ++c)
-        if (ct.feat[c] >= 0) rank[2 * (size_t)ct.feat[c] + ct.dleft[c]] = 0;
-    bool variant = false;
+        if (ct.feat[c] >= 0) {
+          if (ct.cat[c] >= 0)
+            cat_rank[std::make_tuple(ct.feat[c], ct.cat[c], (int32_t)ct.dleft[c])] = 0;
+          else
+            rank[2 * (size_t)ct.feat[c] + ct.dleft[c]] = 0;
+        }
+    std::vector<int32_t> cols;
+    bool variant = !cat_rank.empty();
     for (size_t k = 0; k < rank.size(); ++k)
       if (rank[k] == 0) {
-        rank[k] = (int32_t)h->cols.size();
-        h->cols.push_back((int32_t)(k >> 1) | ((k & 1) ? hb::kColNanLeft : 0));
+        rank[k] = (int32_t)cols.size();
+        cols.push_back((int32_t)(k >> 1) | ((k & 1) ? hb::kColNanLeft : 0));
         variant |= (k & 1) != 0;
       }
-    if (h->cols.empty()) h->cols.push_back(0);  // only single-leaf trees: one dummy column
+    for (auto &kv : cat_rank) {
+      kv.second = (int32_t)cols.size();
+      cols.push_back(0);  // set below, once the descriptors' offset is known
+    }
+    if (cols.empty()) cols.push_back(0);  // only single-leaf trees: one dummy column
     // Pruning costs the kernels a gather through the column list instead of
     // whole-row loads, so it is applied when it removes at least a quarter of
-    // the columns (or when missing values need NaN-as--inf columns).
-    h->pruned = variant || (int64_t)h->cols.size() * 4 <= (int64_t)d->n_features * 3;
-    if (!h->pruned) {
+    // the columns (or when missing values or categories need their own columns).
+    h->pruned = variant || (int64_t)cols.size() * 4 <= (int64_t)d->n_features * 3;
+    if (h->pruned) {
+      n_cols = (int32_t)cols.size();
+      // category descriptors {input column, W, W words} after the columns
+      std::vector<int32_t> pool;
+      for (const auto &kv : cat_rank) {
+        const int64_t at = (int64_t)cols.size() + (int64_t)pool.size();
+        if (at > hb::kColMask) {
+          delete h;
+          return fail(HB_ERR_UNSUPPORTED, "category sets too large");
+        }
+        const std::vector<uint32_t> &set = cat_sets.sets[std::get<1>(kv.first)];
+        cols[kv.second] = (int32_t)at | hb::kColCat | (std::get<2>(kv.first) ? hb::kColNanLeft : 0);
+        pool.push_back(std::get<0>(kv.first));
+        pool.push_back((int32_t)set.size());
+        for (uint32_t w : set) pool.push_back((int32_t)w);
+      }
+      h->cols = cols;
+      h->cols.insert(h->cols.end(), pool.begin(), pool.end());
+      for (CanonTree &ct : trees)
+        for (int32_t c = 0; c < ct.size(); ++c)
+          if (ct.feat[c] >= 0)
+            ct.feat[c] = ct.cat[c] >= 0 ? cat_rank[std::make_tuple(ct.feat[c], ct.cat[c], (int32_t)ct.dleft[c])]
+                                        : rank[2 * (size_t)ct.feat[c] + ct.dleft[c]];
+    } else {
       h->cols.resize(d->n_features);
       for (int32_t f = 0; f < d->n_features; ++f) h->cols[f] = f;
     }
-    if (h->pruned)
-      for (CanonTree &ct : trees)
-        for (int32_t c = 0; c < ct.size(); ++c)
-          if (ct.feat[c] >= 0) ct.feat[c] = rank[2 * (size_t)ct.feat[c] + ct.dleft[c]];
   }
-  const int32_t n_cols = h->pruned ? (int32_t)h->cols.size() : d->n_features;
   hb_info &I = h->info;
   I.n_trees = T;
   I.n_features = d->n_features;

@@ -151,12 +151,28 @@ __device__ __forceinline__ void flush_ids(int32_t *leaf_ids, int64_t n_rows, int
 // stride of one feature column of the row tile is exactly the row count, so a
 // lane's gather x[f] hits bank (lane mod 32) whatever feature each lane needs.
 
+// Category-set indicator of a feature-tile column (kColCat): 0 when the row
+// goes left (its category, the integer part of a non-negative value below
+// 32 W, is in the set; or the value is NaN and the column's nodes send
+// missing values left), else 1. The nodes test it against 0.5.
+__device__ __noinline__ float xcat(const float *row, const int32_t *cols, int c) {
+  const uint32_t *d = reinterpret_cast<const uint32_t *>(cols) + (c & kColMask);
+  const float v = row[d[0]];
+  if (__builtin_isnan(v)) return (c & kColNanLeft) ? 0.0f : 1.0f;
+  if (v >= 0.0f && v < 32.0f * (float)d[1]) {
+    const uint32_t k = (uint32_t)v;  // integer part
+    return ((d[2 + (k >> 5)] >> (k & 31u)) & 1u) ? 0.0f : 1.0f;
+  }
+  return 1.0f;
+}
+
 // Feature-tile column f of an input row: the identity when cols is null, else
 // input column cols[f] & kColMask, with a NaN read as -inf when the column
-// serves nodes that send missing values left.
+// serves nodes that send missing values left, or a category-set indicator.
 __device__ __forceinline__ float xval(const float *row, const int32_t *cols, int f) {
   if (!cols) return row[f];
   const int c = cols[f];
+  if (c & kColCat) return xcat(row, cols, c);
   const float v = row[c & kColMask];
   return ((c & kColNanLeft) && __builtin_isnan(v)) ? -__builtin_inff() : v;
 }

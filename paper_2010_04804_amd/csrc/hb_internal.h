@@ -82,17 +82,22 @@ constexpr int kFastMaxLg = 12;
 static_assert(kFastMaxLg < 15, "fast-kernel leaf ids must fit in 16 bits");
 
 // Ensemble-wide parameters every kernel needs.
-// Feature-tile column flags (in EnsembleDev::cols): the column reads a NaN
-// input value as -inf; the low bits are the input column.
+// Feature-tile column flags (in EnsembleDev::cols): kColNanLeft: a NaN input
+// value goes left (a numeric column reads it as -inf); kColCat: the column is
+// the 0/1 category-set indicator of categorical nodes (0 when the row goes
+// left), and the low bits are the int offset, from the start of cols, of its
+// descriptor {input column, word count W, W words of the set}, which follow
+// the n_cols column entries. Otherwise the low bits are the input column.
 constexpr int32_t kColNanLeft = 1 << 30;
-constexpr int32_t kColMask = kColNanLeft - 1;
+constexpr int32_t kColCat = 1 << 29;
+constexpr int32_t kColMask = kColCat - 1;
 
 struct EnsembleDev {
   int32_t n_trees, n_features, n_outputs, leaf_dim;
   // Feature tile: the kernels stage n_cols columns per row; column i is input
-  // column cols[i] & kColMask, read with NaN -> -inf when kColNanLeft is set
-  // (cols == nullptr: the identity, n_cols == n_features). n_features stays
-  // the row stride of X.
+  // column cols[i] & kColMask, read with NaN -> -inf when kColNanLeft is set,
+  // or a category-set indicator when kColCat is set (cols == nullptr: the
+  // identity, n_cols == n_features). n_features stays the row stride of X.
   int32_t n_cols;
   const int32_t *cols;
   int32_t aggregation, transform;

@@ -37,13 +37,35 @@ def _aggregate(model, values):
 def _tile(h, X, strategy):
     """The feature tile the kernels stage: the input columns some decision node
     tests, in the order the compiled tables index them; a column flagged for
-    nodes that send missing values left reads NaN as -inf."""
-    cols = h.table(strategy, "features", np.int32).astype(np.int64)
-    tile = X[:, cols & ((1 << 30) - 1)].copy()
+    nodes that send missing values left reads NaN as -inf; a categorical
+    column is 0 where the row goes left (its category, the integer part of a
+    non-negative value inside the bit set, is in the set; NaN where the
+    column's nodes send missing values left) and 1 elsewhere."""
+    table = h.table(strategy, "features", np.int32).astype(np.int64)
+    n_cols = h.info()["n_used_features"]
+    cols = table[:n_cols]
+    mask = (1 << 29) - 1
+    cat = (cols >> 29) & 1 == 1
     nan_left = (cols >> 30) & 1 == 1
-    sub = tile[:, nan_left]
-    sub[np.isnan(sub)] = -np.inf
-    tile[:, nan_left] = sub
+    tile = np.empty((X.shape[0], n_cols), np.float32)
+    for j in range(n_cols):
+        if not cat[j]:
+            v = X[:, cols[j] & mask].copy()
+            if nan_left[j]:
+                v[np.isnan(v)] = -np.inf
+            tile[:, j] = v
+            continue
+        at = int(cols[j] & mask)
+        col, W = int(table[at]), int(table[at + 1])
+        words = table[at + 2:at + 2 + W].astype(np.uint32)
+        x = X[:, col].astype(np.float64)
+        left = np.zeros(X.shape[0], bool)
+        ok = (x >= 0) & (x < 32 * W)
+        k = np.where(ok, x, 0).astype(np.int64)
+        if W:
+            left[ok] = (words[k[ok] // 32] >> (k[ok] % 32).astype(np.uint32)) & 1 == 1
+        left[np.isnan(x)] = bool(nan_left[j])
+        tile[:, j] = np.where(left, 0.0, 1.0)
     return tile
 
 

@@ -171,3 +171,31 @@ def test_scratch_entry_point_rejects_sizes_beyond_the_maximum():
     assert e.value.code == -1 and "host-only" in str(e.value)
     src = open(os.path.join(ROOT, "include", "hb.h")).read()
     assert f"#define HB_SCRATCH_BYTES ((int64_t)32 << 20)" in src and hb.SCRATCH_BYTES == 32 << 20
+
+
+def test_categorical_validation():
+    trees, rows = pins.load_golden("hand_traced_categorical.txt")
+    m = pins.model_from_trees(trees, 3)
+    hb.compile(m, device=-1).close()
+    # a categorical node's threshold is not read: NaN, or -inf with NaN left, are accepted
+    thr = m["threshold"].copy()
+    thr[0] = np.nan  # tree A's root, categorical, NaN left
+    hb.compile(dict(m, threshold=thr), device=-1).close()
+    thr[0] = -np.inf
+    hb.compile(dict(m, threshold=thr), device=-1).close()
+    co = m["cat_offset"]
+    _expect(dict(m, cat_offset=co + 1), -2, r"cat_offset\[0\]")
+    dec = co.copy()
+    dec[2] = dec[1] - 1
+    _expect(dict(m, cat_offset=dec), -2, "must not decrease")
+    wide = co.copy()
+    wide[1:] += 65536  # node 0 of tree A: 65,537 words
+    _expect(dict(m, cat_offset=wide, cat_bits=np.zeros(int(wide[-1]), np.uint32)), -2, "category words")
+    # an empty range everywhere is a numeric model
+    h = hb.compile(dict(m, cat_offset=np.zeros_like(co), cat_bits=None), device=-1)
+    h0 = hb.compile(dict(m, cat_offset=None, cat_bits=None), device=-1)
+    for s in ("ptt", "tt", "gemm"):
+        assert np.array_equal(h.table(s, "features", np.int32), h0.table(s, "features", np.int32))
+        assert np.array_equal(h.table(s, "node", np.uint8), h0.table(s, "node", np.uint8))
+    h.close()
+    h0.close()

@@ -247,3 +247,67 @@ def test_tt_packed_tables_walk_in_bounds(cfg):
     assert (s[:, T:] == 0).all()
     _, _, o_ids = oracle.predict(model, X)
     assert np.array_equal(leaf[base + s // 8, 1][:, :T].astype(np.int32), o_ids)
+
+
+@pytest.mark.parametrize("strategy", ["ptt", "tt", "gemm"])
+@pytest.mark.parametrize("seed", range(4))
+def test_categorical_splits_tables_and_emulation(seed, strategy):
+    """Categorical nodes compile to 0/1 indicator columns (one per distinct
+    column, category set and default direction) that the nodes test against
+    0.5; the three algorithms run on the compiled tables give the oracle's
+    leaves, with NaN, negative, fractional, -0.0, +inf and out-of-range
+    category values in the rows."""
+    m, X = pins.random_categorical_ensemble(seed, n_rows=300)
+    h = host(m)
+    n_cols = h.info()["n_used_features"]
+    cols = h.table(strategy, "features", np.int32)[:n_cols]
+    assert ((cols >> 29) & 1).any() and ((cols >> 29) & 1 == 0).any()
+    ids, raw = getattr(emulate, strategy)(h, m, X)
+    o_raw, _, o_ids = oracle.predict(m, X)
+    assert np.array_equal(ids, o_ids)
+    assert np.allclose(raw, o_raw, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("cfg", [1, 5])
+def test_categorical_on_workload_shapes(cfg):
+    m0 = synth.make_model(cfg)
+    m, X = synth.with_categories(m0, synth.make_rows(cfg, 200), seed=cfg, cat_cols=[0, 3], n_categories=40)
+    m, X = synth.with_missing(m, X, seed=cfg + 1, p_missing=0.05)
+    h = host(m)
+    o_raw, _, o_ids = oracle.predict(m, X)
+    for s in ("ptt", "tt", "gemm"):
+        if not h.info()["feasible"][s]:
+            continue
+        ids, raw = getattr(emulate, s)(h, m, X)
+        assert np.array_equal(ids, o_ids), s
+        assert np.allclose(raw, o_raw, rtol=1e-12, atol=1e-12), s
+
+
+def test_categorical_columns_are_shared():
+    """Nodes with the same column, the same categories (trailing zero words
+    aside) and the same default direction share one indicator column; a
+    different set or direction gets its own."""
+    leaf = (-1, 0.0, -1, -1, 1.0, 0)
+    trees = [
+        [(0, 0.0, 1, 2, 0.0, 0, (1, [1, 2])), leaf, leaf],
+        [(0, 0.0, 1, 2, 0.0, 0, (2, [1, 2])), leaf, leaf],   # same set, an extra zero word
+        [(0, 0.0, 1, 2, 0.0, 1, (1, [1, 2])), leaf, leaf],   # NaN left
+        [(0, 0.0, 1, 2, 0.0, 0, (1, [1, 3])), leaf, leaf],   # another set
+        [(0, 0.5, 1, 2, 0.0, 0), leaf, leaf],                # numeric on the same column
+    ]
+    m = pins.model_from_trees(trees, 2)
+    h = host(m)
+    info = h.info()
+    assert info["n_used_features"] == 4
+    table = h.table("ptt", "features", np.int32)
+    cols = table[:4]
+    assert cols[0] == 0 and ((cols[1:] >> 29) & 1).all()
+    descs = sorted((int(table[c & ((1 << 29) - 1)]), int(table[(c & ((1 << 29) - 1)) + 1]),
+                    tuple(table[(c & ((1 << 29) - 1)) + 2:(c & ((1 << 29) - 1)) + 2 + int(table[(c & ((1 << 29) - 1)) + 1])]),
+                    int((c >> 30) & 1)) for c in cols[1:])
+    assert descs == [(0, 1, (6,), 0), (0, 1, (6,), 1), (0, 1, (10,), 0)]
+    X = np.asarray([[1, 0], [2.5, 0], [3, 0], [np.nan, 0], [-1, 0], [0.0, 0]], np.float32)
+    o_raw, _, o_ids = oracle.predict(m, X)
+    for s in ("ptt", "tt", "gemm"):
+        ids, raw = getattr(emulate, s)(h, m, X)
+        assert np.array_equal(ids, o_ids), s

@@ -532,6 +532,60 @@ def test_hand_traced_default_left(strategy):
 
 
 @pytest.mark.parametrize("strategy", STRATEGIES)
+def test_hand_traced_categorical(strategy):
+    trees, rows = pins.load_golden("hand_traced_categorical.txt")
+    m = pins.model_from_trees(trees, 3)
+    X = np.asarray([r[0] for r in rows], np.float32)
+    say("hand-traced categorical", strategy)
+    scores, ids = run(hb.compile(m, device=0), X, strategy)
+    assert np.array_equal(ids, np.asarray([r[1] for r in rows], np.int32))
+    assert np.allclose(scores[:, 0], [r[2] for r in rows], rtol=1e-6, atol=0)
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES)
+@pytest.mark.parametrize("cfg,n", [(1, 1000), (2, 1000), (2, 12_000), (2, 40_000), (3, 2000), (3, 8000),
+                                   (4, 3000), (5, 20_000)])
+def test_categorical_parity(cfg, n, strategy):
+    """Categorical nodes on four columns (40 categories: sets of two words,
+    some with a third all-zero word; rows with fractional, negative, -0.0,
+    +inf, out-of-range and missing values, nodes sending missing values
+    left or right) on every kernel path: tree-parallel, split, row-parallel
+    fast shapes, rows across lanes, general (the 7-class model's 66,000
+    distinct sets exceed every feature tile), GEMM."""
+    model, _ = handle(cfg)
+    m, X = synth.with_categories(model, synth.make_rows(cfg, n), seed=cfg + n, cat_cols=[0, 3, 5, 7],
+                                 n_categories=40)
+    m, X = synth.with_missing(m, X, seed=cfg + n + 1, p_missing=0.03)
+    say("categorical", cfg, n, strategy)
+    h = hb.compile(m, device=0)
+    if not h.info()["feasible"][strategy]:
+        pytest.skip("strategy infeasible (too many indicator columns for TT's 16-bit feature ids)")
+    scores, ids = run(h, X, strategy)
+    check(m, X, scores, ids, f"categorical cfg{cfg}/{n}/{strategy}")
+
+
+@pytest.mark.parametrize("cfg,n,strategy,kernel", [
+    (2, 40_000, "ptt", "fast_kernel<"), (2, 40_000, "tt", "fast_kernel<"), (2, 40_000, "gemm", "gemm_tile_kernel<"),
+    (5, 20_000, "tt", "rows_kernel<"), (1, 20_000, "ptt", "fast_kernel<"), (2, 3000, "gemm", "gemm_tile_kernel<")])
+def test_categorical_few_sets_on_the_fast_kernels(cfg, n, strategy, kernel):
+    """Categorical nodes on one column of 4 categories (at most 16 distinct
+    sets, so a few indicator columns): the row-parallel fast kernels (PTT
+    with leaf values in global memory, TT with leaf records in global
+    memory), the rows-across-lanes kernel and the GEMM tile kernel (with and
+    without the tree split) stage the indicators in their LDS tiles."""
+    model, _ = handle(cfg)
+    m, X = synth.with_categories(model, synth.make_rows(cfg, n), seed=cfg + n, cat_cols=[1], n_categories=4)
+    m, X = synth.with_missing(m, X, seed=cfg + n + 2, p_missing=0.03)
+    h = hb.compile(m, device=0)
+    assert h.info()["n_used_features"] <= 2 * model["n_features"] + 2 * 16  # plain and NaN-left columns, sets
+    plan = [p["kernel"] for p in h.plan(n, strategy, hb.workspace_bytes(h, n, strategy))]
+    say("categorical few sets", cfg, n, strategy, plan)
+    assert plan[0].startswith(kernel), plan
+    scores, ids = run(h, X, strategy)
+    check(m, X, scores, ids, f"categorical few sets cfg{cfg}/{n}/{strategy}")
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES)
 def test_empty_batch_enqueues_nothing(strategy):
     model, h = handle(1)
     say("empty", strategy)
