@@ -725,6 +725,180 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Narrow rows, large batches: 64-row bands. A band's feature tile is small
+// (64 x F floats), so three workgroups share a CU. Wave w keeps the A
+// operands of leaves 64 w .. 64 w + 63 in registers (as the 16-row tiles do)
+// and builds, one tree ahead, the predicate bytes of nodes 64 w .. 64 w + 63
+// for all 64 rows of the band (lane = row): a node's record is the same for
+// the whole wave, the feature reads of a node are 64 consecutive floats of
+// its column, and each lane stores whole 16-byte pieces of its row. The four
+// waves then multiply all four 16-row tiles by their leaves, leave per row
+// and lane group the maximum over their leaves in LDS, and after the one
+// barrier per tree wave t mod 4 picks each row's leaf of tree t from the 16
+// maxima. Each wave adds the leaves of its trees in tree order and the four
+// waves' sums are added in wave order at the end.
+constexpr int kBandRows = 64;
+constexpr int kBandXS = kBandRows;  // floats per feature column of the tile
+// Predicate tile: row r holds 16 pieces of 16 bytes (nodes 16 p .. 16 p + 15
+// in piece p ^ (r mod 16)), so the 16 rows a lane group reads for one piece,
+// and the pieces the 64 rows write at once, fall on distinct banks.
+__device__ __forceinline__ int band_piece(int r, int p) { return r * 256 + 16 * (p ^ (r & 15)); }
+
+template <int KMODE, int KM>
+struct BandLeaf {
+  int t = -1;  // tree of the pending lookup, -1 none
+  int cls = 0;
+  int32_t id = 0;
+  float v[KMODE == 2 ? KM : 1];
+};
+
+// Predicate bytes (64 where x < threshold, else 0) of nodes 64 w + 16 q ..
+// + 15 of tree tn for row `lane` of the band. The records are the same for
+// the whole wave and come by vector loads (one address for all lanes):
+// scalar loads were slower, as waiting for them also waits for every LDS
+// read in flight.
+typedef const uint2 *BandRecs;
+__device__ __forceinline__ void band_build_q(BandRecs rec, int q, const float *xs, unsigned char *dst, int wave,
+                                             int lane) {
+  uint2 r[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) r[i] = rec[q * 16 + i];
+  float x[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) x[i] = xs[r[i].y * kBandXS + lane];
+  u32x4 w;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    uint32_t word = 0;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) word |= (x[j * 4 + b] < as_float(r[j * 4 + b].x) ? 0x40u : 0u) << (8 * b);
+    w[j] = word;
+  }
+  *reinterpret_cast<u32x4 *>(dst + band_piece(lane, wave * 4 + q)) = w;
+}
+
+__device__ __forceinline__ BandRecs band_recs(const GemmArgs &a, int tn, int wave) {
+  return a.node + (size_t)tn * a.k_pad + wave * 64;
+}
+
+template <int KMODE, int KM>
+__device__ __forceinline__ void band_consume(const GemmArgs &a, BandLeaf<KMODE, KM> &p, double (&acc)[KM],
+                                             int64_t row) {
+  if (p.t < 0) return;
+  if (KMODE == 2) {
+#pragma unroll
+    for (int k = 0; k < KM; ++k) acc[k] += (double)p.v[k];
+  } else if (KMODE == 0) {
+    acc[0] += (double)p.v[0];
+  } else {
+#pragma unroll
+    for (int k = 0; k < KM; ++k)
+      if (k == p.cls) acc[k] += (double)p.v[0];
+  }
+  if (a.leaf_ids && row < a.n_rows) a.leaf_ids[row * a.out.T + p.t] = p.id;
+  p.t = -1;
+}
+
+template <int KMODE, int KM>
+__global__ __launch_bounds__(256) void gemm_band_kernel(GemmArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];  // feature tile [F][kBandXS]
+  __shared__ __align__(16) unsigned char bt[2][kBandRows * 256];
+  // per row, the 16 lane groups' maxima clamped to [-1, 255] (only a column
+  // that is not negative is a match)
+  __shared__ __align__(16) short red[2][kBandRows][16];
+  static_assert((size_t)4 * kBandRows * HB_MAX_OUTPUTS * 8 <= sizeof(bt), "partial sums reuse the predicate tiles");
+  const int tid = threadIdx.x, lane = tid & 63, g4 = lane >> 4, r16 = lane & 15;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int T = a.out.T;
+  float *xs = reinterpret_cast<float *>(smem);
+  const int64_t r0 = (int64_t)blockIdx.x * kBandRows;
+  const int64_t row = r0 + lane;
+  for (int e = tid; e < kBandRows * a.F; e += 256) {
+    const int r = e / a.F, f = e - r * a.F;
+    xs[f * kBandXS + r] = r0 + r < a.n_rows ? xval(a.X + (r0 + r) * a.Fs, a.cols, f) : 0.0f;
+  }
+  v4i ctr[4][4], b4[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int lt = wave * 4 + j;
+    b4[j] = *reinterpret_cast<const v4i *>(a.bias + lt * 16 + 4 * g4);
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+      ctr[j][kb] = *reinterpret_cast<const v4i *>(a.ct + (size_t)(lt * 16 + r16) * 256 + kb * 64 + 16 * g4);
+  }
+  lds_sync();
+#pragma unroll
+  for (int q = 0; q < 4; ++q) band_build_q(band_recs(a, 0, wave), q, xs, bt[0], wave, lane);
+  lds_sync();
+  double acc[KM];
+#pragma unroll
+  for (int k = 0; k < KM; ++k) acc[k] = 0.0;
+  BandLeaf<KMODE, KM> pend;
+  for (int t = 0; t < T; ++t) {
+    const int P = t & 1;
+    const BandRecs next = band_recs(a, min(t + 1, T - 1), wave);
+    // tree t's products, 16 rows at a time, each row tile's four leaf tiles
+    // as four independent chains; per row and lane group the maximum over
+    // this wave's leaves (the selected leaf's column, or a negative value).
+    // Then tree t+1's predicate operand (building it between the row tiles
+    // was slower).
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      v4i bop[4];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+        bop[kb] = *reinterpret_cast<const v4i *>(bt[P] + band_piece(16 * rt + r16, kb * 4 + g4));
+      v4i d[4];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          d[j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ctr[j][kb], bop[kb], kb ? d[j] : b4[j], 0, 0, 0);
+      const int best = max(max(hmax4(d[0]), hmax4(d[1])), max(hmax4(d[2]), hmax4(d[3])));
+      red[P][16 * rt + r16][wave * 4 + g4] = (short)min(max(best, -1), 255);
+    }
+    if (t + 1 < T) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) band_build_q(next, q, xs, bt[P ^ 1], wave, lane);
+    }
+    lds_sync();
+    if (wave == (t & 3)) {
+      band_consume<KMODE, KM>(a, pend, acc, row);
+      int col = -1;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) col = max(col, (int)red[P][lane][i]);
+      col = min(max(col, 0), a.l_pad - 1);  // a valid tree always yields a column in range
+      const size_t lrec = (size_t)t * a.l_pad + (size_t)col;
+      pend.t = t;
+      pend.id = a.leaf_id[lrec];
+      if (KMODE == 2) {
+#pragma unroll
+        for (int k = 0; k < KM; ++k) pend.v[k] = k < a.LD ? a.leaf_value[lrec * a.LD + k] : 0.0f;
+      } else {
+        pend.v[0] = a.leaf_value[lrec];
+        if (KMODE == 1) pend.cls = a.tree_class[t];
+      }
+    }
+  }
+  band_consume<KMODE, KM>(a, pend, acc, row);
+  // the four waves' sums in wave order (the predicate tiles are no longer read)
+  double *part = reinterpret_cast<double *>(&bt[0][0]);
+#pragma unroll
+  for (int k = 0; k < KM; ++k) part[(wave * kBandRows + lane) * KM + k] = acc[k];
+  lds_sync();
+  if (wave == 0 && row < a.n_rows) {
+    double s[KM];
+#pragma unroll
+    for (int k = 0; k < KM; ++k) s[k] = 0.0;
+    for (int w = 0; w < 4; ++w) {
+#pragma unroll
+      for (int k = 0; k < KM; ++k) s[k] += part[(w * kBandRows + lane) * KM + k];
+    }
+    finish_row<KM>(a.out, s, row);
+  }
+}
+
 using GemmFn = void (*)(GemmArgs);
 
 template <int KB, bool CT, bool XL, int ROWS, bool COLS = false>
@@ -744,6 +918,15 @@ GemmFn pick_gemm(bool ct, bool xl, int kmode, int rows, bool cols) {
 }
 
 }  // namespace
+
+// Batches from three 64-row bands per CU up take the band kernel.
+constexpr int64_t kBandMinRows = 3 * 256 * kBandRows;
+
+static GemmFn band_fn(int kmode, int width) {
+  if (kmode == 0) return gemm_band_kernel<0, 1>;
+  if (kmode == 1) return width <= 8 ? gemm_band_kernel<1, 8> : gemm_band_kernel<1, 16>;
+  return width <= 2 ? gemm_band_kernel<2, 2> : width <= 8 ? gemm_band_kernel<2, 8> : gemm_band_kernel<2, 16>;
+}
 
 int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t n_rows, float *scores,
                 int32_t *leaf_ids, const Launch &L, hipStream_t stream, std::string *err) {
@@ -799,7 +982,22 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
       piped = true;
     }
   }
-  if (!piped && t.n_shapes == 1 && kb == 4 && t.l_pad == 256) {
+  bool banded = false;
+  if (!piped && t.n_shapes == 1 && kb == 4 && t.l_pad == 256 && n_rows >= kBandMinRows) {
+    // 64-row bands where three of them fit a CU's LDS (narrow rows)
+    const size_t band_dyn = (size_t)e.n_cols * kBandXS * 4;
+    const size_t band_static = (size_t)2 * kBandRows * 256 + (size_t)2 * kBandRows * 16 * 2;
+    if (3 * (band_dyn + band_static) <= (size_t)lds_max) {
+      fn = band_fn(kmode, kmode == 2 ? e.leaf_dim : e.n_outputs);
+      dyn = band_dyn;
+      rows = kBandRows;
+      threads = 256;
+      banded = true;
+      name = std::string("gemm_band_kernel<") + std::to_string(kmode) + ", " +
+             std::to_string(kmode == 0 ? 1 : (kmode == 2 && e.leaf_dim <= 2) ? 2 : (kmode == 2 ? e.leaf_dim : e.n_outputs) <= 8 ? 8 : 16) + ">";
+    }
+  }
+  if (!piped && !banded && t.n_shapes == 1 && kb == 4 && t.l_pad == 256) {
     // 16-row tiles with C^T in registers, unless the pipelined kernel gets
     // 512-row workgroups (two waves per SIMD): wide rows, where its feature
     // tile does not fit, and 256-row workgroups, one wave per SIMD (measured:

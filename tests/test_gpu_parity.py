@@ -585,6 +585,54 @@ def test_categorical_few_sets_on_the_fast_kernels(cfg, n, strategy, kernel):
     check(m, X, scores, ids, f"categorical few sets cfg{cfg}/{n}/{strategy}")
 
 
+def _band_model(F, K, ld, n_trees, seed, depth=8):
+    """Perfect trees over F N(0,1) features: one output (K = 1), K classes
+    with tree t in class t mod K (softmax), or 2-vector leaves (ld = 2)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    leaves = (lambda r, n: np.stack([1 - r.random(n), r.random(n)], 1)) if ld == 2 else (lambda r, n: r.normal(0, .05, n))
+    m = synth.perfect_forest(rng, n_trees, depth, F, lambda r, f: r.normal(0, 1, f.size), leaves, leaf_dim=ld)
+    m.update(n_outputs=max(K, ld), tree_class=(np.arange(n_trees) % K).astype(np.int32) if K > 1 else None,
+             aggregation="mean" if ld == 2 else "sum", transform="softmax" if K > 1 else "sigmoid", base_score=None)
+    return m
+
+
+@pytest.mark.parametrize("F,K,ld,n_trees,n,kernel", [
+    (54, 7, 1, 70, 65_536, "gemm_band_kernel<1, 8>"),     # the 7-class model's shape
+    (60, 1, 1, 37, 49_153, "gemm_band_kernel<0, 1>"),     # ragged last band
+    (60, 10, 1, 41, 52_000, "gemm_band_kernel<1, 16>"),
+    (60, 1, 2, 33, 50_001, "gemm_band_kernel<2, 2>"),
+    (48, 1, 1, 5, 49_152, "gemm_band_kernel<0, 1>"),      # fewer trees than waves
+])
+def test_gemm_band_kernel(F, K, ld, n_trees, n, kernel):
+    """Batches of three 64-row bands per CU and more, with rows too wide for
+    the 512-row pipelined kernel, take the band kernel: every row against the
+    oracle, at ragged batch sizes, with one output, 7 or 10 classes and
+    2-vector leaves."""
+    m = _band_model(F, K, ld, n_trees, seed=F * 100 + n_trees)
+    h = hb.compile(m, device=0)
+    plan = [p["kernel"] for p in h.plan(n, "gemm")]
+    say("gemm band", F, K, ld, n_trees, n, plan)
+    assert plan == [kernel], plan
+    X = np.random.Generator(np.random.PCG64(n)).normal(0, 1, (n, F)).astype(np.float32)
+    scores, ids = run(h, X, "gemm", workspace=False)
+    check(m, X, scores, ids, f"band F{F} K{K} ld{ld} T{n_trees} n{n}")
+
+
+def test_gemm_band_kernel_with_column_list():
+    """Missing values and categorical splits on the band kernel (its feature
+    tile goes through the column list)."""
+    m = _band_model(24, 1, 1, 64, seed=5)
+    X = np.random.Generator(np.random.PCG64(6)).normal(0, 1, (50_000, 24)).astype(np.float32)
+    m, X = synth.with_categories(m, X, seed=7, cat_cols=[2], n_categories=2)
+    m, X = synth.with_missing(m, X, seed=8, p_missing=0.05)
+    h = hb.compile(m, device=0)
+    plan = [p["kernel"] for p in h.plan(50_000, "gemm")]
+    say("gemm band with column list", plan, h.info()["n_used_features"])
+    assert plan == ["gemm_band_kernel<0, 1>"], plan
+    scores, ids = run(h, X, "gemm", workspace=False)
+    check(m, X, scores, ids, "band with column list")
+
+
 @pytest.mark.parametrize("strategy", STRATEGIES)
 def test_empty_batch_enqueues_nothing(strategy):
     model, h = handle(1)
