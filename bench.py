@@ -394,7 +394,8 @@ def run_configs():
                 print(json.dumps({"workload": cfg, "name": name, "rows": n,
                                   "strategy": s, "auto": s == auto, "leaf_ids": leaves,
                                   "ms": round(ms, 4), "rows_per_s": n / (ms * 1e-3),
-                                  "bound": "mfma" if s == "gemm" else "hbm", "frac": frac}), flush=True)
+                                  "bound": "mfma" if s == "gemm" else "hbm", "frac": frac,
+                                  "kernel": kernel_label(h, s, n)}), flush=True)
         del X, scores, ids
         h.close()
         torch.cuda.empty_cache()
