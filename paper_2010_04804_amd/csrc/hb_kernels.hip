@@ -485,7 +485,11 @@ struct RowsPrefetch {
   }
 };
 
-template <bool PERFECT, int KMAX, bool LEAF_VEC, int RW>
+// CONTIG: the tiles are whole contiguous rows in 16-byte pieces (no column
+// list), loaded ahead with the contiguous prefetch; otherwise they are staged
+// through the column list when needed (a gather ahead of the walk was slower:
+// its loads queue in front of the walk's node reads).
+template <bool PERFECT, int KMAX, bool LEAF_VEC, int RW, bool CONTIG>
 __global__ __launch_bounds__(kRowsThreads) void rows_kernel(TravArgs a) {
   constexpr int TPW = 64 / RW;                    // trees of one wave-level read
   constexpr int WAVES = kRowsThreads / 64;
@@ -500,9 +504,8 @@ __global__ __launch_bounds__(kRowsThreads) void rows_kernel(TravArgs a) {
   const int r = lane & (RW - 1), q = lane / RW;
   const int64_t n_tiles = (a.n_rows + RW - 1) / RW;
   // a workgroup walks tiles blockIdx.x, + gridDim.x, ...; the next tile's
-  // rows arrive in registers during the walk when the rows are contiguous
-  const bool pf = a.cols == nullptr && a.Fs == a.F && (a.F & 3) == 0 && a.F <= 2000 &&
-                  (reinterpret_cast<uintptr_t>(a.X) & 15) == 0;
+  // rows arrive in registers during the walk
+  constexpr bool pf = CONTIG;
   RowsPrefetch<RW> next;
   auto stage_rows = [&](int64_t tile) {  // load and store at once (no prefetch)
     const int64_t r0 = tile * RW;
@@ -895,10 +898,12 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const void *leaf, int chu
 }
 
 using RowsFn = void (*)(TravArgs);
-template <bool PERFECT, int RW>
+template <bool PERFECT, int RW, bool CONTIG>
 RowsFn pick_rows(int kmax, bool vec) {
-  if (vec) return kmax == 2 ? rows_kernel<PERFECT, 2, true, RW> : nullptr;
-  return kmax == 1 ? rows_kernel<PERFECT, 1, false, RW> : kmax == 2 ? rows_kernel<PERFECT, 2, false, RW> : nullptr;
+  if (vec) return kmax == 2 ? rows_kernel<PERFECT, 2, true, RW, CONTIG> : nullptr;
+  return kmax == 1   ? rows_kernel<PERFECT, 1, false, RW, CONTIG>
+         : kmax == 2 ? rows_kernel<PERFECT, 2, false, RW, CONTIG>
+                     : nullptr;
 }
 
 // Launches rows_kernel for batches whose rows are too wide for the
@@ -916,8 +921,13 @@ int launch_rows(bool perfect, const TravArgs &a, const Launch &L, hipStream_t st
   int RW = 16;
   if (rows_lds(a.F, RW, kmax) > (size_t)lds_max) RW = 8;
   if (rows_lds(a.F, RW, kmax) > (size_t)lds_max) return kNotApplicable;
-  RowsFn fn = perfect ? (RW == 16 ? pick_rows<true, 16>(kmax, vec) : pick_rows<true, 8>(kmax, vec))
-                      : (RW == 16 ? pick_rows<false, 16>(kmax, vec) : pick_rows<false, 8>(kmax, vec));
+  // whole rows in 16-byte pieces go through the contiguous prefetch
+  const bool contig = a.cols == nullptr && a.Fs == a.F && (a.F & 3) == 0 && a.F <= 2000 &&
+                      (reinterpret_cast<uintptr_t>(a.X) & 15) == 0;
+  RowsFn fn = perfect ? (RW == 16 ? (contig ? pick_rows<true, 16, true>(kmax, vec) : pick_rows<true, 16, false>(kmax, vec))
+                                  : (contig ? pick_rows<true, 8, true>(kmax, vec) : pick_rows<true, 8, false>(kmax, vec)))
+                      : (RW == 16 ? (contig ? pick_rows<false, 16, true>(kmax, vec) : pick_rows<false, 16, false>(kmax, vec))
+                                  : (contig ? pick_rows<false, 8, true>(kmax, vec) : pick_rows<false, 8, false>(kmax, vec)));
   if (!fn) return kNotApplicable;
   const size_t lds = rows_lds(a.F, RW, kmax);
   // persistent: as many workgroups as run at once (the row tiles are dealt
@@ -933,7 +943,7 @@ int launch_rows(bool perfect, const TravArgs &a, const Launch &L, hipStream_t st
   if (L.plan) {
     plan_line(L.plan,
               std::string("rows_kernel<") + tf(perfect) + ", " + std::to_string(kmax) + ", " + tf(vec) + ", " +
-                  std::to_string(RW) + ">",
+                  std::to_string(RW) + ", " + tf(contig) + ">",
               blocks, 1, kRowsThreads, lds);
     return HB_OK;
   }

@@ -779,7 +779,7 @@ def test_full_size_wide_forest_every_row():
     model, h = handle(3)
     n = 100_000
     X = synth.make_rows(3, n)
-    assert [p["kernel"] for p in h.plan(n, "auto")] == ["rows_kernel<true, 2, true, 16>"], h.plan(n, "auto")
+    assert [p["kernel"] for p in h.plan(n, "auto")] == ["rows_kernel<true, 2, true, 16, true>"], h.plan(n, "auto")
     say("full size every row", 3, n)
     Xd = torch.from_numpy(X).cuda()
     s, ids = hb.predict(h, Xd, strategy="auto", workspace=False)
