@@ -274,11 +274,16 @@ HB_API int hb_query(const hb_handle *h, hb_info *info);
  *         "shape" (int32 [T]), "ct" (int8 [S][l_pad][k_pad], 4*C^T),
  *         "bias" (int32 [S][l_pad]), "leaf_value" (float [T][l_pad][leaf_dim]),
  *         "leaf_id" (int32 [T][l_pad]), "dims" (int32 {k_pad, l_pad, S})
- *   any : "features" (int32 [n_used_features]: the input column of each
- *         feature index the tables above use, in bits 0-29; bit 30 set
- *         means that index reads a NaN input as -inf, for the nodes that
- *         send missing values left. Unless this is the identity, the tables
- *         hold these indices instead of input columns)
+ *   any : "features" (int32: n_used_features entries, one per feature index
+ *         the tables above use: the input column in bits 0-28; bit 30 set
+ *         means a NaN input goes left (a numeric index reads it as -inf);
+ *         bit 29 set means the index is the 0/1 indicator of a category set
+ *         (0 where the row goes left; its nodes test it against 0.5) and bits
+ *         0-28 are the offset, in entries from the start of this array, of
+ *         its descriptor {input column, word count W, W words of the set};
+ *         the descriptors follow the n_used_features entries. Unless this is
+ *         the identity, the tables hold these indices instead of input
+ *         columns)
  * Returns HB_ERR_INVALID_ARG for an unknown name or an infeasible strategy.
  */
 HB_API int hb_table(const hb_handle *h, int strategy, const char *name, const void **data, int64_t *bytes);

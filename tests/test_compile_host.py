@@ -311,3 +311,41 @@ def test_categorical_columns_are_shared():
     for s in ("ptt", "tt", "gemm"):
         ids, raw = getattr(emulate, s)(h, m, X)
         assert np.array_equal(ids, o_ids), s
+
+
+def _node_depths(model, t):
+    off = model["tree_node_offset"]
+    a, b = int(off[t]), int(off[t + 1])
+    d = np.zeros(b - a, np.int64)
+    stack = [0]
+    while stack:
+        v = stack.pop()
+        if model["feature"][a + v] >= 0:
+            for c in (model["left"][a + v], model["right"][a + v]):
+                d[c] = d[v] + 1
+                stack.append(int(c))
+    return d
+
+
+def test_tt_walk_levels_on_the_leafwise_workload():
+    """The row-parallel TT walk of the leaf-wise workload: a chunk of 8 trees
+    walks as many levels as its deepest tree (12 for every chunk here), while a
+    row needs only the depth of the leaf it reaches (5.2 on average). The
+    wave's 64 rows move in lockstep, and some row reaches depth 11-12 in most
+    trees, so stopping a tree once all 64 rows of a wave sit at leaves would
+    save only about 7% of the levels."""
+    m = synth.make_model(5)
+    X = synth.make_rows(5, 4096)
+    h = host(m)
+    depth = h.table("tt", "depth", np.int32)
+    T, TC = m["n_trees"], 8
+    chunk_levels = sum(TC * int(depth[c:c + TC].max()) for c in range(0, T, TC))
+    _, _, ids = oracle.predict(m, X)
+    L = np.stack([_node_depths(m, t)[ids[:, t]] for t in range(T)], 1)
+    useful = L.mean(0).sum()                      # levels a row needs, over all trees
+    wave_tree = L.reshape(-1, 64, T).max(1).mean()  # levels a wave needs per tree
+    print(f"[tt levels] walked per row {chunk_levels}, needed {useful:.1f} "
+          f"({useful / chunk_levels:.3f}), per-wave tree need {wave_tree:.2f} of 12")
+    assert int(depth.max()) == 12 and chunk_levels == 6048
+    assert 0.42 < useful / chunk_levels < 0.45
+    assert 11.0 < wave_tree < 11.4
