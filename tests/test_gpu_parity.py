@@ -587,12 +587,18 @@ def test_categorical_few_sets_on_the_fast_kernels(cfg, n, strategy, kernel):
 
 def _band_model(F, K, ld, n_trees, seed, depth=8):
     """Perfect trees over F N(0,1) features: one output (K = 1), K classes
-    with tree t in class t mod K (softmax), or 2-vector leaves (ld = 2)."""
+    with tree t in class t mod K (softmax), or vector leaves of ld class
+    probabilities (ld > 1, averaged)."""
     rng = np.random.Generator(np.random.PCG64(seed))
-    leaves = (lambda r, n: np.stack([1 - r.random(n), r.random(n)], 1)) if ld == 2 else (lambda r, n: r.normal(0, .05, n))
+    if ld > 1:
+        def leaves(r, n):
+            p = r.random((n, ld))
+            return p / p.sum(1, keepdims=True)
+    else:
+        leaves = lambda r, n: r.normal(0, .05, n)
     m = synth.perfect_forest(rng, n_trees, depth, F, lambda r, f: r.normal(0, 1, f.size), leaves, leaf_dim=ld)
     m.update(n_outputs=max(K, ld), tree_class=(np.arange(n_trees) % K).astype(np.int32) if K > 1 else None,
-             aggregation="mean" if ld == 2 else "sum", transform="softmax" if K > 1 else "sigmoid", base_score=None)
+             aggregation="mean" if ld > 1 else "sum", transform="softmax" if K > 1 else "sigmoid", base_score=None)
     return m
 
 
@@ -602,12 +608,14 @@ def _band_model(F, K, ld, n_trees, seed, depth=8):
     (60, 10, 1, 41, 52_000, "gemm_band_kernel<1, 16>"),
     (60, 1, 2, 33, 50_001, "gemm_band_kernel<2, 2>"),
     (48, 1, 1, 5, 49_152, "gemm_band_kernel<0, 1>"),      # fewer trees than waves
+    (60, 1, 5, 23, 49_999, "gemm_band_kernel<2, 8>"),     # 5-vector leaves
+    (60, 1, 10, 17, 50_113, "gemm_band_kernel<2, 16>"),   # 10-vector leaves
 ])
 def test_gemm_band_kernel(F, K, ld, n_trees, n, kernel):
     """Batches of three 64-row bands per CU and more, with rows too wide for
     the 512-row pipelined kernel, take the band kernel: every row against the
     oracle, at ragged batch sizes, with one output, 7 or 10 classes and
-    2-vector leaves."""
+    2-, 5- and 10-vector leaves (every instantiation of the kernel)."""
     m = _band_model(F, K, ld, n_trees, seed=F * 100 + n_trees)
     h = hb.compile(m, device=0)
     plan = [p["kernel"] for p in h.plan(n, "gemm")]
