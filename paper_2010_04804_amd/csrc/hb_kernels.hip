@@ -921,13 +921,15 @@ int launch_rows(bool perfect, const TravArgs &a, const Launch &L, hipStream_t st
   int RW = 16;
   if (rows_lds(a.F, RW, kmax) > (size_t)lds_max) RW = 8;
   if (rows_lds(a.F, RW, kmax) > (size_t)lds_max) return kNotApplicable;
-  // whole rows in 16-byte pieces go through the contiguous prefetch
-  const bool contig = a.cols == nullptr && a.Fs == a.F && (a.F & 3) == 0 && a.F <= 2000 &&
+  // whole rows in 16-byte pieces go through the contiguous prefetch; its
+  // 2,000-feature cap always leaves room for 16 rows per workgroup, so the
+  // 8-row kernels stage through the column list only
+  const bool contig = RW == 16 && a.cols == nullptr && a.Fs == a.F && (a.F & 3) == 0 && a.F <= 2000 &&
                       (reinterpret_cast<uintptr_t>(a.X) & 15) == 0;
   RowsFn fn = perfect ? (RW == 16 ? (contig ? pick_rows<true, 16, true>(kmax, vec) : pick_rows<true, 16, false>(kmax, vec))
-                                  : (contig ? pick_rows<true, 8, true>(kmax, vec) : pick_rows<true, 8, false>(kmax, vec)))
+                                  : pick_rows<true, 8, false>(kmax, vec))
                       : (RW == 16 ? (contig ? pick_rows<false, 16, true>(kmax, vec) : pick_rows<false, 16, false>(kmax, vec))
-                                  : (contig ? pick_rows<false, 8, true>(kmax, vec) : pick_rows<false, 8, false>(kmax, vec)));
+                                  : pick_rows<false, 8, false>(kmax, vec));
   if (!fn) return kNotApplicable;
   const size_t lds = rows_lds(a.F, RW, kmax);
   // persistent: as many workgroups as run at once (the row tiles are dealt

@@ -881,3 +881,76 @@ def test_invalid_arguments_raise():
         hb.predict_ptr(h, 1, -1, 1, None)
     with pytest.raises(hb.HBError):
         hb.predict_ptr(h, 1, 1, 1, None, strategy=7)
+
+
+def _shape_model(kind, size, F, T, K, ld, seed, spread=1):
+    """Perfect trees of depth `size` or leaf-wise trees of `size` leaves (depth
+    <= 14) over F N(0,1) features, each feature index times `spread` (so that
+    the input has F * spread columns); K > 1: tree t in class t mod K
+    (softmax); ld > 1: probability vectors averaged."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    thr = lambda r, f: r.normal(0, 1, f.size)
+    if ld > 1:
+        def leaves(r, n):
+            p = r.random((n, ld))
+            return p / p.sum(1, keepdims=True)
+    else:
+        leaves = lambda r, n: r.normal(0, .05, n)
+    if kind == "perfect":
+        m = synth.perfect_forest(rng, T, size, F, thr, leaves, leaf_dim=ld)
+    else:
+        m = synth.leafwise_forest(rng, T, size, 14, 0.7, F, thr, lambda r, n: r.normal(0, .05, n))
+        if ld > 1:
+            m["leaf_value"] = leaves(np.random.Generator(np.random.PCG64(seed + 1)), m["feature"].size).reshape(-1)
+            m["leaf_dim"] = ld
+    if spread > 1:
+        m["feature"] = np.where(m["feature"] >= 0, m["feature"] * spread, m["feature"]).astype(m["feature"].dtype)
+        m["n_features"] = F * spread
+    m.update(n_outputs=max(K, ld), tree_class=(np.arange(T) % K).astype(np.int32) if K > 1 else None,
+             aggregation="mean" if ld > 1 else "sum", transform="softmax" if K > 1 or ld > 1 else "none",
+             base_score=None)
+    return m
+
+
+@pytest.mark.parametrize("kind,size,F,spread,T,K,ld,n,strategy,expect", [
+    # PTT deeper than the row-parallel kernels hold, at batches past the tree-parallel kernel
+    ("perfect", 11, 28, 1, 24, 1, 1, 20_000, "ptt", "traverse_kernel<true, true, 1, false, false>"),
+    ("perfect", 11, 28, 1, 24, 3, 1, 20_000, "ptt", "traverse_kernel<true, true, 8, false, false>"),
+    ("perfect", 11, 28, 1, 24, 1, 2, 20_000, "ptt", "traverse_kernel<true, true, 2, true, false>"),
+    # pruned inputs: the column list is applied while the feature tile is staged
+    ("perfect", 11, 28, 3, 24, 1, 1, 20_001, "ptt", "traverse_kernel<true, true, 1, false, false>"),
+    # TT trees of more than 2,048 nodes
+    ("leafwise", 1500, 28, 1, 12, 1, 1, 20_000, "tt", "traverse_kernel<false, true, 1, false, false>"),
+    ("leafwise", 1500, 28, 1, 12, 1, 3, 20_000, "tt", "traverse_kernel<false, true, 8, true, false>"),
+    ("leafwise", 1500, 28, 3, 12, 2, 1, 20_001, "tt", "traverse_kernel<false, true, 2, false, false>"),
+    # rows wider than LDS (over 40,960 staged features): features read from
+    # global memory, whole or through the column list
+    ("perfect", 12, 45_000, 1, 24, 1, 1, 300, "ptt", "traverse_kernel<true, false, 1, false, false>"),
+    ("perfect", 12, 60_000, 1, 18, 1, 1, 301, "ptt", "traverse_kernel<true, false, 1, false, true>"),
+    # more than about 2,300 used columns: 8 rows per workgroup instead of 16
+    ("perfect", 6, 4000, 1, 120, 1, 1, 8_000, "ptt", "rows_kernel<true, 1, false, 8, false>"),
+    ("perfect", 6, 4000, 1, 120, 1, 2, 8_001, "ptt", "rows_kernel<true, 2, true, 8, false>"),
+    ("leafwise", 40, 4000, 1, 120, 2, 1, 8_002, "tt", "rows_kernel<false, 2, false, 8, false>"),
+    # several outputs on the tree-parallel kernel, one and four rows per workgroup
+    ("perfect", 7, 28, 1, 90, 2, 1, 700, "ptt", "lanes_kernel<true, 2, false, 1>"),
+    ("perfect", 7, 28, 1, 90, 2, 1, 3000, "ptt", "lanes_kernel<true, 2, false, 4>"),
+    ("leafwise", 60, 28, 1, 90, 5, 1, 3000, "tt", "lanes_kernel<false, 8, false, 4>"),
+    ("leafwise", 60, 28, 1, 90, 12, 1, 3000, "tt", "lanes_kernel<false, 16, false, 1>"),
+    ("perfect", 7, 28, 1, 90, 1, 12, 3000, "ptt", "lanes_kernel<true, 16, true, 1>"),
+    ("leafwise", 60, 28, 1, 90, 1, 2, 3000, "tt", "lanes_kernel<false, 2, true, 4>"),
+])
+def test_general_and_wide_kernel_paths(kind, size, F, spread, T, K, ld, n, strategy, expect):
+    """Kernels the workloads do not reach: the general traversal kernel (trees
+    beyond the row-parallel kernels, rows wider than LDS), the
+    rows-across-lanes kernel with 8 rows per workgroup, and the tree-parallel
+    kernel with several outputs; each case asserts the launch plan and
+    compares every row with the oracle."""
+    m = _shape_model(kind, size, F, T, K, ld, seed=size * 1000 + F + T, spread=spread)
+    h = hb.compile(m, device=0)
+    assert h.info()["feasible"][strategy]
+    plan = [p["kernel"] for p in h.plan(n, strategy)]
+    say("kernel path", kind, size, F, spread, T, K, ld, n, strategy, plan)
+    assert plan == [expect], plan
+    X = np.random.Generator(np.random.PCG64(n + F)).normal(0, 1, (n, F * spread)).astype(np.float32)
+    scores, ids = run(h, X, strategy, workspace=False)
+    check(m, X, scores, ids, f"path {kind}{size} F{F}x{spread} T{T} K{K} ld{ld} n{n} {strategy}")
