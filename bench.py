@@ -135,6 +135,33 @@ def mfma_peak_measured():
     return v.value if rc == 0 else None
 
 
+LDS_READS = ["b32, each lane its own word", "b32, hashed slot of 256 (1 KiB)", "b64, each lane its own word pair",
+             "b64, hashed slot of 256 (2 KiB)", "u16, each lane its own half-word", "b128, each lane its own 16 bytes",
+             "b128, hashed slot of 64 (1 KiB)", "b64 hashed of 256 and b32 own, alternating"]
+
+
+def run_lds_probe():
+    """Nanoseconds per wave-wide LDS read instruction per CU for the read
+    shapes of the traversal walks (16 waves per CU, eight reads in flight per
+    wave), from the probe library built beside libhb.so: one JSON line per
+    shape."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2010_04804_amd", "libhb_probe.so")
+    if not os.path.exists(path):
+        print(json.dumps({"error": "libhb_probe.so is not built (run the package build)"}))
+        sys.exit(1)
+    lib = ctypes.CDLL(path)
+    lib.hb_probe_lds_read.restype = ctypes.c_int
+    lib.hb_probe_lds_read.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    for mode, name in enumerate(LDS_READS):
+        v = ctypes.c_double(0.0)
+        rc = lib.hb_probe_lds_read(0, mode, ctypes.byref(v))
+        if rc:
+            print(json.dumps({"error": f"hb_probe_lds_read({mode}) returned {rc}"}))
+            sys.exit(1)
+        print(json.dumps({"lds_read": name, "mode": mode, "ns_per_read_per_cu": v.value}), flush=True)
+
+
 def end_to_end(hb, h, X, n, info, leaves, strategy, dev, reps=3):
     """The whole request from host memory: X copied in from pinned host
     memory, the scoring call, scores (and leaf ids) copied back to pinned host
@@ -425,6 +452,8 @@ def main():
                     help="wide inputs whose trees test few columns, instead of the bench line")
     ap.add_argument("--configs", action="store_true",
                     help="every workload and strategy against its roofline, instead of the bench line")
+    ap.add_argument("--lds-probe", action="store_true",
+                    help="LDS read rates of the traversal walks' read shapes (probe library)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": f"--gpus {args.gpus}: this benchmark runs on one GPU only. Rows are "
@@ -442,6 +471,8 @@ def main():
         return run_pruning()
     if args.configs:
         return run_configs()
+    if args.lds_probe:
+        return run_lds_probe()
 
     import torch
 
@@ -462,9 +493,20 @@ def main():
     ids = torch.empty((n, info["n_trees"]), dtype=torch.int32, device=dev) if leaves else None
     stream = torch.cuda.current_stream(dev)
 
+    # each strategy gets the workspace the library asks for at this batch
+    # size (hb_workspace_bytes: the inputs' ranks for large PTT batches, a
+    # tree split for small ones), allocated once, outside the timed calls
+    ws = {}
+    for s in ("ptt", "tt", "gemm"):
+        if info["feasible"][s]:
+            nws = hb.workspace_bytes(h, n, s)
+            ws[s] = (torch.empty(nws, dtype=torch.uint8, device=dev), nws) if nws else (None, 0)
+
     def step(strat):
+        buf, nws = ws[strat]
         hb.predict_ptr(h, Xd.data_ptr(), n, scores.data_ptr(),
-                       ids.data_ptr() if ids is not None else None, strat, stream.cuda_stream)
+                       ids.data_ptr() if ids is not None else None, strat, stream.cuda_stream,
+                       buf.data_ptr() if buf is not None else None, nws)
 
     per_call = {}
 
@@ -494,7 +536,7 @@ def main():
             achieved = ops / (ms * 1e-3)
             r = {"bound": "mfma", "achieved": achieved / 1e12, "peak": INT8_PEAK / 1e12,
                  "unit": "TOP/s", "frac": achieved / INT8_PEAK, "traffic": None,
-                 "kernel": kernel_label(h, strat, n), "avg_launch_ms": ms, "ops_per_launch": ops}
+                 "kernel": kernel_label(h, strat, n, ws[strat][1]), "avg_launch_ms": ms, "ops_per_launch": ops}
             if mfma_measured:
                 r["peak_measured"] = mfma_measured / 1e12
                 r["frac_of_measured"] = achieved / mfma_measured
@@ -503,7 +545,7 @@ def main():
         achieved = b / (ms * 1e-3)
         return {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
                 "frac": achieved / HBM_PEAK, "traffic": recorded_traffic(cfg, strat, n, leaves),
-                "kernel": kernel_label(h, strat, n), "avg_launch_ms": ms, "bytes_per_launch": b}
+                "kernel": kernel_label(h, strat, n, ws[strat][1]), "avg_launch_ms": ms, "bytes_per_launch": b}
 
     print(f"[bench] config {cfg}: {n} rows, strategy {strategy}, leaf ids {leaves}", flush=True)
     t_wall = time.perf_counter()

@@ -520,7 +520,7 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   // and before the blocks (waiting for a load issued behind the prefetch
   // would mean waiting for the whole prefetch)
   int dep_next = 0;
-  if (MODE != 0) dep_next = a.tree_depth[min((more ? c + 1 : c) * TC + ((int)threadIdx.x & (TC - 1)), a.out.T - 1)];
+  if (MODE == 1 || MODE == 2) dep_next = a.tree_depth[min((more ? c + 1 : c) * TC + ((int)threadIdx.x & (TC - 1)), a.out.T - 1)];
   __builtin_amdgcn_sched_barrier(0);
   ChunkPrefetch<ROWS, C::CHUNK16> next;
   next.load(a.blocks + (size_t)(more ? c + 1 : c) * C::CHUNK16);
@@ -755,7 +755,7 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   for (int k = 0; k < C::KMAX; ++k) acc[k] = 0.0;
   typename C::Pack ids;
   int cls = C::MULTI && !a.vec ? a.tree_class[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
-  int dep = MODE != 0 ? a.tree_depth[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
+  int dep = (MODE == 1 || MODE == 2) ? a.tree_depth[min(c_begin * C::TC + (tid & (C::TC - 1)), a.out.T - 1)] : 0;
   float2 vh[C::VH];
 #pragma unroll
   for (int g = 0; g < C::VH; ++g) vh[g] = make_float2(0.0f, 0.0f);
