@@ -311,10 +311,11 @@ void build_fast(hb_handle *h, const hb_ensemble_desc *d, const std::vector<Canon
     const size_t S = (size_t)1 << D;
     const size_t padded = (size_t)(T + hb::kFastIdGroup - 1) / hb::kFastIdGroup * hb::kFastIdGroup;
     // Mode 3 (leaf values apart, in global memory, ids formed from the leaf
-    // slot): one scalar output, depth <= 8 (slots fit a byte), every leaf's
-    // caller id its slot plus one base (heap-ordered perfect trees), and the
-    // values small enough to stay in an XCD's L2.
-    bool affine = d->n_outputs == 1 && ld == 1 && D <= 8 && (int64_t)(padded * S * 4) <= hb::kTtLeafGlobalMax;
+    // slot): scalar leaves (one output, or one per tree class), depth <= 8
+    // (slots fit a byte), every leaf's caller id its slot plus one base
+    // (heap-ordered perfect trees), and the values small enough to stay in
+    // an XCD's L2.
+    bool affine = ld == 1 && D <= 8 && (int64_t)(padded * S * 4) <= hb::kTtLeafGlobalMax;
     const int32_t base = h->ptt_leaf_id.empty() ? 0 : h->ptt_leaf_id[0];
     for (size_t i = 0; affine && i < (size_t)T * S; ++i) affine = h->ptt_leaf_id[i] == base + (int32_t)(i % S);
     if (affine) {

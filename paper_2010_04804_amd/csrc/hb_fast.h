@@ -99,6 +99,9 @@ struct FastCfg {
   // hides behind a walk; the ids are the leaves' slots, held as bytes
   static constexpr bool GV = MODE == 3;
   static constexpr int GVH = GV ? TC : 1;
+  // several outputs (one per tree class): the output column of each held
+  // value, wave-uniform
+  static constexpr int GKH = GV && MULTI ? TC : 1;
   using Pack = typename std::conditional<GV, IdPack8, IdPack>::type;
 };
 
@@ -509,7 +512,8 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
                                            typename FastCfg<MODE, LG, KM, ROWS, BUDGET>::Pack &ids, int &cls, int &dep,
                                            float2 (&vh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::VH],
                                            uint2 (&lh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::LH],
-                                           float (&gv)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::GVH], const IdOut &io) {
+                                           float (&gv)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::GVH],
+                                           int (&gk)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::GKH], const IdOut &io) {
   using C = FastCfg<MODE, LG, KM, ROWS, BUDGET>;
   constexpr int TC = C::TC;
   constexpr int TB = C::TB;
@@ -636,7 +640,13 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
     for (int g = 0; g < TC; ++g) {
       const uint32_t slot = (s[g] >> 3) & ((1u << LG) - 1u);
       lrs[g] = make_uint2(0u, slot);
-      acc[0] += (double)gv[g < C::GVH ? g : 0];
+      if constexpr (C::MULTI) {
+        // the column is uniform across the wave: one register-indexed update
+        acc[gk[g]] += (double)gv[g];
+        gk[g] = __builtin_amdgcn_readlane(cls, g) & (C::KMAX - 1);
+      } else {
+        acc[0] += (double)gv[g < C::GVH ? g : 0];
+      }
       gv[g < C::GVH ? g : 0] = a.leafv[((size_t)(t0 + g) << LG) | slot];
     }
   }
@@ -705,12 +715,13 @@ __device__ __forceinline__ void fast_group(const FastArgs &a, int c0, uint4 (*tb
                                            typename FastCfg<MODE, LG, KM, ROWS, BUDGET>::Pack &ids, int &cls, int &dep,
                                            float2 (&vh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::VH],
                                            uint2 (&lh)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::LH],
-                                           float (&gv)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::GVH], const IdOut &io) {
+                                           float (&gv)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::GVH],
+                                           int (&gk)[FastCfg<MODE, LG, KM, ROWS, BUDGET>::GKH], const IdOut &io) {
   using C = FastCfg<MODE, LG, KM, ROWS, BUDGET>;
   if constexpr (Q < C::CPF) {
     fast_chunk<MODE, LG, KM, ROWS, BUDGET, C::BUFS == 2 ? (Q & 1) : 0, Q>(a, c0 + Q, tbuf, xs, lane4, acc, ids,
-                                                                           cls, dep, vh, lh, gv, io);
-    fast_group<MODE, LG, KM, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls, dep, vh, lh, gv, io);
+                                                                           cls, dep, vh, lh, gv, gk, io);
+    fast_group<MODE, LG, KM, ROWS, BUDGET, Q + 1>(a, c0, tbuf, xs, lane4, acc, ids, cls, dep, vh, lh, gv, gk, io);
   }
 }
 
@@ -765,10 +776,13 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   float gv[C::GVH];
 #pragma unroll
   for (int g = 0; g < C::GVH; ++g) gv[g] = 0.0f;
+  int gk[C::GKH];
+#pragma unroll
+  for (int g = 0; g < C::GKH; ++g) gk[g] = 0;
   const IdOut io = make_id_out<ROWS>(a.leaf_ids != nullptr && a.ids_vec != 0, idstage[tid >> 6], c_begin * C::TC,
                                      (uint32_t)a.id_base, a.out.T);
   for (int c = c_begin; c < a.n_chunks; c += C::CPF) {  // chunk counts are multiples of CPF
-    fast_group<MODE, LG, KM, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, vh, lh, gv, io);
+    fast_group<MODE, LG, KM, ROWS, BUDGET, 0>(a, c, tbuf, fxs, lane4, acc, ids, cls, dep, vh, lh, gv, gk, io);
     if (!C::LAG && a.leaf_ids && !a.ids_vec) flush_scalar(a.leaf_ids, a.n_rows, a.out.T, ids, io, c * C::TC);
   }
   if constexpr (C::DEFER && !C::LAG)  // the last chunk's inside lines and ids
@@ -797,7 +811,12 @@ __global__ __launch_bounds__(ROWS) void fast_kernel(FastArgs a) {
   }
   if (C::GV) {  // the last chunk's values
 #pragma unroll
-    for (int g = 0; g < C::GVH; ++g) acc[0] += (double)gv[g];
+    for (int g = 0; g < C::GVH; ++g) {
+      if constexpr (C::MULTI)
+        acc[gk[g]] += (double)gv[g];
+      else
+        acc[0] += (double)gv[g];
+    }
   }
   if (C::VHOLD && a.vec) {  // the last chunk's 2-vector leaves
 #pragma unroll

@@ -1,10 +1,14 @@
 // hb_fast_pttg_128.hip -- instantiations of the fast PerfectTreeTraversal
 // kernel with the leaf values in global memory (mode 3) for 128-row
-// workgroups: one output, depth <= 8, 8-bit leaf-slot ids.
+// workgroups: scalar leaves (one output, or one per tree class), depth <= 8, 8-bit leaf-slot ids.
 #include "hb_fast.h"
 
 namespace hb {
 
-FastFn fast_pttg_kernel_128(int lg, int km) { return km == 1 ? pick_fast<3, 1, 128, kFastTableSmall>(lg) : nullptr; }
+FastFn fast_pttg_kernel_128(int lg, int km) {
+  return km == 1 ? pick_fast<3, 1, 128, kFastTableSmall>(lg)
+         : km == 2 ? pick_fast<3, 2, 128, kFastTableSmall>(lg)
+                   : pick_fast<3, HB_MAX_OUTPUTS, 128, kFastTableSmall>(lg);
+}
 
 }  // namespace hb

@@ -718,7 +718,7 @@ int launch_fast(int mode, int lg, const uint4 *blocks, const void *leaf, int chu
                 const float *vec, int vec_stride, int id_base, const EnsembleDev &e, const float *X, int64_t n_rows,
                 float *scores, int32_t *leaf_ids, const Launch &ws, hipStream_t stream, std::string *err) {
   if (!blocks || (mode >= 2 && !leaf) || lg < 1 || lg > kFastMaxLg) return kNotApplicable;
-  if (mode == 3 && (e.n_outputs != 1 || e.leaf_dim != 1 || lg > 8)) return kNotApplicable;
+  if (mode == 3 && (e.leaf_dim != 1 || lg > 8)) return kNotApplicable;
   if (e.leaf_dim != 1 && (!vec || e.leaf_dim != e.n_outputs || e.leaf_dim > HB_MAX_OUTPUTS)) return kNotApplicable;
   const int lds_max = max_dynamic_lds(err);
   if (lds_max <= 0) return HB_ERR_HIP;

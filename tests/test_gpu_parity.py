@@ -954,3 +954,33 @@ def test_general_and_wide_kernel_paths(kind, size, F, spread, T, K, ld, n, strat
     X = np.random.Generator(np.random.PCG64(n + F)).normal(0, 1, (n, F * spread)).astype(np.float32)
     scores, ids = run(h, X, strategy, workspace=False)
     check(m, X, scores, ids, f"path {kind}{size} F{F}x{spread} T{T} K{K} ld{ld} n{n} {strategy}")
+
+
+@pytest.mark.parametrize("K,permuted,expect", [
+    (7, False, "fast_kernel<3, 8, 16, "),
+    (7, True, "fast_kernel<0, 8, 16, "),
+    (2, False, "fast_kernel<3, 8, 2, "),
+    (2, True, "fast_kernel<0, 8, 2, "),
+])
+def test_class_trees_on_both_ptt_layouts(K, permuted, expect):
+    """One output column per tree class (softmax over K): heap-ordered perfect
+    trees keep their leaf values apart and add each held value to its tree's
+    column (mode 3); a permuted numbering keeps the leaf records in the
+    blocks (mode 0). Every row is compared with the oracle, leaf ids and
+    scores, at a batch past the tree-parallel kernel's range."""
+    rng = np.random.Generator(np.random.PCG64(900 + K + 10 * permuted))
+    T = 20 * K
+    model = synth.perfect_forest(rng, T, 8, 28, lambda r, f: r.standard_normal(f.size),
+                                 lambda r, n: r.normal(0.0, 0.05, n))
+    model.update(n_outputs=K, tree_class=(np.arange(T) % K).astype(np.int32), aggregation="sum",
+                 transform="softmax", base_score=None)
+    if permuted:
+        model = synth.permute_nodes(model, T)
+    h = hb.compile(model, device=0)
+    n = 20_003
+    plan = [p["kernel"] for p in h.plan(n, "ptt")]
+    say("class trees", K, "permuted" if permuted else "heap", plan)
+    assert plan[0].startswith(expect), plan
+    X = synth.make_rows(2, n)
+    scores, ids = run(h, X, "ptt", workspace=False)
+    check(model, X, scores, ids, f"class trees K={K} permuted={permuted}")
