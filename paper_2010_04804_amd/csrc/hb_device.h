@@ -237,7 +237,8 @@ FastFn fast_ptt_kernel_512s(int lg, int km);
 FastFn fast_ptt_kernel_768(int lg, int km);
 FastFn fast_ptt_kernel_1024(int lg, int km);
 // PTT with the leaf values in global memory and 8-bit slot ids (mode 3):
-// one output only (km == 1), lg <= 8, 32 KiB of double-buffered chunks.
+// scalar leaves, one output (km 1) or one per tree class (km 2, or 16 below
+// 1024-row workgroups), lg <= 8, 32 KiB of double-buffered chunks.
 FastFn fast_pttg_kernel_1024(int lg, int km);
 FastFn fast_pttg_kernel_512(int lg, int km);
 FastFn fast_pttg_kernel_256(int lg, int km);

@@ -30,6 +30,11 @@ constexpr int64_t kTreeLdsLimit = 160 * 1024 - 4 * 1024;
 //     records only, and the leaf records live in a separate array
 //     [trees][2^lg] read from global memory once per walk, so a chunk holds
 //     twice the trees; used while that array fits in an XCD's L2.
+//   PTT mode 3 (lg = D <= 8; scalar leaves whose caller ids are the leaf slot
+//     plus one base, as in heap-ordered perfect trees): the block holds the
+//     node records only; the leaf values live in a float array [trees][2^D]
+//     read from global memory once per walk, and the ids are formed from
+//     the slots.
 // Blocks are grouped in chunks of fast_tc() trees staged through LDS, either
 // double-buffered (the next chunk is stored while nobody reads its buffer) or
 // single-buffered with twice as many trees per chunk (more independent walks
@@ -39,11 +44,11 @@ constexpr int64_t kTreeLdsLimit = 160 * 1024 - 4 * 1024;
 // multiple of kFastIdGroup (so every chunk size divides it).
 constexpr int kFastTableLds = 64 * 1024;
 constexpr int kFastIdGroup = 32;
-// The fast kernels hold and stage leaf ids as 16-bit halves: every caller id
-// they report is a local node id of a tree with at most 2^(kFastMaxLg + 1)
-// nodes. Each wave stages up to 16 of its 64 rows at a time (the 32 ids of
-// one 128-byte output line per row, for two lines), so the staging costs 16
-// bytes per row of a workgroup.
+// The fast kernels hold and stage leaf ids as 16-bit halves (mode 3: byte
+// slots, half the staging): every caller id they report is a local node id
+// of a tree with at most 2^(kFastMaxLg + 1) nodes. Each wave stages up to 16
+// of its 64 rows at a time (the 32 ids of one 128-byte output line per row,
+// for two lines), so the staging costs 16 bytes per row of a workgroup.
 constexpr int kFastIdStageBytes = 2 * 8 * kFastIdGroup * 2 / 64;
 constexpr int fast_node_bytes(int mode) { return (void)mode, 8; }
 // modes 2 (TT) and 3 (PTT) keep the leaves apart, in global memory
