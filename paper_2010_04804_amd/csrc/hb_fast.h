@@ -520,6 +520,26 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
   // chunk c is in tbuf[B] (the barrier that ended the previous chunk made it
   // visible); fetch chunk c+1 into registers while walking chunk c
   const bool more = c + 1 < a.n_chunks;
+  // The chunk's root records (PTT: heap index 1, at byte 8 of a block; TT:
+  // node 0) are the same for every lane. In 1024-row workgroups they come
+  // by scalar loads (issued here, used after the chunk's leaf-id passes) and
+  // the walk's first level reads no node record from LDS: one LDS read of
+  // the 16 of a depth-8 walk, about 3% of the headline's time. With fewer
+  // waves per CU the scalar loads' wait at each chunk costs more than that
+  // (measured on the 512-row 7-class and 256-row leaf-wise shapes), and the
+  // root comes from LDS like the other levels.
+  constexpr bool kRootS = ROWS >= 1024;
+  constexpr uint32_t kRootOff = (MODE == 0 || MODE == 3) ? 8u : 0u;
+  typedef __attribute__((address_space(4))) const uint32_t cword_t;
+  uint32_t root_t[kRootS ? TC : 1], root_f[kRootS ? TC : 1];
+  if constexpr (kRootS) {
+    const cword_t *cb = (const cword_t *)(reinterpret_cast<const unsigned char *>(a.blocks) + (size_t)c * TC * TB);
+#pragma unroll
+    for (int g = 0; g < TC; ++g) {
+      root_t[g] = cb[(g * TB + kRootOff) / 4];
+      root_f[g] = cb[(g * TB + kRootOff) / 4 + 1];
+    }
+  }
   // TT: lane g holds the depth of tree g of the chunk, loaded one chunk ahead
   // and before the blocks (waiting for a load issued behind the prefetch
   // would mean waiting for the whole prefetch)
@@ -577,13 +597,26 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
     // for the oldest read and about TC reads stay in flight per wave.
     uint2 rec[TC];
     float xv[TC];
+    if constexpr (kRootS) {
+      // level 0 from the scalar root records: heap index 1 -> 2 or 3
 #pragma unroll
-    for (int g = 0; g < TC; ++g) {
-      s[g] = 8u;  // heap index 1
-      rec[g] = *reinterpret_cast<const uint2 *>(base + g * TB + 8u);
+      for (int g = 0; g < TC; ++g)
+        xv[g] = *reinterpret_cast<const float *>(xb + root_f[g] * (ROWS * 4u) + lane4);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int g = 0; g < TC; ++g) {
+        s[g] = xv[g] < as_float(root_t[g]) ? 16u : 24u;
+        if (LG > 1) rec[g] = *reinterpret_cast<const uint2 *>(base + g * TB + s[g]);
+      }
+    } else {
+#pragma unroll
+      for (int g = 0; g < TC; ++g) {
+        s[g] = 8u;  // heap index 1
+        rec[g] = *reinterpret_cast<const uint2 *>(base + g * TB + 8u);
+      }
     }
 #pragma unroll
-    for (int lvl = 0; lvl < LG; ++lvl) {
+    for (int lvl = kRootS ? 1 : 0; lvl < LG; ++lvl) {
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int g = 0; g < TC; ++g)
@@ -607,12 +640,26 @@ __device__ __forceinline__ void fast_chunk(const FastArgs &a, int c, uint4 (*tbu
     const uint32_t xlane = (uint32_t)(uintptr_t)xs + lane4;
     uint64_t rec[TC];  // {threshold bits, feature | 8 * right << 16}, one 8-byte read
     float xv[TC];
+    if constexpr (kRootS) {
+      // level 0 from the scalar root records (a chunk of leaves only, levels
+      // 0, takes the step too: a leaf loops to itself)
 #pragma unroll
-    for (int g = 0; g < TC; ++g) {
-      s[g] = 0u;  // root record
-      rec[g] = *reinterpret_cast<const uint64_t *>(base + g * TB);
+      for (int g = 0; g < TC; ++g)
+        xv[g] = *reinterpret_cast<lds_f32 *>((uintptr_t)(xlane + (root_f[g] & 0xffffu) * (ROWS * 4u)));
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int g = 0; g < TC; ++g) {
+        s[g] = (root_f[g] >> 16) - (xv[g] < as_float(root_t[g]) ? 8u : 0u);
+        rec[g] = *reinterpret_cast<const uint64_t *>(base + g * TB + s[g]);
+      }
+    } else {
+#pragma unroll
+      for (int g = 0; g < TC; ++g) {
+        s[g] = 0u;  // root record
+        rec[g] = *reinterpret_cast<const uint64_t *>(base + g * TB);
+      }
     }
-    for (int lvl = 0; lvl < levels; ++lvl) {
+    for (int lvl = kRootS ? 1 : 0; lvl < levels; ++lvl) {
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int g = 0; g < TC; ++g)
