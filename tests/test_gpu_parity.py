@@ -956,13 +956,16 @@ def test_general_and_wide_kernel_paths(kind, size, F, spread, T, K, ld, n, strat
     check(m, X, scores, ids, f"path {kind}{size} F{F}x{spread} T{T} K{K} ld{ld} n{n} {strategy}")
 
 
-@pytest.mark.parametrize("K,permuted,expect", [
-    (7, False, "fast_kernel<3, 8, 16, "),
-    (7, True, "fast_kernel<0, 8, 16, "),
-    (2, False, "fast_kernel<3, 8, 2, "),
-    (2, True, "fast_kernel<0, 8, 2, "),
+@pytest.mark.parametrize("K,permuted,n,expect", [
+    (7, False, 20_003, "fast_kernel<3, 8, 16, "),
+    (7, True, 20_003, "fast_kernel<0, 8, 16, "),
+    (2, False, 20_003, "fast_kernel<3, 8, 2, "),
+    (2, True, 20_003, "fast_kernel<0, 8, 2, "),
+    # batches wide enough for 1024-row workgroups (root records in scalar registers)
+    (2, False, 70_001, "fast_kernel<3, 8, 2, 1024, "),
+    (2, True, 70_001, "fast_kernel<0, 8, 2, 1024, "),
 ])
-def test_class_trees_on_both_ptt_layouts(K, permuted, expect):
+def test_class_trees_on_both_ptt_layouts(K, permuted, n, expect):
     """One output column per tree class (softmax over K): heap-ordered perfect
     trees keep their leaf values apart and add each held value to its tree's
     column (mode 3); a permuted numbering keeps the leaf records in the
@@ -977,9 +980,8 @@ def test_class_trees_on_both_ptt_layouts(K, permuted, expect):
     if permuted:
         model = synth.permute_nodes(model, T)
     h = hb.compile(model, device=0)
-    n = 20_003
     plan = [p["kernel"] for p in h.plan(n, "ptt")]
-    say("class trees", K, "permuted" if permuted else "heap", plan)
+    say("class trees", K, "permuted" if permuted else "heap", n, plan)
     assert plan[0].startswith(expect), plan
     X = synth.make_rows(2, n)
     scores, ids = run(h, X, "ptt", workspace=False)
