@@ -462,12 +462,13 @@ __global__ __launch_bounds__(ROWS) void gemm_pipe_kernel(GemmArgs a) {
 // one row per thread, into a double-buffered LDS tile; each wave then runs
 // its 16 matrix instructions and reduces its leaves to four maxima per row
 // (one per lane group), and the sixteen maxima meet in LDS. Trees go in
-// pairs, one barrier per pair, so that the latencies of two trees' LDS round
-// trips overlap (a 16-row tile of 2000 features leaves room for one
-// workgroup per CU only). Node records pass through LDS one pair ahead
+// pairs, one barrier per pair. Node records pass through LDS one pair ahead
 // (loaded two pairs ahead); the leaf of tree t is looked up by wave t mod 4,
 // whose loads are consumed when that wave's turn comes again, and the four
-// waves' partial sums are added in wave order at the end.
+// waves' partial sums are added in wave order at the end. This four-wave
+// kernel runs where the tile leaves room for two workgroups per CU; where it
+// leaves room for one (a 16-row tile of 2,000 features), gemm_tile2_kernel
+// puts eight waves on the one tile.
 constexpr int kTileRows = 16;
 constexpr int kTileBStride = 256 + 16;  // bytes per row of the predicate tile (spreads the 16 rows over banks)
 
@@ -519,42 +520,11 @@ __device__ __forceinline__ void tile_leaf_consume(const GemmArgs &a, TileLeaf<KM
   p.t = -1;
 }
 
-// Predicate operands of two trees: thread (row tid % 16, nodes 16 (tid / 16)
-// .. + 15) compares its row's features with the 16 records of each tree and
-// writes the 16 outcome bytes per tree to the tiles. All record reads go
-// first, then all feature reads, so that the LDS round trips overlap.
-__device__ __forceinline__ void tile_build2(const float *xs, int XS, const uint2 (*rtab)[256],
-                                            unsigned char (*bt)[kTileRows * kTileBStride]) {
-  const int tid = threadIdx.x;
-  const int r = tid & 15, nb = tid >> 4;
-  uint2 rec[2][16];
-#pragma unroll
-  for (int u = 0; u < 2; ++u)
-#pragma unroll
-    for (int q = 0; q < 16; ++q) rec[u][q] = rtab[u][nb * 16 + q];
-  float x[2][16];
-#pragma unroll
-  for (int u = 0; u < 2; ++u)
-#pragma unroll
-    for (int q = 0; q < 16; ++q) x[u][q] = xs[r * XS + (int)rec[u][q].y];
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    u32x4 w;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      uint32_t word = 0;
-#pragma unroll
-      for (int b = 0; b < 4; ++b) word |= (x[u][q * 4 + b] < as_float(rec[u][q * 4 + b].x) ? 0x40u : 0u) << (8 * b);
-      w[q] = word;
-    }
-    *reinterpret_cast<u32x4 *>(bt[u] + r * kTileBStride + nb * 16) = w;
-  }
-}
-
-// The same for one tree, with a quarter of the registers: where LDS leaves
-// room for two or more workgroups per CU, occupancy hides the round trips.
-__device__ __forceinline__ void tile_build1(const float *xs, int XS, const uint2 *rtab, unsigned char *bt) {
-  const int tid = threadIdx.x;
+// Predicate operand of one tree: thread (row tid % 16, nodes 16 (tid / 16)
+// .. + 15) compares its row's features with its 16 records and writes the 16
+// outcome bytes (64 where x < threshold) to the tile.
+__device__ __forceinline__ void tile_build1(const float *xs, int XS, const uint2 *rtab, unsigned char *bt, int tid) {
+  // tid: the thread's index among the 256 that build this tree
   const int r = tid & 15, nb = tid >> 4;
   const uint2 *rec = rtab + nb * 16;
   u32x4 w;
@@ -598,7 +568,7 @@ __device__ __forceinline__ int tile_best(const v4i (&d)[4]) {
 // loads) and are discarded, so the pair is one straight block: the builds
 // are issued while the matrix instructions execute, and only then are the
 // accumulators read.
-template <int KMODE, bool WIDE, int P>
+template <int KMODE, int P>
 __device__ __forceinline__ void tile_pair(const GemmArgs &a, int t, const float *xs, int XS,
                                           unsigned char (*bt)[2][kTileRows * kTileBStride], uint2 (*rtab)[2][256],
                                           int (*red)[2][16][kTileRows], uint2 (&rset)[2][2], const v4i (&ctr)[4][4],
@@ -614,12 +584,8 @@ __device__ __forceinline__ void tile_pair(const GemmArgs &a, int t, const float 
   v4i d0[4], d1[4];
   tile_product(bt[P][0], ctr, b4, d0);
   tile_product(bt[P][1], ctr, b4, d1);
-  if (WIDE) {
-    tile_build2(xs, XS, rtab[P ^ 1], bt[P ^ 1]);
-  } else {
-    tile_build1(xs, XS, rtab[P ^ 1][0], bt[P ^ 1][0]);
-    tile_build1(xs, XS, rtab[P ^ 1][1], bt[P ^ 1][1]);
-  }
+  tile_build1(xs, XS, rtab[P ^ 1][0], bt[P ^ 1][0], tid);
+  tile_build1(xs, XS, rtab[P ^ 1][1], bt[P ^ 1][1], tid);
   red[P][0][wave * 4 + g4][r16] = tile_best(d0);  // 16 partial maxima per row, combined by the leaf's wave
   red[P][1][wave * 4 + g4][r16] = tile_best(d1);
   lds_sync();
@@ -636,10 +602,7 @@ __device__ __forceinline__ void tile_pair(const GemmArgs &a, int t, const float 
   }
 }
 
-// WIDE: the feature tile leaves room for one workgroup per CU; both trees'
-// predicate operands are built together (more registers, overlapped LDS
-// round trips) instead of one after the other.
-template <int KMODE, bool WIDE>
+template <int KMODE>
 __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
   constexpr int KMAX = TileLeaf<KMODE>::KMAX;
   extern __shared__ __align__(16) unsigned char smem[];  // feature tile [16][XS], then the waves' partial sums
@@ -688,15 +651,16 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
     rset[u >> 1][u & 1] = a.node[(size_t)min(tb + u + 4, T - 1) * 256 + tid];
   }
   lds_sync();
-  tile_build2(xs, XS, rtab[0], bt[0]);
+  tile_build1(xs, XS, rtab[0][0], bt[0][0], tid);
+  tile_build1(xs, XS, rtab[0][1], bt[0][1], tid);
   lds_sync();
   double acc[KMAX];
 #pragma unroll
   for (int k = 0; k < KMAX; ++k) acc[k] = 0.0;
   TileLeaf<KMODE> pend;
   for (int t = tb; t < T; t += 4) {
-    tile_pair<KMODE, WIDE, 0>(a, t, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0, T);
-    if (t + 2 < T) tile_pair<KMODE, WIDE, 1>(a, t + 2, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0, T);
+    tile_pair<KMODE, 0>(a, t, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0, T);
+    if (t + 2 < T) tile_pair<KMODE, 1>(a, t + 2, xs, XS, bt, rtab, red, rset, ctr, b4, pend, acc, r0, T);
   }
   if (lane < kTileRows) tile_leaf_consume<KMODE>(a, pend, acc, r0 + lane);
   // partial sums in wave order (the feature tile is no longer read)
@@ -711,6 +675,133 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
 #pragma unroll
     for (int k = 0; k < KMAX; ++k) s[k] = 0.0;
     for (int w = 0; w < 4; ++w) {
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k) s[k] += part[(w * kTileRows + lane) * KMAX + k];
+    }
+    if (a.split) {
+      double *dst = a.partial + ((size_t)blockIdx.y * a.n_rows + r0 + lane) * a.out.K;
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k)
+        if (k < a.out.K) dst[k] = s[k];
+    } else {
+      finish_row<KMAX>(a.out, s, r0 + lane);
+    }
+  }
+}
+
+// Wide rows with two groups of four waves on one 16-row feature tile (eight
+// waves, two per SIMD, where the four-wave kernel leaves one per SIMD, with
+// the predicate build's LDS round trips exposed). Group g takes trees
+// tb + g, tb + g + 2, ..., one per step between two barriers: in step k it
+// multiplies its tree k (built in step k - 1) and builds its tree k + 1, so
+// each wave overlaps its own matrix instructions with LDS reads, and the
+// other group's wave on the same SIMD fills its waits. Each group has its
+// own double-buffered predicate tile, record table and maxima (the same LDS
+// as the four-wave kernel's pairs). Tree k of a group is looked up by the
+// group's wave k mod 4; the eight waves' sums are added in wave order.
+constexpr int kTile2Threads = 512;
+
+template <int KMODE, int P>
+__device__ __forceinline__ void tile2_step(const GemmArgs &a, int k, int grp, int mine, int tb, int T, const float *xs,
+                                           int XS, unsigned char (*bt)[kTileRows * kTileBStride], uint2 (*rtab)[256],
+                                           int (*red)[16][kTileRows], uint2 (&rset)[2], const v4i (&ctr)[4][4],
+                                           const v4i (&b4)[4], TileLeaf<KMODE> &pend,
+                                           double (&acc)[TileLeaf<KMODE>::KMAX], int64_t r0) {
+  // bt, rtab, red: this group's buffers; group tree k is tree tb + grp + 2k
+  const int gt = threadIdx.x & 255, lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) & 3;
+  const int g4 = lane >> 4, r16 = lane & 15;
+  rtab[P][gt] = rset[P];  // records of group tree k + 2 (loaded two steps ago)
+  rset[P] = a.node[(size_t)min(tb + grp + 2 * (k + 4), T - 1) * 256 + gt];
+  v4i d[4];
+  tile_product(bt[P], ctr, b4, d);
+  tile_build1(xs, XS, rtab[P ^ 1], bt[P ^ 1], gt);
+  red[P][wave * 4 + g4][r16] = tile_best(d);
+  lds_sync();
+  if (k < mine && wave == (k & 3) && lane < kTileRows) {
+    tile_leaf_consume<KMODE>(a, pend, acc, r0 + lane);
+    int col = red[P][0][lane];
+#pragma unroll
+    for (int q = 1; q < 16; ++q) col = max(col, red[P][q][lane]);
+    col = min(max(col, 0), a.l_pad - 1);  // a valid tree always yields a column in range
+    tile_leaf_issue<KMODE>(a, pend, tb + grp + 2 * k, col);
+  }
+}
+
+template <int KMODE>
+__global__ __launch_bounds__(kTile2Threads) void gemm_tile2_kernel(GemmArgs a) {
+  constexpr int KMAX = TileLeaf<KMODE>::KMAX;
+  extern __shared__ __align__(16) unsigned char smem[];  // feature tile [16][XS], then the waves' partial sums
+  __shared__ __align__(16) unsigned char bt[2][2][kTileRows * kTileBStride];  // [group][buffer]
+  __shared__ __align__(16) uint2 rtab[2][2][256];
+  __shared__ int red[2][2][16][kTileRows];
+  const int tid = threadIdx.x, lane = tid & 63, grp = tid >> 8, gt = tid & 255, wave = (tid >> 6) & 3;
+  const int g4 = lane >> 4, r16 = lane & 15;
+  const int tb = a.split ? (int)blockIdx.y * a.split : 0;
+  const int T = a.split ? min(tb + a.split, a.out.T) : a.out.T;
+  const int steps = (T - tb + 1) >> 1;      // group 0's tree count, the larger
+  const int mine = (T - tb - grp + 1) >> 1;  // this group's
+  const int XS = gemm_tile_xs(a.F);
+  float *xs = reinterpret_cast<float *>(smem);
+  const int64_t r0 = (int64_t)blockIdx.x * kTileRows;
+  if (!a.cols && (a.F & 3) == 0 && (a.Fs & 3) == 0 && (reinterpret_cast<uintptr_t>(a.X) & 15) == 0) {
+    const int F4 = a.F >> 2;
+#pragma unroll 4
+    for (int r = 0; r < kTileRows; ++r) {
+      const bool ok = r0 + r < a.n_rows;
+      const float4 *src = reinterpret_cast<const float4 *>(a.X + (ok ? r0 + r : (int64_t)0) * a.Fs);
+      for (int f = tid; f < F4; f += kTile2Threads)
+        *reinterpret_cast<float4 *>(xs + r * XS + 4 * f) = ok ? src[f] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  } else {
+    for (int r = 0; r < kTileRows; ++r) {
+      const bool ok = r0 + r < a.n_rows;
+      const float *src = a.X + (ok ? r0 + r : (int64_t)0) * a.Fs;
+      for (int f = tid; f < a.F; f += kTile2Threads) xs[r * XS + f] = ok ? xval(src, a.cols, f) : 0.0f;
+    }
+  }
+  v4i ctr[4][4], b4[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int lt = wave * 4 + j;
+    b4[j] = *reinterpret_cast<const v4i *>(a.bias + lt * 16 + 4 * g4);
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+      ctr[j][kb] = *reinterpret_cast<const v4i *>(a.ct + (size_t)(lt * 16 + r16) * 256 + kb * 64 + 16 * g4);
+  }
+  // records of group trees 0, 1 in LDS, 2, 3 in registers (trees past the
+  // last are clamped to it; their results are not used)
+  uint2 rset[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    rtab[grp][u][gt] = a.node[(size_t)min(tb + grp + 2 * u, T - 1) * 256 + gt];
+    rset[u] = a.node[(size_t)min(tb + grp + 2 * (u + 2), T - 1) * 256 + gt];
+  }
+  lds_sync();
+  tile_build1(xs, XS, rtab[grp][0], bt[grp][0], gt);
+  lds_sync();
+  double acc[KMAX];
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) acc[k] = 0.0;
+  TileLeaf<KMODE> pend;
+  for (int k = 0; k < steps; k += 2) {
+    tile2_step<KMODE, 0>(a, k, grp, mine, tb, T, xs, XS, bt[grp], rtab[grp], red[grp], rset, ctr, b4, pend, acc, r0);
+    if (k + 1 < steps)
+      tile2_step<KMODE, 1>(a, k + 1, grp, mine, tb, T, xs, XS, bt[grp], rtab[grp], red[grp], rset, ctr, b4, pend, acc,
+                           r0);
+  }
+  if (lane < kTileRows) tile_leaf_consume<KMODE>(a, pend, acc, r0 + lane);
+  double *part = reinterpret_cast<double *>(smem);
+  const int w8 = tid >> 6;
+  if (lane < kTileRows) {
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) part[(w8 * kTileRows + lane) * KMAX + k] = acc[k];
+  }
+  lds_sync();
+  if (w8 == 0 && lane < kTileRows && r0 + lane < a.n_rows) {
+    double s[KMAX];
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) s[k] = 0.0;
+    for (int w = 0; w < kTile2Threads / 64; ++w) {
 #pragma unroll
       for (int k = 0; k < KMAX; ++k) s[k] += part[(w * kTileRows + lane) * KMAX + k];
     }
@@ -1009,12 +1100,22 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
     if (tile_dyn + tile_static <= (size_t)lds_max) {
       const bool wide = 2 * (tile_dyn + tile_static) > (size_t)lds_max;  // one workgroup per CU
       tile_wide = wide;
-      fn = wide ? (kmode == 0 ? gemm_tile_kernel<0, true> : kmode == 1 ? gemm_tile_kernel<1, true> : gemm_tile_kernel<2, true>)
-                : (kmode == 0 ? gemm_tile_kernel<0, false> : kmode == 1 ? gemm_tile_kernel<1, false> : gemm_tile_kernel<2, false>);
-      dyn = tile_dyn;
+      // one workgroup per CU: eight waves in two groups on the one feature
+      // tile (the same static LDS; the eight waves' partial sums in the tile
+      // at the end, which a tile this wide always holds)
+      const size_t tile2_dyn = std::max(tile_dyn, (size_t)8 * kTileRows * kmax * 8);
+      if (!wide) {
+        fn = kmode == 0 ? gemm_tile_kernel<0> : kmode == 1 ? gemm_tile_kernel<1> : gemm_tile_kernel<2>;
+        dyn = tile_dyn;
+        threads = 256;
+        name = "gemm_tile_kernel<" + std::to_string(kmode) + ">";
+      } else if (tile2_dyn + tile_static <= (size_t)lds_max) {
+        fn = kmode == 0 ? gemm_tile2_kernel<0> : kmode == 1 ? gemm_tile2_kernel<1> : gemm_tile2_kernel<2>;
+        dyn = tile2_dyn;
+        threads = kTile2Threads;
+        name = "gemm_tile2_kernel<" + std::to_string(kmode) + ">";
+      }
       rows = kTileRows;
-      threads = 256;
-      name = "gemm_tile_kernel<" + std::to_string(kmode) + ", " + (wide ? "true" : "false") + ">";
     }
   }
   if (!fn) {

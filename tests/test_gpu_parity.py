@@ -233,12 +233,16 @@ def test_leaf_id_lines_at_any_offset(n_trees, depth, heap):
 
 
 @pytest.mark.parametrize("kind", ["scalar", "classes", "vector"])
-@pytest.mark.parametrize("n_trees,n", [(1, 17), (2, 16), (3, 33), (37, 1007), (64, 4099)])
+@pytest.mark.parametrize("n_trees,n", [(1, 17), (2, 16), (3, 33), (9, 40), (10, 300), (37, 1007), (64, 4099)])
 def test_gemm_wide_rows(kind, n_trees, n):
     """Depth-8 trees over 1,500 features: the GEMM tables' 256-row feature
     tile does not fit in LDS, so 16-row tiles with C^T in registers take
-    the batch (tree counts of 1 to 3 exercise the two-tree software
-    pipeline's start; rows hold ties, NaN and infinities)."""
+    the batch. From 9 trees on the used columns leave room for one tile
+    workgroup per CU, which runs two groups of four waves (odd tree counts
+    end on a pair of one tree, and the tree split's last part of one tree
+    leaves the second group without a pair); 1 to 3 trees use a few hundred
+    columns and take the four-wave tiles, two per CU. Rows hold ties, NaN
+    and infinities; with and without the tree split."""
     rng = np.random.Generator(np.random.PCG64(4200 + n_trees + n))
     F = 1500
     ld = 2 if kind == "vector" else 1
@@ -252,8 +256,13 @@ def test_gemm_wide_rows(kind, n_trees, n):
     X = np.ascontiguousarray(pins.tricky_rows(rng, model, n))
     h = hb.compile(model, device=0)
     say("gemm wide rows", kind, n_trees, n)
+    for ws in (True, False):
+        plan = [p["kernel"] for p in h.plan(n, "gemm", hb.workspace_bytes(h, n, "gemm") if ws else 0)]
+        assert plan[0].startswith("gemm_tile2_kernel<" if n_trees >= 9 else "gemm_tile_kernel<"), plan
     scores, ids = run(h, X, "gemm")
     check(model, X, scores, ids, f"gemm wide {kind}/{n_trees}/{n}")
+    scores, ids = run(h, X, "gemm", workspace=False)
+    check(model, X, scores, ids, f"gemm wide unsplit {kind}/{n_trees}/{n}")
 
 
 def _gemm_512_model(kind):
