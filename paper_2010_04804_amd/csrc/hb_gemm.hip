@@ -479,41 +479,43 @@ __host__ __device__ inline int gemm_tile_xs(int F) {
   return (xs & 7) ? xs : xs + 4;
 }
 
-template <int KMODE>
+// KM: outputs a row's sums hold (1 for one output; the class count or leaf
+// width rounded up to a compiled size, else HB_MAX_OUTPUTS)
+template <int KMODE, int KM = (KMODE == 0 ? 1 : HB_MAX_OUTPUTS)>
 struct TileLeaf {
-  static constexpr int KMAX = KMODE == 0 ? 1 : HB_MAX_OUTPUTS;
+  static constexpr int KMAX = KM;
   int t = -1;  // tree of the pending lookup, -1 none
   int cls = 0;
   int32_t id = 0;
   float v[KMODE == 2 ? KMAX : 1];
 };
 
-template <int KMODE>
-__device__ __forceinline__ void tile_leaf_issue(const GemmArgs &a, TileLeaf<KMODE> &p, int t, int col) {
+template <int KMODE, int KM>
+__device__ __forceinline__ void tile_leaf_issue(const GemmArgs &a, TileLeaf<KMODE, KM> &p, int t, int col) {
   const size_t lrec = (size_t)t * a.l_pad + (size_t)col;
   p.t = t;
   p.id = a.leaf_id[lrec];
   if (KMODE == 2) {
 #pragma unroll
-    for (int k = 0; k < TileLeaf<KMODE>::KMAX; ++k) p.v[k] = k < a.LD ? a.leaf_value[lrec * a.LD + k] : 0.0f;
+    for (int k = 0; k < KM; ++k) p.v[k] = k < a.LD ? a.leaf_value[lrec * a.LD + k] : 0.0f;
   } else {
     p.v[0] = a.leaf_value[lrec];
     if (KMODE == 1) p.cls = a.tree_class[t];
   }
 }
 
-template <int KMODE>
-__device__ __forceinline__ void tile_leaf_consume(const GemmArgs &a, TileLeaf<KMODE> &p, double (&acc)[TileLeaf<KMODE>::KMAX],
+template <int KMODE, int KM>
+__device__ __forceinline__ void tile_leaf_consume(const GemmArgs &a, TileLeaf<KMODE, KM> &p, double (&acc)[KM],
                                                   int64_t row) {
   if (p.t < 0) return;
   if (KMODE == 2) {
 #pragma unroll
-    for (int k = 0; k < TileLeaf<KMODE>::KMAX; ++k) acc[k] += (double)p.v[k];
+    for (int k = 0; k < KM; ++k) acc[k] += (double)p.v[k];
   } else if (KMODE == 0) {
     acc[0] += (double)p.v[0];
   } else {
 #pragma unroll
-    for (int k = 0; k < TileLeaf<KMODE>::KMAX; ++k)
+    for (int k = 0; k < KM; ++k)
       if (k == p.cls) acc[k] += (double)p.v[0];
   }
   if (a.leaf_ids && row < a.n_rows) a.leaf_ids[row * a.out.T + p.t] = p.id;
@@ -701,12 +703,12 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
 // group's wave k mod 4; the eight waves' sums are added in wave order.
 constexpr int kTile2Threads = 512;
 
-template <int KMODE, int P>
+template <int KMODE, int KM, int P>
 __device__ __forceinline__ void tile2_step(const GemmArgs &a, int k, int grp, int mine, int tb, int T, const float *xs,
                                            int XS, unsigned char (*bt)[kTileRows * kTileBStride], uint2 (*rtab)[256],
                                            int (*red)[16][kTileRows], uint2 (&rset)[2], const v4i (&ctr)[4][4],
-                                           const v4i (&b4)[4], TileLeaf<KMODE> &pend,
-                                           double (&acc)[TileLeaf<KMODE>::KMAX], int64_t r0) {
+                                           const v4i (&b4)[4], TileLeaf<KMODE, KM> &pend, double (&acc)[KM],
+                                           int64_t r0) {
   // bt, rtab, red: this group's buffers; group tree k is tree tb + grp + 2k
   const int gt = threadIdx.x & 255, lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) & 3;
   const int g4 = lane >> 4, r16 = lane & 15;
@@ -718,18 +720,18 @@ __device__ __forceinline__ void tile2_step(const GemmArgs &a, int k, int grp, in
   red[P][wave * 4 + g4][r16] = tile_best(d);
   lds_sync();
   if (k < mine && wave == (k & 3) && lane < kTileRows) {
-    tile_leaf_consume<KMODE>(a, pend, acc, r0 + lane);
+    tile_leaf_consume(a, pend, acc, r0 + lane);
     int col = red[P][0][lane];
 #pragma unroll
     for (int q = 1; q < 16; ++q) col = max(col, red[P][q][lane]);
     col = min(max(col, 0), a.l_pad - 1);  // a valid tree always yields a column in range
-    tile_leaf_issue<KMODE>(a, pend, tb + grp + 2 * k, col);
+    tile_leaf_issue(a, pend, tb + grp + 2 * k, col);
   }
 }
 
-template <int KMODE>
+template <int KMODE, int KM>
 __global__ __launch_bounds__(kTile2Threads) void gemm_tile2_kernel(GemmArgs a) {
-  constexpr int KMAX = TileLeaf<KMODE>::KMAX;
+  constexpr int KMAX = KM;
   extern __shared__ __align__(16) unsigned char smem[];  // feature tile [16][XS], then the waves' partial sums
   __shared__ __align__(16) unsigned char bt[2][2][kTileRows * kTileBStride];  // [group][buffer]
   __shared__ __align__(16) uint2 rtab[2][2][256];
@@ -782,14 +784,14 @@ __global__ __launch_bounds__(kTile2Threads) void gemm_tile2_kernel(GemmArgs a) {
   double acc[KMAX];
 #pragma unroll
   for (int k = 0; k < KMAX; ++k) acc[k] = 0.0;
-  TileLeaf<KMODE> pend;
+  TileLeaf<KMODE, KM> pend;
   for (int k = 0; k < steps; k += 2) {
-    tile2_step<KMODE, 0>(a, k, grp, mine, tb, T, xs, XS, bt[grp], rtab[grp], red[grp], rset, ctr, b4, pend, acc, r0);
+    tile2_step<KMODE, KM, 0>(a, k, grp, mine, tb, T, xs, XS, bt[grp], rtab[grp], red[grp], rset, ctr, b4, pend, acc, r0);
     if (k + 1 < steps)
-      tile2_step<KMODE, 1>(a, k + 1, grp, mine, tb, T, xs, XS, bt[grp], rtab[grp], red[grp], rset, ctr, b4, pend, acc,
+      tile2_step<KMODE, KM, 1>(a, k + 1, grp, mine, tb, T, xs, XS, bt[grp], rtab[grp], red[grp], rset, ctr, b4, pend, acc,
                            r0);
   }
-  if (lane < kTileRows) tile_leaf_consume<KMODE>(a, pend, acc, r0 + lane);
+  if (lane < kTileRows) tile_leaf_consume(a, pend, acc, r0 + lane);
   double *part = reinterpret_cast<double *>(smem);
   const int w8 = tid >> 6;
   if (lane < kTileRows) {
@@ -1110,10 +1112,16 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
         threads = 256;
         name = "gemm_tile_kernel<" + std::to_string(kmode) + ">";
       } else if (tile2_dyn + tile_static <= (size_t)lds_max) {
-        fn = kmode == 0 ? gemm_tile2_kernel<0> : kmode == 1 ? gemm_tile2_kernel<1> : gemm_tile2_kernel<2>;
+        const int width = kmode == 2 ? e.leaf_dim : e.n_outputs;
+        const int km = kmode == 0 ? 1 : kmode == 2 && width <= 2 ? 2 : width <= 8 ? 8 : HB_MAX_OUTPUTS;
+        fn = kmode == 0    ? gemm_tile2_kernel<0, 1>
+             : kmode == 1  ? (km == 8 ? gemm_tile2_kernel<1, 8> : gemm_tile2_kernel<1, HB_MAX_OUTPUTS>)
+             : km == 2     ? gemm_tile2_kernel<2, 2>
+             : km == 8     ? gemm_tile2_kernel<2, 8>
+                           : gemm_tile2_kernel<2, HB_MAX_OUTPUTS>;
         dyn = tile2_dyn;
         threads = kTile2Threads;
-        name = "gemm_tile2_kernel<" + std::to_string(kmode) + ">";
+        name = "gemm_tile2_kernel<" + std::to_string(kmode) + ", " + std::to_string(km) + ">";
       }
       rows = kTileRows;
     }

@@ -232,7 +232,7 @@ def test_leaf_id_lines_at_any_offset(n_trees, depth, heap):
                     assert np.all(b[:off] == -7) and np.all(b[off + n * n_trees:] == -7), "write outside the output"
 
 
-@pytest.mark.parametrize("kind", ["scalar", "classes", "vector"])
+@pytest.mark.parametrize("kind", ["scalar", "classes", "vector", "classes12", "vector5"])
 @pytest.mark.parametrize("n_trees,n", [(1, 17), (2, 16), (3, 33), (9, 40), (10, 300), (37, 1007), (64, 4099)])
 def test_gemm_wide_rows(kind, n_trees, n):
     """Depth-8 trees over 1,500 features: the GEMM tables' 256-row feature
@@ -241,24 +241,29 @@ def test_gemm_wide_rows(kind, n_trees, n):
     workgroup per CU, which runs two groups of four waves (odd tree counts
     end on a pair of one tree, and the tree split's last part of one tree
     leaves the second group without a pair); 1 to 3 trees use a few hundred
-    columns and take the four-wave tiles, two per CU. Rows hold ties, NaN
-    and infinities; with and without the tree split."""
+    columns and take the four-wave tiles, two per CU. One output, 3 and 12
+    classes, 2- and 5-vector leaves: each output count the eight-wave kernel
+    is compiled for. Rows hold ties, NaN and infinities; with and without
+    the tree split."""
     rng = np.random.Generator(np.random.PCG64(4200 + n_trees + n))
     F = 1500
-    ld = 2 if kind == "vector" else 1
+    K = {"scalar": 1, "classes": 3, "vector": 2, "classes12": 12, "vector5": 5}[kind]
+    ld = K if kind.startswith("vector") else 1
     model = synth.perfect_forest(rng, n_trees, 8, F, lambda r, f: r.standard_normal(f.size),
                                  lambda r, k: r.standard_normal(k * ld), leaf_dim=ld)
-    K = {"scalar": 1, "classes": 3, "vector": 2}[kind]
-    model.update(n_outputs=K, aggregation="mean" if kind == "vector" else "sum",
-                 transform="softmax" if kind == "classes" else "none", base_score=None,
-                 tree_class=(np.arange(n_trees) % 3).astype(np.int32) if kind == "classes" else None)
+    classes = kind.startswith("classes")
+    model.update(n_outputs=K, aggregation="mean" if ld > 1 else "sum",
+                 transform="softmax" if classes else "none", base_score=None,
+                 tree_class=(np.arange(n_trees) % K).astype(np.int32) if classes else None)
     model = synth.permute_nodes(model, n_trees + n)
     X = np.ascontiguousarray(pins.tricky_rows(rng, model, n))
     h = hb.compile(model, device=0)
     say("gemm wide rows", kind, n_trees, n)
     for ws in (True, False):
         plan = [p["kernel"] for p in h.plan(n, "gemm", hb.workspace_bytes(h, n, "gemm") if ws else 0)]
-        assert plan[0].startswith("gemm_tile2_kernel<" if n_trees >= 9 else "gemm_tile_kernel<"), plan
+        km = {"scalar": 1, "classes": 8, "vector": 2, "classes12": 16, "vector5": 8}[kind]
+        mode = 1 if classes else 2 if ld > 1 else 0
+        assert plan[0] == (f"gemm_tile2_kernel<{mode}, {km}>" if n_trees >= 9 else f"gemm_tile_kernel<{mode}>"), plan
     scores, ids = run(h, X, "gemm")
     check(model, X, scores, ids, f"gemm wide {kind}/{n_trees}/{n}")
     scores, ids = run(h, X, "gemm", workspace=False)
