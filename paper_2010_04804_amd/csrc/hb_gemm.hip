@@ -702,11 +702,16 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
 // as the four-wave kernel's pairs). Tree k of a group is looked up by the
 // group's wave k mod 4; the eight waves' sums are added in wave order.
 constexpr int kTile2Threads = 512;
+// Maxima of a tree: per row, the 16 lane groups' values in one 80-byte row
+// (the lookup reads a row with four 16-byte loads; the 64 lanes writing at
+// once, rows 20 words apart, fall on 64 different banks).
+constexpr int kTile2RedStride = 20;
 
 template <int KMODE, int KM, int P>
 __device__ __forceinline__ void tile2_step(const GemmArgs &a, int k, int grp, int mine, int tb, int T, const float *xs,
                                            int XS, unsigned char (*bt)[kTileRows * kTileBStride], uint2 (*rtab)[256],
-                                           int (*red)[16][kTileRows], uint2 (&rset)[2], const v4i (&ctr)[4][4],
+                                           int (*red)[kTileRows][kTile2RedStride], uint2 (&rset)[2],
+                                           const v4i (&ctr)[4][4],
                                            const v4i (&b4)[4], TileLeaf<KMODE, KM> &pend, double (&acc)[KM],
                                            int64_t r0) {
   // bt, rtab, red: this group's buffers; group tree k is tree tb + grp + 2k
@@ -717,7 +722,7 @@ __device__ __forceinline__ void tile2_step(const GemmArgs &a, int k, int grp, in
   v4i d[4];
   tile_product(bt[P], ctr, b4, d);
   tile_build1(xs, XS, rtab[P ^ 1], bt[P ^ 1], gt);
-  red[P][wave * 4 + g4][r16] = tile_best(d);
+  red[P][r16][wave * 4 + g4] = tile_best(d);
   lds_sync();
   if (k < mine && wave == (k & 3)) {
     // the lookup makes this wave the last to reach the next barrier: its
@@ -727,9 +732,9 @@ __device__ __forceinline__ void tile2_step(const GemmArgs &a, int k, int grp, in
     __builtin_amdgcn_s_setprio(2);
     if (lane < kTileRows) {
       tile_leaf_consume(a, pend, acc, r0 + lane);
-      int col = red[P][0][lane];
-#pragma unroll
-      for (int q = 1; q < 16; ++q) col = max(col, red[P][q][lane]);
+      const v4i *m = reinterpret_cast<const v4i *>(red[P][lane]);
+      const v4i m0 = m[0], m1 = m[1], m2 = m[2], m3 = m[3];
+      int col = max(max(hmax4(m0), hmax4(m1)), max(hmax4(m2), hmax4(m3)));
       col = min(max(col, 0), a.l_pad - 1);  // a valid tree always yields a column in range
       tile_leaf_issue(a, pend, tb + grp + 2 * k, col);
     }
@@ -743,7 +748,7 @@ __global__ __launch_bounds__(kTile2Threads) void gemm_tile2_kernel(GemmArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];  // feature tile [16][XS], then the waves' partial sums
   __shared__ __align__(16) unsigned char bt[2][2][kTileRows * kTileBStride];  // [group][buffer]
   __shared__ __align__(16) uint2 rtab[2][2][256];
-  __shared__ int red[2][2][16][kTileRows];
+  __shared__ __align__(16) int red[2][2][kTileRows][kTile2RedStride];
   const int tid = threadIdx.x, lane = tid & 63, grp = tid >> 8, gt = tid & 255, wave = (tid >> 6) & 3;
   const int g4 = lane >> 4, r16 = lane & 15;
   const int tb = a.split ? (int)blockIdx.y * a.split : 0;
@@ -1114,12 +1119,13 @@ int launch_gemm(const EnsembleDev &e, const GemmDev &t, const float *X, int64_t 
       // tile (the same static LDS; the eight waves' partial sums in the tile
       // at the end, which a tile this wide always holds)
       const size_t tile2_dyn = std::max(tile_dyn, (size_t)8 * kTileRows * kmax * 8);
+      const size_t tile2_static = (size_t)4 * kTileRows * kTileBStride + 4 * 256 * 8 + 4 * kTileRows * kTile2RedStride * 4;
       if (!wide) {
         fn = kmode == 0 ? gemm_tile_kernel<0> : kmode == 1 ? gemm_tile_kernel<1> : gemm_tile_kernel<2>;
         dyn = tile_dyn;
         threads = 256;
         name = "gemm_tile_kernel<" + std::to_string(kmode) + ">";
-      } else if (tile2_dyn + tile_static <= (size_t)lds_max) {
+      } else if (tile2_dyn + tile2_static <= (size_t)lds_max) {
         const int width = kmode == 2 ? e.leaf_dim : e.n_outputs;
         const int km = kmode == 0 ? 1 : kmode == 2 && width <= 2 ? 2 : width <= 8 ? 8 : HB_MAX_OUTPUTS;
         fn = kmode == 0    ? gemm_tile2_kernel<0, 1>
