@@ -60,7 +60,7 @@ struct GemmArgs {
   const int32_t *leaf_id;   // [T][l_pad]
   int32_t k_pad, l_pad;
   int32_t ids_vec;
-  // tree split (small batches, gemm_tile_kernel): workgroup (x, y) takes
+  // tree split (small batches, the 16-row tile kernels): workgroup (x, y) takes
   // trees [y * split, min((y + 1) * split, T)) of row tile x and stores its
   // raw sums in partial[y][row][K]; 0 = every tree, rows finished in place
   int32_t split;
@@ -698,9 +698,9 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmArgs a) {
 // multiplies its tree k (built in step k - 1) and builds its tree k + 1, so
 // each wave overlaps its own matrix instructions with LDS reads, and the
 // other group's wave on the same SIMD fills its waits. Each group has its
-// own double-buffered predicate tile, record table and maxima (the same LDS
-// as the four-wave kernel's pairs). Tree k of a group is looked up by the
-// group's wave k mod 4; the eight waves' sums are added in wave order.
+// own double-buffered predicate tile, record table and maxima (1 KiB more
+// LDS than the four-wave kernel's pairs). Tree k of a group is looked up by
+// the group's wave k mod 4; the eight waves' sums are added in wave order.
 constexpr int kTile2Threads = 512;
 // Maxima of a tree: per row, the 16 lane groups' values in one 80-byte row
 // (the lookup reads a row with four 16-byte loads; the 64 lanes writing at
